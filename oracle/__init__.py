@@ -1,0 +1,55 @@
+"""Plain CPU oracle for the SpecFLASH draft-verify hot path (arXiv 2505.12728).
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports, calls or
+links this package: only the test suite, the smoke check and the CPU-baseline
+leg of the benchmark do.  It shares no code with the HIP library and imports
+nothing from it.
+
+Every function is a direct, unblocked, float64 statement of what the paper
+defines (or, for acceptance, of the step-by-step rule the paper cites), so a
+reader can check it against the paper by eye:
+
+* ``latent_compress``  -- the visual-token compressor, Sec. 3.2, Eq. 3
+  (also Algorithm 1, Appendix B).
+* ``verify_attention`` -- attention of the K drafted positions over the
+  target's KV cache during the single parallel verification pass, Sec. 3.1.
+* ``spec_accept``      -- token-wise acceptance / rejection with residual
+  resampling (Sec. 3.1, Sec. 3.3), and greedy verification for temperature 0
+  (Sec. 4.2).
+
+Readings of points the paper leaves open are stated in each module.  No
+function here is "parity unpinned": every one is checked in
+``tests/test_oracle_pins.py`` against closed forms, invariants, exact
+enumeration or brute force.
+"""
+
+from .compress import latent_compress, softmax_rows
+from .verify import verify_attention, gather_paged, merge_partials
+from .accept import (
+    spec_accept,
+    spec_accept_one,
+    accept_flags,
+    residual_weights,
+    fixed_point_sample,
+    ACCEPT_GREEDY,
+    ACCEPT_SAMPLED,
+    FIXED_POINT_BITS,
+    UNIFORM_BITS,
+)
+
+__all__ = [
+    "latent_compress",
+    "softmax_rows",
+    "verify_attention",
+    "gather_paged",
+    "merge_partials",
+    "spec_accept",
+    "spec_accept_one",
+    "accept_flags",
+    "residual_weights",
+    "fixed_point_sample",
+    "ACCEPT_GREEDY",
+    "ACCEPT_SAMPLED",
+    "FIXED_POINT_BITS",
+    "UNIFORM_BITS",
+]

@@ -1,0 +1,69 @@
+"""Oracle for latent-guided visual-token compression (Sec. 3.2, Eq. 3).
+
+Test infrastructure only (see the package docstring).
+
+Eq. 3 maps the N visual features F_V (N x d) to C compressed features with a
+learnable query set (C x d):  F_hat_V = softmax(Cq . F_V^T) . F_V, where the
+learned queries are the attention queries and F_V is both key and value.
+
+Readings (the paper is silent on these points):
+* Scale: Eq. 3 has no 1/sqrt(d) factor; ``scale`` multiplies the scores and
+  the literal equation is scale = 1.
+* Heads: with ``num_heads`` = H > 1 the width d is cut into H contiguous
+  column slices of width d/H and Eq. 3 is applied to each slice on its own;
+  H = 1 is Eq. 3 exactly.
+* The query set is shared by every sequence of the batch; there are no
+  projections or norms around Eq. 3.
+* Softmax normalises over the N visual tokens (each latent's scores).
+"""
+
+import numpy as np
+
+
+def softmax_rows(s):
+    """Row-wise softmax of a float64 matrix: exp(s - rowmax) / rowsum.
+
+    Subtracting the row maximum leaves the value unchanged (it cancels in the
+    ratio) and keeps exp finite.  Entries equal to -inf get weight 0.
+    """
+    s = np.asarray(s, dtype=np.float64)
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def latent_compress(latents, feats, num_heads=1, scale=1.0, return_probs=False):
+    """Eq. 3 applied per sequence and per head.
+
+    latents: [C, d] learned queries (any real dtype; widened to float64).
+    feats:   [B, N, d] visual features F_V of each sequence.
+    Returns out [B, C, d] float64 with
+        out[b][:, hs] = softmax(scale * latents[:, hs] @ feats[b][:, hs].T) @ feats[b][:, hs]
+    for each head slice hs of width d / num_heads.  With ``return_probs`` the
+    attention matrices [B, H, C, N] are returned as well.
+    """
+    lat = np.asarray(latents, dtype=np.float64)
+    F = np.asarray(feats, dtype=np.float64)
+    C, d = lat.shape
+    B, N, d2 = F.shape
+    if d2 != d:
+        raise ValueError("latents and feats disagree on the feature width")
+    if num_heads < 1 or d % num_heads != 0:
+        raise ValueError("feature width must split evenly into heads")
+    if N < 1:
+        raise ValueError("need at least one visual token")
+    dh = d // num_heads
+    out = np.empty((B, C, d), dtype=np.float64)
+    probs = np.empty((B, num_heads, C, N), dtype=np.float64) if return_probs else None
+    for b in range(B):
+        for h in range(num_heads):
+            cols = slice(h * dh, (h + 1) * dh)
+            query = lat[:, cols]          # the learned query set, C x dh
+            kv = F[b][:, cols]            # F_V is both key and value, N x dh
+            p = softmax_rows(scale * (query @ kv.T))   # C x N
+            out[b][:, cols] = p @ kv
+            if return_probs:
+                probs[b, h] = p
+    if return_probs:
+        return out, probs
+    return out

@@ -1,0 +1,290 @@
+"""Seeded synthetic workloads for the draft-verify hot path.
+
+This module only draws inputs: it holds none of the method's arithmetic
+(no compression, attention or acceptance).  Both the HIP path and the CPU
+oracle are fed from it, so the two always see the same bytes.
+
+The paper's workloads (Kinetics-400 video captioning and LLaVA-instruct
+visual instruction tuning, Sec. 4.1) are not available; seeded tensors with
+the shapes of its image and video settings stand in for them:
+
+* features, latents, queries, keys and values ~ N(0, 1), drawn in float32
+  and, for bfloat16 workloads, rounded once to bfloat16 (round to nearest
+  even); both sides consume the rounded values;
+* target logits ~ N(0, 3^2) of shape [B, k+1, V]; draft logits are the
+  first k target rows plus N(0, 1) noise; p = softmax(z / tau) and
+  q = softmax(z' / tau) are formed in float64 and stored as float32 once;
+* drafted ids: in sampled mode x_i ~ q_i (float64 inverse CDF on a
+  separate stream), in greedy mode x_i = argmax q_i;
+* acceptance uniforms on the 2^-24 grid, one stream per sequence;
+* paged caches: per-sequence lengths uniform in a range, 16-token pages
+  with a random page permutation, padding slots and spare pages poisoned.
+
+Every tensor has its own Philox stream spawned from one seed in a fixed
+order, so changing one size does not change the other tensors' values.
+"""
+
+import dataclasses
+import math
+
+import numpy as np
+
+BASE_SEED = 2505_12728
+PAGE_SIZE = 16
+POISON = 8192.0          # exact in bfloat16 and float32
+
+# stream order for SeedSequence.spawn; never reorder (it changes every value)
+_STREAMS = ("latents", "feats", "q", "k", "v", "target_logits", "draft_noise",
+            "draft_uniforms", "accept_uniforms", "kv_lens", "page_perm")
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """Shapes of one synthetic workload (all three operations)."""
+    name: str
+    dtype: str                  # "f32" or "bf16"
+    # verification attention
+    batch: int
+    hq: int
+    hkv: int
+    head_dim: int
+    kv_len: int                 # contiguous length, or the upper bound when paged
+    block: int                  # k drafted tokens verified in one pass
+    paged: bool = False
+    kv_len_min: int = 0         # paged workloads draw lengths in [kv_len_min, kv_len]
+    # latent compression (Eq. 3)
+    c_batch: int = 1
+    c_tokens: int = 0           # N visual tokens
+    c_width: int = 0            # d
+    c_latents: int = 0          # C learned queries
+    c_heads: int = 1
+    # acceptance
+    vocab: int = 0
+    modes: tuple = ("sampled",)
+    temperature: float = 1.0
+
+    @property
+    def seed(self):
+        return BASE_SEED + WORKLOADS.index(self)
+
+
+WORKLOADS = [
+    Workload("tiny-f32", "f32", batch=1, hq=4, hkv=1, head_dim=64, kv_len=608,
+             block=4, c_batch=1, c_tokens=576, c_width=256, c_latents=16,
+             c_heads=1, vocab=1024, modes=("sampled", "greedy"),
+             temperature=1.0),
+    Workload("llava-7b-image", "bf16", batch=1, hq=32, hkv=32, head_dim=128,
+             kv_len=1200, block=5, c_batch=1, c_tokens=576, c_width=4096,
+             c_latents=64, c_heads=32, vocab=32000, modes=("sampled",),
+             temperature=1.0),
+    Workload("qwen2vl-7b-video", "bf16", batch=1, hq=28, hkv=4, head_dim=128,
+             kv_len=6528, block=8, c_batch=1, c_tokens=6272, c_width=3584,
+             c_latents=256, c_heads=28, vocab=152064,
+             modes=("greedy", "sampled"), temperature=1.0),
+    Workload("batched-paged", "bf16", batch=16, hq=32, hkv=8, head_dim=128,
+             kv_len=16384, kv_len_min=2048, block=6, paged=True, c_batch=16,
+             c_tokens=1024, c_width=4096, c_latents=128, c_heads=32,
+             vocab=32000, modes=("sampled",), temperature=1.0),
+    Workload("long-video", "bf16", batch=4, hq=64, hkv=8, head_dim=128,
+             kv_len=65536, block=8, c_batch=4, c_tokens=16384, c_width=8192,
+             c_latents=512, c_heads=64, vocab=152064, modes=("sampled",),
+             temperature=0.7),
+]
+
+
+def workload(index_or_name):
+    if isinstance(index_or_name, int):
+        return WORKLOADS[index_or_name]
+    for w in WORKLOADS:
+        if w.name == index_or_name:
+            return w
+    raise KeyError(index_or_name)
+
+
+# ---------------------------------------------------------------- helpers
+
+def streams(seed):
+    """One independent Philox generator per named tensor."""
+    children = np.random.SeedSequence(seed).spawn(len(_STREAMS))
+    return {name: np.random.Generator(np.random.Philox(child))
+            for name, child in zip(_STREAMS, children)}
+
+
+def bf16_bits(x):
+    """Round float32 values to bfloat16 (nearest even); returns uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    bits = x.view(np.uint32)
+    bias = np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1))
+    return ((bits + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_to_f32(bits):
+    """Widen bfloat16 bit patterns to the float32 values they denote."""
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+class Tensor:
+    """A host tensor as both sides see it.
+
+    ``values`` holds the exact float32 values (already bfloat16-rounded for
+    bf16 tensors); ``bits`` holds the uint16 storage for bf16 tensors.
+    """
+
+    def __init__(self, values, dtype):
+        self.dtype = dtype
+        if dtype == "bf16":
+            self.bits = bf16_bits(values)
+            self.values = bf16_to_f32(self.bits)
+        elif dtype == "f32":
+            self.bits = None
+            self.values = np.ascontiguousarray(values, dtype=np.float32)
+        else:
+            raise ValueError(dtype)
+
+    @property
+    def shape(self):
+        return self.values.shape
+
+
+def normal(rng, shape, chunk=1 << 24):
+    """N(0, 1) float32 draws, produced in chunks to bound peak memory."""
+    total = int(np.prod(shape))
+    out = np.empty(total, dtype=np.float32)
+    for s in range(0, total, chunk):
+        e = min(total, s + chunk)
+        out[s:e] = rng.standard_normal(e - s, dtype=np.float32)
+    return out.reshape(shape)
+
+
+# ------------------------------------------------------ per-operation inputs
+
+def compress_inputs(w, seed=None, batch=None, tokens=None):
+    """Learned queries [C, d] and visual features [B, N, d] for Eq. 3."""
+    rs = streams(w.seed if seed is None else seed)
+    B = w.c_batch if batch is None else batch
+    N = w.c_tokens if tokens is None else tokens
+    latents = Tensor(normal(rs["latents"], (w.c_latents, w.c_width)), w.dtype)
+    feats = Tensor(normal(rs["feats"], (B, N, w.c_width)), w.dtype)
+    return latents, feats
+
+
+def kv_lengths(w, seed=None):
+    rs = streams(w.seed if seed is None else seed)
+    if not w.paged:
+        return np.full(w.batch, w.kv_len, dtype=np.int32)
+    return rs["kv_lens"].integers(w.kv_len_min, w.kv_len + 1,
+                                  size=w.batch).astype(np.int32)
+
+
+def verify_inputs(w, seed=None, kv_len=None, poison=POISON):
+    """Queries, KV cache (contiguous or paged) and lengths for verification.
+
+    Returns a dict with q [B, k, Hq, D]; k_cache / v_cache as
+    [B, Lmax, Hkv, D] (contiguous) or [P, Hkv, 16, D] page pools; kv_len [B];
+    page_table [B, max_pages] int32 or None.  Cache slots that no sequence
+    owns (padding, spare pages) hold ``poison``.
+    """
+    seed = w.seed if seed is None else seed
+    rs = streams(seed)
+    lens = kv_lengths(w, seed) if kv_len is None else np.asarray(kv_len, np.int32)
+    B, k, Hq, Hkv, D = w.batch, w.block, w.hq, w.hkv, w.head_dim
+    q = Tensor(normal(rs["q"], (B, k, Hq, D)), w.dtype)
+    if not w.paged:
+        Lmax = int(max(w.kv_len, int(lens.max()) if lens.size else 0))
+        kf = normal(rs["k"], (B, Lmax, Hkv, D))
+        vf = normal(rs["v"], (B, Lmax, Hkv, D))
+        for b in range(B):
+            kf[b, lens[b]:] = poison
+            vf[b, lens[b]:] = poison
+        return {"q": q, "k_cache": Tensor(kf, w.dtype), "v_cache": Tensor(vf, w.dtype),
+                "kv_len": lens, "page_table": None, "max_pages": 0, "lmax": Lmax}
+    pages = [int(math.ceil(int(L) / PAGE_SIZE)) for L in lens]
+    max_pages = max(1, int(math.ceil(w.kv_len / PAGE_SIZE)))
+    n_pool = sum(pages) + 64
+    perm = rs["page_perm"].permutation(n_pool).astype(np.int32)
+    page_table = np.zeros((B, max_pages), dtype=np.int32)
+    pos = 0
+    for b in range(B):
+        page_table[b, :pages[b]] = perm[pos:pos + pages[b]]
+        # entries past the sequence's last page point at a spare page; they
+        # are never read for valid keys
+        page_table[b, pages[b]:] = perm[-1]
+        pos += pages[b]
+    kf = np.full((n_pool, Hkv, PAGE_SIZE, D), poison, dtype=np.float32)
+    vf = np.full((n_pool, Hkv, PAGE_SIZE, D), poison, dtype=np.float32)
+    kg = rs["k"]
+    vg = rs["v"]
+    for b in range(B):
+        L = int(lens[b])
+        for i in range(pages[b]):
+            valid = min(PAGE_SIZE, L - i * PAGE_SIZE)
+            pg = page_table[b, i]
+            kf[pg, :, :valid] = normal(kg, (valid, Hkv, D)).transpose(1, 0, 2)
+            vf[pg, :, :valid] = normal(vg, (valid, Hkv, D)).transpose(1, 0, 2)
+    return {"q": q, "k_cache": Tensor(kf, w.dtype), "v_cache": Tensor(vf, w.dtype),
+            "kv_len": lens, "page_table": page_table, "max_pages": max_pages,
+            "lmax": 0}
+
+
+def _probs(z, tau):
+    """softmax(z / tau) along the last axis in float64, stored as float32."""
+    z = np.asarray(z, dtype=np.float64) / tau
+    z = z - z.max(axis=-1, keepdims=True)
+    e = np.exp(z)
+    return (e / e.sum(axis=-1, keepdims=True)).astype(np.float32)
+
+
+def accept_inputs(w, mode, seed=None, batch=None):
+    """Target / draft probabilities, drafted ids and uniforms.
+
+    Returns a dict with p [B, k+1, V] float32, q [B, k, V] float32,
+    draft [B, k] int32 and u [B, k+1] float32 (multiples of 2^-24).
+    """
+    rs = streams(w.seed if seed is None else seed)
+    B = w.batch if batch is None else batch
+    k, V = w.block, w.vocab
+    tau = w.temperature if mode == "sampled" else 1.0
+    z = 3.0 * normal(rs["target_logits"], (B, k + 1, V)).astype(np.float64)
+    zd = z[:, :k] + normal(rs["draft_noise"], (B, k, V)).astype(np.float64)
+    p = _probs(z, tau)
+    q = _probs(zd, tau)
+    if mode == "greedy":
+        draft = np.argmax(q, axis=-1).astype(np.int32)
+    else:
+        draft = np.empty((B, k), dtype=np.int32)
+        du = rs["draft_uniforms"].random((B, k))
+        for b in range(B):
+            for i in range(k):
+                c = np.cumsum(q[b, i].astype(np.float64))
+                draft[b, i] = min(V - 1, int(np.searchsorted(c, du[b, i] * c[-1],
+                                                             side="right")))
+    # one independent uniform stream per sequence
+    seqs = np.random.SeedSequence(w.seed if seed is None else seed).spawn(
+        len(_STREAMS) + B)[len(_STREAMS):]
+    u = np.empty((B, k + 1), dtype=np.float32)
+    for b in range(B):
+        g = np.random.Generator(np.random.Philox(seqs[b]))
+        u[b] = (g.integers(0, 1 << 24, size=k + 1).astype(np.float64)
+                * 2.0 ** -24).astype(np.float32)
+    return {"p": p, "q": q, "draft": draft, "u": u, "temperature": tau}
+
+
+# --------------------------------------------------------- byte / flop counts
+
+def verify_kv_bytes(w, lens=None):
+    """K and V bytes the verification must read once: 2 * Hkv * D * es per token."""
+    es = 4 if w.dtype == "f32" else 2
+    lens = kv_lengths(w) if lens is None else lens
+    return int(np.sum(lens, dtype=np.int64)) * 2 * w.hkv * w.head_dim * es
+
+
+def compress_flops(w):
+    """4 * d_h flops per (latent, token, head): 4 * B * C * N * d in total."""
+    return 4 * w.c_batch * w.c_latents * w.c_tokens * w.c_width
+
+
+def compress_bytes(w):
+    es = 4 if w.dtype == "f32" else 2
+    return (w.c_batch * w.c_tokens * w.c_width * es + w.c_latents * w.c_width * es
+            + w.c_batch * w.c_latents * w.c_width * 4)

@@ -1,0 +1,590 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, an invariant, an exact enumeration, hand-worked cases, or brute force
+on tiny inputs.  They run on the CPU only.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# ================================================================ compression
+# Eq. 3 (Sec. 3.2): out = softmax(scale * Cq F_V^T) F_V, per head slice.
+
+@pytest.mark.parametrize("heads,scale", [(1, 1.0), (4, 0.5), (2, 1 / math.sqrt(8))])
+def test_compress_zero_queries_is_average_pooling(heads, scale):
+    # Cq = 0 makes every score equal, so each latent averages all N tokens:
+    # global average pooling (the pooling compressor of Sec. 4.4, Tab. 4).
+    r = rng(1)
+    feats = r.standard_normal((3, 7, 16))
+    out = oracle.latent_compress(np.zeros((5, 16)), feats, heads, scale)
+    expect = np.broadcast_to(feats.mean(axis=1)[:, None, :], out.shape)
+    np.testing.assert_allclose(out, expect, rtol=0, atol=1e-13)
+
+
+def test_compress_two_token_logistic_closed_form():
+    # N = 2: weights are the logistic function of the score difference.
+    r = rng(2)
+    f = r.standard_normal((1, 2, 6))
+    c = r.standard_normal((3, 6))
+    scale = 0.37
+    out = oracle.latent_compress(c, f, 1, scale)
+    for i in range(3):
+        s0 = scale * float(np.dot(c[i], f[0, 0]))
+        s1 = scale * float(np.dot(c[i], f[0, 1]))
+        w0 = 1.0 / (1.0 + math.exp(s1 - s0))
+        expect = w0 * f[0, 0] + (1.0 - w0) * f[0, 1]
+        np.testing.assert_allclose(out[0, i], expect, rtol=0, atol=1e-13)
+
+
+def test_compress_value_is_the_feature_itself():
+    # One-hot limit: a query equal to lambda * (unit row j) attends to row j
+    # only, and returns that row: F_V is both key and value.
+    r = rng(3)
+    f = r.standard_normal((1, 9, 12))
+    f /= np.linalg.norm(f, axis=-1, keepdims=True)
+    picks = [4, 0, 8]
+    c = 400.0 * f[0, picks]
+    out = oracle.latent_compress(c, f, 1, 1.0)
+    np.testing.assert_allclose(out[0], f[0, picks], rtol=0, atol=1e-12)
+
+
+def test_compress_token_order_does_not_matter():
+    r = rng(4)
+    f = r.standard_normal((2, 11, 8))
+    c = r.standard_normal((4, 8))
+    perm = r.permutation(11)
+    a = oracle.latent_compress(c, f, 2, 0.7)
+    b = oracle.latent_compress(c, f[:, perm], 2, 0.7)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_compress_single_and_repeated_token():
+    r = rng(5)
+    row = r.standard_normal(8)
+    c = r.standard_normal((3, 8))
+    one = oracle.latent_compress(c, row[None, None, :], 2, 1.0)
+    np.testing.assert_allclose(one[0], np.broadcast_to(row, (3, 8)), atol=1e-15)
+    many = oracle.latent_compress(c, np.broadcast_to(row, (1, 6, 8)).copy(), 2, 1.0)
+    np.testing.assert_allclose(many[0], np.broadcast_to(row, (3, 8)), atol=1e-14)
+
+
+def test_compress_heads_are_contiguous_slices():
+    # Head 0 has zero queries (mean of its slice); head 1 has one-hot queries
+    # (the picked row of its slice).  Only contiguous slices give both.
+    r = rng(6)
+    f = r.standard_normal((1, 5, 8))
+    f[0, :, 4:] /= np.linalg.norm(f[0, :, 4:], axis=-1, keepdims=True)
+    c = np.zeros((2, 8))
+    c[0, 4:] = 500.0 * f[0, 3, 4:]
+    c[1, 4:] = 500.0 * f[0, 1, 4:]
+    out = oracle.latent_compress(c, f, 2, 1.0)
+    np.testing.assert_allclose(out[0, :, :4], np.broadcast_to(f[0, :, :4].mean(0), (2, 4)), atol=1e-13)
+    np.testing.assert_allclose(out[0, 0, 4:], f[0, 3, 4:], atol=1e-12)
+    np.testing.assert_allclose(out[0, 1, 4:], f[0, 1, 4:], atol=1e-12)
+
+
+def test_compress_probabilities_sum_to_one():
+    r = rng(7)
+    _, probs = oracle.latent_compress(r.standard_normal((4, 8)),
+                                      r.standard_normal((2, 13, 8)) * 5, 2, 1.0,
+                                      return_probs=True)
+    np.testing.assert_allclose(probs.sum(-1), 1.0, rtol=0, atol=1e-12)
+    assert np.all(probs >= 0)
+
+
+def test_compress_brute_force_tiny():
+    # Pure-Python loops over (b, head, latent, token) on a tiny case.
+    r = rng(8)
+    C, N, d, H, B = 3, 5, 8, 2, 2
+    c = r.standard_normal((C, d))
+    f = r.standard_normal((B, N, d))
+    scale = 0.8
+    out = oracle.latent_compress(c, f, H, scale)
+    dh = d // H
+    for b in range(B):
+        for h in range(H):
+            for i in range(C):
+                s = [scale * sum(c[i, h * dh + t] * f[b, n, h * dh + t] for t in range(dh))
+                     for n in range(N)]
+                z = sum(math.exp(x) for x in s)
+                for t in range(dh):
+                    v = sum(math.exp(s[n]) / z * f[b, n, h * dh + t] for n in range(N))
+                    assert abs(v - out[b, i, h * dh + t]) < 1e-12
+
+
+# ============================================================== verification
+# Attention of the k-token block over the cache (Sec. 3.1), causal in block.
+
+def test_verify_single_key_returns_its_value():
+    r = rng(10)
+    q = r.standard_normal((1, 1, 2, 4))
+    K = r.standard_normal((1, 1, 1, 4))
+    V = r.standard_normal((1, 1, 1, 4))
+    out, lse = oracle.verify_attention(q, K, V, [1], 0.5)
+    np.testing.assert_allclose(out[0, 0], np.broadcast_to(V[0, 0, 0], (2, 4)), atol=1e-15)
+    np.testing.assert_allclose(lse[0, 0], 0.5 * q[0, 0] @ K[0, 0, 0], atol=1e-15)
+
+
+def test_verify_equal_keys_average_exactly_the_visible_prefix():
+    # With identical keys every visible score is equal, so row j returns the
+    # mean of the first L - k + j + 1 values and lse = s + log(count).
+    r = rng(11)
+    B, k, Hq, Hkv, D, L = 2, 3, 2, 1, 4, 9
+    q = r.standard_normal((B, k, Hq, D))
+    key = r.standard_normal(D)
+    K = np.broadcast_to(key, (B, L, Hkv, D)).copy()
+    V = r.standard_normal((B, L, Hkv, D))
+    lens = [9, 5]
+    out, lse = oracle.verify_attention(q, K, V, lens, 0.3)
+    for b in range(B):
+        for j in range(k):
+            n_vis = lens[b] - k + j + 1
+            for h in range(Hq):
+                np.testing.assert_allclose(out[b, j, h], V[b, :n_vis, 0].mean(0), atol=1e-14)
+                s = 0.3 * float(q[b, j, h] @ key)
+                assert abs(lse[b, j, h] - (s + math.log(n_vis))) < 1e-13
+
+
+def test_verify_two_key_logistic_closed_form():
+    r = rng(12)
+    q = r.standard_normal((1, 1, 1, 5))
+    K = r.standard_normal((1, 2, 1, 5))
+    V = r.standard_normal((1, 2, 1, 5))
+    scale = 0.61
+    out, lse = oracle.verify_attention(q, K, V, [2], scale)
+    s0 = scale * float(q[0, 0, 0] @ K[0, 0, 0])
+    s1 = scale * float(q[0, 0, 0] @ K[0, 1, 0])
+    w0 = 1.0 / (1.0 + math.exp(s1 - s0))
+    np.testing.assert_allclose(out[0, 0, 0], w0 * V[0, 0, 0] + (1 - w0) * V[0, 1, 0], atol=1e-14)
+    assert abs(lse[0, 0, 0] - math.log(math.exp(s0) + math.exp(s1))) < 1e-13
+
+
+def test_verify_gqa_heads_read_contiguous_groups():
+    # Value rows of KV head c are all (c + 1): query head h must return
+    # h // g + 1 whatever the scores are.
+    r = rng(13)
+    B, k, Hq, Hkv, D, L = 1, 2, 8, 2, 4, 6
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, L, Hkv, D))
+    V = np.zeros((B, L, Hkv, D))
+    for c in range(Hkv):
+        V[:, :, c, :] = c + 1.0
+    out, _ = oracle.verify_attention(q, K, V, [L], 0.5)
+    g = Hq // Hkv
+    for h in range(Hq):
+        np.testing.assert_allclose(out[0, :, h], h // g + 1.0, atol=1e-14)
+
+
+def test_verify_gqa_equals_repeated_kv():
+    r = rng(14)
+    B, k, Hq, Hkv, D, L = 2, 3, 6, 2, 8, 10
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, L, Hkv, D))
+    V = r.standard_normal((B, L, Hkv, D))
+    a, la = oracle.verify_attention(q, K, V, [10, 7], 0.4)
+    Kr = np.repeat(K, Hq // Hkv, axis=2)
+    Vr = np.repeat(V, Hq // Hkv, axis=2)
+    b, lb = oracle.verify_attention(q, Kr, Vr, [10, 7], 0.4)
+    np.testing.assert_allclose(a, b, atol=1e-14)
+    np.testing.assert_allclose(la, lb, atol=1e-14)
+
+
+def test_verify_block_row_is_a_single_query_decode():
+    # Row j of the block equals one-query attention over the first
+    # L - k + j + 1 cache entries; the last row sees the whole cache.
+    r = rng(15)
+    B, k, Hq, Hkv, D, L = 1, 4, 4, 2, 8, 12
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, L, Hkv, D))
+    V = r.standard_normal((B, L, Hkv, D))
+    out, lse = oracle.verify_attention(q, K, V, [L], 0.25)
+    for j in range(k):
+        n_vis = L - k + j + 1
+        o1, l1 = oracle.verify_attention(q[:, j:j + 1], K[:, :n_vis], V[:, :n_vis], [n_vis], 0.25)
+        np.testing.assert_allclose(out[:, j], o1[:, 0], atol=1e-14)
+        np.testing.assert_allclose(lse[:, j], l1[:, 0], atol=1e-14)
+
+
+def test_verify_masked_entries_are_never_read():
+    # Poisoning cache slots past kv_len (NaN) changes nothing, and changing
+    # the last block entry changes only the last block row.
+    r = rng(16)
+    B, k, Hq, Hkv, D, Lmax = 2, 3, 2, 1, 4, 10
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, Lmax, Hkv, D))
+    V = r.standard_normal((B, Lmax, Hkv, D))
+    lens = [8, 6]
+    base, lb = oracle.verify_attention(q, K, V, lens, 0.5)
+    Kp, Vp = K.copy(), V.copy()
+    for b, L in enumerate(lens):
+        Kp[b, L:] = np.nan
+        Vp[b, L:] = np.nan
+    pois, lp = oracle.verify_attention(q, Kp, Vp, lens, 0.5)
+    np.testing.assert_array_equal(base, pois)
+    np.testing.assert_array_equal(lb, lp)
+    K2, V2 = K.copy(), V.copy()
+    K2[0, lens[0] - 1] += 3.0
+    V2[0, lens[0] - 1] -= 2.0
+    changed, _ = oracle.verify_attention(q, K2, V2, lens, 0.5)
+    np.testing.assert_array_equal(changed[0, :k - 1], base[0, :k - 1])
+    assert np.max(np.abs(changed[0, k - 1] - base[0, k - 1])) > 1e-3
+
+
+def test_verify_rows_without_keys_are_zero():
+    r = rng(17)
+    q = r.standard_normal((1, 4, 2, 4))
+    K = r.standard_normal((1, 4, 1, 4))
+    V = r.standard_normal((1, 4, 1, 4))
+    out, lse = oracle.verify_attention(q, K, V, [2], 1.0)
+    # kv_len 2 < k 4: rows 0 and 1 see no key, rows 2, 3 see 1 and 2 keys
+    assert np.all(out[0, :2] == 0) and np.all(np.isneginf(lse[0, :2]))
+    np.testing.assert_allclose(out[0, 2], np.broadcast_to(V[0, 0, 0], (2, 4)), atol=1e-15)
+
+
+def test_verify_paged_equals_contiguous():
+    r = rng(18)
+    B, k, Hq, Hkv, D, ps = 3, 2, 4, 2, 8, 16
+    lens = [40, 17, 33]
+    Lmax = 48
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, Lmax, Hkv, D))
+    V = r.standard_normal((B, Lmax, Hkv, D))
+    pages = [math.ceil(L / ps) for L in lens]
+    n_pool = sum(pages) + 3
+    perm = r.permutation(n_pool)
+    table = np.zeros((B, 3), dtype=np.int32)
+    kp = np.full((n_pool, Hkv, ps, D), np.nan)
+    vp = np.full((n_pool, Hkv, ps, D), np.nan)
+    pos = 0
+    for b in range(B):
+        for i in range(pages[b]):
+            pg = perm[pos]
+            pos += 1
+            table[b, i] = pg
+            for s in range(ps):
+                t = i * ps + s
+                if t < lens[b]:
+                    kp[pg, :, s] = K[b, t]
+                    vp[pg, :, s] = V[b, t]
+    a, la = oracle.verify_attention(q, K, V, lens, 0.3)
+    b_, lb = oracle.verify_attention(q, kp, vp, lens, 0.3, page_table=table, page_size=ps)
+    np.testing.assert_array_equal(a, b_)
+    np.testing.assert_array_equal(la, lb)
+
+
+def test_verify_merge_of_key_partition_equals_whole():
+    # The log-sum-exp merge of attention over disjoint key ranges equals
+    # attention over their union; this pins lse.
+    r = rng(19)
+    D, L, Hq = 8, 30, 3
+    q = r.standard_normal((1, 1, Hq, D))
+    K = r.standard_normal((1, L, 1, D)) * 2
+    V = r.standard_normal((1, L, 1, D))
+    whole, lw = oracle.verify_attention(q, K, V, [L], 0.7)
+    cuts = [0, 4, 5, 19, 30]
+    outs, lses = [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        o, l_ = oracle.verify_attention(q, K[:, a:b], V[:, a:b], [b - a], 0.7)
+        outs.append(o)
+        lses.append(l_)
+    o, l_ = oracle.merge_partials(np.stack(outs), np.stack(lses))
+    np.testing.assert_allclose(o, whole, atol=1e-13)
+    np.testing.assert_allclose(l_, lw, atol=1e-13)
+
+
+def test_verify_probabilities_sum_to_one():
+    r = rng(20)
+    q = r.standard_normal((2, 3, 4, 8)) * 3
+    K = r.standard_normal((2, 12, 2, 8))
+    V = r.standard_normal((2, 12, 2, 8))
+    _, _, probs = oracle.verify_attention(q, K, V, [12, 9], 0.5, return_probs=True)
+    for b, L in enumerate([12, 9]):
+        for j in range(3):
+            np.testing.assert_allclose(probs[b][j].sum(-1), 1.0, atol=1e-12)
+            assert np.all(probs[b][j][:, L - 3 + j + 1:] == 0)
+
+
+def test_verify_brute_force_tiny():
+    r = rng(21)
+    B, k, Hq, Hkv, D, L = 2, 3, 4, 2, 4, 7
+    q = r.standard_normal((B, k, Hq, D))
+    K = r.standard_normal((B, L, Hkv, D))
+    V = r.standard_normal((B, L, Hkv, D))
+    lens = [7, 5]
+    scale = 0.45
+    out, lse = oracle.verify_attention(q, K, V, lens, scale)
+    for b in range(B):
+        for j in range(k):
+            for h in range(Hq):
+                c = h // (Hq // Hkv)
+                ts = range(lens[b] - k + j + 1)
+                s = [scale * sum(q[b, j, h, e] * K[b, t, c, e] for e in range(D)) for t in ts]
+                z = sum(math.exp(x) for x in s)
+                assert abs(lse[b, j, h] - math.log(z)) < 1e-12
+                for e in range(D):
+                    v = sum(math.exp(s[t]) / z * V[b, t, c, e] for t in ts)
+                    assert abs(v - out[b, j, h, e]) < 1e-12
+
+
+# ================================================================ acceptance
+# Token-wise acceptance / residual resampling (Sec. 3.1, Sec. 3.3) and greedy
+# verification at temperature 0 (Sec. 4.2).
+
+def test_accept_hand_worked_cases():
+    with open(os.path.join(GOLDEN, "accept_hand_cases.json")) as fh:
+        cases = json.load(fh)["cases"]
+    for c in cases:
+        mode = oracle.ACCEPT_GREEDY if c["mode"] == "greedy" else oracle.ACCEPT_SAMPLED
+        p = np.array(c["p"], dtype=np.float32)
+        q = None if c["q"] is None else np.array(c["q"], dtype=np.float32)
+        u = None if c["u"] is None else np.array(c["u"], dtype=np.float32)
+        n, toks = oracle.spec_accept_one(p, q, c["draft"], u, mode)
+        assert (n, toks) == (c["n"], c["tokens"]), c["name"]
+
+
+def _random_probs(r, shape, temp=1.0):
+    z = r.standard_normal(shape) * 3 / temp
+    e = np.exp(z - z.max(-1, keepdims=True))
+    return (e / e.sum(-1, keepdims=True)).astype(np.float32)
+
+
+def test_accept_draft_equal_to_target_accepts_everything():
+    r = rng(30)
+    k, V = 6, 50
+    for trial in range(20):
+        p = _random_probs(r, (k + 1, V))
+        draft = [int(r.integers(0, V)) for _ in range(k)]
+        # keep drafted ids where p > 0 (float32 underflow could zero them)
+        p[np.arange(k), draft] = np.maximum(p[np.arange(k), draft], 1e-6)
+        u = (r.integers(0, 1 << 24, size=k + 1) * 2.0 ** -24).astype(np.float32)
+        n, toks = oracle.spec_accept_one(p, p[:k], draft, u, oracle.ACCEPT_SAMPLED)
+        assert n == k and toks[:k] == draft and 0 <= toks[k] < V
+
+
+def test_accept_special_uniforms_and_ratios():
+    p_x = np.array([0.3, 0.3, 0.0, 0.5, 1e-30], dtype=np.float32)
+    q_x = np.array([0.1, 0.3, 0.2, 0.0, 0.0], dtype=np.float32)
+    # u = 0 accepts iff p(x) > 0
+    assert list(oracle.accept_flags(p_x, q_x, np.zeros(5, np.float32))) == [True, True, False, True, True]
+    # p >= q accepts for every u < 1
+    top = np.float32(1 - 2 ** -24)
+    assert list(oracle.accept_flags(p_x[:2], q_x[:2], np.full(2, top))) == [True, True]
+    # p = 0 rejects for every u
+    assert not oracle.accept_flags(np.float32(0), np.float32(0.5), np.float32(0))
+
+
+def test_accept_ratio_threshold_is_exact():
+    # accept iff u < p/q exactly: on the 2^-24 grid the number of accepting
+    # uniforms is ceil(2^24 * p / q) (capped at 2^24).
+    r = rng(31)
+    a = np.arange(1 << 24, dtype=np.float64) * 2.0 ** -24
+    u = a.astype(np.float32)
+    for _ in range(4):
+        p_x = np.float32(r.random() * 0.5)
+        q_x = np.float32(r.random() * 0.5 + 0.1)
+        count = int(np.sum(oracle.accept_flags(np.full_like(u, p_x), np.full_like(u, q_x), u)))
+        expect = min(1 << 24, math.ceil(Fraction(float(p_x)) / Fraction(float(q_x)) * (1 << 24)))
+        assert count == expect
+
+
+def test_accept_greedy_planted_mismatch():
+    r = rng(32)
+    k, V = 5, 40
+    for m in range(k + 1):
+        p = _random_probs(r, (k + 1, V))
+        g = np.argmax(p, axis=-1)
+        draft = [int(x) for x in g[:k]]
+        if m < k:
+            draft[m] = (draft[m] + 1) % V
+        n, toks = oracle.spec_accept_one(p, None, draft, None, oracle.ACCEPT_GREEDY)
+        assert n == m
+        assert toks[:m] == draft[:m] and toks[m] == int(g[m])
+        assert toks[m + 1:] == [-1] * (k - m)
+
+
+def test_accept_invalid_draft_id_is_rejected():
+    p = np.full((3, 4), 0.25, dtype=np.float32)
+    n, toks = oracle.spec_accept_one(p, p[:2], [7, 1], np.zeros(3, np.float32), oracle.ACCEPT_SAMPLED)
+    assert n == 0 and 0 <= toks[0] < 4
+    n, toks = oracle.spec_accept_one(p, None, [-1, 1], None, oracle.ACCEPT_GREEDY)
+    assert n == 0 and toks[0] == 0
+
+
+def test_residual_weights_fixed_point():
+    # exactly representable differences map to exact integers; anything
+    # below 2^-40 weighs zero; negatives clamp to zero
+    p = np.array([0.75, 0.25, 2.0 ** -41, 0.0, 2.0 ** -40], dtype=np.float32)
+    q = np.array([0.25, 0.5, 0.0, 0.0, 0.0], dtype=np.float32)
+    R = oracle.residual_weights(p, q)
+    assert list(R) == [2 ** 39, 0, 0, 0, 1]
+    # fp32 rounding of the subtraction: 1 - 2^-30 rounds to 1 in float32
+    R2 = oracle.residual_weights(np.array([1.0], np.float32), np.array([2.0 ** -30], np.float32))
+    assert list(R2) == [2 ** 40]
+
+
+def test_fixed_point_sample_matches_python_integers():
+    r = rng(33)
+    R = r.integers(0, 2 ** 40, size=300).astype(np.uint64)
+    R[r.integers(0, 300, size=100)] = 0
+    S = int(sum(int(x) for x in R))
+    cum = np.cumsum([int(x) for x in R])
+    for a in list(r.integers(0, 1 << 24, size=200)) + [0, (1 << 24) - 1]:
+        T = (int(a) * S) >> 24
+        expect = next(j for j in range(len(R)) if int(cum[j]) > T)
+        assert oracle.fixed_point_sample(R, int(a)) == expect
+
+
+def test_fixed_point_sample_exhaustive_counts():
+    # All 2^24 uniforms: each token is drawn exactly
+    # ceil(c_t 2^24 / S) - ceil(c_{t-1} 2^24 / S) times (c = prefix sums),
+    # and a token of zero weight is never drawn.
+    r = rng(34)
+    V = 16
+    R = r.integers(0, 2 ** 40, size=V).astype(np.uint64)
+    R[[3, 7, 8]] = 0
+    S = int(sum(int(x) for x in R))
+    toks = oracle.fixed_point_sample(R, np.arange(1 << 24, dtype=np.uint64))
+    counts = np.bincount(toks, minlength=V)
+    prev = 0
+    c = 0
+    for t in range(V):
+        c += int(R[t])
+        hi = -((-c * (1 << 24)) // S)
+        assert counts[t] == hi - prev, t
+        prev = hi
+    assert counts[[3, 7, 8]].sum() == 0
+
+
+def _exact_first_token_distribution(p, q):
+    """Exact distribution of the first output token, k = 1, draft x ~ q.
+
+    Enumerates every uniform on the 2^-24 grid through the oracle's own
+    acceptance test and final draw.
+    """
+    V = p.shape[1]
+    grid = (np.arange(1 << 24, dtype=np.float64) * 2.0 ** -24).astype(np.float32)
+    R = oracle.residual_weights(p[0], q[0])
+    rho = np.bincount(oracle.fixed_point_sample(R, np.arange(1 << 24, dtype=np.uint64)),
+                      minlength=V)
+    dist = [Fraction(0)] * V
+    for x in range(V):
+        acc = int(np.sum(oracle.accept_flags(np.full_like(grid, p[0, x]),
+                                             np.full_like(grid, q[0, x]), grid)))
+        alpha = Fraction(acc, 1 << 24)
+        qx = Fraction(float(q[0, x]))
+        dist[x] += qx * alpha
+        for t in range(V):
+            dist[t] += qx * (1 - alpha) * Fraction(int(rho[t]), 1 << 24)
+    return dist
+
+
+def test_accept_output_distribution_is_the_target_exactly():
+    # Speculative sampling leaves the target distribution unchanged
+    # (Sec. 3.1 and the rule it cites).  With dyadic p, q summing to 1, the
+    # implementation's exact output law differs from p only by the 2^-24
+    # grids of the acceptance test and of the final draw: at most 3 * 2^-24.
+    r = rng(35)
+    V = 16
+    for trial in range(2):
+        P = r.multinomial(1 << 20, r.dirichlet(np.ones(V) * 0.7))
+        Q = r.multinomial(1 << 20, r.dirichlet(np.ones(V) * 0.7))
+        p = np.stack([P, P]).astype(np.float64) / (1 << 20)
+        q = (Q.astype(np.float64) / (1 << 20))[None]
+        p = p.astype(np.float32)
+        q = q.astype(np.float32)
+        # the ideal rule with exact rationals reproduces p exactly
+        pf = [Fraction(int(x), 1 << 20) for x in P]
+        qf = [Fraction(int(x), 1 << 20) for x in Q]
+        beta = sum(min(a, b) for a, b in zip(pf, qf))
+        resid = [max(Fraction(0), a - b) for a, b in zip(pf, qf)]
+        zr = sum(resid)
+        ideal = [qf[t] * min(Fraction(1), pf[t] / qf[t]) if qf[t] > 0 else Fraction(0)
+                 for t in range(V)]
+        ideal = [ideal[t] + (1 - beta) * resid[t] / zr for t in range(V)]
+        assert ideal == pf
+        dist = _exact_first_token_distribution(p, q)
+        assert sum(dist) == 1
+        worst = max(abs(dist[t] - pf[t]) for t in range(V))
+        assert worst <= Fraction(3, 1 << 24), float(worst)
+
+
+def test_accept_monte_carlo_first_token_law():
+    # The composed per-sequence rule (tests, rejection, final draw with the
+    # last uniform) reproduces p for the first output token.
+    r = rng(36)
+    V, k, n_samp = 12, 2, 12000
+    p = _random_probs(r, (k + 1, V))
+    q = _random_probs(r, (k, V))
+    counts = np.zeros(V)
+    for _ in range(n_samp):
+        c = np.cumsum(q[0].astype(np.float64))
+        x0 = min(V - 1, int(np.searchsorted(c, r.random() * c[-1], side="right")))
+        c1 = np.cumsum(q[1].astype(np.float64))
+        x1 = min(V - 1, int(np.searchsorted(c1, r.random() * c1[-1], side="right")))
+        u = (r.integers(0, 1 << 24, size=k + 1) * 2.0 ** -24).astype(np.float32)
+        _, toks = oracle.spec_accept_one(p, q, [x0, x1], u, oracle.ACCEPT_SAMPLED)
+        counts[toks[0]] += 1
+    expect = p[0].astype(np.float64) * n_samp
+    chi2 = float(np.sum((counts - expect) ** 2 / np.maximum(expect, 1e-9)))
+    # chi-square with 11 degrees of freedom: P(chi2 > 31.3) ~ 0.001
+    assert chi2 < 31.3, chi2
+
+
+def test_accept_uniform_roles():
+    # u_0..u_{k-1} drive the tests and u_k the final draw: moving u_0 inside
+    # the accepting range leaves the output alone; u_k never changes n.
+    p = np.array([[0.5, 0.5, 0, 0], [0.1, 0.2, 0.3, 0.4]], dtype=np.float32)
+    q = np.array([[0.25, 0.75, 0, 0]], dtype=np.float32)
+    outs = set()
+    for u0 in [0.0, 0.3, 0.6]:
+        outs.add(tuple(oracle.spec_accept_one(p, q, [1], np.array([u0, 0.55], np.float32),
+                                              oracle.ACCEPT_SAMPLED)[1]))
+    assert len(outs) == 1
+    ns = {oracle.spec_accept_one(p, q, [1], np.array([0.9, uk], np.float32),
+                                 oracle.ACCEPT_SAMPLED)[0] for uk in [0.0, 0.4, 0.99]}
+    assert ns == {0}
+
+
+def test_accept_degenerate_residual_falls_back():
+    # Unnormalised rows: p <= q everywhere on a rejected row leaves no
+    # residual mass; the draw then uses p_n itself, then argmax.
+    p = np.array([[0.1, 0.2, 0.1], [0.3, 0.3, 0.4]], dtype=np.float32)
+    q = np.array([[0.5, 0.5, 0.5]], dtype=np.float32)
+    n, toks = oracle.spec_accept_one(p, q, [1], np.array([0.99, 0.0], np.float32),
+                                     oracle.ACCEPT_SAMPLED)
+    assert n == 0 and toks[0] == 0           # a = 0 picks the first weighted token
+    n, toks = oracle.spec_accept_one(p, q, [1], np.array([0.99, 0.99], np.float32),
+                                     oracle.ACCEPT_SAMPLED)
+    assert n == 0 and toks[0] == 2
+    z = np.zeros((2, 3), dtype=np.float32)
+    n, toks = oracle.spec_accept_one(z, q, [1], np.array([0.5, 0.5], np.float32),
+                                     oracle.ACCEPT_SAMPLED)
+    assert n == 0 and toks[0] == 0
+
+
+def test_accept_batch_matches_per_sequence():
+    r = rng(37)
+    B, k, V = 3, 4, 30
+    p = _random_probs(r, (B, k + 1, V))
+    q = _random_probs(r, (B, k, V))
+    d = r.integers(0, V, size=(B, k)).astype(np.int32)
+    u = (r.integers(0, 1 << 24, size=(B, k + 1)) * 2.0 ** -24).astype(np.float32)
+    n, t = oracle.spec_accept(p, q, d, u, oracle.ACCEPT_SAMPLED)
+    for b in range(B):
+        nb, tb = oracle.spec_accept_one(p[b], q[b], d[b], u[b], oracle.ACCEPT_SAMPLED)
+        assert n[b] == nb and list(t[b]) == tb

@@ -1,0 +1,183 @@
+/*
+ * specflash.h -- C ABI of the SpecFLASH draft-verify hot path on MI355X (gfx950).
+ *
+ * SpecFLASH (arXiv 2505.12728) speeds up large multimodal models with
+ * speculative decoding.  One draft-verify round needs three data-parallel
+ * operations, exported here:
+ *
+ *   sd_latent_compress   learned latent queries attend over the visual
+ *                        features (Sec. 3.2, Eq. 3; Algorithm 1, Appendix B)
+ *   sd_verify_attention  the target model's attention for the K drafted
+ *                        positions, scored in one parallel pass over the KV
+ *                        cache (Sec. 3.1)
+ *   sd_spec_accept       token-wise acceptance / rejection with residual
+ *                        resampling (Sec. 3.1, Sec. 3.3), or greedy
+ *                        verification for temperature 0 (Sec. 4.2)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every tensor pointer is DEVICE memory on the current HIP device, owned by
+ *   the caller, dense and row-major in the layout given at each call.  The
+ *   library never allocates, frees or keeps device memory and holds no
+ *   global state; calls are thread-safe.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Work is enqueued asynchronously; no call synchronises the host.
+ * - Return value: an sd_status.  Arguments are validated on the host before
+ *   anything is enqueued; a non-SD_OK status means nothing was launched.
+ *   Data-dependent conditions (finite values, ids in range) are
+ *   preconditions that the device cannot report; kernels clamp every index
+ *   they read so that a violated precondition yields an unspecified result,
+ *   never an out-of-bounds access.
+ * - dtype: SD_F32 (float32 storage) or SD_BF16 (bfloat16 storage).  All
+ *   arithmetic accumulates in float32 and all floating outputs are float32.
+ * - Workspace: a caller-owned device buffer of at least the size returned by
+ *   the matching *_workspace_size function for the same shape arguments
+ *   (NULL is allowed when that size is 0).  Its contents need not be
+ *   initialised and are garbage afterwards.  Two calls in flight at the
+ *   same time must not share a workspace.
+ */
+#ifndef SPECFLASH_H
+#define SPECFLASH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sd_status {
+  SD_OK = 0,
+  SD_ERR_INVALID_ARG = 1,   /* null pointer, non-positive or inconsistent size */
+  SD_ERR_UNSUPPORTED = 2,   /* valid but not implemented: head size, dtype, ... */
+  SD_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required */
+  SD_ERR_HIP = 4            /* the HIP runtime reported an error at launch */
+} sd_status;
+
+typedef enum sd_dtype { SD_F32 = 0, SD_BF16 = 1 } sd_dtype;
+
+typedef enum sd_accept_mode {
+  SD_ACCEPT_GREEDY = 0,     /* temperature 0: longest prefix equal to the target argmax */
+  SD_ACCEPT_SAMPLED = 1     /* min(1, p/q) acceptance and residual resampling */
+} sd_accept_mode;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* sd_status_string(int status);
+
+/* Library ABI version, (major << 16) | minor. */
+int sd_version(void);
+
+/* ------------------------------------------------------------------------
+ * Latent-guided visual-token compression (Sec. 3.2, Eq. 3).
+ *
+ * The learned query set Cq [C, d] attends over the visual features F_V of
+ * each sequence; F_V is both key and value.  With H = num_heads the width d
+ * is cut into H contiguous slices of width dh = d / H and, for every
+ * sequence b, head h and latent c,
+ *
+ *   out[b, c, h*dh:(h+1)*dh] =
+ *     sum_n softmax_n(scale * Cq[c, hs] . feats[b, n, hs]) * feats[b, n, hs]
+ *
+ * (H = 1 and scale = 1 is Eq. 3 literally.)  The query set is shared by all
+ * sequences.
+ *
+ *   latents  [C, d]     dtype   learned queries
+ *   feats    [B, N, d]  dtype   visual features F_V, token-major
+ *   out      [B, C, d]  float32 compressed features
+ *   scale               score multiplier (finite)
+ * Requirements: B, N, C >= 1; d % num_heads == 0; dh in {64, 128} for
+ * SD_BF16, dh in {64, 128, 256} for SD_F32; N <= 2^24; C <= 2^20.
+ * For SD_BF16 the value aggregation runs on float16 matrix cores, so
+ * |feats| must stay below 65504 (larger magnitudes are a precondition
+ * violation).
+ * ---------------------------------------------------------------------- */
+size_t sd_latent_compress_workspace_size(int B, int N, int C, int d,
+                                         int num_heads, int dtype);
+
+int sd_latent_compress(const void* latents, const void* feats, float* out,
+                       int B, int N, int C, int d, int num_heads, float scale,
+                       int dtype, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/* ------------------------------------------------------------------------
+ * Verification attention of the drafted block (Sec. 3.1).
+ *
+ * The target scores the k drafted tokens in one pass; per layer that is
+ * attention of the k block queries over the KV cache, causal inside the
+ * block, with grouped-query heads.  kv_len[b] counts every cache entry of
+ * sequence b including the k block entries, which are its last k.  For
+ * block row j, query head h and g = Hq / Hkv:
+ *
+ *   visible keys t = 0 .. kv_len[b] - k + j,
+ *   s_t = scale * q[b, j, h] . K[b, t, h / g],
+ *   out[b, j, h] = sum_t softmax(s)_t V[b, t, h / g],
+ *   lse[b, j, h] = log sum_t exp(s_t)            (natural log)
+ *
+ * A row with no visible key gets out = 0 and lse = -inf.
+ *
+ *   q           [B, k, Hq, D]    dtype  queries of the block (after RoPE)
+ *   k_cache,    contiguous (page_table == NULL): [B, Lmax, Hkv, D] dtype
+ *   v_cache     paged: page pools [num_pages, Hkv, 16, D] dtype; token t of
+ *               sequence b lives in page page_table[b, t / 16], slot t % 16
+ *   kv_len      [B] int32, device; values are clamped to [0, capacity] with
+ *               capacity = Lmax (contiguous) or 16 * max_pages (paged)
+ *   page_table  [B, max_pages] int32, device, or NULL for contiguous caches;
+ *               page ids outside [0, num_pages) are a precondition violation
+ *   out         [B, k, Hq, D] float32
+ *   lse         [B, k, Hq] float32, or NULL when not wanted
+ * Requirements: 1 <= k <= 16; Hq % Hkv == 0; k * (Hq / Hkv) <= 256;
+ * D in {64, 128}; Lmax >= 1 (contiguous) or max_pages, num_pages >= 1
+ * (paged); scale finite.
+ * ---------------------------------------------------------------------- */
+size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D,
+                                int capacity, int dtype);
+
+int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* kv_len, const int32_t* page_table,
+                        int max_pages, int num_pages, int Lmax,
+                        float* out, float* lse,
+                        int B, int k, int Hq, int Hkv, int D, float scale,
+                        int dtype, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/* ------------------------------------------------------------------------
+ * Speculative acceptance (Sec. 3.1, Sec. 3.3; greedy at temperature 0,
+ * Sec. 4.2).  Per sequence b, drafted ids x_i = draft[b, i] (i < k):
+ *
+ * SD_ACCEPT_SAMPLED: accept position i iff u[b,i] * q[b,i,x_i] < p[b,i,x_i]
+ *   (exact float64 test, i.e. u < min(1, p/q)); ids outside [0, V) are
+ *   rejected.  n = number of leading accepted positions.  The extra token
+ *   is drawn with a = floor(u[b,k] * 2^24) by inverse CDF over integer
+ *   weights R_v = floor(r_v * 2^40): r = max(0, p[b,n] - q[b,n]) (float32
+ *   subtraction) when n < k, r = p[b,k] when n == k; T = floor(a * S / 2^24)
+ *   with S = sum R; the token is the smallest j whose inclusive prefix sum
+ *   of R exceeds T.  If S == 0, R = floor(p[b,n] * 2^40) is used; if that
+ *   is 0 too, the token is argmax p[b,n].  The result is bit-exact and
+ *   independent of summation order.
+ * SD_ACCEPT_GREEDY: g_i = argmax_v p[b,i,v] (lowest index on ties);
+ *   n = longest prefix with x_i == g_i; the extra token is g_n.  q and u
+ *   are not read (may be NULL).
+ *
+ * Temperature is the caller's: p and q are already softmax(logits / tau).
+ *
+ *   p           [B, k+1, V] float32  target probabilities
+ *   q           [B, k, V]   float32  draft probabilities
+ *   draft       [B, k]      int32    drafted ids
+ *   u           [B, k+1]    float32  uniforms in [0, 1) (multiples of 2^-24)
+ *   n_accepted  [B]         int32    out: accepted drafts per sequence
+ *   tokens      [B, k+1]    int32    out: draft[0..n-1], the extra token,
+ *                                    then -1 padding
+ * Requirements: B >= 1; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1].
+ * ---------------------------------------------------------------------- */
+size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode);
+
+int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
+                   const float* u, int32_t* n_accepted, int32_t* tokens,
+                   int B, int k, int V, int mode,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECFLASH_H */

@@ -1,0 +1,256 @@
+"""SpecFLASH draft-verify hot path on MI355X: Python binding of libspecflash.
+
+The three entry points mirror the C ABI in include/specflash.h and only
+marshal arguments: every step of the computation runs in the HIP kernels of
+libspecflash.so (built by ``paper_2505_12728_amd.build``).  torch supplies
+device memory and the current HIP stream.  There is no fallback: if the
+library is missing or the tensors are not on the GPU, the calls raise.
+
+    sd_latent_compress   Sec. 3.2, Eq. 3 (learned queries attend over F_V)
+    sd_verify_attention  Sec. 3.1 (one parallel pass over the K drafts)
+    sd_spec_accept       Sec. 3.1 / 3.3 acceptance; greedy for Sec. 4.2
+"""
+
+import ctypes
+import math
+import os
+
+__all__ = [
+    "SD_OK", "SD_ERR_INVALID_ARG", "SD_ERR_UNSUPPORTED", "SD_ERR_WORKSPACE", "SD_ERR_HIP",
+    "SD_F32", "SD_BF16", "SD_ACCEPT_GREEDY", "SD_ACCEPT_SAMPLED",
+    "SDError", "library", "library_path",
+    "sd_status_string", "sd_version",
+    "sd_latent_compress_workspace_size", "sd_latent_compress",
+    "sd_verify_workspace_size", "sd_verify_attention",
+    "sd_spec_accept_workspace_size", "sd_spec_accept",
+]
+
+SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
+SD_F32, SD_BF16 = 0, 1
+SD_ACCEPT_GREEDY, SD_ACCEPT_SAMPLED = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libspecflash.so")
+_lib = None
+
+_c = ctypes
+_vp, _sz, _i, _f = _c.c_void_p, _c.c_size_t, _c.c_int, _c.c_float
+_SIGNATURES = {
+    "sd_status_string": (_c.c_char_p, [_i]),
+    "sd_version": (_i, []),
+    "sd_latent_compress_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i]),
+    "sd_latent_compress": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
+    "sd_verify_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
+    "sd_verify_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _vp, _vp,
+                                 _i, _i, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
+    "sd_spec_accept_workspace_size": (_sz, [_i, _i, _i, _i]),
+    "sd_spec_accept": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _sz, _vp]),
+}
+
+
+class SDError(RuntimeError):
+    """A non-zero sd_status returned by the library."""
+
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {sd_status_string(status)}")
+
+
+def library():
+    """Load libspecflash.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(library_path):
+            raise RuntimeError(
+                f"{library_path} is missing: build it with `python -m paper_2505_12728_amd.build`")
+        lib = ctypes.CDLL(library_path)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def sd_status_string(status):
+    return library().sd_status_string(int(status)).decode()
+
+
+def sd_version():
+    return library().sd_version()
+
+
+# ----------------------------------------------------------------- helpers
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return SD_F32
+    if t.dtype == torch.bfloat16:
+        return SD_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}: use float32 or bfloat16")
+
+
+def _check(t, name, dtype=None, ndim=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _workspace(nbytes, device, given):
+    if nbytes == 0:
+        return None, 0
+    if given is not None:
+        return given, given.numel() * given.element_size()
+    torch = _torch()
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+def _raise(status, where):
+    if status != SD_OK:
+        raise SDError(status, where)
+
+
+# ------------------------------------------------------------- compression
+
+def sd_latent_compress_workspace_size(B, N, C, d, num_heads, dtype):
+    return library().sd_latent_compress_workspace_size(B, N, C, d, num_heads, dtype)
+
+
+def sd_latent_compress(latents, feats, num_heads=1, scale=1.0, out=None, workspace=None,
+                       stream=None):
+    """Eq. 3 per head slice: latents [C, d], feats [B, N, d] -> out [B, C, d] fp32."""
+    torch = _torch()
+    _check(latents, "latents", ndim=2)
+    _check(feats, "feats", dtype=latents.dtype, ndim=3)
+    C, d = latents.shape
+    B, N, d2 = feats.shape
+    if d2 != d:
+        raise ValueError("latents and feats disagree on the feature width")
+    dt = _dtype_code(latents)
+    if out is None:
+        out = torch.empty((B, C, d), dtype=torch.float32, device=feats.device)
+    _check(out, "out", dtype=torch.float32)
+    ws_bytes = sd_latent_compress_workspace_size(B, N, C, d, num_heads, dt)
+    ws, ws_len = _workspace(ws_bytes, feats.device, workspace)
+    st = library().sd_latent_compress(_ptr(latents), _ptr(feats), _ptr(out), B, N, C, d,
+                                      num_heads, float(scale), dt, _ptr(ws), ws_len,
+                                      _stream(stream))
+    _raise(st, "sd_latent_compress")
+    return out
+
+
+# ------------------------------------------------------------ verification
+
+def sd_verify_workspace_size(B, k, Hq, Hkv, D, capacity, dtype):
+    return library().sd_verify_workspace_size(B, k, Hq, Hkv, D, capacity, dtype)
+
+
+def sd_verify_attention(q, k_cache, v_cache, kv_len, scale=None, page_table=None,
+                        num_pages=None, out=None, lse=True, workspace=None, stream=None):
+    """Attention of the k block queries over the cache (causal inside the block).
+
+    q [B, k, Hq, D]; caches [B, Lmax, Hkv, D], or page pools [P, Hkv, 16, D]
+    with page_table [B, max_pages] int32; kv_len [B] int32 (block included).
+    Returns (out [B, k, Hq, D] fp32, lse [B, k, Hq] fp32 or None).
+    """
+    torch = _torch()
+    _check(q, "q", ndim=4)
+    _check(k_cache, "k_cache", dtype=q.dtype, ndim=4)
+    _check(v_cache, "v_cache", dtype=q.dtype, ndim=4)
+    _check(kv_len, "kv_len", dtype=torch.int32, ndim=1)
+    B, k, Hq, D = q.shape
+    if tuple(k_cache.shape) != tuple(v_cache.shape):
+        raise ValueError("k_cache and v_cache must have the same shape")
+    if kv_len.shape[0] != B:
+        raise ValueError("kv_len needs one entry per sequence")
+    dt = _dtype_code(q)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if page_table is None:
+        if k_cache.shape[0] != B or k_cache.shape[3] != D:
+            raise ValueError("contiguous caches must be [B, Lmax, Hkv, D]")
+        Lmax, Hkv = k_cache.shape[1], k_cache.shape[2]
+        max_pages = num_pages_ = 0
+        capacity = Lmax
+    else:
+        _check(page_table, "page_table", dtype=torch.int32, ndim=2)
+        if k_cache.shape[2] != 16 or k_cache.shape[3] != D or page_table.shape[0] != B:
+            raise ValueError("paged caches must be [P, Hkv, 16, D] with a [B, max_pages] table")
+        Hkv = k_cache.shape[1]
+        max_pages = page_table.shape[1]
+        num_pages_ = k_cache.shape[0] if num_pages is None else num_pages
+        Lmax = 0
+        capacity = 16 * max_pages
+    if out is None:
+        out = torch.empty((B, k, Hq, D), dtype=torch.float32, device=q.device)
+    _check(out, "out", dtype=torch.float32)
+    lse_t = None
+    if lse is True:
+        lse_t = torch.empty((B, k, Hq), dtype=torch.float32, device=q.device)
+    elif lse is not None and lse is not False:
+        lse_t = lse
+        _check(lse_t, "lse", dtype=torch.float32)
+    ws_bytes = sd_verify_workspace_size(B, k, Hq, Hkv, D, capacity, dt)
+    ws, ws_len = _workspace(ws_bytes, q.device, workspace)
+    st = library().sd_verify_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
+                                       _ptr(page_table), max_pages, num_pages_, Lmax, _ptr(out),
+                                       _ptr(lse_t), B, k, Hq, Hkv, D, float(scale), dt,
+                                       _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_verify_attention")
+    return out, lse_t
+
+
+# -------------------------------------------------------------- acceptance
+
+def sd_spec_accept_workspace_size(B, k, V, mode):
+    return library().sd_spec_accept_workspace_size(B, k, V, mode)
+
+
+def sd_spec_accept(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, tokens=None,
+                   workspace=None, stream=None):
+    """Speculative acceptance: p [B, k+1, V], q [B, k, V], draft [B, k] int32,
+    u [B, k+1] fp32.  Returns (n_accepted [B] int32, tokens [B, k+1] int32)."""
+    torch = _torch()
+    _check(p, "p", dtype=torch.float32, ndim=3)
+    _check(draft, "draft", dtype=torch.int32, ndim=2)
+    B, kp1, V = p.shape
+    k = kp1 - 1
+    if tuple(draft.shape) != (B, k):
+        raise ValueError("draft must be [B, k]")
+    if mode == SD_ACCEPT_SAMPLED:
+        _check(q, "q", dtype=torch.float32, ndim=3)
+        _check(u, "u", dtype=torch.float32, ndim=2)
+        if tuple(q.shape) != (B, k, V) or tuple(u.shape) != (B, k + 1):
+            raise ValueError("q must be [B, k, V] and u [B, k+1]")
+    if n_accepted is None:
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=p.device)
+    if tokens is None:
+        tokens = torch.empty((B, k + 1), dtype=torch.int32, device=p.device)
+    ws_bytes = sd_spec_accept_workspace_size(B, k, V, mode)
+    ws, ws_len = _workspace(ws_bytes, p.device, workspace)
+    st = library().sd_spec_accept(_ptr(p), _ptr(q), _ptr(draft), _ptr(u), _ptr(n_accepted),
+                                  _ptr(tokens), B, k, V, int(mode), _ptr(ws), ws_len,
+                                  _stream(stream))
+    _raise(st, "sd_spec_accept")
+    return n_accepted, tokens

@@ -1,0 +1,83 @@
+// Host-side launch interfaces between the C ABI layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sd {
+
+// ---------------------------------------------------------------- verify
+struct VerifyPlan {
+  int g;            // query heads per KV head
+  int rows;         // k * g query rows that share one KV head
+  int row_blocks;   // 16-row blocks per work-group (1..4), bf16 path
+  int row_groups;   // work-groups along the rows of one KV head
+  int rows_padded;  // row_groups * row_blocks * 16 (partial row stride)
+  int capacity;     // Lmax or 16 * max_pages
+  int keys_per_split;
+  int nsplit;
+  size_t workspace_bytes;
+};
+
+VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype);
+
+struct VerifyArgs {
+  const void* q;
+  const void* kc;
+  const void* vc;
+  const int32_t* kv_len;
+  const int32_t* page_table;
+  int max_pages;
+  int num_pages;
+  int Lmax;
+  float* out;
+  float* lse;
+  int B, k, Hq, Hkv, D;
+  float scale;          // score multiplier as given
+  float scale_log2;     // scale * log2(e)
+  float* part_o;        // [B, Hkv, nsplit, rows_padded, D]
+  float* part_lse;      // [B, Hkv, nsplit, rows_padded] (log2 units)
+};
+
+hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hipStream_t s);
+
+// -------------------------------------------------------------- compress
+struct CompressPlan {
+  int dh;
+  int lat_tile;        // latents per work-group
+  int lat_tiles;
+  int nsplit;          // splits of the N tokens
+  int tokens_per_split;
+  size_t workspace_bytes;
+};
+
+CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype);
+
+struct CompressArgs {
+  const void* latents;
+  const void* feats;
+  float* out;
+  int B, N, C, d, H;
+  float scale;
+  float scale_log2;
+  float* part_o;       // [B, H, nsplit, C, dh]
+  float* part_lse;     // [B, H, nsplit, C]
+};
+
+hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dtype, hipStream_t s);
+
+// ---------------------------------------------------------------- accept
+struct AcceptArgs {
+  const float* p;
+  const float* q;
+  const int32_t* draft;
+  const float* u;
+  int32_t* n_accepted;
+  int32_t* tokens;
+  int B, k, V, mode;
+};
+
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+
+}  // namespace sd

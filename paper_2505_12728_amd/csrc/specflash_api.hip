@@ -1,0 +1,188 @@
+// C ABI entry points: host-side validation, planning and launch.  Nothing is
+// enqueued unless every argument check passes; the library allocates no
+// device memory and keeps no state between calls.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/specflash.h"
+#include "launch.hpp"
+
+namespace {
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+int status_from(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
+
+bool verify_shape_ok(int B, int k, int Hq, int Hkv, int D, int dtype, int* status) {
+  if (B < 1 || k < 1 || Hq < 1 || Hkv < 1 || (dtype != SD_F32 && dtype != SD_BF16)) {
+    *status = SD_ERR_INVALID_ARG;
+    return false;
+  }
+  if (Hq % Hkv != 0) {
+    *status = SD_ERR_INVALID_ARG;
+    return false;
+  }
+  const int rows = k * (Hq / Hkv);
+  if (k > 16 || (D != 64 && D != 128) || rows > 256 || (dtype == SD_F32 && rows > 64)) {
+    *status = SD_ERR_UNSUPPORTED;
+    return false;
+  }
+  return true;
+}
+
+bool compress_shape_ok(int B, int N, int C, int d, int H, int dtype, int* status) {
+  if (B < 1 || N < 1 || C < 1 || d < 1 || H < 1 || d % H != 0 ||
+      (dtype != SD_F32 && dtype != SD_BF16)) {
+    *status = SD_ERR_INVALID_ARG;
+    return false;
+  }
+  const int dh = d / H;
+  const bool ok = dtype == SD_BF16 ? (dh == 64 || dh == 128) : (dh == 64 || dh == 128 || dh == 256);
+  if (!ok || N > (1 << 24) || C > (1 << 20)) {
+    *status = SD_ERR_UNSUPPORTED;
+    return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sd_status_string(int status) {
+  switch (status) {
+    case SD_OK: return "SD_OK";
+    case SD_ERR_INVALID_ARG: return "SD_ERR_INVALID_ARG: invalid argument";
+    case SD_ERR_UNSUPPORTED: return "SD_ERR_UNSUPPORTED: shape or dtype not supported";
+    case SD_ERR_WORKSPACE: return "SD_ERR_WORKSPACE: workspace missing or too small";
+    case SD_ERR_HIP: return "SD_ERR_HIP: HIP runtime error at launch";
+    default: return "unknown sd_status";
+  }
+}
+
+int sd_version(void) { return (1 << 16) | 0; }
+
+// ------------------------------------------------------------- compress
+size_t sd_latent_compress_workspace_size(int B, int N, int C, int d, int num_heads, int dtype) {
+  int st;
+  if (!compress_shape_ok(B, N, C, d, num_heads, dtype, &st)) return 0;
+  return sd::plan_compress(B, N, C, d, num_heads, dtype).workspace_bytes;
+}
+
+int sd_latent_compress(const void* latents, const void* feats, float* out, int B, int N, int C,
+                       int d, int num_heads, float scale, int dtype, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = SD_OK;
+  if (!compress_shape_ok(B, N, C, d, num_heads, dtype, &st)) return st;
+  if (!latents || !feats || !out || !isfinite(scale)) return SD_ERR_INVALID_ARG;
+  if (!aligned(latents, 16) || !aligned(feats, 16) || !aligned(out, 16)) return SD_ERR_INVALID_ARG;
+  const sd::CompressPlan plan = sd::plan_compress(B, N, C, d, num_heads, dtype);
+  if (plan.workspace_bytes > 0 && (!workspace || workspace_bytes < plan.workspace_bytes ||
+                                   !aligned(workspace, 16)))
+    return SD_ERR_WORKSPACE;
+  sd::CompressArgs a{};
+  a.latents = latents;
+  a.feats = feats;
+  a.out = out;
+  a.B = B;
+  a.N = N;
+  a.C = C;
+  a.d = d;
+  a.H = num_heads;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  if (plan.workspace_bytes > 0) {
+    a.part_o = static_cast<float*>(workspace);
+    a.part_lse = a.part_o + (size_t)B * num_heads * plan.nsplit * C * plan.dh;
+  }
+  return status_from(sd::launch_compress(a, plan, dtype, static_cast<hipStream_t>(stream)));
+}
+
+// --------------------------------------------------------------- verify
+size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype) {
+  int st;
+  if (!verify_shape_ok(B, k, Hq, Hkv, D, dtype, &st) || capacity < 1) return 0;
+  return sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype).workspace_bytes;
+}
+
+int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* kv_len, const int32_t* page_table, int max_pages,
+                        int num_pages, int Lmax, float* out, float* lse, int B, int k, int Hq,
+                        int Hkv, int D, float scale, int dtype, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  int st = SD_OK;
+  if (!verify_shape_ok(B, k, Hq, Hkv, D, dtype, &st)) return st;
+  if (!q || !k_cache || !v_cache || !kv_len || !out || !isfinite(scale)) return SD_ERR_INVALID_ARG;
+  const size_t al = dtype == SD_BF16 ? 16 : 4;
+  if (!aligned(q, al) || !aligned(k_cache, al) || !aligned(v_cache, al) || !aligned(out, 16) ||
+      !aligned(kv_len, 4) || (lse && !aligned(lse, 4)))
+    return SD_ERR_INVALID_ARG;
+  int capacity;
+  if (page_table) {
+    if (max_pages < 1 || num_pages < 1 || max_pages > (1 << 26) || !aligned(page_table, 4))
+      return SD_ERR_INVALID_ARG;
+    capacity = max_pages * 16;
+  } else {
+    if (Lmax < 1) return SD_ERR_INVALID_ARG;
+    capacity = Lmax;
+  }
+  const sd::VerifyPlan plan = sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype);
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned(workspace, 16))
+    return SD_ERR_WORKSPACE;
+  sd::VerifyArgs a{};
+  a.q = q;
+  a.kc = k_cache;
+  a.vc = v_cache;
+  a.kv_len = kv_len;
+  a.page_table = page_table;
+  a.max_pages = max_pages;
+  a.num_pages = num_pages;
+  a.Lmax = Lmax;
+  a.out = out;
+  a.lse = lse;
+  a.B = B;
+  a.k = k;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.part_o = static_cast<float*>(workspace);
+  a.part_lse = a.part_o + (size_t)B * Hkv * plan.nsplit * plan.rows_padded * D;
+  return status_from(sd::launch_verify(a, plan, dtype, static_cast<hipStream_t>(stream)));
+}
+
+// --------------------------------------------------------------- accept
+size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode) {
+  (void)B;
+  (void)k;
+  (void)V;
+  (void)mode;
+  return 0;
+}
+
+int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const float* u,
+                   int32_t* n_accepted, int32_t* tokens, int B, int k, int V, int mode,
+                   void* workspace, size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
+    return SD_ERR_INVALID_ARG;
+  if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (!p || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
+  if (mode == SD_ACCEPT_SAMPLED && (!q || !u)) return SD_ERR_INVALID_ARG;
+  sd::AcceptArgs a{};
+  a.p = p;
+  a.q = q;
+  a.draft = draft;
+  a.u = u;
+  a.n_accepted = n_accepted;
+  a.tokens = tokens;
+  a.B = B;
+  a.k = k;
+  a.V = V;
+  a.mode = mode;
+  return status_from(sd::launch_accept(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

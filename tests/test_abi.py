@@ -1,0 +1,134 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol
+the header declares, and rejects bad arguments before touching HIP."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2505_12728_amd as sd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specflash.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sd_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(sd.library_path):
+        pytest.fail("libspecflash.so is not built (run __graft_entry__.build())")
+    return sd.library()
+
+
+def test_header_declares_the_three_entry_points():
+    names = header_functions()
+    for n in ["sd_latent_compress", "sd_verify_attention", "sd_spec_accept"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+    assert set(header_functions()) <= set(sd._SIGNATURES)
+
+
+def test_status_strings_and_version(lib):
+    assert sd.sd_status_string(sd.SD_OK) == "SD_OK"
+    for s in range(1, 5):
+        assert sd.sd_status_string(s).startswith("SD_ERR")
+    assert "unknown" in sd.sd_status_string(99)
+    assert sd.sd_version() >> 16 == 1
+
+
+def _fake(n=1):
+    # aligned non-null host addresses: validation never dereferences them
+    buf = ctypes.create_string_buffer(4096 + 64)
+    base = (ctypes.addressof(buf) + 255) // 256 * 256
+    return buf, [ctypes.c_void_p(base + 256 * i) for i in range(n)]
+
+
+def test_verify_validation_errors(lib):
+    keep, (q, kc, vc, kl, out, ws) = _fake(6)
+    f = lib.sd_verify_attention
+    args = dict(q=q, kc=kc, vc=vc, kl=kl, pt=None, mp=0, npg=0, lmax=64, out=out, lse=None,
+                B=1, k=4, Hq=8, Hkv=2, D=128, scale=0.1, dt=1, ws=ws, wsb=1 << 30, st=None)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["q"], a["kc"], a["vc"], a["kl"], a["pt"], a["mp"], a["npg"], a["lmax"],
+                 a["out"], a["lse"], a["B"], a["k"], a["Hq"], a["Hkv"], a["D"], a["scale"],
+                 a["dt"], a["ws"], a["wsb"], a["st"])
+
+    assert call(q=None) == sd.SD_ERR_INVALID_ARG
+    assert call(kl=None) == sd.SD_ERR_INVALID_ARG
+    assert call(Hq=6, Hkv=4) == sd.SD_ERR_INVALID_ARG
+    assert call(B=0) == sd.SD_ERR_INVALID_ARG
+    assert call(dt=7) == sd.SD_ERR_INVALID_ARG
+    assert call(scale=float("nan")) == sd.SD_ERR_INVALID_ARG
+    assert call(lmax=0) == sd.SD_ERR_INVALID_ARG
+    assert call(k=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(D=96) == sd.SD_ERR_UNSUPPORTED
+    assert call(Hq=512, Hkv=1) == sd.SD_ERR_UNSUPPORTED
+    assert call(dt=0, Hq=32, Hkv=1) == sd.SD_ERR_UNSUPPORTED   # fp32 path: <= 64 rows
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=16) == sd.SD_ERR_WORKSPACE
+    # paged: needs a page count
+    assert call(pt=kl, mp=0, npg=4) == sd.SD_ERR_INVALID_ARG
+    assert call(pt=kl, mp=4, npg=0) == sd.SD_ERR_INVALID_ARG
+    misaligned = ctypes.c_void_p(q.value + 2)
+    assert call(q=misaligned) == sd.SD_ERR_INVALID_ARG
+
+
+def test_compress_validation_errors(lib):
+    keep, (lat, feats, out, ws) = _fake(4)
+    f = lib.sd_latent_compress
+
+    def call(lat=lat, feats=feats, out=out, B=1, N=64, C=16, d=256, H=2, scale=1.0, dt=1,
+             ws=ws, wsb=1 << 30):
+        return f(lat, feats, out, B, N, C, d, H, scale, dt, ws, wsb, None)
+
+    assert call(lat=None) == sd.SD_ERR_INVALID_ARG
+    assert call(N=0) == sd.SD_ERR_INVALID_ARG
+    assert call(d=250, H=4) == sd.SD_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == sd.SD_ERR_INVALID_ARG
+    assert call(d=96, H=1) == sd.SD_ERR_UNSUPPORTED
+    assert call(d=512, H=2) == sd.SD_ERR_UNSUPPORTED     # bf16 head width 256
+    need = lib.sd_latent_compress_workspace_size(1, 65536, 16, 256, 2, 1)
+    assert need > 0
+    assert f(lat, feats, out, 1, 65536, 16, 256, 2, 1.0, 1, None, 0, None) == sd.SD_ERR_WORKSPACE
+
+
+def test_accept_validation_errors(lib):
+    keep, (p, q, d, u, n, t) = _fake(6)
+    f = lib.sd_spec_accept
+
+    def call(p=p, q=q, d=d, u=u, n=n, t=t, B=1, k=4, V=100, mode=1):
+        return f(p, q, d, u, n, t, B, k, V, mode, None, 0, None)
+
+    assert call(p=None) == sd.SD_ERR_INVALID_ARG
+    assert call(q=None) == sd.SD_ERR_INVALID_ARG          # sampled needs q
+    assert call(u=None) == sd.SD_ERR_INVALID_ARG
+    assert call(mode=5) == sd.SD_ERR_INVALID_ARG
+    assert call(V=0) == sd.SD_ERR_INVALID_ARG
+    assert call(k=0) == sd.SD_ERR_INVALID_ARG
+    assert call(k=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
+
+
+def test_workspace_sizes_cover_the_partials(lib):
+    # verify: one (D + 1)-float partial row per (sequence, KV head, split, row)
+    for B, k, Hq, Hkv, D, cap in [(1, 4, 4, 1, 64, 608), (4, 8, 64, 8, 128, 65536),
+                                  (16, 6, 32, 8, 128, 16384)]:
+        for dt in (0, 1):
+            if dt == 0 and k * Hq // Hkv > 64:
+                continue
+            n = lib.sd_verify_workspace_size(B, k, Hq, Hkv, D, cap, dt)
+            assert n > 0 and n % 4 == 0
+            assert n >= B * Hkv * k * (Hq // Hkv) * (D + 1) * 4
+    assert lib.sd_verify_workspace_size(1, 4, 6, 4, 128, 100, 1) == 0   # invalid shape

@@ -1,0 +1,171 @@
+"""GPU parity of sd_verify_attention against the oracle (same seeded inputs)."""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_12728_amd import synth
+from tests.gpu_util import assert_close, assert_lse_close, np_to_device, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gpu(d, scale=None):
+    import torch
+    import paper_2505_12728_amd as sd
+    q = to_device(d["q"])
+    kc = to_device(d["k_cache"])
+    vc = to_device(d["v_cache"])
+    kl = np_to_device(d["kv_len"].astype(np.int32))
+    pt = None if d["page_table"] is None else np_to_device(d["page_table"].astype(np.int32))
+    out, lse = sd.sd_verify_attention(q, kc, vc, kl, scale=scale, page_table=pt)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy()
+
+
+def oracle_slice(d, b, hk, g, scale):
+    """Oracle for one (sequence, KV head): its g query heads over its cache."""
+    q = d["q"].values[b:b + 1, :, hk * g:(hk + 1) * g]
+    if d["page_table"] is None:
+        kc = d["k_cache"].values[b:b + 1, :, hk:hk + 1]
+        vc = d["v_cache"].values[b:b + 1, :, hk:hk + 1]
+        return oracle.verify_attention(q, kc, vc, d["kv_len"][b:b + 1], scale)
+    kc = d["k_cache"].values[:, hk:hk + 1]
+    vc = d["v_cache"].values[:, hk:hk + 1]
+    return oracle.verify_attention(q, kc, vc, d["kv_len"][b:b + 1], scale,
+                                   page_table=d["page_table"][b:b + 1])
+
+
+def check_pairs(d, w, out, lse, pairs, dtype):
+    scale = 1.0 / math.sqrt(w.head_dim)
+    g = w.hq // w.hkv
+    for b, hk in pairs:
+        ro, rl = oracle_slice(d, b, hk, g, scale)
+        assert_close(out[b:b + 1, :, hk * g:(hk + 1) * g], ro, dtype, f"out b={b} hk={hk}")
+        assert_lse_close(lse[b:b + 1, :, hk * g:(hk + 1) * g], rl, dtype, f"lse b={b} hk={hk}")
+
+
+@pytest.mark.parametrize("wi", [0, 1, 2])
+def test_verify_workload_full_oracle(wi):
+    w = synth.workload(wi)
+    print(f"verify workload {w.name}", flush=True)
+    d = synth.verify_inputs(w)
+    out, lse = run_gpu(d)
+    ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                     d["kv_len"], 1.0 / math.sqrt(w.head_dim))
+    assert_close(out, ro, w.dtype, w.name)
+    assert_lse_close(lse, rl, w.dtype, w.name)
+
+
+def test_verify_paged_workload_sampled():
+    # batched paged workload at full size; oracle on sampled (sequence, KV head)
+    w = synth.workload(3)
+    print(f"verify workload {w.name}", flush=True)
+    d = synth.verify_inputs(w)
+    out, lse = run_gpu(d)
+    lens = d["kv_len"]
+    pairs = [(int(np.argmin(lens)), 0), (int(np.argmax(lens)), 7), (5, 3)]
+    check_pairs(d, w, out, lse, pairs, w.dtype)
+    assert np.all(np.isfinite(out))
+
+
+def test_verify_long_workload_sampled():
+    w = synth.workload(4)
+    print(f"verify workload {w.name}", flush=True)
+    d = synth.verify_inputs(w)
+    out, lse = run_gpu(d)
+    check_pairs(d, w, out, lse, [(0, 0), (3, 7)], w.dtype)
+    assert np.all(np.isfinite(out))
+
+
+CASES = [
+    # name, dtype, B, k, Hq, Hkv, D, lens, paged
+    ("ragged-tail", "bf16", 2, 3, 8, 2, 128, [1000, 517], False),
+    ("single-key", "bf16", 1, 1, 4, 4, 128, [1], False),
+    ("short-rows-empty", "bf16", 2, 5, 4, 1, 128, [3, 0], False),
+    ("head-dim-64", "bf16", 2, 4, 12, 3, 64, [700, 130], False),
+    ("mha-one-row", "bf16", 1, 1, 8, 8, 128, [4096], False),
+    ("two-row-groups", "bf16", 1, 16, 8, 1, 128, [777], False),
+    ("paged-ragged", "bf16", 3, 6, 8, 2, 128, [33, 1000, 2049], True),
+    ("paged-d64", "bf16", 2, 2, 4, 2, 64, [17, 300], True),
+    ("f32-ragged", "f32", 2, 4, 8, 2, 64, [608, 99], False),
+    ("f32-paged", "f32", 2, 3, 4, 1, 128, [50, 700], True),
+    ("f32-empty-rows", "f32", 1, 4, 4, 1, 64, [2], False),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_verify_edge_cases(case):
+    name, dt, B, k, Hq, Hkv, D, lens, paged = case
+    print(f"verify case {name}", flush=True)
+    w = synth.Workload(name, dt, batch=B, hq=Hq, hkv=Hkv, head_dim=D,
+                       kv_len=max(max(lens), 1), block=k, paged=paged)
+    d = synth.verify_inputs(w, seed=11, kv_len=np.array(lens, np.int32))
+    scale = 0.7 / math.sqrt(D)
+    out, lse = run_gpu(d, scale=scale)
+    if paged:
+        ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                         d["kv_len"], scale, page_table=d["page_table"])
+    else:
+        ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                         d["kv_len"], scale)
+    if np.any(ro != 0):
+        assert_close(out, ro, dt, name)
+    else:
+        assert np.all(out == 0)
+    assert_lse_close(lse, rl, dt, name)
+    # rows without a visible key are exactly zero
+    assert np.all(out[np.isneginf(rl)] == 0)
+
+
+def test_verify_nan_poison_beyond_length_is_never_read():
+    w = synth.Workload("poison", "bf16", batch=2, hq=8, hkv=2, head_dim=128, kv_len=640, block=4)
+    lens = np.array([600, 333], np.int32)
+    clean = synth.verify_inputs(w, seed=3, kv_len=lens)
+    dirty = synth.verify_inputs(w, seed=3, kv_len=lens, poison=float("nan"))
+    a, la = run_gpu(clean)
+    b, lb = run_gpu(dirty)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+
+
+def test_verify_paged_equals_contiguous_bitwise():
+    import torch
+    import paper_2505_12728_amd as sd
+    rng = np.random.default_rng(5)
+    B, k, Hq, Hkv, D = 3, 5, 16, 4, 128
+    lens = np.array([1111, 40, 2000], np.int32)
+    Lmax = 2048
+    kf = synth.Tensor(rng.standard_normal((B, Lmax, Hkv, D)).astype(np.float32), "bf16")
+    vf = synth.Tensor(rng.standard_normal((B, Lmax, Hkv, D)).astype(np.float32), "bf16")
+    q = synth.Tensor(rng.standard_normal((B, k, Hq, D)).astype(np.float32), "bf16")
+    pages = (lens + 15) // 16
+    n_pool = int(pages.sum()) + 5
+    perm = rng.permutation(n_pool)
+    table = np.zeros((B, Lmax // 16), np.int32)
+    kb = np.zeros((n_pool, Hkv, 16, D), np.uint16)
+    vb = np.zeros((n_pool, Hkv, 16, D), np.uint16)
+    pos = 0
+    for b in range(B):
+        for i in range(pages[b]):
+            pg = perm[pos]
+            pos += 1
+            table[b, i] = pg
+            kb[pg] = kf.bits[b, i * 16:(i + 1) * 16].transpose(1, 0, 2)
+            vb[pg] = vf.bits[b, i * 16:(i + 1) * 16].transpose(1, 0, 2)
+    to_bf = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    kl = np_to_device(lens)
+    o1, l1 = sd.sd_verify_attention(to_device(q), to_device(kf), to_device(vf), kl)
+    o2, l2 = sd.sd_verify_attention(to_device(q), to_bf(kb), to_bf(vb), kl,
+                                    page_table=np_to_device(table))
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_verify_is_deterministic():
+    w = synth.workload(2)
+    d = synth.verify_inputs(w)
+    a, la = run_gpu(d)
+    b, lb = run_gpu(d)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)

@@ -1,0 +1,276 @@
+"""Benchmark of the SpecFLASH draft-verify hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one pass of the whole hot path over one batch of synthetic
+input with every tensor already resident in HBM:
+    sd_latent_compress  (Eq. 3)  ->  sd_verify_attention  ->  sd_spec_accept
+Default workload: "long-video" (batch 4, GQA 64/8 heads, head dim 128, KV
+length 65536, block k = 8; compression of 16384 tokens of width 8192 to 512
+latents over 64 heads; sampled acceptance over a 152064-token vocabulary at
+temperature 0.7).
+
+Prints one JSON line.  `value` is the verify step's KV-read rate: bytes of
+K and V the step must read once, divided by the time of verification
+attention plus acceptance, in TB/s.  Per-kernel times come from HIP events
+on the stream the kernels run on.  `roofline` describes the dominant kernel
+(the longest per step); `rooflines` lists all three.  `cpu_baseline` times
+the plain CPU oracle on a bounded sample of the same workload and scales it
+to the whole step.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("verify-step µs & KV-read HBM TB/s at long KV; "
+          "latent-compress MFMA TFLOP/s")
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 / fp16 matrix cores
+FP32_VALU_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long-video")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip timing the CPU oracle")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (for counter scaling)")
+    return ap.parse_args()
+
+
+def to_dev(t, dev):
+    import numpy as np
+    import torch
+    if t.dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(t.bits).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+    return torch.from_numpy(np.ascontiguousarray(t.values)).to(dev)
+
+
+def accept_bytes(p, n):
+    """Algorithmic bytes of one acceptance call: the k test scalars plus one
+    full vocabulary pass over the row that is sampled (p_n and q_n when a
+    draft was rejected, p_k alone when all were accepted)."""
+    B, kp1, V = p.shape
+    k = kp1 - 1
+    total = 0
+    for nb in n:
+        total += (2 * V if nb < k else V) * 4 + k * 4 * 3
+    return total
+
+
+def cpu_baseline(w, comp, ver, acc, mode):
+    """Time the oracle on a bounded sample and scale it to one whole step."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    lat, feats = comp
+    dh = w.c_width // w.c_heads
+    g = w.hq // w.hkv
+    scale = 1.0 / math.sqrt(w.head_dim)
+    # compression: up to 16 (sequence, head) pairs, every latent and token
+    t0 = time.perf_counter()
+    pairs_c = [(i % w.c_batch, (7 * i) % w.c_heads) for i in range(min(16, w.c_batch * w.c_heads))]
+    for b, h in pairs_c:
+        cols = slice(h * dh, (h + 1) * dh)
+        oracle.latent_compress(lat.values[:, cols], feats.values[b:b + 1, :, cols], 1, 1.0)
+    tc = (time.perf_counter() - t0) / len(pairs_c) * (w.c_batch * w.c_heads)
+    # verification: up to 8 (sequence, KV head) pairs over the whole cache
+    t0 = time.perf_counter()
+    pairs_v = [(i % w.batch, (3 * i) % w.hkv) for i in range(min(8, w.batch * w.hkv))]
+    for b, hk in pairs_v:
+        q = ver["q"].values[b:b + 1, :, hk * g:(hk + 1) * g]
+        if ver["page_table"] is None:
+            oracle.verify_attention(q, ver["k_cache"].values[b:b + 1, :, hk:hk + 1],
+                                    ver["v_cache"].values[b:b + 1, :, hk:hk + 1],
+                                    ver["kv_len"][b:b + 1], scale)
+        else:
+            oracle.verify_attention(q, ver["k_cache"].values[:, hk:hk + 1],
+                                    ver["v_cache"].values[:, hk:hk + 1], ver["kv_len"][b:b + 1],
+                                    scale, page_table=ver["page_table"][b:b + 1])
+    tv = (time.perf_counter() - t0) / len(pairs_v) * (w.batch * w.hkv)
+    # acceptance: every sequence
+    t0 = time.perf_counter()
+    oracle.spec_accept(acc["p"], acc["q"], acc["draft"], acc["u"], mode)
+    ta = time.perf_counter() - t0
+    return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "threads": threads,
+            "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
+                      f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
+                      f"pairs, acceptance of all {w.batch} sequences; scaled linearly"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the hot path is "
+              "measured on one GPU's share; no multi-GPU run exists in this build.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2505_12728_amd as sd
+    from paper_2505_12728_amd import synth
+
+    sd.library()   # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.workload(args.workload)
+    mode = "sampled" if "sampled" in w.modes else "greedy"
+    print(f"[bench] generating workload {w.name}", file=sys.stderr, flush=True)
+    comp = synth.compress_inputs(w)
+    ver = synth.verify_inputs(w)
+    acc = synth.accept_inputs(w, mode)
+
+    lat_d, feats_d = to_dev(comp[0], dev), to_dev(comp[1], dev)
+    q_d, k_d, v_d = to_dev(ver["q"], dev), to_dev(ver["k_cache"], dev), to_dev(ver["v_cache"], dev)
+    kl_d = torch.from_numpy(ver["kv_len"]).to(dev)
+    pt_d = None if ver["page_table"] is None else torch.from_numpy(ver["page_table"]).to(dev)
+    p_d = torch.from_numpy(acc["p"]).to(dev)
+    qq_d = torch.from_numpy(acc["q"]).to(dev)
+    dr_d = torch.from_numpy(acc["draft"]).to(dev)
+    u_d = torch.from_numpy(acc["u"]).to(dev)
+    dt_code = sd.SD_BF16 if w.dtype == "bf16" else sd.SD_F32
+    amode = sd.SD_ACCEPT_SAMPLED if mode == "sampled" else sd.SD_ACCEPT_GREEDY
+
+    # outputs and workspaces allocated once, outside the timed region
+    c_out = torch.empty((w.c_batch, w.c_latents, w.c_width), dtype=torch.float32, device=dev)
+    c_ws_n = sd.sd_latent_compress_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width,
+                                                  w.c_heads, dt_code)
+    c_ws = torch.empty(max(c_ws_n, 1), dtype=torch.uint8, device=dev) if c_ws_n else None
+    v_out = torch.empty((w.batch, w.block, w.hq, w.head_dim), dtype=torch.float32, device=dev)
+    v_lse = torch.empty((w.batch, w.block, w.hq), dtype=torch.float32, device=dev)
+    cap = w.kv_len if not w.paged else 16 * ver["max_pages"]
+    v_ws = torch.empty(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
+                                                   dt_code), dtype=torch.uint8, device=dev)
+    n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
+    t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
+    scale = 1.0 / math.sqrt(w.head_dim)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        sd.sd_latent_compress(lat_d, feats_d, w.c_heads, 1.0, out=c_out, workspace=c_ws)
+        if ev is not None:
+            ev[1].record()
+        sd.sd_verify_attention(q_d, k_d, v_d, kl_d, scale=scale, page_table=pt_d, out=v_out,
+                               lse=v_lse, workspace=v_ws)
+        if ev is not None:
+            ev[2].record()
+        sd.sd_spec_accept(p_d, qq_d, dr_d, u_d, amode, n_accepted=n_out, tokens=t_out)
+        if ev is not None:
+            ev[3].record()
+
+    if args.copy_calibration_mib:
+        src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    comp_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    ver_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    acc_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+
+    kv_bytes = synth.verify_kv_bytes(w, ver["kv_len"])
+    flops = synth.compress_flops(w)
+    c_bytes = synth.compress_bytes(w)
+    n_host = n_out.cpu().numpy()
+    a_bytes = accept_bytes(acc["p"], n_host)
+    t_c, t_v, t_a = float(comp_ms.mean()), float(ver_ms.mean()), float(acc_ms.mean())
+    verify_step_ms = t_v + t_a
+    value = kv_bytes / (verify_step_ms * 1e-3) / 1e12
+
+    peak_c = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_VALU_PEAK_TFLOPS
+    rl = {
+        "latent_compress": {"bound": "mfma", "achieved": flops / (t_c * 1e-3) / 1e12,
+                            "peak": peak_c, "unit": "TFLOP/s", "traffic": None,
+                            "algorithmic": flops, "us": t_c * 1e3,
+                            "hbm_gbs": c_bytes / (t_c * 1e-3) / 1e9},
+        "verify_attention": {"bound": "hbm", "achieved": kv_bytes / (t_v * 1e-3) / 1e9,
+                             "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
+                             "algorithmic": kv_bytes, "us": t_v * 1e3},
+        "spec_accept": {"bound": "hbm", "achieved": a_bytes / (t_a * 1e-3) / 1e9,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
+                        "algorithmic": a_bytes, "us": t_a * 1e3},
+    }
+    for r in rl.values():
+        r["frac"] = r["achieved"] / r["peak"]
+    dominant = max(rl, key=lambda k_: rl[k_]["us"])
+    roof = {k_: rl[dominant][k_] for k_ in ("bound", "achieved", "peak", "unit", "frac",
+                                             "traffic")}
+    roof["kernel"] = dominant
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": w.batch, "q_heads": w.hq, "kv_heads": w.hkv, "head_dim": w.head_dim,
+            "kv_len": w.kv_len, "paged": w.paged, "block_k": w.block,
+            "compress_tokens": w.c_tokens, "compress_width": w.c_width,
+            "latents": w.c_latents, "compress_heads": w.c_heads,
+            "vocab": w.vocab, "accept_mode": mode, "temperature": acc["temperature"],
+        },
+        "verify_step_us": verify_step_ms * 1e3,
+        "verify_attention_us": t_v * 1e3,
+        "spec_accept_us": t_a * 1e3,
+        "latent_compress_us": t_c * 1e3,
+        "latent_compress_tflops": rl["latent_compress"]["achieved"],
+        "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
+        "accepted_mean": float(n_host.mean()),
+        "roofline": roof,
+        "rooflines": rl,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        cb = cpu_baseline(w, comp, ver, acc,
+                          0 if mode == "greedy" else 1)
+        cpu_step = cb["verify_s"] + cb["accept_s"]
+        result["cpu_baseline"] = {
+            "value": kv_bytes / cpu_step / 1e12, "unit": "TB/s", "cores": cb["threads"],
+            "kind": "oracle", "sample": cb["sample"],
+            "verify_step_s": cpu_step, "latent_compress_s": cb["compress_s"],
+            "whole_step_s": cpu_step + cb["compress_s"],
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -20,12 +20,15 @@ the shapes of its image and video settings stand in for them:
 * paged caches: per-sequence lengths uniform in a range, 16-token pages
   with a random page permutation, padding slots and spare pages poisoned.
 
-Every tensor has its own Philox stream spawned from one seed in a fixed
-order, so changing one size does not change the other tensors' values.
+Every tensor has its own Philox streams keyed by (seed, tensor, chunk), so
+changing one size does not change the other tensors' values, and large
+tensors are drawn in parallel threads without changing any value.
 """
 
 import dataclasses
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -103,25 +106,95 @@ def workload(index_or_name):
 
 # ---------------------------------------------------------------- helpers
 
+_THREADS = max(1, min(16, os.cpu_count() or 1))
+_CHUNK = 1 << 22
+
+
+class Stream:
+    """A named, seeded source of random draws.
+
+    Scalar-sized draws come from one Philox generator keyed by
+    (seed, stream index); large normal tensors are cut into 2^22-element
+    chunks, each with its own Philox generator keyed by (seed, stream index,
+    chunk index), and filled in parallel threads.  The values depend only on
+    the seed, the stream and the shape, never on the thread count.
+    """
+
+    def __init__(self, seed, index):
+        self.seed = seed
+        self.index = index
+        self.gen = np.random.Generator(np.random.Philox(
+            np.random.SeedSequence(seed, spawn_key=(index,))))
+        self._calls = 0
+
+    def normal(self, shape):
+        """N(0, 1) float32 draws of the given shape."""
+        call = self._calls
+        self._calls += 1
+        total = int(np.prod(shape))
+        out = np.empty(total, dtype=np.float32)
+
+        def fill(job):
+            ci, s = job
+            g = np.random.Generator(np.random.Philox(
+                np.random.SeedSequence(self.seed, spawn_key=(self.index, call, ci))))
+            g.standard_normal(min(total, s + _CHUNK) - s, dtype=np.float32,
+                              out=out[s:min(total, s + _CHUNK)])
+
+        jobs = list(enumerate(range(0, total, _CHUNK)))
+        if len(jobs) > 1 and _THREADS > 1:
+            with ThreadPoolExecutor(_THREADS) as ex:
+                list(ex.map(fill, jobs))
+        else:
+            for j in jobs:
+                fill(j)
+        return out.reshape(shape)
+
+
 def streams(seed):
-    """One independent Philox generator per named tensor."""
-    children = np.random.SeedSequence(seed).spawn(len(_STREAMS))
-    return {name: np.random.Generator(np.random.Philox(child))
-            for name, child in zip(_STREAMS, children)}
+    """One independent stream per named tensor."""
+    return {name: Stream(seed, i) for i, name in enumerate(_STREAMS)}
+
+
+def _parallel_map(fn, x, out):
+    """Apply an elementwise numpy function chunk by chunk in threads."""
+    xf = x.reshape(-1)
+    of = out.reshape(-1)
+    jobs = range(0, xf.size, _CHUNK)
+
+    def run(s):
+        of[s:s + _CHUNK] = fn(xf[s:s + _CHUNK])
+
+    if xf.size > _CHUNK and _THREADS > 1:
+        with ThreadPoolExecutor(_THREADS) as ex:
+            list(ex.map(run, jobs))
+    else:
+        for s in jobs:
+            run(s)
+    return out
+
+
+def _bf16_round(x):
+    bits = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    bias = np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1))
+    return ((bits + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def _bf16_widen(bits):
+    return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32)
+            << np.uint32(16)).view(np.float32)
 
 
 def bf16_bits(x):
     """Round float32 values to bfloat16 (nearest even); returns uint16 bits."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    bits = x.view(np.uint32)
-    bias = np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1))
-    return ((bits + bias) >> np.uint32(16)).astype(np.uint16)
+    return _parallel_map(_bf16_round, x, np.empty(x.shape, np.uint16))
 
 
 def bf16_to_f32(bits):
     """Widen bfloat16 bit patterns to the float32 values they denote."""
     bits = np.ascontiguousarray(bits, dtype=np.uint16)
-    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    return _parallel_map(_bf16_widen, bits, np.empty(bits.shape, np.float32))
 
 
 class Tensor:
@@ -147,14 +220,8 @@ class Tensor:
         return self.values.shape
 
 
-def normal(rng, shape, chunk=1 << 24):
-    """N(0, 1) float32 draws, produced in chunks to bound peak memory."""
-    total = int(np.prod(shape))
-    out = np.empty(total, dtype=np.float32)
-    for s in range(0, total, chunk):
-        e = min(total, s + chunk)
-        out[s:e] = rng.standard_normal(e - s, dtype=np.float32)
-    return out.reshape(shape)
+def normal(stream, shape):
+    return stream.normal(shape)
 
 
 # ------------------------------------------------------ per-operation inputs
@@ -173,7 +240,7 @@ def kv_lengths(w, seed=None):
     rs = streams(w.seed if seed is None else seed)
     if not w.paged:
         return np.full(w.batch, w.kv_len, dtype=np.int32)
-    return rs["kv_lens"].integers(w.kv_len_min, w.kv_len + 1,
+    return rs["kv_lens"].gen.integers(w.kv_len_min, w.kv_len + 1,
                                   size=w.batch).astype(np.int32)
 
 
@@ -202,7 +269,7 @@ def verify_inputs(w, seed=None, kv_len=None, poison=POISON):
     pages = [int(math.ceil(int(L) / PAGE_SIZE)) for L in lens]
     max_pages = max(1, int(math.ceil(w.kv_len / PAGE_SIZE)))
     n_pool = sum(pages) + 64
-    perm = rs["page_perm"].permutation(n_pool).astype(np.int32)
+    perm = rs["page_perm"].gen.permutation(n_pool).astype(np.int32)
     page_table = np.zeros((B, max_pages), dtype=np.int32)
     pos = 0
     for b in range(B):
@@ -217,11 +284,13 @@ def verify_inputs(w, seed=None, kv_len=None, poison=POISON):
     vg = rs["v"]
     for b in range(B):
         L = int(lens[b])
+        kl = normal(kg, (L, Hkv, D))          # the sequence's logical cache
+        vl = normal(vg, (L, Hkv, D))
         for i in range(pages[b]):
             valid = min(PAGE_SIZE, L - i * PAGE_SIZE)
             pg = page_table[b, i]
-            kf[pg, :, :valid] = normal(kg, (valid, Hkv, D)).transpose(1, 0, 2)
-            vf[pg, :, :valid] = normal(vg, (valid, Hkv, D)).transpose(1, 0, 2)
+            kf[pg, :, :valid] = kl[i * PAGE_SIZE:i * PAGE_SIZE + valid].transpose(1, 0, 2)
+            vf[pg, :, :valid] = vl[i * PAGE_SIZE:i * PAGE_SIZE + valid].transpose(1, 0, 2)
     return {"q": q, "k_cache": Tensor(kf, w.dtype), "v_cache": Tensor(vf, w.dtype),
             "kv_len": lens, "page_table": page_table, "max_pages": max_pages,
             "lmax": 0}
@@ -253,18 +322,19 @@ def accept_inputs(w, mode, seed=None, batch=None):
         draft = np.argmax(q, axis=-1).astype(np.int32)
     else:
         draft = np.empty((B, k), dtype=np.int32)
-        du = rs["draft_uniforms"].random((B, k))
+        du = rs["draft_uniforms"].gen.random((B, k))
         for b in range(B):
             for i in range(k):
                 c = np.cumsum(q[b, i].astype(np.float64))
                 draft[b, i] = min(V - 1, int(np.searchsorted(c, du[b, i] * c[-1],
                                                              side="right")))
     # one independent uniform stream per sequence
-    seqs = np.random.SeedSequence(w.seed if seed is None else seed).spawn(
-        len(_STREAMS) + B)[len(_STREAMS):]
+    base = w.seed if seed is None else seed
+    ui = _STREAMS.index("accept_uniforms")
     u = np.empty((B, k + 1), dtype=np.float32)
     for b in range(B):
-        g = np.random.Generator(np.random.Philox(seqs[b]))
+        g = np.random.Generator(np.random.Philox(
+            np.random.SeedSequence(base, spawn_key=(ui, 1 << 20, b))))
         u[b] = (g.integers(0, 1 << 24, size=k + 1).astype(np.float64)
                 * 2.0 ** -24).astype(np.float32)
     return {"p": p, "q": q, "draft": draft, "u": u, "temperature": tau}

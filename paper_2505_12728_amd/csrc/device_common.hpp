@@ -19,6 +19,10 @@ namespace sd {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float floatx4;
+// 16 raw bytes as a native vector (HIP's uint4 is a class that register
+// promotion of arrays does not always see through)
+typedef __attribute__((__vector_size__(4 * sizeof(unsigned)))) unsigned u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(unsigned)))) unsigned u32x2;
 
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -49,25 +53,85 @@ __device__ __forceinline__ float bf16_to_float(__bf16 x) {
   return (float)x;
 }
 
+// 2^x with the hardware instruction (inputs far below -126 give 0)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // 16-byte vector of 8 bf16 values viewed as raw words
 union Pack8 {
-  uint4 u;
+  u32x4 u;
   bf16x8 b;
   f16x8 h;
   uint16_t s[8];
 };
 
+// LDS reads issued as inline asm.  The compiler does not see them as LDS
+// loads, so it never holds them back behind LDS-DMA copies it cannot prove
+// disjoint; the caller orders them with lds_wait() + tie() instead.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void*)p);
+}
+
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+
+__device__ __forceinline__ u32x2 lds_read_b64(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+
+// 8-byte transposing read: within each 16-lane group, lane i receives
+// element i % 4 of the 8-byte blocks addressed by lanes i/4, i/4 + 4,
+// i/4 + 8 and i/4 + 12 of that group.
+__device__ __forceinline__ u32x2 lds_read_tr16_b64(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+
+// Wait for every LDS operation of this wave (asm reads included).
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Make a register value depend on the preceding volatile asm (the wait), so
+// no use of it can be scheduled before the wait.
+template <typename T>
+__device__ __forceinline__ void tie(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
+// Reductions over the four lanes l, l^16, l^32, l^48 (same column c, the
+// four groups).  gfx950's v_permlane32_swap / v_permlane16_swap exchange
+// halves / odd-even rows of two registers; applied to two copies of v they
+// hand every lane its partner's value without an LDS round trip.
+__device__ __forceinline__ float partner32(float v, float* other) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  *other = __uint_as_float(r[1]);
+  return __uint_as_float(r[0]);
+}
+
+__device__ __forceinline__ float partner16(float v, float* other) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  *other = __uint_as_float(r[1]);
+  return __uint_as_float(r[0]);
+}
+
 __device__ __forceinline__ float wave_max_across_groups(float v) {
-  // reduce over lanes l, l^16, l^32, l^48 (same column, four groups)
-  v = fmaxf(v, __shfl_xor(v, 16, 64));
-  v = fmaxf(v, __shfl_xor(v, 32, 64));
-  return v;
+  float o;
+  float a = partner32(v, &o);
+  v = fmaxf(a, o);
+  a = partner16(v, &o);
+  return fmaxf(a, o);
 }
 
 __device__ __forceinline__ float wave_sum_across_groups(float v) {
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  float o;
+  float a = partner32(v, &o);
+  v = a + o;
+  a = partner16(v, &o);
+  return a + o;
 }
 
 }  // namespace sd

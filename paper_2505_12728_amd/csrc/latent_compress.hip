@@ -95,8 +95,8 @@ __global__ __launch_bounds__(NW * 64) void compress_bf16(CompressArgs a, int n_b
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
       Pack8 pk;
-      pk.u = r < a.C ? *reinterpret_cast<const uint4*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
-                     : make_uint4(0, 0, 0, 0);
+      pk.u = r < a.C ? *reinterpret_cast<const u32x4*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
+                     : u32x4{0u, 0u, 0u, 0u};
       qf[rb][dc] = pk.b;
     }
   }
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(NW * 64) void compress_bf16(CompressArgs a, int n_b
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
         Pack8 pk;
-        pk.u = *reinterpret_cast<const uint4*>(tb + tk * (DH * 2) + (((dc * 4 + G) ^ swz(tk)) * 16));
+        pk.u = *reinterpret_cast<const u32x4*>(tb + tk * (DH * 2) + (((dc * 4 + G) ^ swz(tk)) * 16));
         xf[dc] = pk.b;
       }
 #pragma unroll
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(NW * 64) void compress_bf16(CompressArgs a, int n_b
         w4[2] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v1[0] | ((uint32_t)(uint16_t)v1[1] << 16));
         w4[3] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v1[2] | ((uint32_t)(uint16_t)v1[3] << 16));
         Pack8 vt;
-        vt.u = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        vt.u = u32x4{w4[0], w4[1], w4[2], w4[3]};
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) o[rb][db] = mfma_f16(vt.h, pf[hf][rb], o[rb][db]);
       }

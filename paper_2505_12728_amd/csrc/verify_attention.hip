@@ -38,12 +38,13 @@
 namespace sd {
 namespace {
 
-constexpr int kTile = 32;       // keys per wave iteration
-constexpr int kWaves = 4;       // waves per work-group
-constexpr int kVPad = 8;        // bf16 padding per LDS row of the V tile
+constexpr int kTile = 32;       // keys per tile of the bf16 kernel
+constexpr int kWaves = 4;       // waves per work-group of the fp32 kernel
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_cvoid;
 
 // Offset (in elements) of the D-channel slice of token t, KV head hk.
 template <bool PAGED>
@@ -63,16 +64,55 @@ __device__ __forceinline__ int seq_len(const VerifyArgs& a, int b, bool paged) {
 }
 
 // ----------------------------------------------------------- bf16 split
-template <int D, int RB, bool PAGED>
-__global__ __launch_bounds__(256) void verify_split_bf16(VerifyArgs a, int keys_per_split,
-                                                         int nsplit, int row_groups,
-                                                         int rows_padded) {
-  constexpr int DC = D / 32;              // 32-channel K slices (QK^T)
-  constexpr int DB = D / 16;              // 16-channel output blocks (PV)
-  constexpr int PK = D / 8;               // 16-byte pieces per key row
-  constexpr int VSTR = D + kVPad;         // LDS row stride of V (elements)
-  constexpr int NV = kTile * PK / kWave;  // V pieces per lane per tile
-  extern __shared__ __align__(16) unsigned char smem[];
+// Wait until at most N vector-memory operations of this wave are in flight
+// (and all of its LDS operations are done), then meet the other waves.  The
+// empty asm statements keep the compiler from moving memory accesses across
+// the barrier; the barrier itself carries no fence, because a fence would
+// wait for every LDS DMA in flight (including the tiles being prefetched).
+template <int N>
+__device__ __forceinline__ void wait_vm_then_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One work-group = NW waves = NW 16-row blocks of one (sequence, KV head,
+// key split).  All waves walk the same 32-key tiles.  Tiles are copied
+// HBM -> LDS by the global_load_lds DMA (no VGPR staging) into a ring of
+// NBUF buffers, NBUF - 1 tiles ahead of the compute; with two or three
+// work-groups per compute unit about 96 KB per unit is in flight.  Each key
+// row keeps its 16-byte pieces XOR-swizzled by (key & 7), so the K-fragment
+// reads (16 keys x one piece) and the transposed V reads (4 keys x 8 bytes
+// per 16 lanes) fall on distinct banks.
+//
+// Per tile a wave does 8 + 16 matrix-core ops and little else: the causal
+// mask is applied only on the tail tile, the running maximum is raised (and
+// O, l rescaled) only when a row's scores exceed it by more than 2^8 (the
+// stale maximum is exact for the final o = O / l; p stays below 256), and
+// copy addresses are per-lane constants plus a per-tile scalar offset.
+template <int D, int NW, bool PAGED>
+__global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int keys_per_split,
+                                                             int nsplit, int row_groups,
+                                                             int rows_padded) {
+  constexpr int TK = kTile;
+  constexpr int DC = D / 32;                   // 32-channel K slices (QK^T)
+  constexpr int DB = D / 16;                   // 16-channel output blocks (PV)
+  constexpr int PK = D / 8;                    // 16-byte pieces per key row
+  constexpr int ROW_BYTES = D * 2;
+  constexpr int HALF_BYTES = TK * ROW_BYTES;   // K (or V) part of a buffer
+  constexpr int BUF_BYTES = 2 * HALF_BYTES;
+  constexpr int DMA_PER_HALF = TK * PK / 64;   // 64-lane copies per K (or V) tile
+  constexpr int DMA_PER_WAVE = 2 * DMA_PER_HALF / NW;
+  static_assert((2 * DMA_PER_HALF) % NW == 0, "tile copy must split evenly");
+  static_assert(TK == 32, "one P V step per tile");
+  // ring depth: NBUF - 1 tiles in flight; two (NW = 4) or three (NW < 4)
+  // work-groups share a compute unit, so every SIMD runs two or more waves
+  constexpr int NBUF = (NW == 4) ? 4 : 3;
+  static_assert((NBUF - 2) * DMA_PER_WAVE < 64, "vmcnt range");
+  constexpr float kRescale = 8.f;              // log2 headroom before rescaling
+  __shared__ __align__(16) unsigned char ring[NBUF][BUF_BYTES];
 
   const int split = blockIdx.x;
   const int hk = blockIdx.y / row_groups;
@@ -80,260 +120,270 @@ __global__ __launch_bounds__(256) void verify_split_bf16(VerifyArgs a, int keys_
   const int b = blockIdx.z;
   const int L = seq_len(a, b, PAGED);
   const int k0 = split * keys_per_split;
-  if (k0 >= L) return;                    // the merge skips empty splits
-  const int k1 = min(L, k0 + keys_per_split);
-
   const int tid = threadIdx.x;
   const int w = tid >> 6, lane = tid & 63, G = lane >> 4, c = lane & 15;
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
-  const int row0 = rg * RB * 16;
+  const int rblk = rg * NW * 16 + w * 16;      // this wave's first row
+  if (k0 >= L) {
+    // empty split: the merge skips it; with a single split (nothing to
+    // merge) this work-group writes its rows directly: o = 0, lse = -inf
+    if (nsplit == 1 && split == 0 && rblk + c < R) {
+      const int r = rblk + c;
+      const int j = r / g;
+      const int orow = (b * a.k + j) * a.Hq + hk * g + (r - j * g);
+      for (int d4 = G; d4 < D / 4; d4 += 4)
+        *reinterpret_cast<floatx4*>(a.out + (size_t)orow * D + d4 * 4) = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (a.lse != nullptr && G == 0) a.lse[orow] = -INFINITY;
+    }
+    return;
+  }
+  const int k1 = min(L, k0 + keys_per_split);
+  // a wave whose rows are all padding (R not a multiple of 16 * NW) runs the
+  // same loop on zero queries and writes nothing
+  const bool active = rblk < R;                // wave-uniform
 
-  // This lane's query rows: row row0 + rb*16 + c, block position j = row / g,
-  // query head hk * g + row % g.  B operand of S^T = K Q^T.
-  bf16x8 qf[RB][DC];
-  int lim[RB];
+  // This lane's query row r = rblk + c: block position j = r / g, query head
+  // hk * g + r % g.  B operand of S^T = K Q^T.
+  bf16x8 qf[DC];
+  int lim = -1;
+  int orow = -1;
+  {
+    const int r = rblk + c;
+    Pack8 pk;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = row0 + rb * 16 + c;
+    for (int dc = 0; dc < DC; ++dc) {
+      pk.u = u32x4{0u, 0u, 0u, 0u};
+      qf[dc] = pk.b;
+    }
     if (r < R) {
       const int j = r / g;
       const int h = hk * g + (r - j * g);
-      const uint4* src = reinterpret_cast<const uint4*>(
-          static_cast<const uint16_t*>(a.q) + (((size_t)b * a.k + j) * a.Hq + h) * D);
+      orow = (b * a.k + j) * a.Hq + h;
+      const u32x4* src = reinterpret_cast<const u32x4*>(
+          static_cast<const uint16_t*>(a.q) + (size_t)orow * D);
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
-        Pack8 pk;
         pk.u = src[dc * 4 + G];
-        qf[rb][dc] = pk.b;
+        qf[dc] = pk.b;
       }
-      lim[rb] = L - a.k + j;              // last visible key of this row
-    } else {
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) {
-        Pack8 pk;
-        pk.u = make_uint4(0, 0, 0, 0);
-        qf[rb][dc] = pk.b;
-      }
-      lim[rb] = -1;
+      lim = L - a.k + j;                       // last visible key of this row
     }
   }
+  // every row sees keys 0 .. L - k; tiles ending there need no mask
+  const int unmasked_end = L - a.k;
 
-  float m[RB], l[RB];
-  floatx4 o[RB][DB];
+  float m = -INFINITY, l = 0.f;
+  floatx4 o[DB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = -INFINITY;
-    l[rb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[rb][db] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  uint16_t* vs = reinterpret_cast<uint16_t*>(smem) + w * kTile * VSTR;
   const uint16_t* kbase = static_cast<const uint16_t*>(a.kc);
   const uint16_t* vbase = static_cast<const uint16_t*>(a.vc);
-  const int ntiles = (k1 - k0 + kTile - 1) / kTile;
+  const int ntiles = (k1 - k0 + TK - 1) / TK;
+  const int last = ntiles - 1;
 
-  // register prefetch of one tile ahead
-  uint4 kn[2][DC];
-  uint4 vn[NV];
-  auto load_tile = [&](int tile) {
-    const int t0 = k0 + tile * kTile;
+  // Copy i of this wave (ii = w * DMA_PER_WAVE + i) covers half
+  // ii / DMA_PER_HALF (K or V) and pieces P = (ii % DMA_PER_HALF) * 64 +
+  // lane: key P / PK, LDS slot P % PK holding global piece slot ^ (key & 7).
+  // Its source is a per-lane constant plus a per-tile offset, except in the
+  // tail tile, where keys past the sequence re-read its last key (masked).
+  // Page ids are scalar loads, so they do not count against vmcnt.
+  size_t cbase[DMA_PER_WAVE];
+  int ckey[DMA_PER_WAVE];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int t = min(t0 + kb * 16 + c, L - 1);
-      const uint4* src = reinterpret_cast<const uint4*>(kbase + kv_offset<PAGED>(a, b, hk, t, D));
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) kn[kb][dc] = src[dc * 4 + G];
+  for (int i = 0; i < DMA_PER_WAVE; ++i) {
+    const int ii = w * DMA_PER_WAVE + i;
+    const int P = (ii % DMA_PER_HALF) * 64 + lane;
+    const int key = P / PK, piece = P % PK;
+    ckey[i] = key;
+    const size_t pieceoff = (size_t)((piece ^ (key & 7)) * 8);
+    if constexpr (PAGED)
+      cbase[i] = (((size_t)hk * 16 + (key & 15)) * D) + pieceoff;
+    else
+      cbase[i] = (((size_t)b * a.Lmax + k0 + key) * a.Hkv + hk) * (size_t)D + pieceoff;
+  }
+  const size_t tile_stride = (size_t)TK * a.Hkv * D;   // contiguous: elements per tile
+  auto issue = [&](int tile, unsigned char* slot) {
+    const int t0 = k0 + tile * TK;
+    const bool tail = t0 + TK > L;
+    int pg0 = 0, pg1 = 0;
+    if constexpr (PAGED) {
+      // the page table is read-only here: constant-space loads become
+      // scalar loads, which leave the vector-memory counter to the copies
+      const __attribute__((address_space(4))) int32_t* pt =
+          (const __attribute__((address_space(4))) int32_t*)(a.page_table + (size_t)b * a.max_pages);
+      const int lastp = (L - 1) >> 4;
+      pg0 = min(max((int)pt[min(t0 >> 4, lastp)], 0), a.num_pages - 1);
+      pg1 = min(max((int)pt[min((t0 >> 4) + 1, lastp)], 0), a.num_pages - 1);
     }
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int p = lane + kWave * i;
-      const int t = min(t0 + p / PK, L - 1);
-      vn[i] = reinterpret_cast<const uint4*>(vbase + kv_offset<PAGED>(a, b, hk, t, D))[p % PK];
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const int ii = w * DMA_PER_WAVE + i;
+      const int half = ii / DMA_PER_HALF;
+      size_t off;
+      if constexpr (PAGED) {
+        int key = ckey[i];
+        size_t base = cbase[i];
+        if (tail && t0 + key > L - 1) {        // re-read the last key
+          const int t = L - 1;
+          key = t - t0;
+          base = (((size_t)hk * 16 + (t & 15)) * D) + (cbase[i] & (size_t)(PK * 8 - 1));
+        }
+        const int pg = key < 16 ? pg0 : pg1;
+        off = base + (size_t)pg * a.Hkv * 16 * D;
+      } else {
+        off = cbase[i] + (size_t)tile * tile_stride;
+        if (tail && t0 + ckey[i] > L - 1)      // re-read the last key
+          off -= (size_t)(t0 + ckey[i] - (L - 1)) * a.Hkv * D;
+      }
+      __builtin_amdgcn_global_load_lds((gbl_cvoid*)((half ? vbase : kbase) + off),
+                                       (lds_void*)(slot + half * HALF_BYTES + (ii % DMA_PER_HALF) * 1024),
+                                       16, 0, 0);
     }
   };
 
-  if (w < ntiles) load_tile(w);
-  for (int tile = w; tile < ntiles; tile += kWaves) {
-    const int t0 = k0 + tile * kTile;
-    bf16x8 kf[2][DC];
+  // per-lane LDS offsets of the fragment reads inside a buffer
+  uint32_t koff[2][DC];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc) {
+      const int key = kb * 16 + c;
+      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G) ^ (key & 7)) * 16);
+    }
+  // ds_read_tr16_b64: lane j of group G addresses key 4G + j/4 (+16) at
+  // channels db*16 + 4*(j%4); lane c then receives 4 keys at channel db*16 + c
+  uint32_t voff[2][DB];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int key = hh * 16 + 4 * G + (c >> 2);
+      const int ch = db * 16 + 4 * (c & 3);
+      voff[hh][db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ (key & 7)) * 16) + (ch & 7) * 2;
+    }
+
+  auto compute = [&](int it, const unsigned char* slot) {
+    const uint32_t sb = lds_addr(slot);
+    const int t0 = k0 + it * TK;
+
+    u32x4 kr[2][DC];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) kr[kb][dc] = lds_read_b128(sb + koff[kb][dc]);
+    lds_wait();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) tie(kr[kb][dc]);
+    // V^T fragments for P V, issued now so they overlap the scores
+    u32x2 vr[2][DB];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) vr[hh][db] = lds_read_tr16_b64(sb + voff[hh][db]);
+
+    // S^T = K Q^T: lane holds S[row c][key t0 + kb*16 + 4G + i] (log2 units)
+    float x[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
         Pack8 pk;
-        pk.u = kn[kb][dc];
-        kf[kb][dc] = pk.b;
+        pk.u = kr[kb][dc];
+        acc = mfma_bf16(pk.b, qf[dc], acc);
       }
-    // stage V in this wave's LDS slice, row-major [key][channel]
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int p = lane + kWave * i;
-      *reinterpret_cast<uint4*>(vs + (p / PK) * VSTR + (p % PK) * 8) = vn[i];
+      for (int i = 0; i < 4; ++i) x[kb * 4 + i] = acc[i] * a.scale_log2;
     }
-    if (tile + kWaves < ntiles) load_tile(tile + kWaves);
-
-    // S^T = K Q^T: lane holds S[row rb*16 + c][key t0 + kb*16 + 4G + i]
-    floatx4 s[2][RB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int dc = 0; dc < DC; ++dc) acc = mfma_bf16(kf[kb][dc], qf[rb][dc], acc);
-        s[kb][rb] = acc;
-      }
-
-    // online softmax, one row per lane and row block
-    bf16x8 ph[RB], pl[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      float x[8];
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = t0 + kb * 16 + 4 * G + i;
-          const float v = (t <= lim[rb]) ? s[kb][rb][i] * a.scale_log2 : -INFINITY;
-          x[kb * 4 + i] = v;
-          tmax = fmaxf(tmax, v);
-        }
-      tmax = wave_max_across_groups(tmax);
-      const float mnew = fmaxf(m[rb], tmax);
-      float alpha = 1.f;
-      if (mnew == -INFINITY) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = 0.f;
-      } else {
-        alpha = exp2f(m[rb] - mnew);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = exp2f(x[e] - mnew);
-      }
-      m[rb] = mnew;
-      float psum = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) psum += x[e];
-      l[rb] = l[rb] * alpha + psum;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+    if (t0 + TK - 1 > unmasked_end) {          // tail tile: causal mask
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const __bf16 hi = float_to_bf16(x[e]);
-        ph[rb][e] = hi;
-        pl[rb][e] = float_to_bf16(x[e] - bf16_to_float(hi));
+        const int t = t0 + (e >> 2) * 16 + 4 * G + (e & 3);
+        if (t > lim) x[e] = -INFINITY;
       }
     }
 
-    // LDS writes of this wave must land before its lanes read them back
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // online softmax with a lazily raised maximum
+    float tmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                       fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    tmax = wave_max_across_groups(tmax);
+    if (__ballot(tmax > m + kRescale) != 0ull) {
+      const float mnew = fmaxf(m, tmax);
+      const float alpha = (mnew == -INFINITY) ? 1.f : fast_exp2(m - mnew);
+      l *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+      m = mnew;
+    }
+    bf16x8 ph, pl;
+    float psum = 0.f;
+    const bool none = m == -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pv = none ? 0.f : fast_exp2(x[e] - m);
+      psum += pv;
+      const __bf16 hi = float_to_bf16(pv);
+      ph[e] = hi;
+      pl[e] = float_to_bf16(pv - bf16_to_float(hi));
+    }
+    l += psum;
 
-    // O^T += V^T P^T.  K index of the product = keys {4G..4G+3, 16+4G..16+4G+3},
-    // the same order in which the accumulator handed this lane its P values.
-    // ds_read_tr16_b64: lane j of group G addresses key 4G + j/4 (+16) at
-    // channels db*16 + 4*(j%4); lane c then receives 4 keys at channel db*16 + c.
-    const int key_a = 4 * G + (c >> 2);
+    // O^T += V^T P^T.  The product's K index runs over keys {4G..4G+3,
+    // 16+4G..16+4G+3}, the order in which the score accumulator handed this
+    // lane its P values; accumulator element i of block db is channel
+    // db*16 + 4G + i of row c.
+    lds_wait();
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) tie(vr[hh][db]);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int ch = db * 16 + 4 * (c & 3);
-      const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_shortx4*)((__attribute__((address_space(3))) uint16_t*)(vs + key_a * VSTR + ch)));
-      const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_shortx4*)((__attribute__((address_space(3))) uint16_t*)(vs + (key_a + 16) * VSTR + ch)));
-      Pack8 vt;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt.s[e] = (uint16_t)v0[e];
-        vt.s[4 + e] = (uint16_t)v1[e];
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        o[rb][db] = mfma_bf16(vt.b, ph[rb], o[rb][db]);
-        o[rb][db] = mfma_bf16(vt.b, pl[rb], o[rb][db]);
-      }
+      Pack8 vv;
+      vv.u = u32x4{vr[0][db][0], vr[0][db][1], vr[1][db][0], vr[1][db][1]};
+      o[db] = mfma_bf16(vv.b, ph, o[db]);
+      o[db] = mfma_bf16(vv.b, pl, o[db]);
     }
-  }
+  };
 
-  // ---- merge the 4 waves of this work-group (fixed order, no atomics)
-  float* sm = reinterpret_cast<float*>(smem);
-  float* sm_m = sm;                        // [4][RB*16]
-  float* sm_l = sm + kWaves * RB * 16;     // [4][RB*16]
-  float* ob = sm + 2 * kWaves * RB * 16;   // [RB*16][D + 4]
-  constexpr int OSTR = D + 4;
-  __syncthreads();                         // all waves are done with V tiles
+  // Every step issues one tile (past the end it re-reads the last one, which
+  // is still cached), so exactly (NBUF - 2) * DMA_PER_WAVE newer copies are
+  // in flight at each wait and the wait covers precisely the tile about to
+  // be read.  The tile reads are asm, so the compiler adds no waits of its
+  // own between them and the copies.
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    l[rb] = wave_sum_across_groups(l[rb]);
-    if (G == 0) {
-      sm_m[w * RB * 16 + rb * 16 + c] = m[rb];
-      sm_l[w * RB * 16 + rb * 16 + c] = l[rb];
-    }
+  for (int i = 0; i < NBUF - 1; ++i) issue(min(i, last), ring[i]);
+  for (int it = 0; it < ntiles; ++it) {
+    wait_vm_then_barrier<(NBUF - 2) * DMA_PER_WAVE>();   // tile it landed; slot it-1 free
+    issue(min(it + NBUF - 1, last), ring[(it + NBUF - 1) % NBUF]);
+    compute(it, ring[it % NBUF]);
   }
-  __syncthreads();
-  float ltot[RB], mtot[RB];
+  // no copy may still be writing this work-group's LDS when it exits
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
+  if (!active) return;
+
+  l = wave_sum_across_groups(l);
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  auto store_row = [&](float* dst) {
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) mx = fmaxf(mx, sm_m[ww * RB * 16 + rb * 16 + c]);
-    float lt = 0.f;
-    if (mx != -INFINITY) {
-#pragma unroll
-      for (int ww = 0; ww < kWaves; ++ww)
-        lt += sm_l[ww * RB * 16 + rb * 16 + c] * exp2f(sm_m[ww * RB * 16 + rb * 16 + c] - mx);
-    }
-    const float f = (mx == -INFINITY) ? 0.f : exp2f(m[rb] - mx);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[rb][db] *= f;
-    mtot[rb] = mx;
-    ltot[rb] = lt;
-  }
-  auto store_o = [&]() {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<floatx4*>(ob + (rb * 16 + c) * OSTR + db * 16 + 4 * G) = o[rb][db];
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[db] * inv;
   };
-  auto add_o = [&]() {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        o[rb][db] += *reinterpret_cast<const floatx4*>(ob + (rb * 16 + c) * OSTR + db * 16 + 4 * G);
-  };
-  // one staging buffer, fixed order: (O0 + O1) + (O2 + O3)
-  if (w == 1) store_o();
-  __syncthreads();
-  if (w == 0) add_o();
-  __syncthreads();
-  if (w == 3) store_o();
-  __syncthreads();
-  if (w == 2) add_o();
-  __syncthreads();
-  if (w == 2) store_o();
-  __syncthreads();
-  if (w == 0) {
-    add_o();
-    const size_t base = ((size_t)(b * a.Hkv + hk) * nsplit + split) * rows_padded + row0;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const float inv = ltot[rb] > 0.f ? 1.f / ltot[rb] : 0.f;
-      float* dst = a.part_o + (base + rb * 16 + c) * D;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        floatx4 v = o[rb][db] * inv;
-        *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = v;
-      }
-      if (G == 0)
-        a.part_lse[base + rb * 16 + c] =
-            ltot[rb] > 0.f ? mtot[rb] + log2f(ltot[rb]) : -INFINITY;
+  if (nsplit == 1) {
+    if (orow >= 0) {
+      store_row(a.out + (size_t)orow * D);
+      if (a.lse != nullptr && G == 0)
+        a.lse[orow] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
     }
+    return;
   }
+  const size_t prow = ((size_t)(b * a.Hkv + hk) * nsplit + split) * rows_padded + rblk + c;
+  store_row(a.part_o + prow * D);
+  if (G == 0) a.part_lse[prow] = l > 0.f ? m + log2f(l) : -INFINITY;
 }
 
 // ----------------------------------------------------------- fp32 split
@@ -421,52 +471,54 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 }
 
 // ---------------------------------------------------------------- merge
-// One work-group per (sequence, KV head); threads over (row, 4 channels).
+// One wave per output row of one (sequence, KV head): the lanes find the
+// largest split lse, then lanes d4 < D/4 accumulate the weighted partial
+// outputs (4 channels each).  Grid (rows / 4, sequence x KV head).
 __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_split,
                                                     int nsplit, int rows_padded, int paged) {
-  const int hk = blockIdx.x;
-  const int b = blockIdx.y;
+  const int pair = blockIdx.y;
+  const int hk = pair % a.Hkv;
+  const int b = pair / a.Hkv;
   const int D = a.D;
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + w;
+  if (r >= R) return;
   const int L = seq_len(a, b, paged != 0);
   const int nvalid = min(nsplit, (L + keys_per_split - 1) / keys_per_split);
-  const size_t base = (size_t)(b * a.Hkv + hk) * nsplit * rows_padded;
-  const int D4 = D / 4;
-  for (int i = threadIdx.x; i < R * D4; i += blockDim.x) {
-    const int r = i / D4, d4 = i % D4;
-    float mx = -INFINITY;
-    for (int s = 0; s < nvalid; ++s) mx = fmaxf(mx, a.part_lse[base + (size_t)s * rows_padded + r]);
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;
-    if (mx != -INFINITY) {
-      for (int s = 0; s < nvalid; ++s) {
-        const size_t pr = base + (size_t)s * rows_padded + r;
-        const float ls = a.part_lse[pr];
-        if (ls == -INFINITY) continue;
-        const float wgt = exp2f(ls - mx);
-        wsum += wgt;
+  const size_t base = (size_t)pair * nsplit * rows_padded + r;
+  float mx = -INFINITY;
+  for (int s = lane; s < nvalid; s += 64) mx = fmaxf(mx, a.part_lse[base + (size_t)s * rows_padded]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  const int d4 = lane;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  if (mx != -INFINITY) {
+#pragma unroll 4
+    for (int s = 0; s < nvalid; ++s) {
+      const size_t pr = base + (size_t)s * rows_padded;
+      const float ls = a.part_lse[pr];
+      const float wgt = ls == -INFINITY ? 0.f : exp2f(ls - mx);
+      wsum += wgt;
+      if (d4 < D / 4 && wgt != 0.f)
         acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
-      }
     }
-    const int j = r / g;
-    const int h = hk * g + (r - j * g);
-    const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
-    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
-    if (a.lse != nullptr && d4 == 0)
-      a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
   }
+  const int j = r / g;
+  const int h = hk * g + (r - j * g);
+  const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  if (d4 < D / 4) *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
+  if (a.lse != nullptr && lane == 0)
+    a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
 }
 
-template <int D, int RB, bool PAGED>
+template <int D, int NW, bool PAGED>
 hipError_t launch_bf16(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
-  constexpr int VSTR = D + kVPad;
-  const size_t v_bytes = (size_t)kWaves * kTile * VSTR * 2;
-  const size_t m_bytes = (size_t)(2 * kWaves * RB * 16 + RB * 16 * (D + 4)) * 4;
-  const size_t lds = std::max(v_bytes, m_bytes);
   dim3 grid(p.nsplit, a.Hkv * p.row_groups, a.B);
-  hipLaunchKernelGGL((verify_split_bf16<D, RB, PAGED>), grid, dim3(256), lds, st, a,
+  hipLaunchKernelGGL((verify_split_bf16<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, a,
                      p.keys_per_split, p.nsplit, p.row_groups, p.rows_padded);
   return hipGetLastError();
 }
@@ -476,7 +528,6 @@ hipError_t dispatch_rb(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st)
   switch (p.row_blocks) {
     case 1: return launch_bf16<D, 1, PAGED>(a, p, st);
     case 2: return launch_bf16<D, 2, PAGED>(a, p, st);
-    case 3: return launch_bf16<D, 3, PAGED>(a, p, st);
     default: return launch_bf16<D, 4, PAGED>(a, p, st);
   }
 }
@@ -498,16 +549,19 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     int kps = ((65536 - 4 * p.rows * D - 16 * p.rows) / (8 * std::max(p.rows, 1))) / 32 * 32;
     p.keys_per_split = std::max(32, std::min(1024, kps));
   } else {
-    p.row_blocks = std::min(4, blocks16);
+    // one wave per 16-row block, 1, 2 or 4 waves per work-group
+    p.row_blocks = blocks16 <= 1 ? 1 : (blocks16 == 2 ? 2 : 4);
     p.row_groups = (blocks16 + p.row_blocks - 1) / p.row_blocks;
     p.rows_padded = p.row_groups * p.row_blocks * 16;
-    // Enough work-groups to fill 256 compute units about twice, with at
-    // least 128 keys (one tile per wave) per split.
+    // A work-group holds a 64 KB (4 waves) or 48 KB (1-2 waves) LDS ring,
+    // so two or three run per compute unit.  Aim for that many work-groups
+    // per unit on 256 units, all resident at once; at least one 32-key tile
+    // per split.
     const long long pairs = (long long)B * Hkv * p.row_groups;
-    const long long target = 512;
+    const long long target = p.row_blocks == 4 ? 512 : 768;
     long long nsplit = std::max(1LL, (target + pairs - 1) / pairs);
     long long kps = (capacity + nsplit - 1) / nsplit;
-    kps = std::max(128LL, (kps + 127) / 128 * 128);
+    kps = std::max((long long)kTile, (kps + kTile - 1) / kTile * kTile);
     p.keys_per_split = (int)kps;
   }
   p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
@@ -535,8 +589,9 @@ hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hi
     e = paged ? dispatch_rb<64, true>(a, p, st) : dispatch_rb<64, false>(a, p, st);
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(verify_merge, dim3(a.Hkv, a.B), dim3(256), 0, st, a, p.keys_per_split,
-                     p.nsplit, p.rows_padded, paged ? 1 : 0);
+  if (dtype != 0 && p.nsplit == 1) return hipSuccess;   // the split kernel wrote out / lse
+  hipLaunchKernelGGL(verify_merge, dim3((p.rows + 3) / 4, a.Hkv * a.B), dim3(256), 0, st, a,
+                     p.keys_per_split, p.nsplit, p.rows_padded, paged ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -159,6 +159,8 @@ def main():
     cap = w.kv_len if not w.paged else 16 * ver["max_pages"]
     v_ws = torch.empty(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
                                                    dt_code), dtype=torch.uint8, device=dev)
+    a_ws = torch.empty(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
+                       dtype=torch.uint8, device=dev)
     n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
     scale = 1.0 / math.sqrt(w.head_dim)
@@ -173,7 +175,8 @@ def main():
                                lse=v_lse, workspace=v_ws)
         if ev is not None:
             ev[2].record()
-        sd.sd_spec_accept(p_d, qq_d, dr_d, u_d, amode, n_accepted=n_out, tokens=t_out)
+        sd.sd_spec_accept(p_d, qq_d, dr_d, u_d, amode, n_accepted=n_out, tokens=t_out,
+                          workspace=a_ws)
         if ev is not None:
             ev[3].record()
 

@@ -167,7 +167,10 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
  *   n_accepted  [B]         int32    out: accepted drafts per sequence
  *   tokens      [B, k+1]    int32    out: draft[0..n-1], the extra token,
  *                                    then -1 padding
- * Requirements: B >= 1; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1].
+ *   workspace   sd_spec_accept_workspace_size(B, k, V, mode) bytes
+ *               (per-chunk partial sums or maxima of the vocabulary pass)
+ * Requirements: B >= 1; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1]
+ * (values outside are clamped when forming the weights).
  * ---------------------------------------------------------------------- */
 size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode);
 

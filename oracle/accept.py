@@ -32,7 +32,8 @@ Readings (the paper does not spell these out):
   p_k (the "bonus" token) when every draft is accepted.  The output always
   holds n + 1 tokens; unused slots are -1.
 * Residual weights in fixed point: r_v = max(0, p_n(v) - q_n(v)) in float32
-  (round to nearest even), R_v = floor(r_v * 2^40) as an unsigned integer.
+  (round to nearest even), R_v = floor(r_v * 2^40) as an unsigned integer;
+  r is clamped to [0, 1] (only invalid inputs reach the clamp).
   Values below 2^-40 weigh nothing, so flushing denormals cannot change the
   result.  S = sum_v R_v is exact for probabilities in [0, 1] and V <= 2^18.
 * Inverse CDF: T = floor(a * S / 2^24); the token is the smallest j whose
@@ -75,10 +76,9 @@ def residual_weights(p_row, q_row=None):
         r = p_row
     else:
         r = np.maximum(np.float32(0.0), p_row - np.asarray(q_row, dtype=np.float32))
-    r = np.maximum(r, np.float32(0.0))
+    # probabilities lie in [0, 1]; values outside (invalid input) are clamped
+    r = np.minimum(np.maximum(r, np.float32(0.0)), np.float32(1.0))
     scaled = np.floor(r.astype(np.float64) * float(2 ** FIXED_POINT_BITS))
-    if np.any(scaled >= 2.0 ** 63):
-        raise ValueError("probabilities must lie in [0, 1]")
     return scaled.astype(np.uint64)
 
 

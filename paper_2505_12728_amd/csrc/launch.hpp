@@ -78,6 +78,7 @@ struct AcceptArgs {
   int B, k, V, mode;
 };
 
-hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+size_t accept_workspace_bytes(int B, int k, int V, int mode);
+hipError_t launch_accept(const AcceptArgs& a, void* workspace, hipStream_t s);
 
 }  // namespace sd

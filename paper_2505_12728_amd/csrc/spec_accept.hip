@@ -1,24 +1,26 @@
 // Speculative acceptance with residual resampling (SpecFLASH Sec. 3.1 and
 // Sec. 3.3; greedy verification at temperature 0, Sec. 4.2).
 //
-// One 1024-thread work-group per sequence.  The vocabulary is cut into 16
-// contiguous segments, one per wave; inside a segment the 64 lanes read
-// consecutive entries, so every pass is a coalesced stream.
+// Two kernels, so that the vocabulary passes use the whole chip:
 //
-// Sampled mode
-//   1. the k acceptance tests u_i q_i(x_i) < p_i(x_i) are exact float64
-//      products of 24-bit significands; a ballot over the first k lanes and
-//      a count of trailing ones give n;
-//   2. fixed-point weights R_v = floor(r_v 2^40) of the residual
-//      r = max(0, p_n - q_n) (one float32 subtraction) or of p_k;
-//      per-wave uint64 sums, then the total S (exact: no rounding, so the
-//      order of the additions does not matter);
-//   3. T = floor(a S / 2^24) from the 24-bit uniform a = u_k 2^24, formed as
-//      a (S >> 24) + ((a (S mod 2^24)) >> 24) without overflow;
-//   4. the wave whose segment holds T rescans it with 64-wide inclusive
-//      prefix sums and the first lane whose prefix exceeds T names the token.
-// Greedy mode: a block-wide (value, lowest index) argmax per target row,
-// row by row until the first draft that differs.
+// 1. chunk pass, grid (vocabulary chunk, sequence), 256 threads.
+//    Sampled mode: every work-group of a sequence repeats the k acceptance
+//    tests u_i q_i(x_i) < p_i(x_i) (exact float64 products of 24-bit
+//    significands; a ballot and a count of trailing ones give n), then sums
+//    over its chunk the fixed-point weights of the row that will be sampled,
+//    R_v = floor(r_v 2^40) with r = max(0, p_n - q_n) (one float32
+//    subtraction) or r = p_k, and the fallback weights floor(p_n 2^40).
+//    Integer sums are exact, so the order of additions does not matter.
+//    Greedy mode: the (value, lowest index) maximum of every target row
+//    over the chunk.
+// 2. finish pass, one work-group per sequence, one thread per chunk.
+//    Sampled: a block prefix sum of the chunk sums gives S and each chunk's
+//    starting offset; T = floor(a S / 2^24) from a = u_k 2^24 (formed as
+//    a (S >> 24) + ((a (S mod 2^24)) >> 24) without overflow) picks the
+//    chunk, and inside it the first entry whose inclusive prefix sum
+//    exceeds T (64-wide wave prefix sums).  Greedy: argmax per row from the
+//    chunk maxima, then the longest matching prefix.
+// Every vocabulary access is a coalesced stream.
 #include <math.h>
 
 #include "device_common.hpp"
@@ -27,8 +29,9 @@
 namespace sd {
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kChunk = 1024;     // vocabulary entries per chunk (<= 256 chunks for V <= 2^18)
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
   const uint32_t lo = __shfl_xor((uint32_t)v, m, 64);
@@ -48,198 +51,263 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
-// floor(r * 2^40) for r in [0, 1]: the scaling is exact in float32 and the
-// conversion truncates.
+// floor(r * 2^40) for r in [0, 1] (clamped there): the scaling is exact in
+// float32 and the conversion truncates.
 __device__ __forceinline__ uint64_t fixed_weight(float r) {
+  r = fminf(fmaxf(r, 0.0f), 1.0f);
   const float s = r * 1099511627776.0f;   // 2^40
   return s >= 1.0f ? (uint64_t)s : 0ull;
 }
 
-// Weight of entry v of the row being sampled.
-// mode 0: max(0, p - q); mode 1: p alone.
-__device__ __forceinline__ uint64_t weight_at(const float* prow, const float* qrow, int v,
-                                              int use_q) {
+// Sampled weight of entry v: residual (use_q) or p alone.
+__device__ __forceinline__ uint64_t weight_at(const float* prow, const float* qrow, int v, int use_q) {
   float r = prow[v];
   if (use_q) r = fmaxf(0.0f, r - qrow[v]);
-  r = fmaxf(r, 0.0f);
   return fixed_weight(r);
 }
 
-struct Segment {
-  int begin, end;
-};
-
-__device__ __forceinline__ Segment wave_segment(int w, int V) {
-  const int per = ((V + kWaves - 1) / kWaves + 63) / 64 * 64;
-  Segment s;
-  s.begin = min(V, w * per);
-  s.end = min(V, s.begin + per);
-  return s;
-}
-
-// Exact total of the row's weights; per-wave totals land in wsum[].
-__device__ uint64_t weight_total(const float* prow, const float* qrow, int use_q, int V,
-                                 uint64_t* wsum) {
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const Segment sg = wave_segment(w, V);
-  uint64_t acc = 0;
-  int v = sg.begin + lane;
-#pragma unroll 4
-  for (; v < sg.end; v += 64) acc += weight_at(prow, qrow, v, use_q);
-  acc = wave_sum_u64(acc);
-  if (lane == 0) wsum[w] = acc;
-  __syncthreads();
-  uint64_t total = 0;
-#pragma unroll
-  for (int i = 0; i < kWaves; ++i) total += wsum[i];
-  return total;
-}
-
-// Smallest j with sum_{v<=j} R_v > T (requires T < total).
-__device__ int find_token(const float* prow, const float* qrow, int use_q, int V,
-                          const uint64_t* wsum, uint64_t T, int* result) {
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  uint64_t before = 0;
-  for (int i = 0; i < w; ++i) before += wsum[i];
-  if (wsum[w] != 0 && before <= T && T < before + wsum[w]) {
-    const Segment sg = wave_segment(w, V);
-    uint64_t running = before;
-    for (int v0 = sg.begin; v0 < sg.end; v0 += 64) {
-      const int v = v0 + lane;
-      uint64_t x = v < sg.end ? weight_at(prow, qrow, v, use_q) : 0ull;
-      // inclusive 64-lane prefix sum
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint64_t y = shfl_up_u64(x, d);
-        if (lane >= d) x += y;
+// n for one sequence: leading accepted drafts.  Uses lanes 0..63 of wave 0;
+// the result is returned to every thread through `slot`.
+__device__ int accepted_prefix(const AcceptArgs& a, int b, int* slot) {
+  const int k = a.k, V = a.V;
+  if (threadIdx.x < 64) {
+    const int i = threadIdx.x;
+    bool acc = false;
+    if (i < k) {
+      const int x = a.draft[(size_t)b * k + i];
+      if (x >= 0 && x < V) {
+        const double pu = (double)a.u[(size_t)b * (k + 1) + i] *
+                          (double)a.q[((size_t)b * k + i) * V + x];
+        acc = pu < (double)a.p[((size_t)b * (k + 1) + i) * V + x];
       }
-      const bool hit = running + x > T;
-      const uint64_t mask = __ballot(hit);
-      if (mask != 0ull) {
-        if (lane == 0) *result = v0 + __builtin_ctzll(mask);
-        break;
-      }
-      running += __shfl(x, 63, 64);
     }
+    // bit i set where position i rejects; position k always "rejects"
+    const uint64_t rej = __ballot(!acc) | (1ull << k);
+    if (i == 0) *slot = __builtin_ctzll(rej);
   }
   __syncthreads();
-  return *result;
+  return *slot;
 }
 
-// argmax over a row of float32 values, lowest index on ties.
-__device__ int block_argmax(const float* row, int V, float* sval, int* sidx) {
+struct ArgMax {
+  float v;
+  int i;
+};
+
+__device__ __forceinline__ ArgMax better(ArgMax x, ArgMax y) {
+  // larger value wins; equal values: lower index wins; i < 0 means empty
+  if (y.i < 0) return x;
+  if (x.i < 0) return y;
+  if (y.v > x.v || (y.v == x.v && y.i < x.i)) return y;
+  return x;
+}
+
+__device__ ArgMax block_argmax_range(const float* row, int v0, int v1, ArgMax* sm) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float best = -INFINITY;
-  int bi = 0x7fffffff;
-  for (int v = threadIdx.x; v < V; v += kThreads) {
+  ArgMax best{-INFINITY, -1};
+  for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
     const float x = row[v];
-    if (x > best || bi == 0x7fffffff) {   // indices increase, so ties keep the first
-      best = x;
-      bi = v;
-    }
+    if (best.i < 0 || x > best.v) best = ArgMax{x, v};   // indices increase: ties keep the first
   }
 #pragma unroll
   for (int m = 32; m > 0; m >>= 1) {
-    const float ob = __shfl_xor(best, m, 64);
-    const int oi = __shfl_xor(bi, m, 64);
-    if (ob > best || (ob == best && oi < bi)) {
-      best = ob;
-      bi = oi;
-    }
+    ArgMax o{__shfl_xor(best.v, m, 64), __shfl_xor(best.i, m, 64)};
+    best = better(best, o);
   }
-  if (lane == 0) {
-    sval[w] = best;
-    sidx[w] = bi;
-  }
+  if (lane == 0) sm[w] = best;
   __syncthreads();
-  float fb = sval[0];
-  int fi = sidx[0];
-  for (int i = 1; i < kWaves; ++i) {
-    if (sval[i] > fb || (sval[i] == fb && sidx[i] < fi)) {
-      fb = sval[i];
-      fi = sidx[i];
-    }
-  }
-  __syncthreads();   // sval / sidx are reused by the next call
-  return fi;
+  ArgMax r = sm[0];
+  for (int i = 1; i < kWaves; ++i) r = better(r, sm[i]);
+  __syncthreads();
+  return r;
 }
 
-__global__ __launch_bounds__(kThreads) void spec_accept_kernel(AcceptArgs a) {
-  __shared__ uint64_t wsum[kWaves];
-  __shared__ float sval[kWaves];
-  __shared__ int sidx[kWaves];
+// workspace layout (per sequence b, chunk c):
+//   sampled: uint64 sums[B][C][2]  (residual / p-only)
+//   greedy:  ArgMax best[B][k+1][C]
+__global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, void* ws, int nchunks) {
+  __shared__ uint64_t wsum[kWaves][2];
+  __shared__ ArgMax sm[kWaves];
+  __shared__ int s_n;
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  const int k = a.k, V = a.V;
+  const int v0 = chunk * kChunk, v1 = min(V, v0 + kChunk);
+  if (a.mode == 0) {
+    ArgMax* out = static_cast<ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
+    for (int i = 0; i <= k; ++i) {
+      const ArgMax r = block_argmax_range(a.p + ((size_t)b * (k + 1) + i) * V, v0, v1, sm);
+      if (threadIdx.x == 0) out[(size_t)i * nchunks + chunk] = r;
+    }
+    return;
+  }
+  const int n = accepted_prefix(a, b, &s_n);
+  const float* prow = a.p + ((size_t)b * (k + 1) + n) * V;
+  const float* qrow = n < k ? a.q + ((size_t)b * k + n) * V : nullptr;
+  const int use_q = n < k ? 1 : 0;
+  uint64_t sr = 0, sp = 0;
+  for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
+    const float pv = prow[v];
+    sp += fixed_weight(pv);
+    sr += use_q ? fixed_weight(fmaxf(0.0f, pv - qrow[v])) : fixed_weight(pv);
+  }
+  sr = wave_sum_u64(sr);
+  sp = wave_sum_u64(sp);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) {
+    wsum[w][0] = sr;
+    wsum[w][1] = sp;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t tr = 0, tp = 0;
+    for (int i = 0; i < kWaves; ++i) {
+      tr += wsum[i][0];
+      tp += wsum[i][1];
+    }
+    uint64_t* out = static_cast<uint64_t*>(ws) + ((size_t)b * nchunks + chunk) * 2;
+    out[0] = tr;
+    out[1] = tp;
+  }
+}
+
+// Block-wide exclusive prefix sum of one uint64 per thread; also returns
+// the total.  Uses wave prefix sums and the per-wave totals in `tot`.
+__device__ uint64_t block_exclusive_scan(uint64_t x, uint64_t* tot, uint64_t* total) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint64_t inc = x;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t y = shfl_up_u64(inc, d);
+    if (lane >= d) inc += y;
+  }
+  if (lane == 63) tot[w] = inc;
+  __syncthreads();
+  uint64_t before = 0, all = 0;
+  for (int i = 0; i < kWaves; ++i) {
+    if (i < w) before += tot[i];
+    all += tot[i];
+  }
+  __syncthreads();
+  *total = all;
+  return before + inc - x;
+}
+
+__global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const void* ws, int nchunks) {
+  __shared__ ArgMax sm[kWaves];
+  __shared__ uint64_t tot[kWaves];
   __shared__ int s_n;
   __shared__ int s_tok;
+  __shared__ int s_chunk;
+  __shared__ uint64_t s_before;
   const int b = blockIdx.x;
   const int k = a.k, V = a.V;
-  const float* p = a.p + (size_t)b * (k + 1) * V;
   const int32_t* draft = a.draft + (size_t)b * k;
-  int n = 0;
-  int token = 0;
-
+  const int c = threadIdx.x;                   // one thread per chunk (nchunks <= 256)
+  int n = 0, token = 0;
   if (a.mode == 0) {
-    // greedy: longest prefix of drafts equal to the target argmax
+    const ArgMax* part = static_cast<const ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int nn = 0;
     for (;;) {
-      const int gi = block_argmax(p + (size_t)n * V, V, sval, sidx);
-      if (n < k && draft[n] == gi) {
-        ++n;
+      ArgMax r = c < nchunks ? part[(size_t)nn * nchunks + c] : ArgMax{-INFINITY, -1};
+#pragma unroll
+      for (int m = 32; m > 0; m >>= 1) {
+        ArgMax o{__shfl_xor(r.v, m, 64), __shfl_xor(r.i, m, 64)};
+        r = better(r, o);
+      }
+      if (lane == 0) sm[w] = r;
+      __syncthreads();
+      ArgMax g = sm[0];
+      for (int i = 1; i < kWaves; ++i) g = better(g, sm[i]);
+      __syncthreads();
+      if (nn < k && draft[nn] == g.i) {
+        ++nn;
         continue;
       }
-      token = gi;
+      token = g.i;
       break;
     }
+    n = nn;
   } else {
-    const float* q = a.q + (size_t)b * k * V;
-    const float* u = a.u + (size_t)b * (k + 1);
-    if (threadIdx.x < 64) {
-      const int i = threadIdx.x;
-      bool acc = false;
-      if (i < k) {
-        const int x = draft[i];
-        if (x >= 0 && x < V) {
-          const double pu = (double)u[i] * (double)q[(size_t)i * V + x];
-          acc = pu < (double)p[(size_t)i * V + x];
-        }
-      }
-      // bit i set where position i rejects; position k always "rejects"
-      const uint64_t rej = __ballot(!acc) | (1ull << k);
-      if (i == 0) s_n = __builtin_ctzll(rej);
-    }
-    __syncthreads();
-    n = s_n;
-    const float* prow = p + (size_t)n * V;
-    const float* qrow = n < k ? q + (size_t)n * V : nullptr;
-    int use_q = n < k ? 1 : 0;
-    uint64_t S = weight_total(prow, qrow, use_q, V, wsum);
-    if (S == 0 && use_q) {
-      __syncthreads();
-      use_q = 0;
-      S = weight_total(prow, nullptr, 0, V, wsum);
+    n = accepted_prefix(a, b, &s_n);
+    const uint64_t* sums = static_cast<const uint64_t*>(ws) + (size_t)b * nchunks * 2;
+    const float* prow = a.p + ((size_t)b * (k + 1) + n) * V;
+    const float* qrow = n < k ? a.q + ((size_t)b * k + n) * V : nullptr;
+    // residual weights, else p-only weights, else argmax
+    uint64_t S;
+    uint64_t x = c < nchunks ? sums[2 * c] : 0ull;
+    uint64_t before = block_exclusive_scan(x, tot, &S);
+    int sel = 0;
+    if (S == 0) {
+      sel = 1;
+      x = c < nchunks ? sums[2 * c + 1] : 0ull;
+      before = block_exclusive_scan(x, tot, &S);
     }
     if (S == 0) {
-      token = block_argmax(prow, V, sval, sidx);
+      token = block_argmax_range(prow, 0, V, sm).i;
     } else {
-      float uf = u[k] * 16777216.0f;   // exact: u is a float32
+      const int use_q = (sel == 0 && n < k) ? 1 : 0;
+      float uf = a.u[(size_t)b * (k + 1) + k] * 16777216.0f;   // exact: u is a float32
       uf = fminf(fmaxf(floorf(uf), 0.0f), 16777215.0f);
       const uint64_t av = (uint64_t)uf;
       const uint64_t T = av * (S >> 24) + ((av * (S & 0xffffffull)) >> 24);
-      if (threadIdx.x == 0) s_tok = 0;
+      // the chunk whose [before, before + x) range holds T (exactly one)
+      if (x != 0 && before <= T && T < before + x) {
+        s_chunk = c;
+        s_before = before;
+      }
+      if (threadIdx.x == 0) s_tok = 0x7fffffff;
       __syncthreads();
-      token = find_token(prow, qrow, use_q, V, wsum, T, &s_tok);
+      const int cs = s_chunk;
+      // scan the chunk in 256-entry steps: wave w takes entries
+      // base + 64 w + lane, the waves' totals are prefix-summed in LDS
+      const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+      const int c0 = cs * kChunk, c1 = min(V, c0 + kChunk);
+      uint64_t running = s_before;
+      for (int base = c0; base < c1; base += kThreads) {
+        const int v = base + 64 * w + lane;
+        uint64_t y = v < c1 ? weight_at(prow, qrow, v, use_q) : 0ull;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const uint64_t z = shfl_up_u64(y, d);
+          if (lane >= d) y += z;
+        }
+        if (lane == 63) tot[w] = y;
+        __syncthreads();
+        uint64_t off = running, step = 0;
+        for (int i = 0; i < kWaves; ++i) {
+          if (i < w) off += tot[i];
+          step += tot[i];
+        }
+        const uint64_t mask = __ballot(off + y > T);
+        // prefix sums rise with v, so the smallest hit is the token
+        if (mask != 0ull && lane == __builtin_ctzll(mask)) atomicMin(&s_tok, v);
+        __syncthreads();
+        if (s_tok != 0x7fffffff) break;
+        running += step;
+      }
+      token = s_tok;
     }
   }
-
   int32_t* tok = a.tokens + (size_t)b * (k + 1);
-  for (int i = threadIdx.x; i <= k; i += kThreads) {
-    tok[i] = i < n ? draft[i] : (i == n ? token : -1);
-  }
+  for (int i = threadIdx.x; i <= k; i += kThreads) tok[i] = i < n ? draft[i] : (i == n ? token : -1);
   if (threadIdx.x == 0) a.n_accepted[b] = n;
 }
 
 }  // namespace
 
-hipError_t launch_accept(const AcceptArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(spec_accept_kernel, dim3(a.B), dim3(kThreads), 0, st, a);
+size_t accept_workspace_bytes(int B, int k, int V, int mode) {
+  const int nchunks = (V + kChunk - 1) / kChunk;
+  if (mode == 0) return (size_t)B * (k + 1) * nchunks * sizeof(ArgMax);
+  return (size_t)B * nchunks * 2 * sizeof(uint64_t);
+}
+
+hipError_t launch_accept(const AcceptArgs& a, void* ws, hipStream_t st) {
+  const int nchunks = (a.V + kChunk - 1) / kChunk;
+  hipLaunchKernelGGL(accept_chunks, dim3(nchunks, a.B), dim3(kThreads), 0, st, a, ws, nchunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_finish, dim3(a.B), dim3(kThreads), 0, st, a, ws, nchunks);
   return hipGetLastError();
 }
 

@@ -154,23 +154,25 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
 
 // --------------------------------------------------------------- accept
 size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode) {
-  (void)B;
-  (void)k;
-  (void)V;
-  (void)mode;
-  return 0;
+  if (B < 1 || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
+      (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
+    return 0;
+  return sd::accept_workspace_bytes(B, k, V, mode);
 }
 
 int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const float* u,
                    int32_t* n_accepted, int32_t* tokens, int B, int k, int V, int mode,
                    void* workspace, size_t workspace_bytes, void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
     return SD_ERR_INVALID_ARG;
   if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
   if (!p || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
   if (mode == SD_ACCEPT_SAMPLED && (!q || !u)) return SD_ERR_INVALID_ARG;
+  if (!aligned(p, 4) || !aligned(draft, 4) || !aligned(n_accepted, 4) || !aligned(tokens, 4) ||
+      (q && !aligned(q, 4)) || (u && !aligned(u, 4)))
+    return SD_ERR_INVALID_ARG;
+  const size_t need = sd::accept_workspace_bytes(B, k, V, mode);
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
   sd::AcceptArgs a{};
   a.p = p;
   a.q = q;
@@ -182,7 +184,7 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const f
   a.k = k;
   a.V = V;
   a.mode = mode;
-  return status_from(sd::launch_accept(a, static_cast<hipStream_t>(stream)));
+  return status_from(sd::launch_accept(a, workspace, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -92,6 +92,10 @@ __device__ __forceinline__ u32x2 lds_read_tr16_b64(uint32_t addr) {
   return r;
 }
 
+__device__ __forceinline__ void lds_write_b128(uint32_t addr, const u32x4& v) {
+  asm volatile("ds_write_b128 %0, %1" : : "v"(addr), "v"(v));
+}
+
 // Wait for every LDS operation of this wave (asm reads included).
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
@@ -106,6 +110,31 @@ __device__ __forceinline__ void tie(T& x) {
 // four groups).  gfx950's v_permlane32_swap / v_permlane16_swap exchange
 // halves / odd-even rows of two registers; applied to two copies of v they
 // hand every lane its partner's value without an LDS round trip.
+// Wait until at most N vector-memory operations of this wave are in flight
+// (and all of its LDS operations are done), then meet the other waves.  The
+// empty asm statements keep the compiler from moving memory accesses across
+// the barrier; the barrier itself carries no fence, because a fence would
+// wait for every LDS DMA in flight (including the tiles being prefetched).
+template <int N>
+__device__ __forceinline__ void wait_vm_then_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// two bf16 -> two fp16 (exact inside the fp16 range; round toward zero
+// otherwise, so magnitudes beyond 65504 saturate at 65504)
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t v) {
+  const float lo = __uint_as_float(v << 16);
+  const float hi = __uint_as_float(v & 0xffff0000u);
+  const auto h2 = __builtin_amdgcn_cvt_pkrtz(lo, hi);
+  uint32_t r;
+  __builtin_memcpy(&r, &h2, 4);
+  return r;
+}
+
 __device__ __forceinline__ float partner32(float v, float* other) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   *other = __uint_as_float(r[1]);

@@ -33,24 +33,13 @@
 namespace sd {
 namespace {
 
-constexpr int kTok = 64;   // tokens per LDS tile
+constexpr int kTok = 64;   // tokens per LDS tile of the bf16 kernel
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_cvoid;
 
-__device__ __forceinline__ int swz(int token) { return token & 7; }
-
-__device__ __forceinline__ uint32_t cvt_bf16x2_to_f16x2(uint32_t v) {
-  // two bf16 values -> two fp16 values (exact inside the fp16 range)
-  const float lo = __uint_as_float(v << 16);
-  const float hi = __uint_as_float(v & 0xffff0000u);
-  auto h2 = __builtin_amdgcn_cvt_pkrtz(lo, hi);
-  uint32_t r;
-  __builtin_memcpy(&r, &h2, 4);
-  return r;
-}
 
 // Map the linear work-group id to (sequence*head, latent tile) so that the
 // latent tiles of one (sequence, head) land on the same XCD.
@@ -65,17 +54,37 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
   }
 }
 
+// One work-group = NW waves x 32 latents of one (sequence, head), one token
+// split.  64-token tiles of F_V[b][:, hs] are copied HBM -> LDS by the
+// global_load_lds DMA into a ring of four buffers, so two tiles are in
+// flight while a third is converted and a fourth computed.  One tile ahead
+// of the compute, the work-group converts the tile in place from bf16 to
+// fp16 (each 16-byte piece once per work-group), so every wave then runs
+// both products on fp16 matrix cores with no per-wave conversion:
+//   S^T = F_V Cq^T   (lane = one latent row, 16 tokens per tile and row)
+//   O^T += F_V^T P^T (P = exp2(s - m) in [0, 256] rounded to fp16; F_V^T
+//                     fragments via the transposing ds_read_b64_tr_b16)
+// Token pieces are XOR-swizzled by (token & 7) in LDS.  The running maximum
+// is raised (O, l rescaled) only when a row's scores exceed it by 2^8, and
+// the token mask is applied only on the tail tile.  Tile reads and the
+// in-place conversion are inline asm, and each step has one counted wait
+// and one fence-free barrier.
 template <int NW, int DH>
-__global__ __launch_bounds__(NW * 64) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
                                                          int tokens_per_split, int nsplit) {
+  constexpr int TT = 64;                    // tokens per tile
   constexpr int DC = DH / 32;               // 32-channel slices (QK)
   constexpr int DB = DH / 16;               // 16-channel output blocks (PV)
   constexpr int PK = DH / 8;                // 16-byte pieces per token
-  constexpr int TILE_BYTES = kTok * DH * 2;
-  constexpr int LOADS = kTok * PK / 64;     // DMA instructions per tile
-  constexpr int LOADS_PER_WAVE = LOADS / NW;
-  static_assert(LOADS % NW == 0, "tile copy must split evenly over the waves");
-  __shared__ __align__(16) unsigned char tile_buf[2][TILE_BYTES];
+  constexpr int ROW = DH * 2;               // bytes per token row
+  constexpr int TILE_BYTES = TT * ROW;
+  constexpr int DMA = TT * PK / 64;         // 64-lane copies per tile
+  constexpr int DMA_PER_WAVE = DMA / NW;
+  constexpr int CVT_PER_THREAD = TT * PK / (NW * 64);   // pieces converted per thread
+  constexpr int NBUF = 4;
+  constexpr float kRescale = 8.f;
+  static_assert(DMA % NW == 0 && (TT * PK) % (NW * 64) == 0, "tile work must split evenly");
+  __shared__ __align__(16) unsigned char ring[NBUF][TILE_BYTES];
 
   int bh, lt;
   map_tile(blockIdx.x, n_bh, n_lt, bh, lt);
@@ -83,171 +92,205 @@ __global__ __launch_bounds__(NW * 64) void compress_bf16(CompressArgs a, int n_b
   const int b = bh / a.H, h = bh % a.H;
   const int tok0 = split * tokens_per_split;
   const int tok1 = min(a.N, tok0 + tokens_per_split);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, G = lane >> 4, c = lane & 15;
-  const int lat0 = lt * NW * 64 + w * 64;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, lane = tid & 63, G = lane >> 4, c = lane & 15;
+  const int lat0 = lt * NW * 32 + w * 32;
 
-  // query fragments (B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..]
-  bf16x8 qf[4][DC];
-  const uint16_t* lat = static_cast<const uint16_t*>(a.latents);
+  // query fragments (fp16, B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..]
+  f16x8 qf[2][DC];
+  {
+    const uint16_t* lat = static_cast<const uint16_t*>(a.latents);
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int r = lat0 + rb * 16 + c;
-#pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      Pack8 pk;
-      pk.u = r < a.C ? *reinterpret_cast<const u32x4*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
-                     : u32x4{0u, 0u, 0u, 0u};
-      qf[rb][dc] = pk.b;
-    }
-  }
-
-  float m[4], l[4];
-  floatx4 o[4][DB];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    m[rb] = -INFINITY;
-    l[rb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[rb][db] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  const uint16_t* fbase = static_cast<const uint16_t*>(a.feats) + (size_t)b * a.N * a.d + h * DH;
-  const int ntiles = (tok1 - tok0 + kTok - 1) / kTok;
-
-  // DMA one 64-token tile into buffer `buf`: instruction i of this wave moves
-  // pieces P = (w * LOADS_PER_WAVE + i) * 64 + lane, LDS slot P, i.e. token
-  // P / PK, slot P % PK, holding global piece slot ^ swz(token).
-  auto issue_tile = [&](int tile, int buf) {
-    const int t0 = tok0 + tile * kTok;
-#pragma unroll
-    for (int i = 0; i < LOADS_PER_WAVE; ++i) {
-      const int P = (w * LOADS_PER_WAVE + i) * 64 + lane;
-      const int tk = P / PK, slot = P % PK;
-      const int tg = min(t0 + tk, tok1 - 1);
-      const uint16_t* src = fbase + (size_t)tg * a.d + ((slot ^ swz(tk)) * 8);
-      unsigned char* dst = &tile_buf[buf][(w * LOADS_PER_WAVE + i) * 64 * 16];
-      __builtin_amdgcn_global_load_lds((gbl_cvoid*)src, (lds_void*)dst, 16, 0, 0);
-    }
-  };
-
-  const float sl2 = a.scale_log2;
-  if (ntiles > 0) issue_tile(0, 0);
-  for (int it = 0; it < ntiles; ++it) {
-    const int cur = it & 1;
-    if (it + 1 < ntiles) {
-      issue_tile(it + 1, cur ^ 1);
-      // wait for this wave's copies of tile `it`, leave the next tile in flight
-      constexpr int N = LOADS_PER_WAVE;
-      __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
-    } else {
-      __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
-    }
-    __syncthreads();
-    const unsigned char* tb = tile_buf[cur];
-    const int t0 = tok0 + it * kTok;
-
-    // S^T = F_V Cq^T for the 4 16-token blocks of the tile
-    floatx4 s[4][4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const int tk = kb * 16 + c;
-      bf16x8 xf[DC];
+    for (int rb = 0; rb < 2; ++rb) {
+      const int r = lat0 + rb * 16 + c;
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
         Pack8 pk;
-        pk.u = *reinterpret_cast<const u32x4*>(tb + tk * (DH * 2) + (((dc * 4 + G) ^ swz(tk)) * 16));
-        xf[dc] = pk.b;
-      }
+        pk.u = r < a.C ? *reinterpret_cast<const u32x4*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
+                       : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
+        for (int e = 0; e < 4; ++e) pk.u[e] = bf16x2_to_f16x2(pk.u[e]);
+        qf[rb][dc] = pk.h;
+      }
+    }
+  }
+
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+  floatx4 o[2][DB];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[rb][db] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const uint16_t* fbase = static_cast<const uint16_t*>(a.feats) + (size_t)b * a.N * a.d + h * DH;
+  const int ntiles = (tok1 - tok0 + TT - 1) / TT;
+  const int last = ntiles - 1;
+
+  // copy i of this wave moves pieces P = (w * DMA_PER_WAVE + i) * 64 + lane:
+  // token P / PK, LDS slot P % PK holding global piece slot ^ (token & 7)
+  auto issue = [&](int tile, unsigned char* buf) {
+    const int t0 = tok0 + tile * TT;
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const int P = (w * DMA_PER_WAVE + i) * 64 + lane;
+      const int tk = P / PK, piece = P % PK;
+      const int tg = min(t0 + tk, tok1 - 1);
+      const uint16_t* src = fbase + (size_t)tg * a.d + ((piece ^ (tk & 7)) * 8);
+      __builtin_amdgcn_global_load_lds((gbl_cvoid*)src,
+                                       (lds_void*)(buf + (w * DMA_PER_WAVE + i) * 1024), 16, 0, 0);
+    }
+  };
+  // in-place bf16 -> fp16 conversion of this thread's pieces of a tile
+  auto convert = [&](const unsigned char* buf) {
+    const uint32_t base = lds_addr(buf);
+    u32x4 v[CVT_PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < CVT_PER_THREAD; ++i) v[i] = lds_read_b128(base + (i * NW * 64 + tid) * 16);
+    lds_wait();
+#pragma unroll
+    for (int i = 0; i < CVT_PER_THREAD; ++i) {
+      tie(v[i]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[i][e] = bf16x2_to_f16x2(v[i][e]);
+      lds_write_b128(base + (i * NW * 64 + tid) * 16, v[i]);
+    }
+  };
+
+  // per-lane LDS offsets: score fragments (token kb*16 + c, channels
+  // dc*32 + 8G ..) and transposed value reads (lane j of group G addresses
+  // token 4G + j/4 (+16) of a 32-token half at channels db*16 + 4 (j%4))
+  uint32_t xoff[4][DC];
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc) {
+      const int tk = kb * 16 + c;
+      xoff[kb][dc] = tk * ROW + (((dc * 4 + G) ^ (tk & 7)) * 16);
+    }
+  auto voff = [&](int hf, int half16, int db) -> uint32_t {
+    const int tk = hf * 32 + half16 * 16 + 4 * G + (c >> 2);
+    const int ch = db * 16 + 4 * (c & 3);
+    return tk * ROW + (((ch >> 3) ^ (tk & 7)) * 16) + (ch & 7) * 2;
+  };
+
+  const float sl2 = a.scale_log2;
+  auto compute = [&](int it, const unsigned char* buf) {
+    const uint32_t sb = lds_addr(buf);
+    const int t0 = tok0 + it * TT;
+    // S^T = F_V Cq^T for the tile: s[kb][rb] lane holds S[row rb*16 + c][token kb*16 + 4G + i]
+    floatx4 s[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      u32x4 xr[DC];
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) xr[dc] = lds_read_b128(sb + xoff[kb][dc]);
+      lds_wait();
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) tie(xr[dc]);
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int dc = 0; dc < DC; ++dc) acc = mfma_bf16(xf[dc], qf[rb][dc], acc);
+        for (int dc = 0; dc < DC; ++dc) {
+          Pack8 pk;
+          pk.u = xr[dc];
+          acc = mfma_f16(pk.h, qf[rb][dc], acc);
+        }
         s[kb][rb] = acc;
       }
     }
-
-    // online softmax over the tile; P in fp16, ordered for the two 32-token halves
-    f16x8 pf[2][4];
+    const bool tail = t0 + TT > tok1;
+    f16x8 pf[2][2];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
+    for (int rb = 0; rb < 2; ++rb) {
       float tmax = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int t = t0 + kb * 16 + 4 * G + i;
-          const float v = t < tok1 ? s[kb][rb][i] * sl2 : -INFINITY;
+          float v = s[kb][rb][i] * sl2;
+          if (tail && t0 + kb * 16 + 4 * G + i >= tok1) v = -INFINITY;
           s[kb][rb][i] = v;
           tmax = fmaxf(tmax, v);
         }
-      tmax = wave_max_across_groups(tmax);
-      const float mnew = fmaxf(m[rb], tmax);   // finite: every tile has a valid token
-      const float alpha = exp2f(m[rb] - mnew);
-      m[rb] = mnew;
+      tmax = wave_max_across_groups(tmax);   // every tile holds a valid token: finite
+      if (__ballot(tmax > m[rb] + kRescale) != 0ull) {
+        const float mnew = fmaxf(m[rb], tmax);
+        const float alpha = fast_exp2(m[rb] - mnew);
+        l[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+        m[rb] = mnew;
+      }
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float pv = exp2f(s[kb][rb][i] - mnew);
+          const float pv = fast_exp2(s[kb][rb][i] - m[rb]);
           psum += pv;
           pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)pv;
         }
-      l[rb] = l[rb] * alpha + psum;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+      l[rb] += psum;
     }
-
-    // O^T += F_V^T P^T with transposed fragments from LDS
+    // O^T += F_V^T P^T per 32-token half; the product's K index runs over
+    // tokens {4G..4G+3, 16+4G..16+4G+3} of the half, the order of pf.
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
-      const int tka = hf * 32 + 4 * G + (c >> 2);
-      const int tkb = tka + 16;
+      u32x2 vr[DB][2];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int ch = db * 16 + 4 * (c & 3);       // channel of this lane's 8-byte read
-        const int pc = ch >> 3, sub = (ch & 7) * 2;  // piece and byte offset inside it
-        const unsigned char* pa = tb + tka * (DH * 2) + ((pc ^ swz(tka)) * 16) + sub;
-        const unsigned char* pb = tb + tkb * (DH * 2) + ((pc ^ swz(tkb)) * 16) + sub;
-        const shortx4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_shortx4*)((__attribute__((address_space(3))) unsigned char*)pa));
-        const shortx4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_shortx4*)((__attribute__((address_space(3))) unsigned char*)pb));
-        uint32_t w4[4];
-        w4[0] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v0[0] | ((uint32_t)(uint16_t)v0[1] << 16));
-        w4[1] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v0[2] | ((uint32_t)(uint16_t)v0[3] << 16));
-        w4[2] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v1[0] | ((uint32_t)(uint16_t)v1[1] << 16));
-        w4[3] = cvt_bf16x2_to_f16x2((uint32_t)(uint16_t)v1[2] | ((uint32_t)(uint16_t)v1[3] << 16));
-        Pack8 vt;
-        vt.u = u32x4{w4[0], w4[1], w4[2], w4[3]};
+        vr[db][0] = lds_read_tr16_b64(sb + voff(hf, 0, db));
+        vr[db][1] = lds_read_tr16_b64(sb + voff(hf, 1, db));
+      }
+      lds_wait();
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) o[rb][db] = mfma_f16(vt.h, pf[hf][rb], o[rb][db]);
+      for (int db = 0; db < DB; ++db) {
+        tie(vr[db][0]);
+        tie(vr[db][1]);
+        Pack8 vv;
+        vv.u = u32x4{vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma_f16(vv.h, pf[hf][rb], o[rb][db]);
       }
     }
-    __syncthreads();   // the buffer is refilled two tiles later
+  };
+
+  // Ring schedule: at step it, tile it (converted in step it-1) is computed,
+  // tile it+1 (landed) is converted, tiles it+2 and it+3 are in flight.
+  // Every step issues one tile (re-reading the last past the end), so the
+  // wait count is the same at every step.
+#pragma unroll
+  for (int i = 0; i < NBUF - 1; ++i) issue(min(i, last), ring[i]);
+  wait_vm_then_barrier<(NBUF - 2) * DMA_PER_WAVE>();   // tile 0 landed
+  convert(ring[0]);
+  for (int it = 0; it < ntiles; ++it) {
+    // tile it+1 landed; tile it converted by every wave; slot it-1 free
+    wait_vm_then_barrier<(NBUF - 3) * DMA_PER_WAVE>();
+    issue(min(it + NBUF - 1, last), ring[(it + NBUF - 1) % NBUF]);
+    if (it + 1 < ntiles) convert(ring[(it + 1) % NBUF]);
+    compute(it, ring[it % NBUF]);
   }
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // no copy in flight at exit
 
   // normalise and write (directly, or as a partial for the merge)
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
+  for (int rb = 0; rb < 2; ++rb) {
     const float lt_ = wave_sum_across_groups(l[rb]);
     const int r = lat0 + rb * 16 + c;
     if (r >= a.C) continue;
     const float inv = lt_ > 0.f ? 1.f / lt_ : 0.f;
+    float* dst;
     if (nsplit == 1) {
-      float* dst = a.out + ((size_t)b * a.C + r) * a.d + h * DH;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[rb][db] * inv;
+      dst = a.out + ((size_t)b * a.C + r) * a.d + h * DH;
     } else {
       const size_t pr = ((size_t)bh * nsplit + split) * a.C + r;
-      float* dst = a.part_o + pr * DH;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[rb][db] * inv;
+      dst = a.part_o + pr * DH;
       if (G == 0) a.part_lse[pr] = lt_ > 0.f ? m[rb] + log2f(lt_) : -INFINITY;
     }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[rb][db] * inv;
   }
 }
 
@@ -358,7 +401,7 @@ hipError_t launch_bf16(const CompressArgs& a, const CompressPlan& p, hipStream_t
 
 template <int DH>
 hipError_t dispatch_nw(const CompressArgs& a, const CompressPlan& p, hipStream_t st) {
-  switch (p.lat_tile / 64) {
+  switch (p.lat_tile / 32) {
     case 1: return launch_bf16<1, DH>(a, p, st);
     case 2: return launch_bf16<2, DH>(a, p, st);
     default: return launch_bf16<4, DH>(a, p, st);
@@ -378,8 +421,8 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype) {
     const long long cap = (65536 - 4LL * kF32Rows * p.dh - 16 * kF32Rows) / (8 * kF32Rows);
     p.tokens_per_split = (int)std::max(64LL, std::min(2048LL, cap / 64 * 64));
   } else {
-    const int waves = std::min(4, (C + 63) / 64);
-    p.lat_tile = waves * 64;
+    const int waves = C <= 32 ? 1 : (C <= 64 ? 2 : 4);   // 32 latents per wave
+    p.lat_tile = waves * 32;
     p.lat_tiles = (C + p.lat_tile - 1) / p.lat_tile;
     // split the tokens until about 512 work-groups exist, keeping >= 256 tokens each
     const long long groups = n_bh * p.lat_tiles;

@@ -64,20 +64,6 @@ __device__ __forceinline__ int seq_len(const VerifyArgs& a, int b, bool paged) {
 }
 
 // ----------------------------------------------------------- bf16 split
-// Wait until at most N vector-memory operations of this wave are in flight
-// (and all of its LDS operations are done), then meet the other waves.  The
-// empty asm statements keep the compiler from moving memory accesses across
-// the barrier; the barrier itself carries no fence, because a fence would
-// wait for every LDS DMA in flight (including the tiles being prefetched).
-template <int N>
-__device__ __forceinline__ void wait_vm_then_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // One work-group = NW waves = NW 16-row blocks of one (sequence, KV head,
 // key split).  All waves walk the same 32-key tiles.  Tiles are copied
 // HBM -> LDS by the global_load_lds DMA (no VGPR staging) into a ring of

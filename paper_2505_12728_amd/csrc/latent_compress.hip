@@ -115,12 +115,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
   }
 
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
-  floatx4 o[2][DB];
+  // o[rb][0..DB-1]: O^T blocks; o[rb][DB]: the row sums l, formed on the
+  // matrix cores from the same fp16 P (a "ones" row as the A fragment puts
+  // l of latent c at accumulator row 0, i.e. lane c of group 0, element 0)
+  float m[2] = {-INFINITY, -INFINITY};
+  floatx4 o[2][DB + 1];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) o[rb][db] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int db = 0; db <= DB; ++db) o[rb][db] = floatx4{0.f, 0.f, 0.f, 0.f};
+  f16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = (_Float16)(c == 0 ? 1.f : 0.f);
 
   const uint16_t* fbase = static_cast<const uint16_t*>(a.feats) + (size_t)b * a.N * a.d + h * DH;
   const int ntiles = (tok1 - tok0 + TT - 1) / TT;
@@ -199,39 +205,46 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         s[kb][rb] = acc;
       }
     }
-    const bool tail = t0 + TT > tok1;
+    // Online softmax on raw scores: with sl2 = scale * log2(e), the row
+    // maximum of s * sl2 is (max s) * sl2 for sl2 >= 0 and (min s) * sl2
+    // otherwise, and p = exp2(s * sl2 - m) is one FMA and one exp.
+    if (t0 + TT > tok1) {                   // tail tile: drop tokens past the split
+      const float fill = sl2 >= 0.f ? -INFINITY : INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (t0 + kb * 16 + 4 * G + i >= tok1) {
+            s[kb][0][i] = fill;
+            s[kb][1][i] = fill;
+          }
+    }
     f16x8 pf[2][2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      float tmax = -INFINITY;
+      float hi = s[0][rb][0], lo = s[0][rb][0];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float v = s[kb][rb][i] * sl2;
-          if (tail && t0 + kb * 16 + 4 * G + i >= tok1) v = -INFINITY;
-          s[kb][rb][i] = v;
-          tmax = fmaxf(tmax, v);
+          hi = fmaxf(hi, s[kb][rb][i]);
+          lo = fminf(lo, s[kb][rb][i]);
         }
-      tmax = wave_max_across_groups(tmax);   // every tile holds a valid token: finite
+      // every tile holds a valid token, so the extreme is finite
+      const float tmax = wave_max_across_groups((sl2 >= 0.f ? hi : lo) * sl2);
       if (__ballot(tmax > m[rb] + kRescale) != 0ull) {
         const float mnew = fmaxf(m[rb], tmax);
         const float alpha = fast_exp2(m[rb] - mnew);
-        l[rb] *= alpha;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+        for (int db = 0; db <= DB; ++db) o[rb][db] *= alpha;
         m[rb] = mnew;
       }
-      float psum = 0.f;
+      const float nm = -m[rb];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float pv = fast_exp2(s[kb][rb][i] - m[rb]);
-          psum += pv;
-          pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)pv;
-        }
-      l[rb] += psum;
+        for (int i = 0; i < 4; ++i)
+          pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)fast_exp2(fmaf(s[kb][rb][i], sl2, nm));
     }
     // O^T += F_V^T P^T per 32-token half; the product's K index runs over
     // tokens {4G..4G+3, 16+4G..16+4G+3} of the half, the order of pf.
@@ -253,6 +266,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma_f16(vv.h, pf[hf][rb], o[rb][db]);
       }
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) o[rb][DB] = mfma_f16(ones, pf[hf][rb], o[rb][DB]);
     }
   };
 
@@ -276,7 +291,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // normalise and write (directly, or as a partial for the merge)
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
-    const float lt_ = wave_sum_across_groups(l[rb]);
+    const float lt_ = __shfl(o[rb][DB][0], c, 64);   // l of row c sits in lane c
     const int r = lat0 + rb * 16 + c;
     if (r >= a.C) continue;
     const float inv = lt_ > 0.f ? 1.f / lt_ : 0.f;

@@ -77,6 +77,23 @@ __device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
   return r;
 }
 
+// same, with a compile-time byte offset folded into the instruction
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128_off(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr16_b64_off(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
 __device__ __forceinline__ u32x2 lds_read_b64(uint32_t addr) {
   u32x2 r;
   asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr));

@@ -4,17 +4,16 @@
 // is both key and value, so one staged tile of F_V feeds both products.
 //
 // bf16 path (matrix cores), grid (sequence x head x latent tile, token split):
-//   - a work-group of NW waves owns NW * 64 latents of one (sequence, head);
-//     each wave keeps its 64 latents' query fragments in registers;
+//   - a work-group of NW waves owns NW * 32 latents of one (sequence, head);
+//     each wave keeps its 32 latents' query fragments (fp16) in registers;
 //   - 64-token tiles of F_V[b][:, hs] are copied HBM -> LDS with the
-//     global_load_lds DMA (no VGPR staging), double-buffered, with the
-//     16-byte pieces of each token XOR-swizzled by (token & 7) so that both
-//     read patterns below spread over the LDS banks;
-//   - S^T = F_V Cq^T on bf16 matrix cores (lane = one latent row), online
-//     softmax in fp32 with exp2, then O^T += F_V^T P^T on fp16 matrix cores:
-//     P (in [0, 1]) is rounded to fp16 and the F_V fragment read back with
-//     the transposing ds_read_tr16_b64 is converted bf16 -> fp16, which is
-//     exact for |F_V| in [2^-14, 65504];
+//     global_load_lds DMA (no VGPR staging) into a 4-buffer ring, the 16-byte
+//     pieces of each token XOR-swizzled so that every read pattern below is
+//     free of LDS bank conflicts;
+//   - each tile is converted in place bf16 -> fp16 once per work-group (exact
+//     for |F_V| in [2^-14, 65504]), so both products run on fp16 matrix
+//     cores: S^T = F_V Cq^T (lane = one latent row), online softmax in fp32
+//     with exp2, P (in [0, 256]) rounded to fp16, O^T += F_V^T P^T;
 //   - latent tiles of one (sequence, head) are placed on the same XCD
 //     (work-groups are dealt to the 8 XCDs round-robin) so their F_V reads
 //     hit the same L2.
@@ -26,6 +25,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "device_common.hpp"
 #include "launch.hpp"
@@ -40,6 +40,37 @@ typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_cvoid;
 
+
+// LDS swizzle of the 16-byte pieces of token t: piece p is stored at slot
+// p ^ swz<DH>(t & 15).  gfx950's LDS has 64 four-byte banks; a 16-byte read
+// serves 16 lanes per pass and the 8-byte transposing read 32 lanes, so
+//   - 16 consecutive tokens read at one piece must fill the 256 bank bytes
+//     (score reads), and
+//   - 8 consecutive tokens read at two adjacent pieces each (value reads)
+//     must too.
+// For 256-byte rows (DH = 128) that means swz is a permutation of 0..15 whose
+// bits 1..3 differ within each 8-token half; for 128-byte rows (DH = 64, two
+// tokens per bank row) a permutation of 0..7 on each token parity whose bits
+// 1..2 differ within each quad of that parity.
+template <int DH>
+__device__ __forceinline__ constexpr int swz(int t) {
+  t &= 15;
+  if constexpr (DH == 128) {
+    return ((t & 7) << 1) | ((t >> 3) & 1);
+  } else {
+    const int u = (t >> 1) & 7;
+    return ((u & 3) << 1) | (u >> 2);
+  }
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>{}) for I = B .. E-1.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // Map the linear work-group id to (sequence*head, latent tile) so that the
 // latent tiles of one (sequence, head) land on the same XCD.
@@ -56,19 +87,20 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 
 // One work-group = NW waves x 32 latents of one (sequence, head), one token
 // split.  64-token tiles of F_V[b][:, hs] are copied HBM -> LDS by the
-// global_load_lds DMA into a ring of four buffers, so two tiles are in
-// flight while a third is converted and a fourth computed.  One tile ahead
-// of the compute, the work-group converts the tile in place from bf16 to
-// fp16 (each 16-byte piece once per work-group), so every wave then runs
-// both products on fp16 matrix cores with no per-wave conversion:
+// global_load_lds DMA into a ring of four buffers.  One tile ahead of its
+// score step, the work-group converts a tile in place from bf16 to fp16
+// (each 16-byte piece once per work-group), so every wave then runs both
+// products on fp16 matrix cores with no per-wave conversion:
 //   S^T = F_V Cq^T   (lane = one latent row, 16 tokens per tile and row)
 //   O^T += F_V^T P^T (P = exp2(s - m) in [0, 256] rounded to fp16; F_V^T
 //                     fragments via the transposing ds_read_b64_tr_b16)
-// Token pieces are XOR-swizzled by (token & 7) in LDS.  The running maximum
-// is raised (O, l rescaled) only when a row's scores exceed it by 2^8, and
-// the token mask is applied only on the tail tile.  Tile reads and the
-// in-place conversion are inline asm, and each step has one counted wait
-// and one fence-free barrier.
+// The loop is software-pipelined across tiles (scores of the next tile under
+// the exponentials of the current one) and split into groups whose LDS
+// reads are issued one group ahead.  The running maximum is raised (O, l
+// rescaled) only when a row's scores exceed it by 2^8, and the token mask
+// is applied only on the tail tile.  Tile reads and the in-place conversion
+// are inline asm, and each step has one counted wait and one fence-free
+// barrier.
 template <int NW, int DH>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
                                                          int tokens_per_split, int nsplit) {
@@ -141,7 +173,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       const int P = (w * DMA_PER_WAVE + i) * 64 + lane;
       const int tk = P / PK, piece = P % PK;
       const int tg = min(t0 + tk, tok1 - 1);
-      const uint16_t* src = fbase + (size_t)tg * a.d + ((piece ^ (tk & 7)) * 8);
+      const uint16_t* src = fbase + (size_t)tg * a.d + ((piece ^ swz<DH>(tk)) * 8);
       __builtin_amdgcn_global_load_lds((gbl_cvoid*)src,
                                        (lds_void*)(buf + (w * DMA_PER_WAVE + i) * 1024), 16, 0, 0);
     }
@@ -162,130 +194,327 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
   };
 
-  // per-lane LDS offsets: score fragments (token kb*16 + c, channels
-  // dc*32 + 8G ..) and transposed value reads (lane j of group G addresses
-  // token 4G + j/4 (+16) of a 32-token half at channels db*16 + 4 (j%4))
-  uint32_t xoff[4][DC];
+  // Per-lane LDS bases (the tile offsets below are multiples of 16 tokens, so
+  // token & 15 and the swizzle are fixed per lane).  Score fragments: token
+  // kb*16 + c, piece dc*4 + G, one base per dc plus the immediate kb*16*ROW.
+  // Transposed value reads: lane j of group G addresses token 4G + j/4 of a
+  // 16-token block at channels db*16 + 4*(j%4), i.e. piece 2*db + ((j&3)>>1)
+  // at byte 8*(j&1); one base per db plus the block's immediate offset.
+  uint32_t xbase[DC];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb)
+  for (int dc = 0; dc < DC; ++dc) xbase[dc] = c * ROW + ((dc * 4 + G) ^ swz<DH>(c)) * 16;
+  uint32_t vbase[DB];
+  {
+    const int tt = 4 * G + (c >> 2);
 #pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      const int tk = kb * 16 + c;
-      xoff[kb][dc] = tk * ROW + (((dc * 4 + G) ^ (tk & 7)) * 16);
-    }
-  auto voff = [&](int hf, int half16, int db) -> uint32_t {
-    const int tk = hf * 32 + half16 * 16 + 4 * G + (c >> 2);
-    const int ch = db * 16 + 4 * (c & 3);
-    return tk * ROW + (((ch >> 3) ^ (tk & 7)) * 16) + (ch & 7) * 2;
-  };
+    for (int db = 0; db < DB; ++db)
+      vbase[db] = tt * ROW + ((2 * db + ((c & 3) >> 1)) ^ swz<DH>(tt)) * 16 + (c & 1) * 8;
+  }
 
-  const float sl2 = a.scale_log2;
-  auto compute = [&](int it, const unsigned char* buf) {
-    const uint32_t sb = lds_addr(buf);
-    const int t0 = tok0 + it * TT;
-    // S^T = F_V Cq^T for the tile: s[kb][rb] lane holds S[row rb*16 + c][token kb*16 + 4G + i]
-    floatx4 s[4][2];
+  // A negative scale is folded into the queries (softmax(s * q . x) =
+  // softmax(|s| * (-q) . x)), so the loop below only handles sl2 >= 0.
+  float sl2 = a.scale_log2;
+  if (sl2 < 0.f) {
+    sl2 = -sl2;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      u32x4 xr[DC];
+    for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int dc = 0; dc < DC; ++dc) xr[dc] = lds_read_b128(sb + xoff[kb][dc]);
-      lds_wait();
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) tie(xr[dc]);
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int dc = 0; dc < DC; ++dc) {
-          Pack8 pk;
-          pk.u = xr[dc];
-          acc = mfma_f16(pk.h, qf[rb][dc], acc);
-        }
-        s[kb][rb] = acc;
-      }
-    }
-    // Online softmax on raw scores: with sl2 = scale * log2(e), the row
-    // maximum of s * sl2 is (max s) * sl2 for sl2 >= 0 and (min s) * sl2
-    // otherwise, and p = exp2(s * sl2 - m) is one FMA and one exp.
-    if (t0 + TT > tok1) {                   // tail tile: drop tokens past the split
-      const float fill = sl2 >= 0.f ? -INFINITY : INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (t0 + kb * 16 + 4 * G + i >= tok1) {
-            s[kb][0][i] = fill;
-            s[kb][1][i] = fill;
-          }
-    }
-    f16x8 pf[2][2];
+      for (int dc = 0; dc < DC; ++dc) qf[rb][dc] = -qf[rb][dc];
+  }
+
+  // Scores of one 16-token block of a tile (4 reads, 2 * DC matrix-core ops):
+  // s[rb] lane holds S[row rb*16 + c][token kb*16 + 4G + i].
+#define SD_QK_READ(XR, SB, KB)                                                             \
+  _Pragma("unroll") for (int dc = 0; dc < DC; ++dc)                                        \
+    XR[dc] = lds_read_b128_off<(KB) * 16 * ROW>((SB) + xbase[dc]);
+#define SD_QK_MFMA(XR, S, KB)                                                              \
+  _Pragma("unroll") for (int rb = 0; rb < 2; ++rb) {                                       \
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};                                                    \
+    _Pragma("unroll") for (int dc = 0; dc < DC; ++dc) {                                    \
+      Pack8 pk;                                                                            \
+      pk.u = XR[dc];                                                                       \
+      acc = mfma_f16(pk.h, qf[rb][dc], acc);                                               \
+    }                                                                                      \
+    S[KB][rb] = acc;                                                                       \
+  }
+
+  // Row maxima of a tile's scores (in log2 units), and the raise of the
+  // running maxima with the (rare) rescale of O and l.
+  auto tile_max = [&](const floatx4 (&s)[4][2], float (&tmax)[2]) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      float hi = s[0][rb][0], lo = s[0][rb][0];
+      float ext = s[0][rb][0];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          hi = fmaxf(hi, s[kb][rb][i]);
-          lo = fminf(lo, s[kb][rb][i]);
-        }
-      // every tile holds a valid token, so the extreme is finite
-      const float tmax = wave_max_across_groups((sl2 >= 0.f ? hi : lo) * sl2);
-      if (__ballot(tmax > m[rb] + kRescale) != 0ull) {
-        const float mnew = fmaxf(m[rb], tmax);
+        for (int i = 0; i < 4; ++i) ext = fmaxf(ext, s[kb][rb][i]);
+      // every tile holds a valid token, so the maximum is finite
+      tmax[rb] = wave_max_across_groups(ext * sl2);
+    }
+  };
+  auto raise_max = [&](const float (&tmax)[2]) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      if (__ballot(tmax[rb] > m[rb] + kRescale) != 0ull) {
+        const float mnew = fmaxf(m[rb], tmax[rb]);
         const float alpha = fast_exp2(m[rb] - mnew);
 #pragma unroll
         for (int db = 0; db <= DB; ++db) o[rb][db] *= alpha;
         m[rb] = mnew;
       }
-      const float nm = -m[rb];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)fast_exp2(fmaf(s[kb][rb][i], sl2, nm));
     }
-    // O^T += F_V^T P^T per 32-token half; the product's K index runs over
-    // tokens {4G..4G+3, 16+4G..16+4G+3} of the half, the order of pf.
+  };
+  // tokens at or past the end of the split get score -inf (last tile only)
+  auto mask_tail = [&](floatx4 (&s)[4][2], int t0) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (t0 + kb * 16 + 4 * G + i >= tok1) {
+          s[kb][0][i] = -INFINITY;
+          s[kb][1][i] = -INFINITY;
+        }
+  };
+  // p = exp2(s * sl2 - m) in fp16, for one row block
+#define SD_P_ROW(S, PF, RB)                                                                \
+  {                                                                                        \
+    const float nm = -m[RB];                                                               \
+    _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                       \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                        \
+        PF[kb >> 1][RB][(kb & 1) * 4 + i] = (_Float16)fast_exp2(fmaf(S[kb][RB][i], sl2, nm)); \
+  }
+
+  // O^T += F_V^T P^T for one 32-token half; the product's K index runs over
+  // tokens {4G..4G+3, 16+4G..16+4G+3} of the half, the order of pf.
+#define SD_PV_READ(VR, SB, HF)                                                             \
+  _Pragma("unroll") for (int db = 0; db < DB; ++db) {                                      \
+    VR[db][0] = lds_read_tr16_b64_off<(HF) * 32 * ROW>((SB) + vbase[db]);                  \
+    VR[db][1] = lds_read_tr16_b64_off<(HF) * 32 * ROW + 16 * ROW>((SB) + vbase[db]);       \
+  }
+#define SD_PV_MFMA(VR, PF, HF)                                                             \
+  {                                                                                        \
+    _Pragma("unroll") for (int db = 0; db < DB; ++db) {                                    \
+      Pack8 vv;                                                                            \
+      vv.u = u32x4{VR[db][0][0], VR[db][0][1], VR[db][1][0], VR[db][1][1]};                \
+      _Pragma("unroll") for (int rb = 0; rb < 2; ++rb)                                     \
+        o[rb][db] = mfma_f16(vv.h, PF[HF][rb], o[rb][db]);                                 \
+    }                                                                                      \
+    _Pragma("unroll") for (int rb = 0; rb < 2; ++rb)                                       \
+      o[rb][DB] = mfma_f16(ones, PF[HF][rb], o[rb][DB]);                                   \
+  }
+  // interleave: one matrix-core op, then N VALU ops, `cnt` times (one
+  // scheduling pipeline per phase, named by ID)
+#define SD_INTERLEAVE(cnt, N, ID)                                                          \
+  _Pragma("unroll") for (int q_ = 0; q_ < (cnt); ++q_) {                                   \
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, ID);                                    \
+    __builtin_amdgcn_sched_group_barrier(0x002, (N), ID);                                  \
+  }
+
+  // Ring schedule (4 buffers), software-pipelined across tiles.  Entering
+  // step it, scur holds the scores of tile it and the running maxima already
+  // cover them.  After one barrier the step runs NG groups; each waits for
+  // its own LDS reads (issued one group earlier), issues the next group's
+  // reads, then interleaves its matrix-core ops with VALU work:
+  //   QK groups (one per 32-channel slice dc): scores of tile it+1,
+  //     accumulated over dc (8 independent ops per group) | exponentials of
+  //     tile it (one quarter of them per group for DH = 128)
+  //   PV groups (4 value blocks of one half each): P V of tile it | in-place
+  //     conversion of tile it+2 (first half), row maxima of tile it+1
+  //     (second half)
+  // and raises the maxima (rare rescale) for the next step, while tile it+3
+  // is in flight.  Every step issues one tile (re-reading the last past the
+  // end) and converts one buffer (past the end one that is never read
+  // again), so the wait counts are the same at every step and the groups
+  // form one basic block.
+  constexpr int NQK = DC;              // QK read groups
+  constexpr int NPVH = DB / 4;         // PV read groups per half
+  constexpr int NG = NQK + 2 * NPVH;
+  constexpr int EPG = 4 / NQK;         // exponential quarters per QK group
+  issue(0, ring[0]);
+  issue(min(1, last), ring[1]);
+  issue(min(2, last), ring[2]);
+  wait_vm_then_barrier<2 * DMA_PER_WAVE>();           // tile 0 landed
+  convert(ring[0]);
+  wait_vm_then_barrier<DMA_PER_WAVE>();               // tile 1 landed, tile 0 converted
+  convert(ring[1]);
+  floatx4 scur[4][2];
+  {
+    const uint32_t sb = lds_addr(ring[0]);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      u32x4 xr[DC];
+      if (kb == 0) SD_QK_READ(xr, sb, 0)
+      if (kb == 1) SD_QK_READ(xr, sb, 1)
+      if (kb == 2) SD_QK_READ(xr, sb, 2)
+      if (kb == 3) SD_QK_READ(xr, sb, 3)
+      lds_wait();
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) tie(xr[dc]);
+      SD_QK_MFMA(xr, scur, kb)
+    }
+    if (last == 0) mask_tail(scur, tok0);
+    float tmax[2];
+    tile_max(scur, tmax);
+    raise_max(tmax);
+  }
+
+  // LDS reads of group g into the alternating register sets xr / vr (and
+  // the conversion pieces cv with the first PV group)
+  auto reads = [&](auto gtag, uint32_t nb, uint32_t vb, uint32_t cb, u32x4 (&xr)[2][4],
+                   u32x2 (&vr)[2][4][2], u32x4 (&cv)[CVT_PER_THREAD], auto tie_only) {
+    constexpr int g = decltype(gtag)::value;
+    constexpr bool T = decltype(tie_only)::value;
+    if constexpr (g < NQK) {
+      constexpr int dc = g;
+      auto& x = xr[g & 1];
+      if constexpr (T) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) tie(x[kb]);
+      } else {
+        x[0] = lds_read_b128_off<0 * 16 * ROW>(nb + xbase[dc]);
+        x[1] = lds_read_b128_off<1 * 16 * ROW>(nb + xbase[dc]);
+        x[2] = lds_read_b128_off<2 * 16 * ROW>(nb + xbase[dc]);
+        x[3] = lds_read_b128_off<3 * 16 * ROW>(nb + xbase[dc]);
+      }
+    } else if constexpr (g < NG) {
+      constexpr int q = g - NQK, hf = q / NPVH, pb = q % NPVH;
+      auto& v = vr[g & 1];
+      if constexpr (T) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          tie(v[d][0]);
+          tie(v[d][1]);
+        }
+        if constexpr (q == 0) {
+#pragma unroll
+          for (int i = 0; i < CVT_PER_THREAD; ++i) tie(cv[i]);
+        }
+      } else {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          v[d][0] = lds_read_tr16_b64_off<hf * 32 * ROW>(vb + vbase[4 * pb + d]);
+          v[d][1] = lds_read_tr16_b64_off<hf * 32 * ROW + 16 * ROW>(vb + vbase[4 * pb + d]);
+        }
+        if constexpr (q == 0) {
+#pragma unroll
+          for (int i = 0; i < CVT_PER_THREAD; ++i) cv[i] = lds_read_b128(cb + (i * NW * 64 + tid) * 16);
+        }
+      }
+    }
+  };
+
+  // one step; the mask flag (compile time) is set only for it = last - 1, so
+  // the steady-state loop has no branch between its groups
+  auto step = [&](int it, auto mask_tag) {
+    // tile it+2 landed; tile it+1 converted by every wave; buffer it-1 free
+    wait_vm_then_barrier<0>();
+    const uint32_t nb = lds_addr(ring[(it + 1) % NBUF]);
+    const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);
+    const uint32_t vb = lds_addr(ring[it % NBUF]);
+    u32x4 xr[2][4];
+    u32x2 vr[2][4][2];
+    u32x4 cv[CVT_PER_THREAD];
+    floatx4 snext[4][2];
+    f16x8 pf[2][2];
+    float tmax[2];
+    reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+    issue(min(it + 3, last), ring[(it + 3) % NBUF]);
+    static_for<0, NG>([&](auto gtag) {
+      constexpr int g = decltype(gtag)::value;
+      lds_wait();
+      reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+      reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+      if constexpr (g == NQK + NPVH) {
+        // conversion finished in the first half: write it back
+#pragma unroll
+        for (int i = 0; i < CVT_PER_THREAD; ++i) lds_write_b128(cb + (i * NW * 64 + tid) * 16, cv[i]);
+      }
+      if constexpr (g < NQK) {
+        // scores of tile it+1 for channel slice dc = g
+        const auto& x = xr[g & 1];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          Pack8 pk;
+          pk.u = x[kb];
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb)
+            snext[kb][rb] = mfma_f16(pk.h, qf[rb][g], g == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : snext[kb][rb]);
+        }
+        // exponentials of tile it, quarters e = (rb, h): pf[h][rb]
+#pragma unroll
+        for (int e = g * EPG; e < (g + 1) * EPG; ++e) {
+          const int rb = e >> 1, h = e & 1;
+          const float nm = -m[rb];
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              pf[h][rb][k2 * 4 + i] = (_Float16)fast_exp2(fmaf(scur[2 * h + k2][rb][i], sl2, nm));
+        }
+        SD_INTERLEAVE(8, 3, g + 1)
+      } else {
+        constexpr int q = g - NQK, hf = q / NPVH, pb = q % NPVH;
+        if constexpr (q == 0 && decltype(mask_tag)::value) mask_tail(snext, tok0 + last * TT);
+        const auto& v = vr[g & 1];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          Pack8 vv;
+          vv.u = u32x4{v[d][0][0], v[d][0][1], v[d][1][0], v[d][1][1]};
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) o[rb][4 * pb + d] = mfma_f16(vv.h, pf[hf][rb], o[rb][4 * pb + d]);
+        }
+        if constexpr (pb == NPVH - 1) {
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) o[rb][DB] = mfma_f16(ones, pf[hf][rb], o[rb][DB]);
+        }
+        if constexpr (hf == 0) {
+          // in-place conversion of tile it+2, spread over the first half
+#pragma unroll
+          for (int i = pb; i < CVT_PER_THREAD; i += NPVH)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) cv[i][e] = bf16x2_to_f16x2(cv[i][e]);
+        } else if constexpr (pb == NPVH - 1) {
+          tile_max(snext, tmax);
+        }
+        SD_INTERLEAVE(8 + (pb == NPVH - 1 ? 2 : 0), 3, g + 1)
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    raise_max(tmax);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) scur[kb][rb] = snext[kb][rb];
+  };
+  for (int it = 0; it + 1 < last; ++it) step(it, std::false_type{});
+  if (last >= 1) step(last - 1, std::true_type{});
+  {
+    // last tile (masked and covered by the maxima): softmax and P V
+    wait_vm_then_barrier<0>();
+    const uint32_t vb = lds_addr(ring[last % NBUF]);
+    f16x8 pf[2][2];
+    SD_P_ROW(scur, pf, 0)
+    SD_P_ROW(scur, pf, 1)
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       u32x2 vr[DB][2];
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        vr[db][0] = lds_read_tr16_b64(sb + voff(hf, 0, db));
-        vr[db][1] = lds_read_tr16_b64(sb + voff(hf, 1, db));
-      }
+      if (hf == 0) SD_PV_READ(vr, vb, 0)
+      if (hf == 1) SD_PV_READ(vr, vb, 1)
       lds_wait();
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         tie(vr[db][0]);
         tie(vr[db][1]);
-        Pack8 vv;
-        vv.u = u32x4{vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma_f16(vv.h, pf[hf][rb], o[rb][db]);
       }
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) o[rb][DB] = mfma_f16(ones, pf[hf][rb], o[rb][DB]);
+      SD_PV_MFMA(vr, pf, hf)
     }
-  };
-
-  // Ring schedule: at step it, tile it (converted in step it-1) is computed,
-  // tile it+1 (landed) is converted, tiles it+2 and it+3 are in flight.
-  // Every step issues one tile (re-reading the last past the end), so the
-  // wait count is the same at every step.
-#pragma unroll
-  for (int i = 0; i < NBUF - 1; ++i) issue(min(i, last), ring[i]);
-  wait_vm_then_barrier<(NBUF - 2) * DMA_PER_WAVE>();   // tile 0 landed
-  convert(ring[0]);
-  for (int it = 0; it < ntiles; ++it) {
-    // tile it+1 landed; tile it converted by every wave; slot it-1 free
-    wait_vm_then_barrier<(NBUF - 3) * DMA_PER_WAVE>();
-    issue(min(it + NBUF - 1, last), ring[(it + NBUF - 1) % NBUF]);
-    if (it + 1 < ntiles) convert(ring[(it + 1) % NBUF]);
-    compute(it, ring[it % NBUF]);
   }
+#undef SD_QK_READ
+#undef SD_QK_MFMA
+#undef SD_P_ROW
+#undef SD_PV_READ
+#undef SD_PV_MFMA
+#undef SD_INTERLEAVE
   __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // no copy in flight at exit
 
   // normalise and write (directly, or as a partial for the merge)
@@ -419,7 +648,8 @@ hipError_t dispatch_nw(const CompressArgs& a, const CompressPlan& p, hipStream_t
   switch (p.lat_tile / 32) {
     case 1: return launch_bf16<1, DH>(a, p, st);
     case 2: return launch_bf16<2, DH>(a, p, st);
-    default: return launch_bf16<4, DH>(a, p, st);
+    case 4: return launch_bf16<4, DH>(a, p, st);
+    default: return launch_bf16<8, DH>(a, p, st);
   }
 }
 
@@ -436,7 +666,10 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype) {
     const long long cap = (65536 - 4LL * kF32Rows * p.dh - 16 * kF32Rows) / (8 * kF32Rows);
     p.tokens_per_split = (int)std::max(64LL, std::min(2048LL, cap / 64 * 64));
   } else {
-    const int waves = C <= 32 ? 1 : (C <= 64 ? 2 : 4);   // 32 latents per wave
+    // 32 latents per wave; eight-wave groups (F_V tiles shared by 256
+    // latents) when that still gives a full grid without token splits
+    int waves = C <= 32 ? 1 : (C <= 64 ? 2 : 4);
+    if (C > 128 && (long long)n_bh * ((C + 255) / 256) >= 256) waves = 8;
     p.lat_tile = waves * 32;
     p.lat_tiles = (C + p.lat_tile - 1) / p.lat_tile;
     // split the tokens until about 512 work-groups exist, keeping >= 256 tokens each

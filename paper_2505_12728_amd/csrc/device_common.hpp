@@ -123,6 +123,30 @@ __device__ __forceinline__ void tie(T& x) {
   asm volatile("" : "+v"(x));
 }
 
+// LDS swizzle of the 16-byte pieces of tile row t (a token or key) for rows
+// of PK pieces: piece p is stored at slot p ^ lds_swizzle<PK>(t).  gfx950's
+// LDS has 64 four-byte banks; a 16-byte read serves 16 lanes per pass and
+// the 8-byte transposing read 32 lanes, so
+//   - 16 consecutive rows read at one piece (matrix-core fragments of 16
+//     rows x 8 elements) must fill the 256 bank bytes, and
+//   - 8 consecutive rows read at two adjacent pieces each (transposed
+//     fragments of 4 rows x 4 elements per 16 lanes) must too.
+// For 256-byte rows (PK = 16) the swizzle is a permutation of 0..15 whose
+// bits 1..3 differ within each aligned 8 rows; for 128-byte rows (PK = 8,
+// two rows per bank row) a permutation of 0..7 on each row parity whose
+// bits 1..2 differ within each aligned quad of that parity.
+template <int PK>
+__device__ __forceinline__ constexpr int lds_swizzle(int t) {
+  static_assert(PK == 8 || PK == 16, "rows of 128 or 256 bytes");
+  t &= 15;
+  if constexpr (PK == 16) {
+    return ((t & 7) << 1) | ((t >> 3) & 1);
+  } else {
+    const int u = (t >> 1) & 7;
+    return ((u & 3) << 1) | (u >> 2);
+  }
+}
+
 // Reductions over the four lanes l, l^16, l^32, l^48 (same column c, the
 // four groups).  gfx950's v_permlane32_swap / v_permlane16_swap exchange
 // halves / odd-even rows of two registers; applied to two copies of v they

@@ -41,26 +41,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_cvoid;
 
 
-// LDS swizzle of the 16-byte pieces of token t: piece p is stored at slot
-// p ^ swz<DH>(t & 15).  gfx950's LDS has 64 four-byte banks; a 16-byte read
-// serves 16 lanes per pass and the 8-byte transposing read 32 lanes, so
-//   - 16 consecutive tokens read at one piece must fill the 256 bank bytes
-//     (score reads), and
-//   - 8 consecutive tokens read at two adjacent pieces each (value reads)
-//     must too.
-// For 256-byte rows (DH = 128) that means swz is a permutation of 0..15 whose
-// bits 1..3 differ within each 8-token half; for 128-byte rows (DH = 64, two
-// tokens per bank row) a permutation of 0..7 on each token parity whose bits
-// 1..2 differ within each quad of that parity.
+// LDS swizzle of the F_V tile rows (see lds_swizzle)
 template <int DH>
 __device__ __forceinline__ constexpr int swz(int t) {
-  t &= 15;
-  if constexpr (DH == 128) {
-    return ((t & 7) << 1) | ((t >> 3) & 1);
-  } else {
-    const int u = (t >> 1) & 7;
-    return ((u & 3) << 1) | (u >> 2);
-  }
+  return lds_swizzle<DH / 8>(t);
 }
 
 // Compile-time loop: f(std::integral_constant<int, I>{}) for I = B .. E-1.

@@ -69,9 +69,9 @@ __device__ __forceinline__ int seq_len(const VerifyArgs& a, int b, bool paged) {
 // HBM -> LDS by the global_load_lds DMA (no VGPR staging) into a ring of
 // NBUF buffers, NBUF - 1 tiles ahead of the compute; with two or three
 // work-groups per compute unit about 96 KB per unit is in flight.  Each key
-// row keeps its 16-byte pieces XOR-swizzled by (key & 7), so the K-fragment
-// reads (16 keys x one piece) and the transposed V reads (4 keys x 8 bytes
-// per 16 lanes) fall on distinct banks.
+// row keeps its 16-byte pieces XOR-swizzled by lds_swizzle(key), so the
+// K-fragment reads (16 keys x one piece) and the transposed V reads (4 keys
+// x 8 bytes per 16 lanes) are free of bank conflicts.
 //
 // Per tile a wave does 8 + 16 matrix-core ops and little else: the causal
 // mask is applied only on the tail tile, the running maximum is raised (and
@@ -171,7 +171,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
 
   // Copy i of this wave (ii = w * DMA_PER_WAVE + i) covers half
   // ii / DMA_PER_HALF (K or V) and pieces P = (ii % DMA_PER_HALF) * 64 +
-  // lane: key P / PK, LDS slot P % PK holding global piece slot ^ (key & 7).
+  // lane: key P / PK, LDS slot P % PK holding global piece slot ^ lds_swizzle(key).
   // Its source is a per-lane constant plus a per-tile offset, except in the
   // tail tile, where keys past the sequence re-read its last key (masked).
   // Page ids are scalar loads, so they do not count against vmcnt.
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     const int P = (ii % DMA_PER_HALF) * 64 + lane;
     const int key = P / PK, piece = P % PK;
     ckey[i] = key;
-    const size_t pieceoff = (size_t)((piece ^ (key & 7)) * 8);
+    const size_t pieceoff = (size_t)((piece ^ lds_swizzle<PK>(key)) * 8);
     if constexpr (PAGED)
       cbase[i] = (((size_t)hk * 16 + (key & 15)) * D) + pieceoff;
     else
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
       const int key = kb * 16 + c;
-      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G) ^ (key & 7)) * 16);
+      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G) ^ lds_swizzle<PK>(key)) * 16);
     }
   // ds_read_tr16_b64: lane j of group G addresses key 4G + j/4 (+16) at
   // channels db*16 + 4*(j%4); lane c then receives 4 keys at channel db*16 + c
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     for (int db = 0; db < DB; ++db) {
       const int key = hh * 16 + 4 * G + (c >> 2);
       const int ch = db * 16 + 4 * (c & 3);
-      voff[hh][db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ (key & 7)) * 16) + (ch & 7) * 2;
+      voff[hh][db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ lds_swizzle<PK>(key)) * 16) + (ch & 7) * 2;
     }
 
   auto compute = [&](int it, const unsigned char* slot) {

@@ -457,9 +457,12 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 }
 
 // ---------------------------------------------------------------- merge
-// One wave per output row of one (sequence, KV head): the lanes find the
-// largest split lse, then lanes d4 < D/4 accumulate the weighted partial
-// outputs (4 channels each).  Grid (rows / 4, sequence x KV head).
+// One wave per output row of one (sequence, KV head).  The lanes load the
+// split lse values 64 at a time and form their weights 2^(lse - max) in
+// parallel; then the two half-waves take alternate splits, each lane
+// accumulating 4 channels of the weighted partial outputs (loads of
+// several splits in flight), and the halves are added at the end.
+// Grid (rows / 4, sequence x KV head).
 __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_split,
                                                     int nsplit, int rows_padded, int paged) {
   const int pair = blockIdx.y;
@@ -478,25 +481,36 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
   for (int s = lane; s < nvalid; s += 64) mx = fmaxf(mx, a.part_lse[base + (size_t)s * rows_padded]);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-  const int d4 = lane;
+  const int half = lane >> 5, d4 = lane & 31;
+  const bool active = d4 < D / 4;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
   if (mx != -INFINITY) {
+    for (int s0 = 0; s0 < nvalid; s0 += 64) {
+      const int n = min(64, nvalid - s0);
+      float wl = 0.f;
+      if (lane < n) {
+        const float ls = a.part_lse[base + (size_t)(s0 + lane) * rows_padded];
+        wl = ls == -INFINITY ? 0.f : exp2f(ls - mx);
+      }
+      wsum += wl;
 #pragma unroll 4
-    for (int s = 0; s < nvalid; ++s) {
-      const size_t pr = base + (size_t)s * rows_padded;
-      const float ls = a.part_lse[pr];
-      const float wgt = ls == -INFINITY ? 0.f : exp2f(ls - mx);
-      wsum += wgt;
-      if (d4 < D / 4 && wgt != 0.f)
-        acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
+      for (int j = half; j < n; j += 2) {
+        const float wgt = __shfl(wl, j, 64);
+        const size_t pr = base + (size_t)(s0 + j) * rows_padded;
+        if (active && wgt != 0.f) acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
+      }
     }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wsum += __shfl_xor(wsum, off, 64);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], 32, 64);
   }
   const int j = r / g;
   const int h = hk * g + (r - j * g);
   const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  if (d4 < D / 4) *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
+  if (half == 0 && active) *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
   if (a.lse != nullptr && lane == 0)
     a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
 }

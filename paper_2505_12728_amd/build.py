@@ -24,6 +24,9 @@ FLAGS = [
     "-fPIC",
     "-shared",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the kernels read them with
+    # VALU ops (rescale, normalisation), which AGPRs would turn into copies
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
     "-Wall",
     "-Wno-unused-result",

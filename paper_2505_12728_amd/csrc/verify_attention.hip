@@ -100,9 +100,12 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
   constexpr float kRescale = 8.f;              // log2 headroom before rescaling
   __shared__ __align__(16) unsigned char ring[NBUF][BUF_BYTES];
 
-  const int split = blockIdx.x;
-  const int hk = blockIdx.y / row_groups;
-  const int rg = blockIdx.y % row_groups;
+  // grid (KV head x row group, split, sequence): the work-groups of one key
+  // range are dispatched together, so the heads of a key read their
+  // interleaved cache rows at about the same time
+  const int split = blockIdx.y;
+  const int hk = blockIdx.x / row_groups;
+  const int rg = blockIdx.x % row_groups;
   const int b = blockIdx.z;
   const int L = seq_len(a, b, PAGED);
   const int k0 = split * keys_per_split;
@@ -517,7 +520,7 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
 
 template <int D, int NW, bool PAGED>
 hipError_t launch_bf16(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
-  dim3 grid(p.nsplit, a.Hkv * p.row_groups, a.B);
+  dim3 grid(a.Hkv * p.row_groups, p.nsplit, a.B);
   hipLaunchKernelGGL((verify_split_bf16<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, a,
                      p.keys_per_split, p.nsplit, p.row_groups, p.rows_padded);
   return hipGetLastError();

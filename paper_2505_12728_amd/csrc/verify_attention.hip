@@ -559,9 +559,12 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     // A work-group holds a 64 KB (4 waves) or 48 KB (1-2 waves) LDS ring,
     // so two or three run per compute unit.  Aim for that many work-groups
     // per unit on 256 units, all resident at once; at least one 32-key tile
-    // per split.
+    // per split.  Small work-groups over long caches split four times
+    // finer: the splits are planned for the capacity, so with ragged
+    // sequence lengths the longest sequence would otherwise stream its keys
+    // through few work-groups, each bound by memory latency.
     const long long pairs = (long long)B * Hkv * p.row_groups;
-    const long long target = p.row_blocks == 4 ? 512 : 768;
+    const long long target = p.row_blocks == 4 ? 512 : (capacity >= 8192 ? 3072 : 768);
     long long nsplit = std::max(1LL, (target + pairs - 1) / pairs);
     long long kps = (capacity + nsplit - 1) / nsplit;
     kps = std::max((long long)kTile, (kps + kTile - 1) / kTile * kTile);

@@ -14,7 +14,9 @@ Prints one JSON line.  `value` is the verify step's KV-read rate: bytes of
 K and V the step must read once, divided by the time of verification
 attention plus acceptance, in TB/s.  Per-kernel times come from HIP events
 on the stream the kernels run on.  `roofline` describes the dominant kernel
-(the longest per step); `rooflines` lists all three.  `cpu_baseline` times
+(the longest per step); `rooflines` lists all three.  `traffic` is the HBM
+bytes per launch measured with rocprofv3 counters (profiles/), or null when
+the kernel's sources changed since they were taken.  `cpu_baseline` times
 the plain CPU oracle on a bounded sample of the same workload and scales it
 to the whole step.
 """
@@ -113,6 +115,34 @@ def cpu_baseline(w, comp, ver, acc, mode):
             "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
                       f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
                       f"pairs, acceptance of all {w.batch} sequences; scaled linearly"}
+
+
+def counter_traffic(workload):
+    """HBM bytes per launch from the committed counter summary of `workload`.
+
+    profiles/<workload>_hbm_counters.md holds FETCH_SIZE / WRITE_SIZE per
+    dispatch (calibrated against a plain device copy) together with the
+    SHA-256 of the sources each kernel was built from.  A kernel whose
+    sources have changed since gets None (its counters no longer apply).
+    """
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_counters.md")
+    if not os.path.exists(path):
+        return {}
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return {}
+    data = json.loads(text[start + 7:text.index("```", start + 7)])
+    csrc = os.path.join(ROOT, "paper_2505_12728_amd", "csrc")
+    out = {}
+    for name, k in data["kernels"].items():
+        digest = hashlib.sha256()
+        for f in k["sources"]:
+            with open(os.path.join(csrc, f), "rb") as fh:
+                digest.update(fh.read())
+        out[name] = k["hbm_bytes_per_launch"] if digest.hexdigest()[:16] == k["source_sha256_16"] else None
+    return out
 
 
 def main():
@@ -223,8 +253,10 @@ def main():
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
                         "algorithmic": a_bytes, "us": t_a * 1e3},
     }
-    for r in rl.values():
+    traffic = counter_traffic(w.name)
+    for name_, r in rl.items():
         r["frac"] = r["achieved"] / r["peak"]
+        r["traffic"] = traffic.get(name_)
     dominant = max(rl, key=lambda k_: rl[k_]["us"])
     roof = {k_: rl[dominant][k_] for k_ in ("bound", "achieved", "peak", "unit", "frac",
                                              "traffic")}

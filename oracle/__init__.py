@@ -16,6 +16,9 @@ reader can check it against the paper by eye:
 * ``spec_accept``      -- token-wise acceptance / rejection with residual
   resampling (Sec. 3.1, Sec. 3.3), and greedy verification for temperature 0
   (Sec. 4.2).
+* ``lm_head_probs`` / ``sample_tokens`` -- the LM head's temperature softmax
+  over the vocabulary and categorical sampling of the drafts (Sec. 3.1,
+  Sec. 3.3, Algorithm 1).
 
 Readings of points the paper leaves open are stated in each module.  No
 function here is "parity unpinned": every one is checked in
@@ -25,6 +28,7 @@ enumeration or brute force.
 
 from .compress import latent_compress, softmax_rows
 from .verify import verify_attention, gather_paged, merge_partials
+from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept import (
     spec_accept,
     spec_accept_one,
@@ -52,4 +56,8 @@ __all__ = [
     "ACCEPT_SAMPLED",
     "FIXED_POINT_BITS",
     "UNIFORM_BITS",
+    "lm_head_logits",
+    "softmax_temperature",
+    "lm_head_probs",
+    "sample_tokens",
 ]

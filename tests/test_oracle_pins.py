@@ -588,3 +588,92 @@ def test_accept_batch_matches_per_sequence():
     for b in range(B):
         nb, tb = oracle.spec_accept_one(p[b], q[b], d[b], u[b], oracle.ACCEPT_SAMPLED)
         assert n[b] == nb and list(t[b]) == tb
+
+
+# ---------------------------------------------------------------- LM head
+# Sec. 3.1 (the head maps a feature to a vocabulary distribution), Sec. 3.3
+# and Algorithm 1 (the draft's states projected by the same head, drafts
+# drawn from the result), Sec. 4.2 (temperature).
+
+def test_lm_head_zero_weights_give_uniform():
+    r = rng(41)
+    h = r.standard_normal((3, 8))
+    p = oracle.lm_head_probs(h, np.zeros((7, 8)), 0.7)
+    assert np.allclose(p, 1.0 / 7, atol=1e-15)
+
+
+def test_lm_head_two_token_logistic_closed_form():
+    # V = 2: p_1 = 1 / (1 + exp((z_0 - z_1) / tau)); pins the orientation
+    # (logit v = h . W[v]) and that the logits are divided by tau.
+    h = np.array([[1.5, -2.0, 0.25]])
+    w = np.array([[0.5, 1.0, 2.0], [-1.0, 0.5, 4.0]])
+    z0 = 1.5 * 0.5 - 2.0 * 1.0 + 0.25 * 2.0
+    z1 = 1.5 * -1.0 - 2.0 * 0.5 + 0.25 * 4.0
+    for tau in (0.5, 1.0, 3.0):
+        p = oracle.lm_head_probs(h, w, tau)[0]
+        want = 1.0 / (1.0 + math.exp((z0 - z1) / tau))
+        assert abs(p[1] - want) < 1e-15 and abs(p[0] - (1.0 - want)) < 1e-15
+
+
+def test_lm_head_temperature_is_a_power_law():
+    # softmax(z / tau) is proportional to softmax(z)^(1 / tau)
+    r = rng(42)
+    h, w = r.standard_normal((2, 6)), r.standard_normal((9, 6))
+    p1 = oracle.lm_head_probs(h, w, 1.0)
+    for tau in (0.35, 0.7, 2.5):
+        pt = oracle.lm_head_probs(h, w, tau)
+        q = p1 ** (1.0 / tau)
+        assert np.allclose(pt, q / q.sum(axis=1, keepdims=True), rtol=1e-12, atol=1e-300)
+
+
+def test_lm_head_temperature_limits():
+    h = np.array([[1.0, 0.0]])
+    w = np.array([[0.3, 0.0], [0.9, 0.0], [0.1, 0.0]])
+    assert np.allclose(oracle.lm_head_probs(h, w, 1e7), 1.0 / 3, atol=1e-7)
+    p = oracle.lm_head_probs(h, w, 1e-3)
+    assert p[0, 1] > 1 - 1e-12 and np.argmax(p[0]) == 1
+
+
+def test_lm_head_shift_and_permutation():
+    r = rng(43)
+    h, w = r.standard_normal((3, 5)), r.standard_normal((11, 5))
+    p = oracle.lm_head_probs(h, w, 0.8)
+    # a constant added to every logit (an extra feature of 1 against a
+    # weight column of 2.5) changes nothing
+    h2 = np.concatenate([h, np.ones((3, 1))], axis=1)
+    w2 = np.concatenate([w, np.full((11, 1), 2.5)], axis=1)
+    assert np.allclose(oracle.lm_head_probs(h2, w2, 0.8), p, rtol=1e-12)
+    perm = r.permutation(11)
+    assert np.allclose(oracle.lm_head_probs(h, w[perm], 0.8), p[:, perm], rtol=1e-14)
+    assert np.allclose(p.sum(axis=1), 1.0, atol=1e-14)
+
+
+def test_lm_head_brute_force_tiny():
+    r = rng(44)
+    R, d, V, tau = 2, 3, 4, 0.6
+    h, w = r.standard_normal((R, d)), r.standard_normal((V, d))
+    got = oracle.lm_head_probs(h, w, tau)
+    for i in range(R):
+        z = [sum(h[i][j] * w[v][j] for j in range(d)) / tau for v in range(V)]
+        m = max(z)
+        e = [math.exp(x - m) for x in z]
+        for v in range(V):
+            assert abs(got[i][v] - e[v] / sum(e)) < 1e-14
+
+
+def test_sample_tokens_dyadic_thresholds():
+    # p = (1/4, 1/2, 1/8, 1/8): weights are exact, S = 2^40, T = a * 2^16,
+    # so the token changes exactly at u = 1/4, 3/4 and 7/8
+    p = np.array([[0.25, 0.5, 0.125, 0.125]] * 7, dtype=np.float32)
+    u = np.array([0.0, 0.25 - 2 ** -24, 0.25, 0.75 - 2 ** -24, 0.75, 0.875, 1 - 2 ** -24],
+                 dtype=np.float32)
+    assert list(oracle.sample_tokens(p, u)) == [0, 0, 1, 1, 2, 3, 3]
+
+
+def test_sample_tokens_one_hot_and_degenerate():
+    p = np.zeros((3, 5), dtype=np.float32)
+    p[0, 3] = 1.0
+    p[1, 1] = 1e-13                     # below 2^-40: no weight, argmax decides
+    p[1, 4] = 5e-13
+    u = np.array([0.9, 0.1, 0.3], dtype=np.float32)
+    assert list(oracle.sample_tokens(p, u)) == [3, 4, 0]

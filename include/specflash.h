@@ -14,6 +14,14 @@
  *                        resampling (Sec. 3.1, Sec. 3.3), or greedy
  *                        verification for temperature 0 (Sec. 4.2)
  *
+ * and, on either side of the acceptance, the steps that produce its inputs:
+ *
+ *   sd_lm_head_probs     the LM head: hidden states to token distributions
+ *                        p = softmax(h W^T / tau) (Sec. 3.1; Sec. 3.3 and
+ *                        Algorithm 1 for the draft's P'; tau of Sec. 4.2)
+ *   sd_sample_tokens     drafts drawn from their distributions,
+ *                        T' ~ Categorical(P') (Algorithm 1)
+ *
  * Conventions shared by every entry point
  * ---------------------------------------
  * - Every tensor pointer is DEVICE memory on the current HIP device, owned by
@@ -178,6 +186,55 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
                    const float* u, int32_t* n_accepted, int32_t* tokens,
                    int B, int k, int V, int mode,
                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * LM head with temperature softmax (Sec. 3.1: the head maps a feature to a
+ * distribution over the vocabulary; Sec. 3.3 and Algorithm 1: the draft's K
+ * hidden states go through the target's frozen head to give P'; Sec. 4.2:
+ * temperature tau).  For every row r and vocabulary entry v,
+ *
+ *   probs[r, v] = exp(z[r, v] / tau) / sum_u exp(z[r, u] / tau),
+ *   z[r, v]     = hidden[r] . weight[v]
+ *
+ * (a bias-free linear head; normalisation before it belongs to the model).
+ * Greedy decoding (tau = 0) uses the argmax of the logits, which any
+ * positive tau preserves: pass tau = 1 and take the argmax of probs.
+ *
+ *   hidden  [R, d] dtype    hidden states (target rows, or the draft's rows)
+ *   weight  [V, d] dtype    head weight (nn.Linear layout: one row per entry)
+ *   probs   [R, V] float32  out
+ *   workspace  sd_lm_head_workspace_size(R, d, V, dtype) bytes (per-block
+ *              and per-row softmax statistics)
+ * Requirements: R, d, V >= 1; temperature > 0 and finite; R <= 4096 and
+ * V <= 2^24; SD_BF16 needs d % 64 == 0 and 16-byte aligned hidden and
+ * weight; SD_F32 (float64 dot products, for accuracy checks rather than
+ * speed) takes any d.  The weight is streamed from HBM once per 64 rows.
+ * ---------------------------------------------------------------------- */
+size_t sd_lm_head_workspace_size(int R, int d, int V, int dtype);
+
+int sd_lm_head_probs(const void* hidden, const void* weight, float* probs,
+                     int R, int d, int V, float temperature, int dtype,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Categorical sampling of the drafts (Algorithm 1: T'_i ~ Categorical(P'_i)).
+ * Per row r, with the exact fixed-point inverse CDF of sd_spec_accept's
+ * final draw: weights R_v = floor(probs[r, v] * 2^40) (values clamped to
+ * [0, 1]), a = floor(u[r] * 2^24), T = floor(a * S / 2^24) with S = sum R;
+ * tokens[r] = the smallest v whose inclusive prefix sum of R exceeds T.
+ * All-zero weights give argmax probs[r] (lowest index).  Bit-exact and
+ * independent of summation order.
+ *
+ *   probs   [R, V] float32  distributions
+ *   u       [R]    float32  uniforms in [0, 1) (multiples of 2^-24)
+ *   tokens  [R]    int32    out
+ *   workspace  sd_sample_workspace_size(R, V) bytes
+ * Requirements: R >= 1; 1 <= V <= 2^18.
+ * ---------------------------------------------------------------------- */
+size_t sd_sample_workspace_size(int R, int V);
+
+int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R, int V,
+                     void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,8 @@ library is missing or the tensors are not on the GPU, the calls raise.
     sd_latent_compress   Sec. 3.2, Eq. 3 (learned queries attend over F_V)
     sd_verify_attention  Sec. 3.1 (one parallel pass over the K drafts)
     sd_spec_accept       Sec. 3.1 / 3.3 acceptance; greedy for Sec. 4.2
+    sd_lm_head_probs     Sec. 3.1 / 3.3, Algorithm 1: LM head + softmax(z / tau)
+    sd_sample_tokens     Algorithm 1: drafts drawn from their distributions
 """
 
 import ctypes
@@ -23,6 +25,8 @@ __all__ = [
     "sd_latent_compress_workspace_size", "sd_latent_compress",
     "sd_verify_workspace_size", "sd_verify_attention",
     "sd_spec_accept_workspace_size", "sd_spec_accept",
+    "sd_lm_head_workspace_size", "sd_lm_head_probs",
+    "sd_sample_workspace_size", "sd_sample_tokens",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -45,6 +49,10 @@ _SIGNATURES = {
                                  _i, _i, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
     "sd_spec_accept_workspace_size": (_sz, [_i, _i, _i, _i]),
     "sd_spec_accept": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "sd_lm_head_workspace_size": (_sz, [_i, _i, _i, _i]),
+    "sd_lm_head_probs": (_i, [_vp, _vp, _vp, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
+    "sd_sample_workspace_size": (_sz, [_i, _i]),
+    "sd_sample_tokens": (_i, [_vp, _vp, _vp, _i, _i, _vp, _sz, _vp]),
 }
 
 
@@ -254,3 +262,51 @@ def sd_spec_accept(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, toke
                                   _stream(stream))
     _raise(st, "sd_spec_accept")
     return n_accepted, tokens
+
+
+def sd_lm_head_workspace_size(R, d, V, dtype):
+    return library().sd_lm_head_workspace_size(R, d, V, dtype)
+
+
+def sd_lm_head_probs(hidden, weight, temperature, out=None, workspace=None, stream=None):
+    """LM head + temperature softmax: hidden [R, d], weight [V, d] (bf16 or
+    fp32, same dtype).  Returns probs [R, V] fp32 = softmax(hidden W^T / tau)."""
+    torch = _torch()
+    _check(hidden, "hidden", ndim=2)
+    _check(weight, "weight", dtype=hidden.dtype, ndim=2)
+    R, d = hidden.shape
+    V = weight.shape[0]
+    if weight.shape[1] != d:
+        raise ValueError("weight must be [V, d] with the hidden width d")
+    dt = _dtype_code(hidden)
+    if out is None:
+        out = torch.empty((R, V), dtype=torch.float32, device=hidden.device)
+    ws_bytes = sd_lm_head_workspace_size(R, d, V, dt)
+    ws, ws_len = _workspace(ws_bytes, hidden.device, workspace)
+    st = library().sd_lm_head_probs(_ptr(hidden), _ptr(weight), _ptr(out), R, d, V,
+                                    float(temperature), dt, _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_lm_head_probs")
+    return out
+
+
+def sd_sample_workspace_size(R, V):
+    return library().sd_sample_workspace_size(R, V)
+
+
+def sd_sample_tokens(probs, u, out=None, workspace=None, stream=None):
+    """T_r ~ Categorical(probs[r]) (exact fixed-point inverse CDF): probs [R, V]
+    fp32, u [R] fp32.  Returns tokens [R] int32."""
+    torch = _torch()
+    _check(probs, "probs", dtype=torch.float32, ndim=2)
+    _check(u, "u", dtype=torch.float32, ndim=1)
+    R, V = probs.shape
+    if u.shape[0] != R:
+        raise ValueError("u must be [R]")
+    if out is None:
+        out = torch.empty((R,), dtype=torch.int32, device=probs.device)
+    ws_bytes = sd_sample_workspace_size(R, V)
+    ws, ws_len = _workspace(ws_bytes, probs.device, workspace)
+    st = library().sd_sample_tokens(_ptr(probs), _ptr(u), _ptr(out), R, V, _ptr(ws), ws_len,
+                                    _stream(stream))
+    _raise(st, "sd_sample_tokens")
+    return out

@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspecflash.so")
-SOURCES = ["specflash_api.hip", "verify_attention.hip", "spec_accept.hip", "latent_compress.hip"]
+SOURCES = ["specflash_api.hip", "verify_attention.hip", "spec_accept.hip", "latent_compress.hip",
+           "lm_head.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -67,6 +67,19 @@ struct CompressArgs {
 
 hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dtype, hipStream_t s);
 
+// --------------------------------------------------------------- LM head
+struct LmHeadArgs {
+  const void* hidden;  // [R, d]
+  const void* weight;  // [V, d]
+  float* probs;        // [R, V]
+  int R, d, V;
+  float scale_log2;    // log2(e) / temperature
+  float* stats;        // workspace: [R][ceil(V/16)] block (max, sum), then [R] row (M, L)
+};
+
+size_t lm_head_workspace_bytes(int R, int V);
+hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t s);
+
 // ---------------------------------------------------------------- accept
 struct AcceptArgs {
   const float* p;

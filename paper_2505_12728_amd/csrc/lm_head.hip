@@ -1,0 +1,259 @@
+// LM head with temperature softmax (SpecFLASH Sec. 3.1: the head maps a
+// feature to a distribution over the vocabulary; Sec. 3.3 and Algorithm 1:
+// the draft's hidden states go through the target's frozen head; Sec. 4.2:
+// temperature):
+//   probs[r, v] = softmax_v(hidden[r] . weight[v] / tau)
+//
+// The pass is bound by streaming the weight [V, d] once (R <= 256 rows share
+// every weight byte), so the three kernels are shaped around that stream:
+// 1. logits, grid (vocabulary tile of 128 entries): each of 4 waves owns 32
+//    vocabulary rows and up to 64 hidden rows (more rows: one launch per 64,
+//    each streaming the weight again).  z^T = W H^T on bf16 matrix cores
+//    (lane = one hidden row); weight and hidden fragments come straight
+//    from global memory into registers, 64 channels at a time, the next 64
+//    in flight while the current ones are multiplied (the hidden rows are
+//    small and stay in L2).  The scaled logits s = z log2(e) / tau are
+//    written to `probs` as fp32, with the (max, sum of 2^(s - max)) of every
+//    16-entry vocabulary block and row.
+// 2. statistics, one work-group per row: the per-block pairs are merged
+//    into the row's (M, L).
+// 3. normalisation: probs = 2^(s - M) / L in place.
+// The fp32 path computes the logits as float64 dot products (one thread
+// per row and entry) and shares kernels 2 and 3.
+#include <math.h>
+
+#include <algorithm>
+
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace sd {
+namespace {
+
+// 16-entry vocabulary blocks per wave: two, so that the registers leave room
+// for several waves per SIMD (memory-level parallelism)
+template <int RB>
+constexpr int vblocks() { return 2; }
+template <int RB>
+constexpr int tile_v() { return 4 * vblocks<RB>() * 16; }   // entries per work-group (4 waves)
+
+struct Stat {
+  float m, l;
+};
+
+__device__ __forceinline__ Stat merge(Stat x, Stat y) {
+  if (y.m == -INFINITY) return x;
+  if (x.m == -INFINITY) return y;
+  const float m = fmaxf(x.m, y.m);
+  return Stat{m, x.l * fast_exp2(x.m - m) + y.l * fast_exp2(y.m - m)};
+}
+
+// statistics of 16 values spread as 4 per lane over the lanes c, c+16,
+// c+32, c+48 (one accumulator column); invalid entries are -inf
+__device__ __forceinline__ Stat column_stat(const floatx4& s) {
+  float m = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+  m = wave_max_across_groups(m);
+  float l = 0.f;
+  if (m != -INFINITY) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) l += fast_exp2(s[i] - m);
+  }
+  l = wave_sum_across_groups(l);
+  return Stat{m, l};
+}
+
+template <int RB>
+__global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a, int row0) {
+  constexpr int kVB = vblocks<RB>();
+  constexpr int kTileV = tile_v<RB>();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, G = lane >> 4, c = lane & 15;
+  const int v0 = blockIdx.x * kTileV + w * kVB * 16;   // this wave's first vocabulary row
+  // this launch's rows: row0 .. row0 + RB*16 - 1 of the R rows
+  const int d = a.d, V = a.V, R = min(a.R - row0, RB * 16);
+  const uint16_t* W = static_cast<const uint16_t*>(a.weight);
+  const uint16_t* H = static_cast<const uint16_t*>(a.hidden) + (size_t)row0 * d;
+  // fragment sources: vocabulary row v0 + vb*16 + c and hidden row rb*16 + c
+  // (both clamped into range; their results are discarded), channels
+  // k + 8G .. k + 8G + 7 of each 32-channel step
+  const u32x4* wsrc[kVB];
+  const u32x4* hsrc[RB];
+#pragma unroll
+  for (int vb = 0; vb < kVB; ++vb)
+    wsrc[vb] = reinterpret_cast<const u32x4*>(W + (size_t)min(v0 + vb * 16 + c, V - 1) * d + 8 * G);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+    hsrc[rb] = reinterpret_cast<const u32x4*>(H + (size_t)min(rb * 16 + c, R - 1) * d + 8 * G);
+
+  floatx4 acc[kVB][RB];
+#pragma unroll
+  for (int vb = 0; vb < kVB; ++vb)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // 64-channel groups (two 32-channel steps), double-buffered in registers
+  u32x4 wa[2][kVB], ha[2][RB], wb[2][kVB], hb[2][RB];
+  auto load = [&](u32x4 (&wf)[2][kVB], u32x4 (&hf)[2][RB], int k) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int vb = 0; vb < kVB; ++vb) wf[s][vb] = wsrc[vb][(k + 32 * s) / 8];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) hf[s][rb] = hsrc[rb][(k + 32 * s) / 8];
+    }
+  };
+  auto mma = [&](const u32x4 (&wf)[2][kVB], const u32x4 (&hf)[2][RB]) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int vb = 0; vb < kVB; ++vb) {
+        Pack8 x;
+        x.u = wf[s][vb];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          Pack8 y;
+          y.u = hf[s][rb];
+          acc[vb][rb] = mfma_bf16(x.b, y.b, acc[vb][rb]);
+        }
+      }
+  };
+  load(wa, ha, 0);
+  int k = 0;
+#pragma unroll 1
+  for (; k + 128 <= d; k += 128) {
+    load(wb, hb, k + 64);
+    mma(wa, ha);
+    if (k + 128 < d) load(wa, ha, k + 128);
+    mma(wb, hb);
+  }
+  if (k < d) mma(wa, ha);   // d % 128 == 64: one group left
+
+  // scaled logits, per-block statistics, fp32 logits to probs
+  float2* stats = reinterpret_cast<float2*>(a.stats);
+  const int nblk = (V + 15) / 16;
+#pragma unroll
+  for (int vb = 0; vb < kVB; ++vb) {
+    const int vbase = v0 + vb * 16;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      floatx4 s;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = vbase + 4 * G + i;
+        s[i] = v < V ? acc[vb][rb][i] * a.scale_log2 : -INFINITY;
+      }
+      const Stat st = column_stat(s);
+      const int r = rb * 16 + c;
+      if (r < R && vbase < V) {
+        float* dst = a.probs + (size_t)(row0 + r) * V + vbase + 4 * G;
+        if (vbase + 4 * G + 3 < V && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+          *reinterpret_cast<floatx4*>(dst) = s;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (vbase + 4 * G + i < V) dst[i] = s[i];
+        }
+        if (G == 0) stats[(size_t)(row0 + r) * nblk + vbase / 16] = make_float2(st.m, st.l);
+      }
+    }
+  }
+}
+
+// fp32 inputs: one thread per (row, vocabulary entry), float64 dot product;
+// 16 consecutive lanes form one 16-entry block for the statistics
+__global__ __launch_bounds__(256) void lm_logits_f32(LmHeadArgs a) {
+  const int r = blockIdx.y;
+  const int v = blockIdx.x * 256 + threadIdx.x;
+  const int d = a.d, V = a.V;
+  const float* h = static_cast<const float*>(a.hidden) + (size_t)r * d;
+  float s = -INFINITY;
+  if (v < V) {
+    const float* wr = static_cast<const float*>(a.weight) + (size_t)v * d;
+    double z = 0.0;
+    for (int j = 0; j < d; ++j) z += (double)h[j] * (double)wr[j];
+    s = (float)(z * (double)a.scale_log2);
+    a.probs[(size_t)r * V + v] = s;
+  }
+  float m = s;
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  float l = m == -INFINITY ? 0.f : fast_exp2(s - m);
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) l += __shfl_xor(l, o, 64);
+  const int nblk = (V + 15) / 16;
+  if ((threadIdx.x & 15) == 0 && v < V)
+    reinterpret_cast<float2*>(a.stats)[(size_t)r * nblk + v / 16] = make_float2(m, l);
+}
+
+// one work-group per row: merge the per-block statistics into (M, L)
+__global__ __launch_bounds__(256) void lm_stats(LmHeadArgs a) {
+  __shared__ Stat part[4];
+  const int r = blockIdx.x;
+  const int nblk = (a.V + 15) / 16;
+  const float2* st = reinterpret_cast<const float2*>(a.stats) + (size_t)r * nblk;
+  Stat acc{-INFINITY, 0.f};
+  for (int i = threadIdx.x; i < nblk; i += 256) {
+    const float2 x = st[i];
+    acc = merge(acc, Stat{x.x, x.y});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = merge(acc, Stat{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.l, o, 64)});
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    Stat t = part[0];
+    for (int i = 1; i < 4; ++i) t = merge(t, part[i]);
+    reinterpret_cast<float2*>(a.stats)[(size_t)a.R * nblk + r] = make_float2(t.m, t.l);
+  }
+}
+
+// probs = 2^(s - M) / L, in place
+__global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
+  const int r = blockIdx.y;
+  const int V = a.V;
+  const int nblk = (V + 15) / 16;
+  const float2 ML = reinterpret_cast<const float2*>(a.stats)[(size_t)a.R * nblk + r];
+  const float inv = 1.f / ML.y;
+  float* row = a.probs + (size_t)r * V;
+  for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += gridDim.x * 256) row[v] = fast_exp2(row[v] - ML.x) * inv;
+}
+
+template <int RB>
+hipError_t launch_rb(const LmHeadArgs& a, int row0, hipStream_t st) {
+  hipLaunchKernelGGL((lm_logits_bf16<RB>), dim3((a.V + tile_v<RB>() - 1) / tile_v<RB>()), dim3(256), 0, st,
+                     a, row0);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t lm_head_workspace_bytes(int R, int V) {
+  const size_t nblk = ((size_t)V + 15) / 16;
+  return ((size_t)R * nblk + (size_t)R) * sizeof(float2);
+}
+
+hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t st) {
+  hipError_t e = hipSuccess;
+  if (dtype == 0) {
+    hipLaunchKernelGGL(lm_logits_f32, dim3((a.V + 255) / 256, a.R), dim3(256), 0, st, a);
+    e = hipGetLastError();
+  } else {
+    // at most 64 rows per launch (the weight is streamed once per launch)
+    for (int row0 = 0; row0 < a.R && e == hipSuccess; row0 += 64) {
+      switch ((min(a.R - row0, 64) + 15) / 16) {
+        case 1: e = launch_rb<1>(a, row0, st); break;
+        case 2: e = launch_rb<2>(a, row0, st); break;
+        case 3: e = launch_rb<3>(a, row0, st); break;
+        default: e = launch_rb<4>(a, row0, st); break;
+      }
+    }
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(lm_stats, dim3(a.R), dim3(256), 0, st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int per_row = (a.V + 255) / 256;
+  hipLaunchKernelGGL(lm_normalize, dim3(per_row < 64 ? per_row : 64, a.R), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace sd

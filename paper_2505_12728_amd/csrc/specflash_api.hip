@@ -187,4 +187,70 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const f
   return status_from(sd::launch_accept(a, workspace, static_cast<hipStream_t>(stream)));
 }
 
+// -------------------------------------------------------------- LM head
+size_t sd_lm_head_workspace_size(int R, int d, int V, int dtype) {
+  if (R < 1 || d < 1 || V < 1 || R > 4096 || V > (1 << 24) || (dtype != SD_F32 && dtype != SD_BF16))
+    return 0;
+  return sd::lm_head_workspace_bytes(R, V);
+}
+
+int sd_lm_head_probs(const void* hidden, const void* weight, float* probs, int R, int d, int V,
+                     float temperature, int dtype, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  if (R < 1 || d < 1 || V < 1 || (dtype != SD_F32 && dtype != SD_BF16)) return SD_ERR_INVALID_ARG;
+  if (!(temperature > 0.f) || !isfinite(temperature)) return SD_ERR_INVALID_ARG;
+  if (!hidden || !weight || !probs || !aligned(probs, 4)) return SD_ERR_INVALID_ARG;
+  if (R > 4096 || V > (1 << 24)) return SD_ERR_UNSUPPORTED;
+  if (dtype == SD_BF16) {
+    if (d % 64 != 0) return SD_ERR_UNSUPPORTED;
+    if (!aligned(hidden, 16) || !aligned(weight, 16)) return SD_ERR_INVALID_ARG;
+  } else if (!aligned(hidden, 4) || !aligned(weight, 4)) {
+    return SD_ERR_INVALID_ARG;
+  }
+  const size_t need = sd::lm_head_workspace_bytes(R, V);
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
+  sd::LmHeadArgs a{};
+  a.hidden = hidden;
+  a.weight = weight;
+  a.probs = probs;
+  a.R = R;
+  a.d = d;
+  a.V = V;
+  a.scale_log2 = 1.4426950408889634f / temperature;
+  a.stats = static_cast<float*>(workspace);
+  return status_from(sd::launch_lm_head(a, dtype, static_cast<hipStream_t>(stream)));
+}
+
+// ------------------------------------------------------------- sampling
+// T ~ Categorical(p) is the acceptance rule's final draw with no drafts:
+// the acceptance kernels run with k = 0 (no tests; u[r] drives the draw).
+size_t sd_sample_workspace_size(int R, int V) {
+  if (R < 1 || V < 1 || V > (1 << 18)) return 0;
+  const size_t acc = (sd::accept_workspace_bytes(R, 0, V, SD_ACCEPT_SAMPLED) + 15) / 16 * 16;
+  return acc + (size_t)R * sizeof(int32_t);
+}
+
+int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R, int V,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  if (R < 1 || V < 1) return SD_ERR_INVALID_ARG;
+  if (V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (!probs || !u || !tokens || !aligned(probs, 4) || !aligned(u, 4) || !aligned(tokens, 4))
+    return SD_ERR_INVALID_ARG;
+  const size_t acc = (sd::accept_workspace_bytes(R, 0, V, SD_ACCEPT_SAMPLED) + 15) / 16 * 16;
+  const size_t need = acc + (size_t)R * sizeof(int32_t);
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
+  sd::AcceptArgs a{};
+  a.p = probs;
+  a.q = nullptr;
+  a.draft = nullptr;
+  a.u = u;
+  a.n_accepted = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + acc);
+  a.tokens = tokens;
+  a.B = R;
+  a.k = 0;
+  a.V = V;
+  a.mode = SD_ACCEPT_SAMPLED;
+  return status_from(sd::launch_accept(a, workspace, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -38,7 +38,8 @@ POISON = 8192.0          # exact in bfloat16 and float32
 
 # stream order for SeedSequence.spawn; never reorder (it changes every value)
 _STREAMS = ("latents", "feats", "q", "k", "v", "target_logits", "draft_noise",
-            "draft_uniforms", "accept_uniforms", "kv_lens", "page_perm")
+            "draft_uniforms", "accept_uniforms", "kv_lens", "page_perm",
+            "lm_hidden", "lm_weight", "sample_uniforms")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -65,6 +66,9 @@ class Workload:
     vocab: int = 0
     modes: tuple = ("sampled",)
     temperature: float = 1.0
+    # LM head (hidden width d of the head; its rows are the batch's k+1
+    # target positions)
+    lm_width: int = 0
 
     @property
     def seed(self):
@@ -75,23 +79,23 @@ WORKLOADS = [
     Workload("tiny-f32", "f32", batch=1, hq=4, hkv=1, head_dim=64, kv_len=608,
              block=4, c_batch=1, c_tokens=576, c_width=256, c_latents=16,
              c_heads=1, vocab=1024, modes=("sampled", "greedy"),
-             temperature=1.0),
+             temperature=1.0, lm_width=256),
     Workload("llava-7b-image", "bf16", batch=1, hq=32, hkv=32, head_dim=128,
              kv_len=1200, block=5, c_batch=1, c_tokens=576, c_width=4096,
              c_latents=64, c_heads=32, vocab=32000, modes=("sampled",),
-             temperature=1.0),
+             temperature=1.0, lm_width=4096),
     Workload("qwen2vl-7b-video", "bf16", batch=1, hq=28, hkv=4, head_dim=128,
              kv_len=6528, block=8, c_batch=1, c_tokens=6272, c_width=3584,
              c_latents=256, c_heads=28, vocab=152064,
-             modes=("greedy", "sampled"), temperature=1.0),
+             modes=("greedy", "sampled"), temperature=1.0, lm_width=3584),
     Workload("batched-paged", "bf16", batch=16, hq=32, hkv=8, head_dim=128,
              kv_len=16384, kv_len_min=2048, block=6, paged=True, c_batch=16,
              c_tokens=1024, c_width=4096, c_latents=128, c_heads=32,
-             vocab=32000, modes=("sampled",), temperature=1.0),
+             vocab=32000, modes=("sampled",), temperature=1.0, lm_width=4096),
     Workload("long-video", "bf16", batch=4, hq=64, hkv=8, head_dim=128,
              kv_len=65536, block=8, c_batch=4, c_tokens=16384, c_width=8192,
              c_latents=512, c_heads=64, vocab=152064, modes=("sampled",),
-             temperature=0.7),
+             temperature=0.7, lm_width=8192),
 ]
 
 
@@ -341,6 +345,32 @@ def accept_inputs(w, mode, seed=None, batch=None):
 
 
 # --------------------------------------------------------- byte / flop counts
+
+def lm_inputs(w, seed=None, rows=None, vocab=None):
+    """LM head inputs: hidden states [R, d] ~ N(0, 1) and a head weight
+    [V, d] ~ N(0, 9 / d) (logits then spread like N(0, 3^2), as the
+    synthetic target logits do), in the workload's dtype, plus R sampling
+    uniforms on the 2^-24 grid.  R defaults to batch * (k + 1)."""
+    rs = streams(w.seed if seed is None else seed)
+    R = w.batch * (w.block + 1) if rows is None else rows
+    V = w.vocab if vocab is None else vocab
+    d = w.lm_width
+    hidden = Tensor(normal(rs["lm_hidden"], (R, d)), w.dtype)
+    wv = normal(rs["lm_weight"], (V, d))
+    _parallel_map(lambda x: x * np.float32(3.0 / math.sqrt(d)), wv, wv)
+    weight = Tensor(wv, w.dtype)
+    del wv
+    u = (rs["sample_uniforms"].gen.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    return {"hidden": hidden, "weight": weight, "u": u, "temperature": w.temperature}
+
+
+def lm_bytes(w, rows=None):
+    """Algorithmic HBM bytes of one LM head pass: the weight and the hidden
+    states read once, the probabilities written once."""
+    R = w.batch * (w.block + 1) if rows is None else rows
+    es = 2 if w.dtype == "bf16" else 4
+    return w.vocab * w.lm_width * es + R * w.lm_width * es + R * w.vocab * 4
+
 
 def verify_kv_bytes(w, lens=None):
     """K and V bytes the verification must read once: 2 * Hkv * D * es per token."""

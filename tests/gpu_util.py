@@ -8,6 +8,15 @@ import numpy as np
 TOL = {"bf16": 5e-3, "f32": 1e-5}
 # lse is a log-domain scalar of size O(log L + |s|); absolute bound
 LSE_TOL = {"bf16": 1e-3, "f32": 1e-5}
+# Probability vectors (the LM head's softmax): per entry
+# |p_gpu - p_ref| <= rel * p_ref + abs.  The inputs are exact in float32, so
+# the error is the float32 accumulation of the d-term logit (about
+# 2^-24 sqrt(d) times the size of the terms: ~2e-5 at d = 8192) divided by
+# tau, plus a few ulp in the exponent; rel = 2e-3 bounds the logit error to
+# 2e-3 tau with a wide margin.  fp32 inputs are summed in float64.  (A
+# max / rms norm grows like sqrt(V) for peaked distributions, so it is not
+# used for them.)
+PROB_TOL = {"bf16": (2e-3, 1e-7), "f32": (1e-5, 1e-12)}
 
 
 def to_device(t):
@@ -48,3 +57,15 @@ def assert_lse_close(gpu, ref, dtype, what):
     if fin.any():
         err = float(np.max(np.abs(gpu[fin] - ref[fin])))
         assert err <= LSE_TOL[dtype], f"{what}: lse error {err:.3g}"
+
+
+def assert_probs_close(gpu, ref, dtype, what):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    rel, ab = PROB_TOL[dtype]
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite output"
+    excess = np.abs(gpu - ref) - (rel * ref + ab)
+    i = np.unravel_index(np.argmax(excess), excess.shape)
+    assert excess[i] <= 0, (f"{what}: |gpu - ref| = {abs(gpu[i] - ref[i]):.3g} at {i} "
+                            f"(ref {ref[i]:.3g}) exceeds {rel} * ref + {ab}")
+    return float(np.max(np.abs(gpu - ref) / (ref + ab)))

@@ -132,3 +132,47 @@ def test_workspace_sizes_cover_the_partials(lib):
             assert n > 0 and n % 4 == 0
             assert n >= B * Hkv * k * (Hq // Hkv) * (D + 1) * 4
     assert lib.sd_verify_workspace_size(1, 4, 6, 4, 128, 100, 1) == 0   # invalid shape
+
+
+def test_lm_head_validation_errors(lib):
+    keep, (h, w, out, ws) = _fake(4)
+    f = lib.sd_lm_head_probs
+
+    def call(h=h, w=w, out=out, R=4, d=128, V=1000, tau=1.0, dt=1, ws=ws, wsb=1 << 30):
+        return f(h, w, out, R, d, V, tau, dt, ws, wsb, None)
+
+    assert call(h=None) == sd.SD_ERR_INVALID_ARG
+    assert call(out=None) == sd.SD_ERR_INVALID_ARG
+    assert call(R=0) == sd.SD_ERR_INVALID_ARG
+    assert call(V=0) == sd.SD_ERR_INVALID_ARG
+    assert call(tau=0.0) == sd.SD_ERR_INVALID_ARG
+    assert call(tau=-1.0) == sd.SD_ERR_INVALID_ARG
+    assert call(tau=float("nan")) == sd.SD_ERR_INVALID_ARG
+    assert call(tau=float("inf")) == sd.SD_ERR_INVALID_ARG
+    assert call(dt=3) == sd.SD_ERR_INVALID_ARG
+    assert call(d=100) == sd.SD_ERR_UNSUPPORTED               # bf16: d % 64
+    assert call(R=5000) == sd.SD_ERR_UNSUPPORTED
+    assert call(h=ctypes.c_void_p(h.value + 8)) == sd.SD_ERR_INVALID_ARG   # bf16: 16-byte aligned
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=8) == sd.SD_ERR_WORKSPACE
+    # block (max, sum) pairs of 16 entries per row, then one pair per row
+    n = lib.sd_lm_head_workspace_size(36, 8192, 152064, 1)
+    assert n == (36 * (152064 // 16) + 36) * 8
+    assert lib.sd_lm_head_workspace_size(0, 64, 10, 1) == 0
+
+
+def test_sample_validation_errors(lib):
+    keep, (p, u, t, ws) = _fake(4)
+    f = lib.sd_sample_tokens
+
+    def call(p=p, u=u, t=t, R=3, V=100, ws=ws, wsb=1 << 30):
+        return f(p, u, t, R, V, ws, wsb, None)
+
+    assert call(p=None) == sd.SD_ERR_INVALID_ARG
+    assert call(u=None) == sd.SD_ERR_INVALID_ARG
+    assert call(t=None) == sd.SD_ERR_INVALID_ARG
+    assert call(R=0) == sd.SD_ERR_INVALID_ARG
+    assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=lib.sd_sample_workspace_size(3, 100) - 1) == sd.SD_ERR_WORKSPACE
+    assert lib.sd_sample_workspace_size(3, 100) >= 3 * 4

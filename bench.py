@@ -4,17 +4,20 @@
 
 One step is one pass of the whole hot path over one batch of synthetic
 input with every tensor already resident in HBM:
-    sd_latent_compress  (Eq. 3)  ->  sd_verify_attention  ->  sd_spec_accept
+    sd_latent_compress (Eq. 3) -> sd_verify_attention -> sd_lm_head_probs
+    (the k+1 target rows) -> sd_spec_accept
 Default workload: "long-video" (batch 4, GQA 64/8 heads, head dim 128, KV
 length 65536, block k = 8; compression of 16384 tokens of width 8192 to 512
-latents over 64 heads; sampled acceptance over a 152064-token vocabulary at
-temperature 0.7).
+latents over 64 heads; an LM head of width 8192 over a 152064-token
+vocabulary for the 36 target rows; sampled acceptance over that vocabulary
+at temperature 0.7).  The acceptance consumes synthetic p and q with
+realistic acceptance rates, not the head's output (its weights are random).
 
 Prints one JSON line.  `value` is the verify step's KV-read rate: bytes of
 K and V the step must read once, divided by the time of verification
 attention plus acceptance, in TB/s.  Per-kernel times come from HIP events
 on the stream the kernels run on.  `roofline` describes the dominant kernel
-(the longest per step); `rooflines` lists all three.  `traffic` is the HBM
+(the longest per step); `rooflines` lists all four.  `traffic` is the HBM
 bytes per launch measured with rocprofv3 counters (profiles/), or null when
 the kernel's sources changed since they were taken.  `cpu_baseline` times
 the plain CPU oracle on a bounded sample of the same workload and scales it
@@ -73,7 +76,7 @@ def accept_bytes(p, n):
     return total
 
 
-def cpu_baseline(w, comp, ver, acc, mode):
+def cpu_baseline(w, comp, ver, acc, mode, lm):
     """Time the oracle on a bounded sample and scale it to one whole step."""
     import numpy as np
     import oracle
@@ -111,10 +114,18 @@ def cpu_baseline(w, comp, ver, acc, mode):
     t0 = time.perf_counter()
     oracle.spec_accept(acc["p"], acc["q"], acc["draft"], acc["u"], mode)
     ta = time.perf_counter() - t0
-    return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "threads": threads,
+    # LM head: one row over the whole vocabulary (logits 8192 entries at a time)
+    R = lm["hidden"].shape[0]
+    t0 = time.perf_counter()
+    z = np.concatenate([oracle.lm_head_logits(lm["hidden"].values[:1], lm["weight"].values[v:v + 8192])
+                        for v in range(0, w.vocab, 8192)], axis=1)
+    oracle.softmax_temperature(z, lm["temperature"])
+    tl = (time.perf_counter() - t0) * R
+    return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "lm_head_s": tl, "threads": threads,
             "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
                       f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
-                      f"pairs, acceptance of all {w.batch} sequences; scaled linearly"}
+                      f"pairs, acceptance of all {w.batch} sequences, LM head 1 of {R} rows; "
+                      f"scaled linearly"}
 
 
 def counter_traffic(workload):
@@ -167,6 +178,7 @@ def main():
     comp = synth.compress_inputs(w)
     ver = synth.verify_inputs(w)
     acc = synth.accept_inputs(w, mode)
+    lm = synth.lm_inputs(w)
 
     lat_d, feats_d = to_dev(comp[0], dev), to_dev(comp[1], dev)
     q_d, k_d, v_d = to_dev(ver["q"], dev), to_dev(ver["k_cache"], dev), to_dev(ver["v_cache"], dev)
@@ -176,6 +188,7 @@ def main():
     qq_d = torch.from_numpy(acc["q"]).to(dev)
     dr_d = torch.from_numpy(acc["draft"]).to(dev)
     u_d = torch.from_numpy(acc["u"]).to(dev)
+    h_d, wt_d = to_dev(lm["hidden"], dev), to_dev(lm["weight"], dev)
     dt_code = sd.SD_BF16 if w.dtype == "bf16" else sd.SD_F32
     amode = sd.SD_ACCEPT_SAMPLED if mode == "sampled" else sd.SD_ACCEPT_GREEDY
 
@@ -191,6 +204,10 @@ def main():
                                                    dt_code), dtype=torch.uint8, device=dev)
     a_ws = torch.empty(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
                        dtype=torch.uint8, device=dev)
+    lm_rows = lm["hidden"].shape[0]
+    lm_out = torch.empty((lm_rows, w.vocab), dtype=torch.float32, device=dev)
+    lm_ws = torch.empty(sd.sd_lm_head_workspace_size(lm_rows, w.lm_width, w.vocab, dt_code),
+                        dtype=torch.uint8, device=dev)
     n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
     scale = 1.0 / math.sqrt(w.head_dim)
@@ -205,10 +222,13 @@ def main():
                                lse=v_lse, workspace=v_ws)
         if ev is not None:
             ev[2].record()
+        sd.sd_lm_head_probs(h_d, wt_d, lm["temperature"], out=lm_out, workspace=lm_ws)
+        if ev is not None:
+            ev[3].record()
         sd.sd_spec_accept(p_d, qq_d, dr_d, u_d, amode, n_accepted=n_out, tokens=t_out,
                           workspace=a_ws)
         if ev is not None:
-            ev[3].record()
+            ev[4].record()
 
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
@@ -219,7 +239,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -229,7 +249,8 @@ def main():
     wall = time.perf_counter() - t0
     comp_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     ver_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
-    acc_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    lm_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    acc_ms = np.array([e[3].elapsed_time(e[4]) for e in events])
 
     kv_bytes = synth.verify_kv_bytes(w, ver["kv_len"])
     flops = synth.compress_flops(w)
@@ -237,6 +258,8 @@ def main():
     n_host = n_out.cpu().numpy()
     a_bytes = accept_bytes(acc["p"], n_host)
     t_c, t_v, t_a = float(comp_ms.mean()), float(ver_ms.mean()), float(acc_ms.mean())
+    t_l = float(lm_ms.mean())
+    l_bytes = synth.lm_bytes(w, lm_rows)
     verify_step_ms = t_v + t_a
     value = kv_bytes / (verify_step_ms * 1e-3) / 1e12
 
@@ -252,6 +275,9 @@ def main():
         "spec_accept": {"bound": "hbm", "achieved": a_bytes / (t_a * 1e-3) / 1e9,
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
                         "algorithmic": a_bytes, "us": t_a * 1e3},
+        "lm_head": {"bound": "hbm", "achieved": l_bytes / (t_l * 1e-3) / 1e9,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
+                    "algorithmic": l_bytes, "us": t_l * 1e3},
     }
     traffic = counter_traffic(w.name)
     for name_, r in rl.items():
@@ -282,11 +308,14 @@ def main():
             "compress_tokens": w.c_tokens, "compress_width": w.c_width,
             "latents": w.c_latents, "compress_heads": w.c_heads,
             "vocab": w.vocab, "accept_mode": mode, "temperature": acc["temperature"],
+            "lm_rows": lm_rows, "lm_width": w.lm_width,
         },
         "verify_step_us": verify_step_ms * 1e3,
         "verify_attention_us": t_v * 1e3,
         "spec_accept_us": t_a * 1e3,
         "latent_compress_us": t_c * 1e3,
+        "lm_head_us": t_l * 1e3,
+        "lm_head_tbps": l_bytes / (t_l * 1e-3) / 1e12,
         "latent_compress_tflops": rl["latent_compress"]["achieved"],
         "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
         "accepted_mean": float(n_host.mean()),
@@ -295,14 +324,14 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        cb = cpu_baseline(w, comp, ver, acc,
-                          0 if mode == "greedy" else 1)
+        cb = cpu_baseline(w, comp, ver, acc, 0 if mode == "greedy" else 1, lm)
         cpu_step = cb["verify_s"] + cb["accept_s"]
         result["cpu_baseline"] = {
             "value": kv_bytes / cpu_step / 1e12, "unit": "TB/s", "cores": cb["threads"],
             "kind": "oracle", "sample": cb["sample"],
             "verify_step_s": cpu_step, "latent_compress_s": cb["compress_s"],
-            "whole_step_s": cpu_step + cb["compress_s"],
+            "lm_head_s": cb["lm_head_s"],
+            "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"],
         }
     print(json.dumps(result), flush=True)
 

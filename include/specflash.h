@@ -205,10 +205,10 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
  *   probs   [R, V] float32  out
  *   workspace  sd_lm_head_workspace_size(R, d, V, dtype) bytes (per-block
  *              and per-row softmax statistics)
- * Requirements: R, d, V >= 1; temperature > 0 and finite; R <= 4096 and
- * V <= 2^24; SD_BF16 needs d % 64 == 0 and 16-byte aligned hidden and
- * weight; SD_F32 (float64 dot products, for accuracy checks rather than
- * speed) takes any d.  The weight is streamed from HBM once per 64 rows.
+ * Requirements: R, d, V >= 1; temperature > 0 and finite; V <= 2^24;
+ * SD_BF16: R <= 256, d % 64 == 0, 16-byte aligned hidden and weight (the
+ * weight is streamed from HBM once); SD_F32 (float64 dot products, for
+ * accuracy checks rather than speed): R <= 4096, any d.
  * ---------------------------------------------------------------------- */
 size_t sd_lm_head_workspace_size(int R, int d, int V, int dtype);
 

@@ -6,13 +6,15 @@
 //
 // The pass is bound by streaming the weight [V, d] once (R <= 256 rows share
 // every weight byte), so the three kernels are shaped around that stream:
-// 1. logits, grid (vocabulary tile of 128 entries): each of 4 waves owns 32
-//    vocabulary rows and up to 64 hidden rows (more rows: one launch per 64,
-//    each streaming the weight again).  z^T = W H^T on bf16 matrix cores
-//    (lane = one hidden row); weight and hidden fragments come straight
-//    from global memory into registers, 64 channels at a time, the next 64
-//    in flight while the current ones are multiplied (the hidden rows are
-//    small and stay in L2).  The scaled logits s = z log2(e) / tau are
+// 1. logits, grid (vocabulary tile of 128 entries, or 64 for small
+//    vocabularies): each of 4 waves owns 32 (16) vocabulary rows and all
+//    R <= 256 hidden rows, so the weight is
+//    streamed once.  z^T = W H^T on bf16 matrix cores (lane = one hidden
+//    row).  Weight fragments come straight from global memory into
+//    registers, 64 channels at a time, the next 64 in flight while the
+//    current ones are multiplied; the matching 64 channels of every hidden
+//    row (small, L2-resident) are staged once per work-group in
+//    double-buffered, swizzled LDS.  The scaled logits s = z log2(e) / tau are
 //    written to `probs` as fp32, with the (max, sum of 2^(s - max)) of every
 //    16-entry vocabulary block and row.
 // 2. statistics, one work-group per row: the per-block pairs are merged
@@ -29,13 +31,6 @@
 
 namespace sd {
 namespace {
-
-// 16-entry vocabulary blocks per wave: two, so that the registers leave room
-// for several waves per SIMD (memory-level parallelism)
-template <int RB>
-constexpr int vblocks() { return 2; }
-template <int RB>
-constexpr int tile_v() { return 4 * vblocks<RB>() * 16; }   // entries per work-group (4 waves)
 
 struct Stat {
   float m, l;
@@ -62,27 +57,30 @@ __device__ __forceinline__ Stat column_stat(const floatx4& s) {
   return Stat{m, l};
 }
 
-template <int RB>
-__global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a, int row0) {
-  constexpr int kVB = vblocks<RB>();
-  constexpr int kTileV = tile_v<RB>();
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, G = lane >> 4, c = lane & 15;
+// KVB 16-entry vocabulary blocks per wave (2, or 1 when the vocabulary is
+// too small to give about four work-groups per compute unit otherwise)
+template <int RB, int KVB>
+__global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a) {
+  constexpr int kVB = KVB;
+  constexpr int kTileV = 4 * kVB * 16;             // vocabulary entries per work-group
+  constexpr int HROWS = RB * 16;                   // hidden rows (padded)
+  constexpr int HPIECES = HROWS * 8;               // 16-byte pieces of a 64-channel chunk
+  constexpr int HPT = (HPIECES + 255) / 256;       // pieces staged per thread
+  // hidden chunk (64 channels of every row), double-buffered; the 16-byte
+  // pieces of row r sit at slot p ^ lds_swizzle<8>(r)
+  __shared__ __align__(16) uint16_t hbuf[2][HROWS * 64];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, G = lane >> 4, c = lane & 15;
   const int v0 = blockIdx.x * kTileV + w * kVB * 16;   // this wave's first vocabulary row
-  // this launch's rows: row0 .. row0 + RB*16 - 1 of the R rows
-  const int d = a.d, V = a.V, R = min(a.R - row0, RB * 16);
+  const int d = a.d, V = a.V, R = a.R;
   const uint16_t* W = static_cast<const uint16_t*>(a.weight);
-  const uint16_t* H = static_cast<const uint16_t*>(a.hidden) + (size_t)row0 * d;
-  // fragment sources: vocabulary row v0 + vb*16 + c and hidden row rb*16 + c
-  // (both clamped into range; their results are discarded), channels
-  // k + 8G .. k + 8G + 7 of each 32-channel step
+  const uint16_t* H = static_cast<const uint16_t*>(a.hidden);
+  // weight fragments: vocabulary row v0 + vb*16 + c (clamped; its results
+  // are discarded), channels k + 8G .. k + 8G + 7 of each 32-channel step
   const u32x4* wsrc[kVB];
-  const u32x4* hsrc[RB];
 #pragma unroll
   for (int vb = 0; vb < kVB; ++vb)
     wsrc[vb] = reinterpret_cast<const u32x4*>(W + (size_t)min(v0 + vb * 16 + c, V - 1) * d + 8 * G);
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-    hsrc[rb] = reinterpret_cast<const u32x4*>(H + (size_t)min(rb * 16 + c, R - 1) * d + 8 * G);
 
   floatx4 acc[kVB][RB];
 #pragma unroll
@@ -90,42 +88,77 @@ __global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a, int row0) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // 64-channel groups (two 32-channel steps), double-buffered in registers
-  u32x4 wa[2][kVB], ha[2][RB], wb[2][kVB], hb[2][RB];
-  auto load = [&](u32x4 (&wf)[2][kVB], u32x4 (&hf)[2][RB], int k) {
+  // the hidden chunk at channel k: this thread's pieces, global -> registers
+  u32x4 hreg[HPT];
+  auto h_load = [&](int k) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-#pragma unroll
-      for (int vb = 0; vb < kVB; ++vb) wf[s][vb] = wsrc[vb][(k + 32 * s) / 8];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) hf[s][rb] = hsrc[rb][(k + 32 * s) / 8];
+    for (int i = 0; i < HPT; ++i) {
+      const int P = i * 256 + tid;
+      if (P < HPIECES) {
+        const int row = min(P >> 3, R - 1);
+        hreg[i] = *reinterpret_cast<const u32x4*>(H + (size_t)row * d + k + (P & 7) * 8);
+      }
     }
   };
-  auto mma = [&](const u32x4 (&wf)[2][kVB], const u32x4 (&hf)[2][RB]) {
+  auto h_store = [&](int buf) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int i = 0; i < HPT; ++i) {
+      const int P = i * 256 + tid;
+      if (P < HPIECES) {
+        const int row = P >> 3;
+        *reinterpret_cast<u32x4*>(&hbuf[buf][(row * 8 + ((P & 7) ^ lds_swizzle<8>(row))) * 8]) = hreg[i];
+      }
+    }
+  };
+  // the weight chunk at channel k (two 32-channel steps)
+  auto w_load = [&](u32x4 (&wf)[2][kVB], int k) {
 #pragma unroll
-      for (int vb = 0; vb < kVB; ++vb) {
-        Pack8 x;
-        x.u = wf[s][vb];
+    for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          Pack8 y;
-          y.u = hf[s][rb];
+      for (int vb = 0; vb < kVB; ++vb) wf[st][vb] = wsrc[vb][(k + 32 * st) / 8];
+  };
+  auto mma = [&](const u32x4 (&wf)[2][kVB], int buf) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = rb * 16 + c;
+        Pack8 y;
+        y.u = *reinterpret_cast<const u32x4*>(&hbuf[buf][(row * 8 + ((st * 4 + G) ^ lds_swizzle<8>(row))) * 8]);
+#pragma unroll
+        for (int vb = 0; vb < kVB; ++vb) {
+          Pack8 x;
+          x.u = wf[st][vb];
           acc[vb][rb] = mfma_bf16(x.b, y.b, acc[vb][rb]);
         }
       }
+    }
   };
-  load(wa, ha, 0);
+
+  // chunks of 64 channels: weight double-buffered in registers, hidden in LDS
+  u32x4 wa[2][kVB], wb[2][kVB];
+  w_load(wa, 0);
+  h_load(0);
+  h_store(0);
+  __syncthreads();
   int k = 0;
 #pragma unroll 1
   for (; k + 128 <= d; k += 128) {
-    load(wb, hb, k + 64);
-    mma(wa, ha);
-    if (k + 128 < d) load(wa, ha, k + 128);
-    mma(wb, hb);
+    w_load(wb, k + 64);
+    h_load(k + 64);
+    mma(wa, 0);
+    h_store(1);
+    __syncthreads();   // chunk k+64 staged; every wave is done with buffer 0
+    const bool more = k + 128 < d;
+    if (more) {
+      w_load(wa, k + 128);
+      h_load(k + 128);
+    }
+    mma(wb, 1);
+    if (more) h_store(0);
+    __syncthreads();   // chunk k+128 staged; every wave is done with buffer 1
   }
-  if (k < d) mma(wa, ha);   // d % 128 == 64: one group left
+  if (k < d) mma(wa, 0);   // d % 128 == 64: one chunk left
 
   // scaled logits, per-block statistics, fp32 logits to probs
   float2* stats = reinterpret_cast<float2*>(a.stats);
@@ -144,7 +177,7 @@ __global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a, int row0) {
       const Stat st = column_stat(s);
       const int r = rb * 16 + c;
       if (r < R && vbase < V) {
-        float* dst = a.probs + (size_t)(row0 + r) * V + vbase + 4 * G;
+        float* dst = a.probs + (size_t)r * V + vbase + 4 * G;
         if (vbase + 4 * G + 3 < V && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
           *reinterpret_cast<floatx4*>(dst) = s;
         } else {
@@ -152,7 +185,7 @@ __global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a, int row0) {
           for (int i = 0; i < 4; ++i)
             if (vbase + 4 * G + i < V) dst[i] = s[i];
         }
-        if (G == 0) stats[(size_t)(row0 + r) * nblk + vbase / 16] = make_float2(st.m, st.l);
+        if (G == 0) stats[(size_t)r * nblk + vbase / 16] = make_float2(st.m, st.l);
       }
     }
   }
@@ -218,9 +251,12 @@ __global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
 }
 
 template <int RB>
-hipError_t launch_rb(const LmHeadArgs& a, int row0, hipStream_t st) {
-  hipLaunchKernelGGL((lm_logits_bf16<RB>), dim3((a.V + tile_v<RB>() - 1) / tile_v<RB>()), dim3(256), 0, st,
-                     a, row0);
+hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st) {
+  if ((a.V + 127) / 128 >= 1024) {
+    hipLaunchKernelGGL((lm_logits_bf16<RB, 2>), dim3((a.V + 127) / 128), dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((lm_logits_bf16<RB, 1>), dim3((a.V + 63) / 64), dim3(256), 0, st, a);
+  }
   return hipGetLastError();
 }
 
@@ -237,14 +273,24 @@ hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t st) {
     hipLaunchKernelGGL(lm_logits_f32, dim3((a.V + 255) / 256, a.R), dim3(256), 0, st, a);
     e = hipGetLastError();
   } else {
-    // at most 64 rows per launch (the weight is streamed once per launch)
-    for (int row0 = 0; row0 < a.R && e == hipSuccess; row0 += 64) {
-      switch ((min(a.R - row0, 64) + 15) / 16) {
-        case 1: e = launch_rb<1>(a, row0, st); break;
-        case 2: e = launch_rb<2>(a, row0, st); break;
-        case 3: e = launch_rb<3>(a, row0, st); break;
-        default: e = launch_rb<4>(a, row0, st); break;
-      }
+    switch ((a.R + 15) / 16) {
+      case 1: e = launch_rb<1>(a, st); break;
+      case 2: e = launch_rb<2>(a, st); break;
+      case 3: e = launch_rb<3>(a, st); break;
+      case 4: e = launch_rb<4>(a, st); break;
+      case 5: e = launch_rb<5>(a, st); break;
+      case 6: e = launch_rb<6>(a, st); break;
+      case 7: e = launch_rb<7>(a, st); break;
+      case 8: e = launch_rb<8>(a, st); break;
+      case 9: e = launch_rb<9>(a, st); break;
+      case 10: e = launch_rb<10>(a, st); break;
+      case 11: e = launch_rb<11>(a, st); break;
+      case 12: e = launch_rb<12>(a, st); break;
+      case 13: e = launch_rb<13>(a, st); break;
+      case 14: e = launch_rb<14>(a, st); break;
+      case 15: e = launch_rb<15>(a, st); break;
+      case 16: e = launch_rb<16>(a, st); break;
+      default: return hipErrorInvalidValue;   // R <= 256 is checked by the caller
     }
   }
   if (e != hipSuccess) return e;

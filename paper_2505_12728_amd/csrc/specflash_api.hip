@@ -202,7 +202,7 @@ int sd_lm_head_probs(const void* hidden, const void* weight, float* probs, int R
   if (!hidden || !weight || !probs || !aligned(probs, 4)) return SD_ERR_INVALID_ARG;
   if (R > 4096 || V > (1 << 24)) return SD_ERR_UNSUPPORTED;
   if (dtype == SD_BF16) {
-    if (d % 64 != 0) return SD_ERR_UNSUPPORTED;
+    if (d % 64 != 0 || R > 256) return SD_ERR_UNSUPPORTED;
     if (!aligned(hidden, 16) || !aligned(weight, 16)) return SD_ERR_INVALID_ARG;
   } else if (!aligned(hidden, 4) || !aligned(weight, 4)) {
     return SD_ERR_INVALID_ARG;

@@ -152,6 +152,8 @@ def test_lm_head_validation_errors(lib):
     assert call(dt=3) == sd.SD_ERR_INVALID_ARG
     assert call(d=100) == sd.SD_ERR_UNSUPPORTED               # bf16: d % 64
     assert call(R=5000) == sd.SD_ERR_UNSUPPORTED
+    assert call(R=257) == sd.SD_ERR_UNSUPPORTED                # bf16: one group of <= 16 row blocks
+    assert call(R=257, dt=0) != sd.SD_ERR_UNSUPPORTED
     assert call(h=ctypes.c_void_p(h.value + 8)) == sd.SD_ERR_INVALID_ARG   # bf16: 16-byte aligned
     assert call(ws=None) == sd.SD_ERR_WORKSPACE
     assert call(wsb=8) == sd.SD_ERR_WORKSPACE

@@ -6,17 +6,18 @@
 //
 // The pass is bound by streaming the weight [V, d] once (R <= 256 rows share
 // every weight byte), so the three kernels are shaped around that stream:
-// 1. logits, grid (vocabulary tile of 128 entries, or 64 for small
-//    vocabularies): each of 4 waves owns 32 (16) vocabulary rows and all
-//    R <= 256 hidden rows, so the weight is
-//    streamed once.  z^T = W H^T on bf16 matrix cores (lane = one hidden
-//    row).  Weight fragments come straight from global memory into
-//    registers, 64 channels at a time, the next 64 in flight while the
-//    current ones are multiplied; the matching 64 channels of every hidden
-//    row (small, L2-resident) are staged once per work-group in
-//    double-buffered, swizzled LDS.  The scaled logits s = z log2(e) / tau are
-//    written to `probs` as fp32, with the (max, sum of 2^(s - max)) of every
-//    16-entry vocabulary block and row.
+// 1. logits.  z^T = W H^T on bf16 matrix cores, the lane owning one hidden
+//    row; every wave covers its own vocabulary rows for all R hidden rows,
+//    so each weight byte is read once.  The scaled logits s = z log2(e) / tau
+//    are written to `probs` as fp32, with the (max, sum of 2^(s - max)) of
+//    every 16-entry vocabulary block and row.
+//    - `lm_logits_burst` (R <= 64, d % 256 == 0): 16 vocabulary rows per
+//      wave read in 512-byte runs per row, straight into registers; the
+//      hidden chunk of 256 channels of all rows staged through LDS by DMA.
+//    - `lm_logits_bf16` (the other shapes): 16 or 32 vocabulary rows per
+//      wave read 128 bytes per row at a time, the next 64 channels in
+//      flight while the current ones are multiplied; the hidden chunk of 64
+//      channels staged through double-buffered, swizzled LDS.
 // 2. statistics, one work-group per row: the per-block pairs are merged
 //    into the row's (M, L).
 // 3. normalisation: probs = 2^(s - M) / L in place.
@@ -191,6 +192,125 @@ __global__ __launch_bounds__(256) void lm_logits_bf16(LmHeadArgs a) {
   }
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_cvoid;
+
+// Scaled logits of 16 vocabulary rows (accumulator rows) x 16 hidden rows
+// (columns) to probs, with the (max, sum) of the 16-entry vocabulary block
+// for every hidden row
+__device__ __forceinline__ void write_block(const LmHeadArgs& a, const floatx4& acc, int vbase, int r) {
+  const int lane = threadIdx.x & 63, G = lane >> 4;
+  const int V = a.V;
+  floatx4 s;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int v = vbase + 4 * G + i;
+    s[i] = v < V ? acc[i] * a.scale_log2 : -INFINITY;
+  }
+  const Stat st = column_stat(s);
+  if (r < a.R && vbase < V) {
+    float* dst = a.probs + (size_t)r * V + vbase + 4 * G;
+    if (vbase + 4 * G + 3 < V && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+      *reinterpret_cast<floatx4*>(dst) = s;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (vbase + 4 * G + i < V) dst[i] = s[i];
+    }
+    if (G == 0) reinterpret_cast<float2*>(a.stats)[(size_t)r * ((V + 15) / 16) + vbase / 16] = make_float2(st.m, st.l);
+  }
+}
+
+// Logits for R <= 64 hidden rows and widths d % 256 == 0, shaped for long
+// contiguous weight reads.  Each wave owns VB blocks of 16 vocabulary rows;
+// per chunk of 256 channels lane (c, G) loads 128 contiguous bytes of row c
+// of each block (channels 64 G .. 64 G + 63) as eight back-to-back 16-byte
+// loads, so every row is read in 512-byte runs (about 20% more HBM
+// bandwidth than 128-byte runs on this weight layout).  Matrix-core product i takes the i-th load of every
+// lane, i.e. channels {64 G + 8 i .. 64 G + 8 i + 7}: a fixed permutation of
+// the chunk's channels, which the hidden fragments follow.  The hidden chunk
+// of all rows (RB x 16 rows x 512 bytes) goes HBM/L2 -> LDS by the
+// global_load_lds DMA into two buffers; pieces of row r sit at slot
+// piece ^ (r & 15) so the 16 rows read at one piece hit 16 distinct bank
+// groups.
+template <int RB, int NW, int VB>
+__global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
+  constexpr int HROWS = RB * 16;
+  constexpr int HPIECES = HROWS * 32;          // 16-byte pieces of one hidden chunk
+  constexpr int DMA = HPIECES / (NW * 64);     // copies per thread and chunk
+  static_assert(HPIECES % (NW * 64) == 0, "whole copies per thread");
+  __shared__ __align__(16) unsigned char hbuf[2][HPIECES * 16];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, G = lane >> 4, c = lane & 15;
+  const int v0 = blockIdx.x * (NW * VB * 16) + w * (VB * 16);
+  const int d = a.d, V = a.V, R = a.R;
+  const uint16_t* W = static_cast<const uint16_t*>(a.weight);
+  const uint16_t* H = static_cast<const uint16_t*>(a.hidden);
+  // row c of each block of this wave (clamped; results of rows >= V are
+  // discarded)
+  const u32x4* wsrc[VB];
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb)
+    wsrc[vb] = reinterpret_cast<const u32x4*>(W + (size_t)min(v0 + vb * 16 + c, V - 1) * d + 64 * G);
+  // copy j of this thread moves piece P = (w * DMA + j) * 64 + lane of the
+  // chunk: hidden row P / 32 (clamped; padded rows are discarded), LDS slot
+  // P % 32 holding global piece slot ^ (row & 15)
+  const uint16_t* hsrc[DMA];
+#pragma unroll
+  for (int j = 0; j < DMA; ++j) {
+    const int P = (w * DMA + j) * 64 + lane;
+    const int row = P >> 5, slot = P & 31;
+    hsrc[j] = H + (size_t)min(row, R - 1) * d + ((slot ^ (row & 15)) * 8);
+  }
+  auto issue_hidden = [&](int n, int buf) {
+#pragma unroll
+    for (int j = 0; j < DMA; ++j)
+      __builtin_amdgcn_global_load_lds((gbl_cvoid*)(hsrc[j] + n * 256),
+                                       (lds_void*)(&hbuf[buf][(w * DMA + j) * 1024]), 16, 0, 0);
+  };
+
+  floatx4 acc[VB][RB];
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int nch = d / 256;
+  issue_hidden(0, 0);
+#pragma unroll 1
+  for (int n = 0; n < nch; ++n) {
+    const int buf = n & 1;
+    u32x4 wf[VB][8];
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) wf[vb][i] = wsrc[vb][n * 32 + i];
+    // the weight loads are the newest: everything older (this thread's
+    // copies of chunk n) has landed; after the barrier every wave's copies
+    // have, and every wave is done reading the other buffer
+    wait_vm_then_barrier<8 * VB>();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = rb * 16 + c;
+        Pack8 y;
+        y.u = *reinterpret_cast<const u32x4*>(&hbuf[buf][(row * 32 + ((8 * G + i) ^ c)) * 16]);
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) {
+          Pack8 x;
+          x.u = wf[vb][i];
+          acc[vb][rb] = mfma_bf16(x.b, y.b, acc[vb][rb]);
+        }
+      }
+    }
+    if (n + 1 < nch) issue_hidden(n + 1, buf ^ 1);
+  }
+#pragma unroll
+  for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) write_block(a, acc[vb][rb], v0 + vb * 16, rb * 16 + c);
+}
+
 // fp32 inputs: one thread per (row, vocabulary entry), float64 dot product;
 // 16 consecutive lanes form one 16-entry block for the statistics
 __global__ __launch_bounds__(256) void lm_logits_f32(LmHeadArgs a) {
@@ -217,16 +337,31 @@ __global__ __launch_bounds__(256) void lm_logits_f32(LmHeadArgs a) {
     reinterpret_cast<float2*>(a.stats)[(size_t)r * nblk + v / 16] = make_float2(m, l);
 }
 
-// one work-group per row: merge the per-block statistics into (M, L)
-__global__ __launch_bounds__(256) void lm_stats(LmHeadArgs a) {
-  __shared__ Stat part[4];
+// one work-group of 1024 threads per row: merge the per-block statistics
+// into (M, L).  Each thread takes its pairs eight at a time (eight loads in
+// flight, then one rescale), so the row costs a few memory latencies.
+__global__ __launch_bounds__(1024) void lm_stats(LmHeadArgs a) {
+  __shared__ Stat part[16];
   const int r = blockIdx.x;
   const int nblk = (a.V + 15) / 16;
   const float2* st = reinterpret_cast<const float2*>(a.stats) + (size_t)r * nblk;
   Stat acc{-INFINITY, 0.f};
-  for (int i = threadIdx.x; i < nblk; i += 256) {
-    const float2 x = st[i];
-    acc = merge(acc, Stat{x.x, x.y});
+  for (int base = threadIdx.x; base < nblk; base += 1024 * 8) {
+    float2 x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = base + j * 1024;
+      x[j] = i < nblk ? st[i] : make_float2(-INFINITY, 0.f);
+    }
+    float m = acc.m;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, x[j].x);
+    if (m != -INFINITY) {
+      float l = acc.l * fast_exp2(acc.m - m);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) l += x[j].y * fast_exp2(x[j].x - m);
+      acc = Stat{m, l};
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) acc = merge(acc, Stat{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.l, o, 64)});
@@ -234,12 +369,12 @@ __global__ __launch_bounds__(256) void lm_stats(LmHeadArgs a) {
   __syncthreads();
   if (threadIdx.x == 0) {
     Stat t = part[0];
-    for (int i = 1; i < 4; ++i) t = merge(t, part[i]);
+    for (int i = 1; i < 16; ++i) t = merge(t, part[i]);
     reinterpret_cast<float2*>(a.stats)[(size_t)a.R * nblk + r] = make_float2(t.m, t.l);
   }
 }
 
-// probs = 2^(s - M) / L, in place
+// probs = 2^(s - M) / L, in place; 16-byte accesses when the row allows
 __global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
   const int r = blockIdx.y;
   const int V = a.V;
@@ -247,11 +382,32 @@ __global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
   const float2 ML = reinterpret_cast<const float2*>(a.stats)[(size_t)a.R * nblk + r];
   const float inv = 1.f / ML.y;
   float* row = a.probs + (size_t)r * V;
-  for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += gridDim.x * 256) row[v] = fast_exp2(row[v] - ML.x) * inv;
+  const int stride = gridDim.x * 256;
+  if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(row) & 15) == 0) {
+    floatx4* row4 = reinterpret_cast<floatx4*>(row);
+    for (int v = blockIdx.x * 256 + threadIdx.x; v < V / 4; v += stride) {
+      floatx4 x = row4[v];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = fast_exp2(x[i] - ML.x) * inv;
+      row4[v] = x;
+    }
+  } else {
+    for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += stride) row[v] = fast_exp2(row[v] - ML.x) * inv;
+  }
 }
 
 template <int RB>
 hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st) {
+  if constexpr (RB <= 4) {
+    if (a.d % 256 == 0) {
+      if (a.V >= 65536) {
+        hipLaunchKernelGGL((lm_logits_burst<RB, 8, 1>), dim3((a.V + 127) / 128), dim3(512), 0, st, a);
+      } else {
+        hipLaunchKernelGGL((lm_logits_burst<RB, 4, 1>), dim3((a.V + 63) / 64), dim3(256), 0, st, a);
+      }
+      return hipGetLastError();
+    }
+  }
   if ((a.V + 127) / 128 >= 1024) {
     hipLaunchKernelGGL((lm_logits_bf16<RB, 2>), dim3((a.V + 127) / 128), dim3(256), 0, st, a);
   } else {
@@ -294,11 +450,12 @@ hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t st) {
     }
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lm_stats, dim3(a.R), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(lm_stats, dim3(a.R), dim3(1024), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int per_row = (a.V + 255) / 256;
-  hipLaunchKernelGGL(lm_normalize, dim3(per_row < 64 ? per_row : 64, a.R), dim3(256), 0, st, a);
+  // about two 16-byte pieces per thread
+  const int per_row = (a.V + 2047) / 2048;
+  hipLaunchKernelGGL(lm_normalize, dim3(std::min(per_row, 64), a.R), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

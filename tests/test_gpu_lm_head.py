@@ -63,10 +63,19 @@ def test_lm_head_long_video_sampled_rows():
 
 @pytest.mark.parametrize("R,d,V,tau", [(1, 64, 1, 1.0), (1, 64, 37, 0.5), (5, 128, 1000, 0.05),
                                        (17, 192, 300, 20.0), (65, 64, 129, 1.0),
-                                       (130, 128, 2050, 0.7)])
+                                       (130, 128, 2050, 0.7),
+                                       # widths d % 256 == 0 with R <= 64 (the
+                                       # 512-byte-run kernel): one entry, a
+                                       # partial tile, an odd chunk count, the
+                                       # largest row count, 8-wave tiles with a
+                                       # ragged end and unaligned rows
+                                       (1, 256, 1, 1.0), (3, 256, 50, 0.5),
+                                       (16, 512, 1000, 1.0), (33, 768, 129, 2.0),
+                                       (64, 256, 65600, 0.7), (49, 1024, 70001, 0.3)])
 def test_lm_head_edge_shapes(R, d, V, tau):
     # ragged rows (row blocks of 16, launches of 64), ragged vocabulary
-    # (tiles of 128, blocks of 16), odd channel groups, extreme temperatures
+    # (tiles of 64 / 128, blocks of 16), odd channel groups, extreme
+    # temperatures
     w = synth.workload("llava-7b-image")
     rs = synth.streams(1234 + R + V)
     hidden = synth.Tensor(rs["lm_hidden"].normal((R, d)), "bf16")

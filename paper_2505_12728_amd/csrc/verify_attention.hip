@@ -39,7 +39,6 @@ namespace sd {
 namespace {
 
 constexpr int kTile = 32;       // keys per tile of the bf16 kernel
-constexpr int kWaves = 4;       // waves per work-group of the fp32 kernel
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
@@ -78,7 +77,7 @@ __device__ __forceinline__ int seq_len(const VerifyArgs& a, int b, bool paged) {
 // O, l rescaled) only when a row's scores exceed it by more than 2^8 (the
 // stale maximum is exact for the final o = O / l; p stays below 256), and
 // copy addresses are per-lane constants plus a per-tile scalar offset.
-template <int D, int NW, bool PAGED>
+template <int D, int NW, bool PAGED, int KG>
 __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int keys_per_split,
                                                              int nsplit, int row_groups,
                                                              int rows_padded) {
@@ -90,13 +89,18 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
   constexpr int HALF_BYTES = TK * ROW_BYTES;   // K (or V) part of a buffer
   constexpr int BUF_BYTES = 2 * HALF_BYTES;
   constexpr int DMA_PER_HALF = TK * PK / 64;   // 64-lane copies per K (or V) tile
-  constexpr int DMA_PER_WAVE = 2 * DMA_PER_HALF / NW;
+  constexpr int DMA_PER_WAVE = 2 * DMA_PER_HALF / NW;   // per tile
+  constexpr int NWR = NW / KG;                 // waves per key group = 16-row blocks
   static_assert((2 * DMA_PER_HALF) % NW == 0, "tile copy must split evenly");
+  static_assert(NW % KG == 0 && (KG == 1 || KG == 2), "key groups");
   static_assert(TK == 32, "one P V step per tile");
-  // ring depth: NBUF - 1 tiles in flight; two (NW = 4) or three (NW < 4)
-  // work-groups share a compute unit, so every SIMD runs two or more waves
-  constexpr int NBUF = (NW == 4) ? 4 : 3;
-  static_assert((NBUF - 2) * DMA_PER_WAVE < 64, "vmcnt range");
+  // ring depth: NBUF - KG tiles in flight.  KG = 1: two (NW = 4) or three
+  // (NW < 4) work-groups share a compute unit, so every SIMD runs two or
+  // more waves.  KG = 2: one work-group of 8 waves per unit, the two groups
+  // of 4 waves taking alternate tiles of one deep ring (one long key stream
+  // per unit, two waves per SIMD).
+  constexpr int NBUF = KG == 2 ? 8 : ((NW == 4) ? 4 : 3);
+  static_assert(NBUF % KG == 0 && (NBUF - 2 * KG) * DMA_PER_WAVE < 64, "vmcnt range");
   constexpr float kRescale = 8.f;              // log2 headroom before rescaling
   __shared__ __align__(16) unsigned char ring[NBUF][BUF_BYTES];
 
@@ -113,11 +117,12 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
   const int w = tid >> 6, lane = tid & 63, G = lane >> 4, c = lane & 15;
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
-  const int rblk = rg * NW * 16 + w * 16;      // this wave's first row
+  const int wr = w % NWR, kgrp = w / NWR;      // row block, key group
+  const int rblk = rg * NWR * 16 + wr * 16;    // this wave's first row
   if (k0 >= L) {
     // empty split: the merge skips it; with a single split (nothing to
     // merge) this work-group writes its rows directly: o = 0, lse = -inf
-    if (nsplit == 1 && split == 0 && rblk + c < R) {
+    if (nsplit == 1 && split == 0 && kgrp == 0 && rblk + c < R) {
       const int r = rblk + c;
       const int j = r / g;
       const int orow = (b * a.k + j) * a.Hq + hk * g + (r - j * g);
@@ -128,8 +133,8 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     return;
   }
   const int k1 = min(L, k0 + keys_per_split);
-  // a wave whose rows are all padding (R not a multiple of 16 * NW) runs the
-  // same loop on zero queries and writes nothing
+  // a wave whose rows are all padding (R not a multiple of 16 * NWR) runs
+  // the same loop on zero queries and writes nothing
   const bool active = rblk < R;                // wave-uniform
 
   // This lane's query row r = rblk + c: block position j = r / g, query head
@@ -339,23 +344,51 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     }
   };
 
-  // Every step issues one tile (past the end it re-reads the last one, which
-  // is still cached), so exactly (NBUF - 2) * DMA_PER_WAVE newer copies are
-  // in flight at each wait and the wait covers precisely the tile about to
-  // be read.  The tile reads are asm, so the compiler adds no waits of its
-  // own between them and the copies.
+  // Every step issues KG tiles (past the end it re-reads the last one, which
+  // is still cached), so exactly (NBUF - 2 KG) tiles' copies are newer than
+  // the step's own tiles at each wait, and the wait covers precisely the
+  // tiles about to be read; the barrier also frees the slots of the
+  // previous step for refilling.  The tile reads are asm, so the compiler
+  // adds no waits of its own between them and the copies.
+  const int nsteps = (ntiles + KG - 1) / KG;
 #pragma unroll
-  for (int i = 0; i < NBUF - 1; ++i) issue(min(i, last), ring[i]);
-  for (int it = 0; it < ntiles; ++it) {
-    wait_vm_then_barrier<(NBUF - 2) * DMA_PER_WAVE>();   // tile it landed; slot it-1 free
-    issue(min(it + NBUF - 1, last), ring[(it + NBUF - 1) % NBUF]);
-    compute(it, ring[it % NBUF]);
+  for (int i = 0; i < NBUF - KG; ++i) issue(min(i, last), ring[i]);
+  for (int it = 0; it < nsteps; ++it) {
+    wait_vm_then_barrier<(NBUF - 2 * KG) * DMA_PER_WAVE>();
+#pragma unroll
+    for (int j = 0; j < KG; ++j) {
+      const int t = KG * it + NBUF - KG + j;
+      issue(min(t, last), ring[t % NBUF]);
+    }
+    const int mine = KG * it + kgrp;           // wave-uniform
+    if (KG == 1 || mine < ntiles) compute(mine, ring[mine % NBUF]);
   }
   // no copy may still be writing this work-group's LDS when it exits
   __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
+  l = wave_sum_across_groups(l);
+  if constexpr (KG == 2) {
+    // group 1 hands (m, l, O) of its row block to group 0 through the ring
+    __syncthreads();                           // every wave is done with the ring
+    floatx4* xo = reinterpret_cast<floatx4*>(&ring[0][0]);
+    float2* xml = reinterpret_cast<float2*>(&ring[0][0] + NWR * DB * 64 * 16);
+    if (kgrp == 1) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) xo[(wr * DB + db) * 64 + lane] = o[db];
+      xml[wr * 64 + lane] = make_float2(m, l);
+    }
+    __syncthreads();
+    if (kgrp == 1) return;
+    const float2 ml = xml[wr * 64 + lane];
+    const float mn = fmaxf(m, ml.x);
+    const float f0 = m == -INFINITY ? 0.f : fast_exp2(m - mn);
+    const float f1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - mn);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = o[db] * f0 + xo[(wr * DB + db) * 64 + lane] * f1;
+    l = l * f0 + ml.y * f1;
+    m = mn;
+  }
   if (!active) return;
 
-  l = wave_sum_across_groups(l);
   const float inv = l > 0.f ? 1.f / l : 0.f;
   auto store_row = [&](float* dst) {
 #pragma unroll
@@ -462,7 +495,8 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 // ---------------------------------------------------------------- merge
 // One wave per output row of one (sequence, KV head).  The lanes load the
 // split lse values 64 at a time and form their weights 2^(lse - max) in
-// parallel; then the two half-waves take alternate splits, each lane
+// parallel; then the two half-waves take alternate splits (in lockstep, the
+// weight of split j handed over by a lane shuffle), each lane
 // accumulating 4 channels of the weighted partial outputs (loads of
 // several splits in flight), and the halves are added at the end.
 // Grid (rows / 4, sequence x KV head).
@@ -497,11 +531,14 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
         wl = ls == -INFINITY ? 0.f : exp2f(ls - mx);
       }
       wsum += wl;
-#pragma unroll 4
-      for (int j = half; j < n; j += 2) {
-        const float wgt = __shfl(wl, j, 64);
+      // both halves run the same trip count, so every shuffle reads an
+      // active lane; lanes past the last split (j = n, odd n) get weight 0
+      for (int jj = 0; jj < n; jj += 2) {
+        const int j = jj + half;
+        const float wgt = __shfl(wl, j & 63, 64);
         const size_t pr = base + (size_t)(s0 + j) * rows_padded;
-        if (active && wgt != 0.f) acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
+        if (j < n && active && wgt != 0.f)
+          acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
       }
     }
 #pragma unroll
@@ -518,10 +555,10 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
     a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
 }
 
-template <int D, int NW, bool PAGED>
+template <int D, int NW, bool PAGED, int KG>
 hipError_t launch_bf16(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
   dim3 grid(a.Hkv * p.row_groups, p.nsplit, a.B);
-  hipLaunchKernelGGL((verify_split_bf16<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, a,
+  hipLaunchKernelGGL((verify_split_bf16<D, NW, PAGED, KG>), grid, dim3(NW * 64), 0, st, a,
                      p.keys_per_split, p.nsplit, p.row_groups, p.rows_padded);
   return hipGetLastError();
 }
@@ -529,9 +566,9 @@ hipError_t launch_bf16(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st)
 template <int D, bool PAGED>
 hipError_t dispatch_rb(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
   switch (p.row_blocks) {
-    case 1: return launch_bf16<D, 1, PAGED>(a, p, st);
-    case 2: return launch_bf16<D, 2, PAGED>(a, p, st);
-    default: return launch_bf16<D, 4, PAGED>(a, p, st);
+    case 1: return launch_bf16<D, 1, PAGED, 1>(a, p, st);
+    case 2: return launch_bf16<D, 2, PAGED, 1>(a, p, st);
+    default: return launch_bf16<D, 8, PAGED, 2>(a, p, st);
   }
 }
 
@@ -556,15 +593,15 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     p.row_blocks = blocks16 <= 1 ? 1 : (blocks16 == 2 ? 2 : 4);
     p.row_groups = (blocks16 + p.row_blocks - 1) / p.row_blocks;
     p.rows_padded = p.row_groups * p.row_blocks * 16;
-    // A work-group holds a 64 KB (4 waves) or 48 KB (1-2 waves) LDS ring,
-    // so two or three run per compute unit.  Aim for that many work-groups
-    // per unit on 256 units, all resident at once; at least one 32-key tile
-    // per split.  Small work-groups over long caches split four times
+    // A work-group of 4 row blocks (8 waves in two key groups) holds a
+    // 128 KB LDS ring, one per compute unit; smaller ones (1-2 waves) hold
+    // 48 KB, three per unit.  Aim for that many work-groups per unit on 256
+    // units, all resident at once; at least one 32-key tile per split.  Small work-groups over long caches split four times
     // finer: the splits are planned for the capacity, so with ragged
     // sequence lengths the longest sequence would otherwise stream its keys
     // through few work-groups, each bound by memory latency.
     const long long pairs = (long long)B * Hkv * p.row_groups;
-    const long long target = p.row_blocks == 4 ? 512 : (capacity >= 8192 ? 3072 : 768);
+    const long long target = p.row_blocks == 4 ? 256 : (capacity >= 8192 ? 3072 : 768);
     long long nsplit = std::max(1LL, (target + pairs - 1) / pairs);
     long long kps = (capacity + nsplit - 1) / nsplit;
     kps = std::max((long long)kTile, (kps + kTile - 1) / kTile * kTile);

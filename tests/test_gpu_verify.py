@@ -90,6 +90,13 @@ CASES = [
     ("two-row-groups", "bf16", 1, 16, 8, 1, 128, [777], False),
     ("paged-ragged", "bf16", 3, 6, 8, 2, 128, [33, 1000, 2049], True),
     ("paged-d64", "bf16", 2, 2, 4, 2, 64, [17, 300], True),
+    # 3-4 row blocks per KV head: 8 waves in two key groups
+    ("rows64-ragged", "bf16", 2, 8, 16, 2, 128, [1000, 37], False),
+    ("rows48-short", "bf16", 1, 6, 8, 1, 128, [70], False),
+    ("rows64-d64", "bf16", 2, 8, 8, 1, 64, [2500, 64], False),
+    ("rows64-paged", "bf16", 2, 8, 16, 2, 128, [300, 1500], True),
+    # 47 key splits: an odd count above 32 in one 64-split chunk of the merge
+    ("merge-odd-47", "bf16", 1, 4, 4, 1, 128, [1500], False),
     ("f32-ragged", "f32", 2, 4, 8, 2, 64, [608, 99], False),
     ("f32-paged", "f32", 2, 3, 4, 1, 128, [50, 700], True),
     ("f32-empty-rows", "f32", 1, 4, 4, 1, 64, [2], False),

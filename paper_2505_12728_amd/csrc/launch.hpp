@@ -11,16 +11,22 @@ namespace sd {
 struct VerifyPlan {
   int g;            // query heads per KV head
   int rows;         // k * g query rows that share one KV head
-  int row_blocks;   // 16-row blocks per work-group (1..4), bf16 path
+  int row_blocks;   // 16-row blocks per work-group (1..4)
   int row_groups;   // work-groups along the rows of one KV head
-  int rows_padded;  // row_groups * row_blocks * 16 (partial row stride)
+  int rows_padded;  // row_groups * row_blocks * 16
   int capacity;     // Lmax or 16 * max_pages
-  int keys_per_split;
-  int nsplit;
+  int keys_per_split;   // fp32 path: keys per split
+  int nsplit;           // fp32 path: splits per (sequence, KV head)
+  int rows_wg;          // bf16 path: rows per work-group (row_blocks * 16)
+  int key_groups;       // bf16 path: wave groups taking alternate tiles
+  int stream_wgs;       // bf16 path: grid size (work-groups on the device)
+  size_t part_rows;     // rows of partial results in the workspace
   size_t workspace_bytes;
+  bool ok;              // false: the shape exceeds the kernels' index range
 };
 
-VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype);
+// cus: compute units of the device the call runs on (sizes the bf16 grid)
+VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype, int cus);
 
 struct VerifyArgs {
   const void* q;
@@ -36,8 +42,8 @@ struct VerifyArgs {
   int B, k, Hq, Hkv, D;
   float scale;          // score multiplier as given
   float scale_log2;     // scale * log2(e)
-  float* part_o;        // [B, Hkv, nsplit, rows_padded, D]
-  float* part_lse;      // [B, Hkv, nsplit, rows_padded] (log2 units)
+  float* part_o;        // [part_rows, D] partial outputs (normalised)
+  float* part_lse;      // [part_rows] partial log-sum-exp (log2 units)
 };
 
 hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hipStream_t s);

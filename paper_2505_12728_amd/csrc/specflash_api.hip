@@ -99,10 +99,25 @@ int sd_latent_compress(const void* latents, const void* feats, float* out, int B
 }
 
 // --------------------------------------------------------------- verify
+// Compute units of the current device (cached per device; 256 when no
+// device can be queried, e.g. for sizing on a host without a GPU).
+static int device_cus() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    return 256;
+  if (dev < 64) cached[dev] = n;
+  return n;
+}
+
 size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype) {
   int st;
   if (!verify_shape_ok(B, k, Hq, Hkv, D, dtype, &st) || capacity < 1) return 0;
-  return sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype).workspace_bytes;
+  const sd::VerifyPlan plan = sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype, device_cus());
+  return plan.ok ? plan.workspace_bytes : 0;
 }
 
 int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -126,7 +141,8 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
     if (Lmax < 1) return SD_ERR_INVALID_ARG;
     capacity = Lmax;
   }
-  const sd::VerifyPlan plan = sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype);
+  const sd::VerifyPlan plan = sd::plan_verify(B, k, Hq, Hkv, D, capacity, dtype, device_cus());
+  if (!plan.ok) return SD_ERR_UNSUPPORTED;
   if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned(workspace, 16))
     return SD_ERR_WORKSPACE;
   sd::VerifyArgs a{};
@@ -148,7 +164,7 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
   a.scale = scale;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.part_o = static_cast<float*>(workspace);
-  a.part_lse = a.part_o + (size_t)B * Hkv * plan.nsplit * plan.rows_padded * D;
+  a.part_lse = a.part_o + plan.part_rows * D;
   return status_from(sd::launch_verify(a, plan, dtype, static_cast<hipStream_t>(stream)));
 }
 

@@ -6,25 +6,28 @@
 // grouped query heads), so the design keeps those rows resident and streams
 // the cache.
 //
-// Kernel 1 (split): grid (split, KV head x row group, sequence), 4 waves.
-//   Each work-group owns one contiguous key range of one (sequence, KV head)
-//   and up to 64 query rows; its 4 waves take interleaved 32-key tiles.
-//   Per tile a wave
-//     - loads K as matrix-core A fragments straight from HBM (16 bytes per
-//       lane, 8 contiguous channels of one key), and V in coalesced 16-byte
-//       pieces that it stages in its own LDS slice;
-//     - computes S^T = K Q^T on bf16 matrix cores, so that every lane holds
-//       scores of exactly one query row (column c of the accumulator);
+// Kernel 1 (stream): a fixed grid sized to the device.  All (sequence, KV
+//   head, row group) pairs form one list of 32-key tiles; each work-group
+//   takes an equal contiguous range of it, so ragged sequence lengths stay
+//   balanced to a tile.  A work-group holds up to 64 query rows (one wave
+//   per 16-row block) and streams its tiles HBM -> LDS by the
+//   global_load_lds DMA into a ring shared by its waves; per tile a wave
+//     - computes S^T = K Q^T on bf16 matrix cores from K fragments in LDS,
+//       so that every lane holds scores of exactly one query row (column c
+//       of the accumulator);
 //     - runs the online softmax in fp32 (base-2 exponent, masked by the
-//       causal limit kv_len - k + j of its row);
+//       causal limit kv_len - k + j of its row on tail tiles only);
 //     - accumulates O^T += V^T P^T, reading V^T fragments from LDS with the
-//       transposing ds_read_tr16_b64, and feeding P as a bf16 hi + lo pair
+//       transposing ds_read_b64_tr_b16, and feeding P as a bf16 hi + lo pair
 //       (P = hi + lo to ~2^-16 relative), which keeps the result within the
 //       float tolerance of the fp32 reference without converting V.
-//   The 4 waves then merge their (max, sum, O) through LDS in a fixed order
-//   and write one normalised partial (o, lse) per split.
-// Kernel 2 (merge): combines the splits of each row with the log-sum-exp
-//   rule and writes out / lse in the caller's [B, k, Hq] layout.
+//   Work-groups of 4 row blocks run 8 waves: two key groups of 4 take
+//   alternate tiles of one deep ring.  Wherever its range moves to the next
+//   pair, a work-group writes the normalised partial (o, lse) of the
+//   finished segment.
+// Kernel 2 (merge): finds the partials of each pair from the same tile
+//   arithmetic, combines them with the log-sum-exp rule and writes out / lse
+//   in the caller's [B, k, Hq] layout.
 //
 // fp32 caches take a plain (non matrix-core) split kernel with the same
 // partial format; it computes in float64 so fp32 inputs keep fp32 accuracy.
@@ -39,6 +42,16 @@ namespace sd {
 namespace {
 
 constexpr int kTile = 32;       // keys per tile of the bf16 kernel
+
+// bf16 stream kernel configuration by 16-row blocks per work-group (1, 2
+// or 4): key groups (waves = blocks x key groups), ring slots of one tile
+// (16 KB for D = 128) and work-groups per compute unit
+struct StreamCfg {
+  int kg, nbuf, per_cu;
+};
+constexpr StreamCfg stream_cfg(int row_blocks) {
+  return row_blocks == 4 ? StreamCfg{2, 8, 1} : StreamCfg{1, 4, 2};
+}
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
@@ -62,174 +75,256 @@ __device__ __forceinline__ int seq_len(const VerifyArgs& a, int b, bool paged) {
   return min(max(a.kv_len[b], 0), cap);
 }
 
-// ----------------------------------------------------------- bf16 split
-// One work-group = NW waves = NW 16-row blocks of one (sequence, KV head,
-// key split).  All waves walk the same 32-key tiles.  Tiles are copied
-// HBM -> LDS by the global_load_lds DMA (no VGPR staging) into a ring of
-// NBUF buffers, NBUF - 1 tiles ahead of the compute; with two or three
-// work-groups per compute unit about 96 KB per unit is in flight.  Each key
-// row keeps its 16-byte pieces XOR-swizzled by lds_swizzle(key), so the
-// K-fragment reads (16 keys x one piece) and the transposed V reads (4 keys
-// x 8 bytes per 16 lanes) are free of bank conflicts.
-//
-// Per tile a wave does 8 + 16 matrix-core ops and little else: the causal
-// mask is applied only on the tail tile, the running maximum is raised (and
-// O, l rescaled) only when a row's scores exceed it by more than 2^8 (the
-// stale maximum is exact for the final o = O / l; p stays below 256), and
-// copy addresses are per-lane constants plus a per-tile scalar offset.
-template <int D, int NW, bool PAGED, int KG>
-__global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int keys_per_split,
-                                                             int nsplit, int row_groups,
-                                                             int rows_padded) {
+// ----------------------------------------------------------- bf16 stream
+// All (sequence, KV head, row group) pairs of a call form one list of 32-key
+// tiles, in the order sequence b, then x = KV head * row_groups + row group,
+// then the tiles t of sequence b:
+//   n = cum(b) X + x nt(b) + t,  nt(b) = ceil(kv_len[b] / 32),
+//   cum(b) = nt(0) + ... + nt(b - 1),  X = Hkv row_groups,  T = cum(B) X.
+// Work-group w of G owns the tiles [T w / G, T (w + 1) / G), so the work
+// is balanced to a tile however ragged the lengths are; the bounds come
+// from kv_len on the device (the host sizes nothing by the lengths).
+// Where its range changes pair, a work-group writes the partial (o, lse)
+// of the finished segment to slot (pair + w) KG + key group: along the
+// tile order both the pair and w only grow, so pair + w is distinct for
+// every segment, and P + G slots per key group suffice.
+
+typedef const __attribute__((address_space(4))) int32_t cint32;   // scalar loads
+
+struct TileCursor {
+  int b, x, t;   // sequence, KV head * row_groups + row group, tile
+  int nt, L;     // tiles and length of sequence b
+};
+
+// length of sequence b as a scalar load (no vector-memory counter use)
+__device__ __forceinline__ int seq_len_s(const VerifyArgs& a, int b, int cap) {
+  return min(max(((cint32*)a.kv_len)[b], 0), cap);
+}
+
+// cum(b_end) (tiles of sequences before b_end, times X) over the first
+// b_end sequences; every lane of the wave gets the same value
+__device__ __forceinline__ int tiles_before(const VerifyArgs& a, int X, int cap, int b_end) {
+  const int lane = threadIdx.x & 63;
+  int sum = 0;
+  for (int b0 = 0; b0 < b_end; b0 += 64) {
+    const int b = b0 + lane;
+    int v = 0;
+    if (b < b_end) v = (min(max(a.kv_len[b], 0), cap) + 31) >> 5;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    sum += v;
+  }
+  return sum * X;
+}
+
+// cursor of tile n (0 <= n < T); wave-uniform
+__device__ __forceinline__ TileCursor locate(const VerifyArgs& a, int X, int cap, int n) {
+  const int lane = threadIdx.x & 63;
+  int base = 0;
+  TileCursor cu{0, 0, 0, 0, 0};
+  for (int b0 = 0; b0 < a.B; b0 += 64) {
+    const int b = b0 + lane;
+    const int L = b < a.B ? min(max(a.kv_len[b], 0), cap) : 0;
+    const int span = ((L + 31) >> 5) * X;
+    int incl = span;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
+    }
+    const unsigned long long hit = __ballot(base + incl > n);
+    if (hit != 0ull) {
+      const int f = __builtin_ctzll(hit);
+      const int Lf = __shfl(L, f, 64);
+      const int ex = __shfl(incl - span, f, 64);   // tiles before sequence b0 + f
+      cu.b = b0 + f;
+      cu.L = Lf;
+      cu.nt = (Lf + 31) >> 5;
+      const int rem = n - base - ex;
+      cu.x = rem / cu.nt;
+      cu.t = rem - cu.x * cu.nt;
+      return cu;
+    }
+    base += __shfl(incl, 63, 64);
+  }
+  return cu;   // n >= T: not reached
+}
+
+// Tile bookkeeping from one load of kv_len when B <= 64 (lane b holds
+// sequence b): the total T and the cursors of tiles n_a and n_b, where
+// n_a = T * wg / G and n_b = min(n_a + off_b, T * (wg + 1) / G - 1).
+// Returns false (nothing computed) when B > 64.
+struct TileStart {
+  int T, n0, n1;
+  TileCursor ca, cb;
+};
+
+__device__ __forceinline__ bool tile_start_small(const VerifyArgs& a, int X, int cap, int wg, int G,
+                                                 int off_b, TileStart* ts) {
+  if (a.B > 64) return false;
+  const int lane = threadIdx.x & 63;
+  const int L = lane < a.B ? min(max(a.kv_len[lane], 0), cap) : 0;
+  const int nt = (L + 31) >> 5;
+  const int span = nt * X;
+  int incl = span;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  const int T = __shfl(incl, 63, 64);
+  ts->T = T;
+  ts->n0 = (int)((long long)T * wg / G);
+  ts->n1 = (int)((long long)T * (wg + 1) / G);
+  if (ts->n0 >= ts->n1) return true;
+  auto find = [&](int n) {
+    TileCursor cu;
+    const unsigned long long hit = __ballot(incl > n);
+    const int f = __builtin_ctzll(hit);
+    cu.b = f;
+    cu.L = __shfl(L, f, 64);
+    cu.nt = (cu.L + 31) >> 5;
+    const int rem = n - __shfl(incl - span, f, 64);
+    cu.x = rem / cu.nt;
+    cu.t = rem - cu.x * cu.nt;
+    return cu;
+  };
+  ts->ca = find(ts->n0);
+  ts->cb = find(min(ts->n0 + off_b, ts->n1 - 1));
+  return true;
+}
+
+// the same cursor held in scalar registers
+__device__ __forceinline__ TileCursor uniform(TileCursor cu) {
+  cu.b = __builtin_amdgcn_readfirstlane(cu.b);
+  cu.x = __builtin_amdgcn_readfirstlane(cu.x);
+  cu.t = __builtin_amdgcn_readfirstlane(cu.t);
+  cu.nt = __builtin_amdgcn_readfirstlane(cu.nt);
+  cu.L = __builtin_amdgcn_readfirstlane(cu.L);
+  return cu;
+}
+
+// next tile in the global order; the caller never steps past the last tile
+__device__ __forceinline__ void advance(const VerifyArgs& a, int X, int cap, TileCursor& cu) {
+  if (++cu.t < cu.nt) return;
+  cu.t = 0;
+  if (++cu.x < X) return;
+  cu.x = 0;
+  do {
+    ++cu.b;
+    cu.L = cu.b < a.B ? seq_len_s(a, cu.b, cap) : 0;
+    cu.nt = (cu.L + 31) >> 5;
+  } while (cu.nt == 0 && cu.b < a.B);
+}
+
+// One work-group = NW = NWR x KG waves: NWR 16-row blocks of one pair, KG
+// key groups taking alternate tiles.  Tiles go HBM -> LDS by the
+// global_load_lds DMA into a ring of NBUF slots, NBUF - KG tiles ahead of
+// the compute.  Each key row keeps its 16-byte pieces XOR-swizzled by
+// lds_swizzle(key), so the K-fragment reads (16 keys x one piece) and the
+// transposed V reads (4 keys x 8 bytes per 16 lanes) are free of bank
+// conflicts.  Per tile a wave does 8 + 16 matrix-core ops and little else:
+// the causal mask is applied only on the tail tile of a sequence, the
+// running maximum is raised (and O, l rescaled) only when a row's scores
+// exceed it by more than 2^8 (the stale maximum is exact for the final
+// o = O / l; p stays below 256).
+template <int D, int NWR, int KG, int NBUF, bool PAGED>
+__global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a, int G,
+                                                                    int row_groups) {
+  constexpr int NW = NWR * KG;
   constexpr int TK = kTile;
   constexpr int DC = D / 32;                   // 32-channel K slices (QK^T)
   constexpr int DB = D / 16;                   // 16-channel output blocks (PV)
   constexpr int PK = D / 8;                    // 16-byte pieces per key row
   constexpr int ROW_BYTES = D * 2;
-  constexpr int HALF_BYTES = TK * ROW_BYTES;   // K (or V) part of a buffer
+  constexpr int HALF_BYTES = TK * ROW_BYTES;   // K (or V) part of a slot
   constexpr int BUF_BYTES = 2 * HALF_BYTES;
   constexpr int DMA_PER_HALF = TK * PK / 64;   // 64-lane copies per K (or V) tile
   constexpr int DMA_PER_WAVE = 2 * DMA_PER_HALF / NW;   // per tile
-  constexpr int NWR = NW / KG;                 // waves per key group = 16-row blocks
+  constexpr int ROWS_WG = NWR * 16;
   static_assert((2 * DMA_PER_HALF) % NW == 0, "tile copy must split evenly");
-  static_assert(NW % KG == 0 && (KG == 1 || KG == 2), "key groups");
   static_assert(TK == 32, "one P V step per tile");
-  // ring depth: NBUF - KG tiles in flight.  KG = 1: two (NW = 4) or three
-  // (NW < 4) work-groups share a compute unit, so every SIMD runs two or
-  // more waves.  KG = 2: one work-group of 8 waves per unit, the two groups
-  // of 4 waves taking alternate tiles of one deep ring (one long key stream
-  // per unit, two waves per SIMD).
-  constexpr int NBUF = KG == 2 ? 8 : ((NW == 4) ? 4 : 3);
-  static_assert(NBUF % KG == 0 && (NBUF - 2 * KG) * DMA_PER_WAVE < 64, "vmcnt range");
+  static_assert(NBUF >= 2 * KG + 1 && (NBUF - 2 * KG) * DMA_PER_WAVE < 64,
+                "ring depth and vmcnt range");
   constexpr float kRescale = 8.f;              // log2 headroom before rescaling
   __shared__ __align__(16) unsigned char ring[NBUF][BUF_BYTES];
 
-  // grid (KV head x row group, split, sequence): the work-groups of one key
-  // range are dispatched together, so the heads of a key read their
-  // interleaved cache rows at about the same time
-  const int split = blockIdx.y;
-  const int hk = blockIdx.x / row_groups;
-  const int rg = blockIdx.x % row_groups;
-  const int b = blockIdx.z;
-  const int L = seq_len(a, b, PAGED);
-  const int k0 = split * keys_per_split;
   const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63, G = lane >> 4, c = lane & 15;
+  const int lane = tid & 63, G4 = lane >> 4, c = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = w % NWR, kgrp = w / NWR;      // row block, key group
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
-  const int wr = w % NWR, kgrp = w / NWR;      // row block, key group
-  const int rblk = rg * NWR * 16 + wr * 16;    // this wave's first row
-  if (k0 >= L) {
-    // empty split: the merge skips it; with a single split (nothing to
-    // merge) this work-group writes its rows directly: o = 0, lse = -inf
-    if (nsplit == 1 && split == 0 && kgrp == 0 && rblk + c < R) {
-      const int r = rblk + c;
-      const int j = r / g;
-      const int orow = (b * a.k + j) * a.Hq + hk * g + (r - j * g);
-      for (int d4 = G; d4 < D / 4; d4 += 4)
-        *reinterpret_cast<floatx4*>(a.out + (size_t)orow * D + d4 * 4) = floatx4{0.f, 0.f, 0.f, 0.f};
-      if (a.lse != nullptr && G == 0) a.lse[orow] = -INFINITY;
-    }
-    return;
-  }
-  const int k1 = min(L, k0 + keys_per_split);
-  // a wave whose rows are all padding (R not a multiple of 16 * NWR) runs
-  // the same loop on zero queries and writes nothing
-  const bool active = rblk < R;                // wave-uniform
-
-  // This lane's query row r = rblk + c: block position j = r / g, query head
-  // hk * g + r % g.  B operand of S^T = K Q^T.
-  bf16x8 qf[DC];
-  int lim = -1;
-  int orow = -1;
-  {
-    const int r = rblk + c;
-    Pack8 pk;
-#pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      pk.u = u32x4{0u, 0u, 0u, 0u};
-      qf[dc] = pk.b;
-    }
-    if (r < R) {
-      const int j = r / g;
-      const int h = hk * g + (r - j * g);
-      orow = (b * a.k + j) * a.Hq + h;
-      const u32x4* src = reinterpret_cast<const u32x4*>(
-          static_cast<const uint16_t*>(a.q) + (size_t)orow * D);
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) {
-        pk.u = src[dc * 4 + G];
-        qf[dc] = pk.b;
-      }
-      lim = L - a.k + j;                       // last visible key of this row
+  const int X = a.Hkv * row_groups;
+  const int cap = PAGED ? a.max_pages * 16 : a.Lmax;
+  const int wg = blockIdx.x;
+  TileStart ts;
+  if (!tile_start_small(a, X, cap, wg, G, kgrp, &ts)) {
+    ts.T = tiles_before(a, X, cap, a.B);
+    ts.n0 = (int)((long long)ts.T * wg / G);
+    ts.n1 = (int)((long long)ts.T * (wg + 1) / G);
+    if (ts.n0 < ts.n1) {
+      ts.ca = locate(a, X, cap, ts.n0);
+      ts.cb = locate(a, X, cap, min(ts.n0 + kgrp, ts.n1 - 1));
     }
   }
-  // every row sees keys 0 .. L - k; tiles ending there need no mask
-  const int unmasked_end = L - a.k;
+  const int n0 = __builtin_amdgcn_readfirstlane(ts.n0);
+  const int n1 = __builtin_amdgcn_readfirstlane(ts.n1);
+  if (n0 >= n1) return;
+  const int last = n1 - 1;
 
-  float m = -INFINITY, l = 0.f;
-  floatx4 o[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const uint16_t* kbase = static_cast<const uint16_t*>(a.kc);
-  const uint16_t* vbase = static_cast<const uint16_t*>(a.vc);
-  const int ntiles = (k1 - k0 + TK - 1) / TK;
-  const int last = ntiles - 1;
-
-  // Copy i of this wave (ii = w * DMA_PER_WAVE + i) covers half
-  // ii / DMA_PER_HALF (K or V) and pieces P = (ii % DMA_PER_HALF) * 64 +
-  // lane: key P / PK, LDS slot P % PK holding global piece slot ^ lds_swizzle(key).
-  // Its source is a per-lane constant plus a per-tile offset, except in the
-  // tail tile, where keys past the sequence re-read its last key (masked).
-  // Page ids are scalar loads, so they do not count against vmcnt.
-  size_t cbase[DMA_PER_WAVE];
+  // per-lane constants of the copies: copy i of this wave (ii = w *
+  // DMA_PER_WAVE + i) covers half ii / DMA_PER_HALF (K or V) and pieces
+  // P = (ii % DMA_PER_HALF) * 64 + lane: key P / PK, LDS slot P % PK holding
+  // global piece slot ^ lds_swizzle(key).  The element offset of a copy is
+  // a uniform tile base plus this per-lane part.
   int ckey[DMA_PER_WAVE];
+  uint32_t clane[DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < DMA_PER_WAVE; ++i) {
     const int ii = w * DMA_PER_WAVE + i;
     const int P = (ii % DMA_PER_HALF) * 64 + lane;
-    const int key = P / PK, piece = P % PK;
+    const int key = P / PK;
+    const int piece = ((P % PK) ^ lds_swizzle<PK>(key)) * 8;
     ckey[i] = key;
-    const size_t pieceoff = (size_t)((piece ^ lds_swizzle<PK>(key)) * 8);
-    if constexpr (PAGED)
-      cbase[i] = (((size_t)hk * 16 + (key & 15)) * D) + pieceoff;
-    else
-      cbase[i] = (((size_t)b * a.Lmax + k0 + key) * a.Hkv + hk) * (size_t)D + pieceoff;
+    clane[i] = PAGED ? (uint32_t)((key & 15) * D + piece) : (uint32_t)(key * a.Hkv * D + piece);
   }
-  const size_t tile_stride = (size_t)TK * a.Hkv * D;   // contiguous: elements per tile
-  auto issue = [&](int tile, unsigned char* slot) {
-    const int t0 = k0 + tile * TK;
-    const bool tail = t0 + TK > L;
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.kc);
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.vc);
+  // copies of the tile under cursor cu; keys past the sequence re-read its
+  // last key (masked).  Page ids are scalar loads, so they do not count
+  // against vmcnt.
+  auto issue = [&](const TileCursor& cu, unsigned char* slot) {
+    const int t0 = cu.t * TK;
+    const int hk = cu.x / row_groups;
+    const bool tail = t0 + TK > cu.L;
     int pg0 = 0, pg1 = 0;
     if constexpr (PAGED) {
-      // the page table is read-only here: constant-space loads become
-      // scalar loads, which leave the vector-memory counter to the copies
-      const __attribute__((address_space(4))) int32_t* pt =
-          (const __attribute__((address_space(4))) int32_t*)(a.page_table + (size_t)b * a.max_pages);
-      const int lastp = (L - 1) >> 4;
+      cint32* pt = (cint32*)(a.page_table + (size_t)cu.b * a.max_pages);
+      const int lastp = (cu.L - 1) >> 4;
       pg0 = min(max((int)pt[min(t0 >> 4, lastp)], 0), a.num_pages - 1);
       pg1 = min(max((int)pt[min((t0 >> 4) + 1, lastp)], 0), a.num_pages - 1);
     }
+    const size_t tbase = PAGED ? 0 : (((size_t)cu.b * a.Lmax + t0) * a.Hkv + hk) * D;
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) {
       const int ii = w * DMA_PER_WAVE + i;
       const int half = ii / DMA_PER_HALF;
+      const int key = ckey[i];
       size_t off;
       if constexpr (PAGED) {
-        int key = ckey[i];
-        size_t base = cbase[i];
-        if (tail && t0 + key > L - 1) {        // re-read the last key
-          const int t = L - 1;
-          key = t - t0;
-          base = (((size_t)hk * 16 + (t & 15)) * D) + (cbase[i] & (size_t)(PK * 8 - 1));
+        uint32_t lo = clane[i];
+        int pk = key >> 4;                     // page 0 or 1 of the tile
+        if (tail && t0 + key > cu.L - 1) {     // re-read the last key
+          const int t = cu.L - 1 - t0;
+          lo = (uint32_t)((t & 15) * D) + (clane[i] & (uint32_t)(PK * 8 - 1));
+          pk = t >> 4;
         }
-        const int pg = key < 16 ? pg0 : pg1;
-        off = base + (size_t)pg * a.Hkv * 16 * D;
+        off = ((size_t)(pk ? pg1 : pg0) * a.Hkv + hk) * 16 * D + lo;
       } else {
-        off = cbase[i] + (size_t)tile * tile_stride;
-        if (tail && t0 + ckey[i] > L - 1)      // re-read the last key
-          off -= (size_t)(t0 + ckey[i] - (L - 1)) * a.Hkv * D;
+        off = tbase + clane[i];
+        if (tail && t0 + key > cu.L - 1)       // re-read the last key
+          off -= (size_t)(t0 + key - (cu.L - 1)) * a.Hkv * D;
       }
       __builtin_amdgcn_global_load_lds((gbl_cvoid*)((half ? vbase : kbase) + off),
                                        (lds_void*)(slot + half * HALF_BYTES + (ii % DMA_PER_HALF) * 1024),
@@ -237,31 +332,79 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     }
   };
 
-  // per-lane LDS offsets of the fragment reads inside a buffer
+  // per-lane LDS offsets of the fragment reads inside a slot
   uint32_t koff[2][DC];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int dc = 0; dc < DC; ++dc) {
       const int key = kb * 16 + c;
-      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G) ^ lds_swizzle<PK>(key)) * 16);
+      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G4) ^ lds_swizzle<PK>(key)) * 16);
     }
-  // ds_read_tr16_b64: lane j of group G addresses key 4G + j/4 (+16) at
-  // channels db*16 + 4*(j%4); lane c then receives 4 keys at channel db*16 + c
+  // ds_read_b64_tr_b16: lane j of group G4 addresses key 4 G4 + j / 4 (+16)
+  // at channels db * 16 + 4 (j % 4); lane c then receives 4 keys at channel
+  // db * 16 + c
   uint32_t voff[2][DB];
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int key = hh * 16 + 4 * G + (c >> 2);
+      const int key = hh * 16 + 4 * G4 + (c >> 2);
       const int ch = db * 16 + 4 * (c & 3);
       voff[hh][db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ lds_swizzle<PK>(key)) * 16) + (ch & 7) * 2;
     }
 
-  auto compute = [&](int it, const unsigned char* slot) {
-    const uint32_t sb = lds_addr(slot);
-    const int t0 = k0 + it * TK;
+  // segment state of this wave: pair, query row, its B operand of
+  // S^T = K Q^T, causal limit, running (max, sum, O^T)
+  int cur_pair = -1;
+  bool row_ok = false;
+  int lim = -1, orow = 0, unmasked_end = 0;
+  bf16x8 qf[DC];
+  float m = -INFINITY, l = 0.f;
+  floatx4 o[DB];
 
+  auto start_segment = [&](const TileCursor& cu) {
+    const int hk = cu.x / row_groups, rg = cu.x % row_groups;
+    const int r = rg * ROWS_WG + wr * 16 + c;
+    row_ok = r < R;
+    Pack8 pk;
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc) {
+      pk.u = u32x4{0u, 0u, 0u, 0u};
+      qf[dc] = pk.b;
+    }
+    lim = -1;
+    if (row_ok) {
+      const int j = r / g;
+      const int h = hk * g + (r - j * g);
+      orow = (cu.b * a.k + j) * a.Hq + h;
+      const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.q) + (size_t)orow * D);
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) {
+        pk.u = src[dc * 4 + G4];
+        qf[dc] = pk.b;
+      }
+      lim = cu.L - a.k + j;                    // last visible key of this row
+    }
+    unmasked_end = cu.L - a.k;                 // every row sees keys 0 .. L - k
+    m = -INFINITY;
+    l = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto flush = [&]() {
+    const float lsum = wave_sum_across_groups(l);
+    if (!row_ok) return;
+    const size_t prow = ((size_t)(cur_pair + wg) * KG + kgrp) * ROWS_WG + wr * 16 + c;
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<floatx4*>(a.part_o + prow * D + db * 16 + 4 * G4) = o[db] * inv;
+    if (G4 == 0) a.part_lse[prow] = lsum > 0.f ? m + log2f(lsum) : -INFINITY;
+  };
+
+  auto compute = [&](int t0, const unsigned char* slot) {
+    const uint32_t sb = lds_addr(slot);
     u32x4 kr[2][DC];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -279,7 +422,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
 #pragma unroll
       for (int db = 0; db < DB; ++db) vr[hh][db] = lds_read_tr16_b64(sb + voff[hh][db]);
 
-    // S^T = K Q^T: lane holds S[row c][key t0 + kb*16 + 4G + i] (log2 units)
+    // S^T = K Q^T: lane holds S[row c][key t0 + kb*16 + 4 G4 + i] (log2 units)
     float x[8];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -296,7 +439,7 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     if (t0 + TK - 1 > unmasked_end) {          // tail tile: causal mask
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int t = t0 + (e >> 2) * 16 + 4 * G + (e & 3);
+        const int t = t0 + (e >> 2) * 16 + 4 * G4 + (e & 3);
         if (t > lim) x[e] = -INFINITY;
       }
     }
@@ -326,10 +469,10 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     }
     l += psum;
 
-    // O^T += V^T P^T.  The product's K index runs over keys {4G..4G+3,
-    // 16+4G..16+4G+3}, the order in which the score accumulator handed this
-    // lane its P values; accumulator element i of block db is channel
-    // db*16 + 4G + i of row c.
+    // O^T += V^T P^T.  The product's K index runs over keys {4G4..4G4+3,
+    // 16+4G4..16+4G4+3}, the order in which the score accumulator handed
+    // this lane its P values; accumulator element i of block db is channel
+    // db*16 + 4 G4 + i of row c.
     lds_wait();
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
@@ -344,68 +487,94 @@ __global__ __launch_bounds__(NW * 64) void verify_split_bf16(VerifyArgs a, int k
     }
   };
 
-  // Every step issues KG tiles (past the end it re-reads the last one, which
-  // is still cached), so exactly (NBUF - 2 KG) tiles' copies are newer than
-  // the step's own tiles at each wait, and the wait covers precisely the
-  // tiles about to be read; the barrier also frees the slots of the
+  // Every step issues KG tiles (past the range it re-reads the last one,
+  // which is still cached), so exactly (NBUF - 2 KG) tiles' copies are newer
+  // than the step's own tiles at each wait, and the wait covers precisely
+  // the tiles about to be read; the barrier also frees the slots of the
   // previous step for refilling.  The tile reads are asm, so the compiler
-  // adds no waits of its own between them and the copies.
-  const int nsteps = (ntiles + KG - 1) / KG;
-#pragma unroll
-  for (int i = 0; i < NBUF - KG; ++i) issue(min(i, last), ring[i]);
-  for (int it = 0; it < nsteps; ++it) {
+  // adds no waits of its own between them and the copies.  A new segment
+  // (query loads, partial stores) drains this wave's memory counter first,
+  // so the counted waits only ever see copies.
+  TileCursor ic = uniform(ts.ca);              // issue cursor at tile in
+  int in = n0;
+  TileCursor cc = uniform(ts.cb);              // compute cursor at tile cn
+  int cn = n0 + kgrp;
+  const int nsteps = (n1 - n0 + KG - 1) / KG;
+#pragma unroll 1
+  for (int i = 0; i < NBUF - KG; ++i) {
+    issue(ic, ring[i]);
+    if (in < last) {
+      advance(a, X, cap, ic);
+      ++in;
+    }
+  }
+#pragma unroll 1
+  for (int s = 0; s < nsteps; ++s) {
     wait_vm_then_barrier<(NBUF - 2 * KG) * DMA_PER_WAVE>();
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
-      const int t = KG * it + NBUF - KG + j;
-      issue(min(t, last), ring[t % NBUF]);
+      issue(ic, ring[(s * KG + NBUF - KG + j) % NBUF]);
+      if (in < last) {
+        advance(a, X, cap, ic);
+        ++in;
+      }
     }
-    const int mine = KG * it + kgrp;           // wave-uniform
-    if (KG == 1 || mine < ntiles) compute(mine, ring[mine % NBUF]);
+    if (cn <= last) {                          // wave-uniform
+      const int pair = cc.b * X + cc.x;
+      if (pair != cur_pair) {
+        if (cur_pair >= 0) flush();
+        start_segment(cc);
+        cur_pair = pair;
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
+      }
+      compute(cc.t * TK, ring[(s * KG + kgrp) % NBUF]);
+#pragma unroll
+      for (int j = 0; j < KG; ++j) {
+        if (cn < last) {
+          advance(a, X, cap, cc);
+        }
+        ++cn;
+      }
+    }
   }
   // no copy may still be writing this work-group's LDS when it exits
   __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
-  l = wave_sum_across_groups(l);
   if constexpr (KG == 2) {
-    // group 1 hands (m, l, O) of its row block to group 0 through the ring
+    // When both key groups end on the same pair, group 1 hands its (max,
+    // sum, O) to group 0 through the ring and one combined partial is
+    // written (slot key group 0); otherwise each group writes its own.
     __syncthreads();                           // every wave is done with the ring
-    floatx4* xo = reinterpret_cast<floatx4*>(&ring[0][0]);
-    float2* xml = reinterpret_cast<float2*>(&ring[0][0] + NWR * DB * 64 * 16);
-    if (kgrp == 1) {
+    int* xpair = reinterpret_cast<int*>(&ring[0][0]);
+    floatx4* xo = reinterpret_cast<floatx4*>(&ring[0][0] + 256);
+    float2* xml = reinterpret_cast<float2*>(&ring[0][0] + 256 + NWR * DB * 64 * 16);
+    if (lane == 0) xpair[w] = cur_pair;
+    __syncthreads();
+    const bool joint = cur_pair >= 0 && xpair[wr] == xpair[NWR + wr];   // wave-uniform
+    if (kgrp == 1 && joint) {
+      const float lsum = wave_sum_across_groups(l);
 #pragma unroll
       for (int db = 0; db < DB; ++db) xo[(wr * DB + db) * 64 + lane] = o[db];
-      xml[wr * 64 + lane] = make_float2(m, l);
+      xml[wr * 64 + lane] = make_float2(m, lsum);
     }
     __syncthreads();
-    if (kgrp == 1) return;
-    const float2 ml = xml[wr * 64 + lane];
-    const float mn = fmaxf(m, ml.x);
-    const float f0 = m == -INFINITY ? 0.f : fast_exp2(m - mn);
-    const float f1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - mn);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] = o[db] * f0 + xo[(wr * DB + db) * 64 + lane] * f1;
-    l = l * f0 + ml.y * f1;
-    m = mn;
-  }
-  if (!active) return;
-
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  auto store_row = [&](float* dst) {
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-      *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[db] * inv;
-  };
-  if (nsplit == 1) {
-    if (orow >= 0) {
-      store_row(a.out + (size_t)orow * D);
-      if (a.lse != nullptr && G == 0)
-        a.lse[orow] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
+    if (kgrp == 1) {
+      if (!joint && cur_pair >= 0) flush();
+      return;
     }
-    return;
+    if (joint) {
+      const float2 ml = xml[wr * 64 + lane];
+      const float mn = fmaxf(m, ml.x);
+      const float f0 = m == -INFINITY ? 0.f : fast_exp2(m - mn);
+      const float f1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - mn);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] = o[db] * f0 + xo[(wr * DB + db) * 64 + lane] * f1;
+      // l is per lane until flush sums it over the row; the partner's sum
+      // is added on one lane of the row only
+      l = l * f0 + (G4 == 0 ? ml.y * f1 : 0.f);
+      m = mn;
+    }
   }
-  const size_t prow = ((size_t)(b * a.Hkv + hk) * nsplit + split) * rows_padded + rblk + c;
-  store_row(a.part_o + prow * D);
-  if (G == 0) a.part_lse[prow] = l > 0.f ? m + log2f(l) : -INFINITY;
+  if (cur_pair >= 0) flush();
 }
 
 // ----------------------------------------------------------- fp32 split
@@ -493,12 +662,11 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 }
 
 // ---------------------------------------------------------------- merge
-// One wave per output row of one (sequence, KV head).  The lanes load the
-// split lse values 64 at a time and form their weights 2^(lse - max) in
-// parallel; then the two half-waves take alternate splits (in lockstep, the
-// weight of split j handed over by a lane shuffle), each lane
-// accumulating 4 channels of the weighted partial outputs (loads of
-// several splits in flight), and the halves are added at the end.
+// One wave per output row of one (sequence, KV head).  The splits are taken
+// 16 at a time: lanes 0..15 load their split's lse while each half-wave
+// loads the partial outputs of 8 splits (4 channels per lane), all in one
+// round of memory accesses; the chunk's weights 2^(lse - max) then rescale
+// a running sum as in the online softmax.  Every shuffle runs on all lanes.
 // Grid (rows / 4, sequence x KV head).
 __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_split,
                                                     int nsplit, int rows_padded, int paged) {
@@ -514,38 +682,39 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
   const int L = seq_len(a, b, paged != 0);
   const int nvalid = min(nsplit, (L + keys_per_split - 1) / keys_per_split);
   const size_t base = (size_t)pair * nsplit * rows_padded + r;
-  float mx = -INFINITY;
-  for (int s = lane; s < nvalid; s += 64) mx = fmaxf(mx, a.part_lse[base + (size_t)s * rows_padded]);
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
   const int half = lane >> 5, d4 = lane & 31;
   const bool active = d4 < D / 4;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-  if (mx != -INFINITY) {
-    for (int s0 = 0; s0 < nvalid; s0 += 64) {
-      const int n = min(64, nvalid - s0);
-      float wl = 0.f;
-      if (lane < n) {
-        const float ls = a.part_lse[base + (size_t)(s0 + lane) * rows_padded];
-        wl = ls == -INFINITY ? 0.f : exp2f(ls - mx);
-      }
-      wsum += wl;
-      // both halves run the same trip count, so every shuffle reads an
-      // active lane; lanes past the last split (j = n, odd n) get weight 0
-      for (int jj = 0; jj < n; jj += 2) {
-        const int j = jj + half;
-        const float wgt = __shfl(wl, j & 63, 64);
-        const size_t pr = base + (size_t)(s0 + j) * rows_padded;
-        if (j < n && active && wgt != 0.f)
-          acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * D + d4 * 4);
-      }
+  float mx = -INFINITY, wsum = 0.f;
+  for (int s0 = 0; s0 < nvalid; s0 += 16) {
+    const int n = min(16, nvalid - s0);
+    const float ls = lane < n ? a.part_lse[base + (size_t)(s0 + lane) * rows_padded] : -INFINITY;
+    floatx4 po[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int j = 2 * i + half;
+      po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (j < n && active)
+        po[i] = *reinterpret_cast<const floatx4*>(a.part_o + (base + (size_t)(s0 + j) * rows_padded) * D + d4 * 4);
     }
+    float cm = ls;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) wsum += __shfl_xor(wsum, off, 64);
+    for (int off = 8; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
+    const float nm = fmaxf(mx, __shfl(cm, 0, 64));
+    if (nm == -INFINITY) continue;             // no key in any split so far (uniform)
+    const float keep = mx == -INFINITY ? 0.f : exp2f(mx - nm);
+    const float wl = ls == -INFINITY ? 0.f : exp2f(ls - nm);
+    float ws = wl;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], 32, 64);
+    for (int off = 8; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
+    wsum = wsum * keep + __shfl(ws, 0, 64);
+    acc = acc * keep;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += __shfl(wl, 2 * i + half, 64) * po[i];
+    mx = nm;
   }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], 32, 64);
   const int j = r / g;
   const int h = hk * g + (r - j * g);
   const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
@@ -555,32 +724,142 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
     a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
 }
 
-template <int D, int NW, bool PAGED, int KG>
-hipError_t launch_bf16(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
-  dim3 grid(a.Hkv * p.row_groups, p.nsplit, a.B);
-  hipLaunchKernelGGL((verify_split_bf16<D, NW, PAGED, KG>), grid, dim3(NW * 64), 0, st, a,
-                     p.keys_per_split, p.nsplit, p.row_groups, p.rows_padded);
+// -------------------------------------------------------- stream merge
+// One wave per output row of one pair (sequence b, x = KV head * row_groups
+// + row group).  The pair's tiles [U, U + nt(b)) were spread over work-
+// groups owner(U) .. owner(U + nt - 1), owner(n) = floor(((n + 1) G - 1) /
+// T); key group kg of work-group w wrote slot (pair + w) KG + kg if one of
+// its tiles (every KG-th from the range start) falls in the pair.  The
+// candidate partials are taken 32 at a time: lanes 0..31 find their slots
+// and load their lse while each half-wave loads the outputs of 16 of them
+// (4 channels per lane), in one round of memory accesses; the chunk's weights 2^(lse - max)
+// then rescale a running sum as in the online softmax.  Every shuffle runs
+// on all lanes.  Grid (ceil(rows per pair / 4), pairs).
+__global__ __launch_bounds__(256) void verify_stream_merge(VerifyArgs a, int G, int row_groups,
+                                                           int KG, int rows_wg, int paged) {
+  const int pair = blockIdx.y;
+  const int X = a.Hkv * row_groups;
+  const int b = pair / X, x = pair - b * X;
+  const int hk = x / row_groups, rg = x - hk * row_groups;
+  const int D = a.D;
+  const int g = a.Hq / a.Hkv;
+  const int R = a.k * g;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lr = blockIdx.x * 4 + w;           // row within the pair
+  const int r = rg * rows_wg + lr;
+  if (lr >= rows_wg || r >= R) return;
+  const int cap = paged ? a.max_pages * 16 : a.Lmax;
+  int T, U, nt;
+  if (a.B <= 64) {                             // one load: lane b' holds sequence b'
+    const int Lb = lane < a.B ? min(max(a.kv_len[lane], 0), cap) : 0;
+    const int span = ((Lb + 31) >> 5) * X;
+    int incl = span;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
+    }
+    T = __shfl(incl, 63, 64);
+    nt = (__shfl(Lb, b, 64) + 31) >> 5;
+    U = __shfl(incl - span, b, 64) + x * nt;
+  } else {
+    T = tiles_before(a, X, cap, a.B);
+    nt = (seq_len(a, b, paged != 0) + 31) >> 5;
+    U = tiles_before(a, X, cap, b) + x * nt;
+  }
+  const int half = lane >> 5, d4 = lane & 31;
+  const bool active = d4 < D / 4;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  float mx = -INFINITY, wsum = 0.f;
+  if (nt > 0) {
+    // range start of work-group v: floor(T v / G) = qt v + floor(rt v / G)
+    const unsigned qt = (unsigned)T / (unsigned)G, rt = (unsigned)T % (unsigned)G;
+    auto wstart = [&](int v) { return (int)(qt * (unsigned)v + (rt * (unsigned)v) / (unsigned)G); };
+    auto owner = [&](int n) { return (int)((((long long)n + 1) * G - 1) / T); };
+    const int wf = owner(U), wl = owner(U + nt - 1);
+    const int ncand = (wl - wf + 1) * KG;
+    for (int c0 = 0; c0 < ncand; c0 += 32) {
+      const int n = min(32, ncand - c0);
+      // lane i < n: slot of candidate c0 + i (key group kg of work-group
+      // wv), or -1 when that key group has no tile of the pair
+      int sl = -1;
+      if (lane < n) {
+        const int cand = c0 + lane;
+        const int wv = wf + cand / KG, kg = cand - (cand / KG) * KG;
+        const int s0 = wstart(wv), s1 = wstart(wv + 1);
+        const int lo = max(U, s0), hi = min(U + nt, s1);
+        const int first = s0 + kg + (lo > s0 + kg ? (lo - s0 - kg + KG - 1) / KG * KG : 0);
+        if (first < hi) sl = (pair + wv) * KG + kg;
+        if (KG == 2 && kg == 1 && sl >= 0) {
+          // both groups' last tiles in this pair: one combined partial
+          const int last0 = s0 + (s1 - 1 - s0) / 2 * 2;
+          const int last1 = s0 + 1 + (s1 - 2 - s0) / 2 * 2;
+          if (last0 >= U && last0 < U + nt && last1 >= U && last1 < U + nt) sl = -1;
+        }
+      }
+      const float ls = sl >= 0 ? a.part_lse[(size_t)sl * rows_wg + lr] : -INFINITY;
+      floatx4 po[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int sj = __shfl(sl, 2 * i + half, 64);
+        po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (sj >= 0 && active)
+          po[i] = *reinterpret_cast<const floatx4*>(a.part_o + ((size_t)sj * rows_wg + lr) * D + d4 * 4);
+      }
+      float cm = ls;
+#pragma unroll
+      for (int off = 16; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
+      const float nm = fmaxf(mx, __shfl(cm, 0, 64));
+      if (nm == -INFINITY) continue;           // no key in any partial so far (uniform)
+      const float keep = mx == -INFINITY ? 0.f : exp2f(mx - nm);
+      const float wl8 = ls == -INFINITY ? 0.f : exp2f(ls - nm);
+      float ws = wl8;
+#pragma unroll
+      for (int off = 16; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
+      wsum = wsum * keep + __shfl(ws, 0, 64);
+      acc = acc * keep;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc += __shfl(wl8, 2 * i + half, 64) * po[i];
+      mx = nm;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc[e] += __shfl_xor(acc[e], 32, 64);
+  const int j = r / g;
+  const int h = hk * g + (r - j * g);
+  const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  if (half == 0 && active) *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
+  if (a.lse != nullptr && lane == 0)
+    a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
+}
+
+template <int D, int NWR, int KG, int NBUF, bool PAGED>
+hipError_t launch_stream(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
+  hipLaunchKernelGGL((verify_stream_bf16<D, NWR, KG, NBUF, PAGED>), dim3(p.stream_wgs),
+                     dim3(NWR * KG * 64), 0, st, a, p.stream_wgs, p.row_groups);
   return hipGetLastError();
 }
 
 template <int D, bool PAGED>
 hipError_t dispatch_rb(const VerifyArgs& a, const VerifyPlan& p, hipStream_t st) {
   switch (p.row_blocks) {
-    case 1: return launch_bf16<D, 1, PAGED, 1>(a, p, st);
-    case 2: return launch_bf16<D, 2, PAGED, 1>(a, p, st);
-    default: return launch_bf16<D, 8, PAGED, 2>(a, p, st);
+    case 1: return launch_stream<D, 1, stream_cfg(1).kg, stream_cfg(1).nbuf, PAGED>(a, p, st);
+    case 2: return launch_stream<D, 2, stream_cfg(2).kg, stream_cfg(2).nbuf, PAGED>(a, p, st);
+    default: return launch_stream<D, 4, stream_cfg(4).kg, stream_cfg(4).nbuf, PAGED>(a, p, st);
   }
 }
 
 }  // namespace
 
-VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype) {
+VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype, int cus) {
   VerifyPlan p{};
   p.g = Hq / Hkv;
   p.rows = k * p.g;
   p.capacity = capacity;
+  p.ok = true;
   const int blocks16 = (p.rows + 15) / 16;
-  if (dtype == 0) {  // fp32 path: all rows in one work-group
+  if (dtype == 0) {  // fp32 path: all rows in one work-group, splits by capacity
     p.row_blocks = blocks16;
     p.row_groups = 1;
     p.rows_padded = p.rows;
@@ -588,27 +867,28 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     // statistics stay within 64 KB of LDS
     int kps = ((65536 - 4 * p.rows * D - 16 * p.rows) / (8 * std::max(p.rows, 1))) / 32 * 32;
     p.keys_per_split = std::max(32, std::min(1024, kps));
+    p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
+    p.part_rows = (size_t)B * Hkv * p.nsplit * p.rows_padded;
   } else {
-    // one wave per 16-row block, 1, 2 or 4 waves per work-group
+    // one wave per 16-row block, 1, 2 or 4 blocks per work-group.  Blocks
+    // of 4 run as 8 waves in two key groups over a 128 KB ring, one work-
+    // group per compute unit; smaller ones hold a 48 KB ring, three per
+    // unit.  The grid is that many work-groups, whatever the lengths.
     p.row_blocks = blocks16 <= 1 ? 1 : (blocks16 == 2 ? 2 : 4);
     p.row_groups = (blocks16 + p.row_blocks - 1) / p.row_blocks;
-    p.rows_padded = p.row_groups * p.row_blocks * 16;
-    // A work-group of 4 row blocks (8 waves in two key groups) holds a
-    // 128 KB LDS ring, one per compute unit; smaller ones (1-2 waves) hold
-    // 48 KB, three per unit.  Aim for that many work-groups per unit on 256
-    // units, all resident at once; at least one 32-key tile per split.  Small work-groups over long caches split four times
-    // finer: the splits are planned for the capacity, so with ragged
-    // sequence lengths the longest sequence would otherwise stream its keys
-    // through few work-groups, each bound by memory latency.
+    p.rows_wg = p.row_blocks * 16;
+    p.rows_padded = p.row_groups * p.rows_wg;
+    p.key_groups = stream_cfg(p.row_blocks).kg;
     const long long pairs = (long long)B * Hkv * p.row_groups;
-    const long long target = p.row_blocks == 4 ? 256 : (capacity >= 8192 ? 3072 : 768);
-    long long nsplit = std::max(1LL, (target + pairs - 1) / pairs);
-    long long kps = (capacity + nsplit - 1) / nsplit;
-    kps = std::max((long long)kTile, (kps + kTile - 1) / kTile * kTile);
-    p.keys_per_split = (int)kps;
+    // at least 4 tiles per work-group when every sequence is at capacity
+    const long long tiles_cap = pairs * ((capacity + kTile - 1) / kTile);
+    p.stream_wgs = (int)std::max(1LL, std::min((long long)std::max(1, cus) * stream_cfg(p.row_blocks).per_cu,
+                                               tiles_cap / 4));
+    // tile indices are 32-bit on the device
+    if (pairs * ((capacity + kTile - 1) / kTile) >= (1LL << 30)) p.ok = false;
+    p.part_rows = (size_t)(pairs + p.stream_wgs) * p.key_groups * p.rows_wg;
   }
-  p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
-  p.workspace_bytes = (size_t)B * Hkv * p.nsplit * p.rows_padded * ((size_t)D + 1) * sizeof(float);
+  p.workspace_bytes = p.part_rows * ((size_t)D + 1) * sizeof(float);
   return p;
 }
 
@@ -632,9 +912,13 @@ hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hi
     e = paged ? dispatch_rb<64, true>(a, p, st) : dispatch_rb<64, false>(a, p, st);
   }
   if (e != hipSuccess) return e;
-  if (dtype != 0 && p.nsplit == 1) return hipSuccess;   // the split kernel wrote out / lse
-  hipLaunchKernelGGL(verify_merge, dim3((p.rows + 3) / 4, a.Hkv * a.B), dim3(256), 0, st, a,
-                     p.keys_per_split, p.nsplit, p.rows_padded, paged ? 1 : 0);
+  if (dtype == 0)
+    hipLaunchKernelGGL(verify_merge, dim3((p.rows + 3) / 4, a.Hkv * a.B), dim3(256), 0, st, a,
+                       p.keys_per_split, p.nsplit, p.rows_padded, paged ? 1 : 0);
+  else
+    hipLaunchKernelGGL(verify_stream_merge, dim3((p.rows_wg + 3) / 4, a.B * a.Hkv * p.row_groups),
+                       dim3(256), 0, st, a, p.stream_wgs, p.row_groups, p.key_groups, p.rows_wg,
+                       paged ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -135,7 +135,13 @@ int sd_latent_compress(const void* latents, const void* feats, float* out,
  *   lse         [B, k, Hq] float32, or NULL when not wanted
  * Requirements: 1 <= k <= 16; Hq % Hkv == 0; k * (Hq / Hkv) <= 256;
  * D in {64, 128}; Lmax >= 1 (contiguous) or max_pages, num_pages >= 1
- * (paged); scale finite.
+ * (paged); scale finite.  bf16: B * Hkv * ceil(capacity / 32) * ceil(k *
+ * (Hq / Hkv) / 64) < 2^30, else SD_ERR_UNSUPPORTED (the workspace size is
+ * then 0).
+ * The bf16 workspace holds partial results per work-group, and the
+ * work-group count follows the compute units of the current device: query
+ * sd_verify_workspace_size with the device the call will run on current
+ * (a smaller workspace is rejected with SD_ERR_WORKSPACE, never overrun).
  * ---------------------------------------------------------------------- */
 size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D,
                                 int capacity, int dtype);

@@ -76,6 +76,9 @@ def test_verify_validation_errors(lib):
     assert call(D=96) == sd.SD_ERR_UNSUPPORTED
     assert call(Hq=512, Hkv=1) == sd.SD_ERR_UNSUPPORTED
     assert call(dt=0, Hq=32, Hkv=1) == sd.SD_ERR_UNSUPPORTED   # fp32 path: <= 64 rows
+    # bf16 tile list beyond 32-bit device indices: 4096 x 8 pairs x 2^15 tiles
+    assert call(B=4096, Hq=8, Hkv=8, lmax=1 << 20) == sd.SD_ERR_UNSUPPORTED
+    assert lib.sd_verify_workspace_size(4096, 4, 8, 8, 128, 1 << 20, 1) == 0
     assert call(ws=None) == sd.SD_ERR_WORKSPACE
     assert call(wsb=16) == sd.SD_ERR_WORKSPACE
     # paged: needs a page count

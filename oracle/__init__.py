@@ -19,6 +19,9 @@ reader can check it against the paper by eye:
 * ``lm_head_probs`` / ``sample_tokens`` -- the LM head's temperature softmax
   over the vocabulary and categorical sampling of the drafts (Sec. 3.1,
   Sec. 3.3, Algorithm 1).
+* ``spec_accept_logits`` / ``philox_uniforms`` -- acceptance from logits: the
+  temperature softmax in front of the rule and counter-based uniforms
+  (Philox-4x64-10, Salmon et al., SC'11).
 
 Readings of points the paper leaves open are stated in each module.  No
 function here is "parity unpinned": every one is checked in
@@ -29,6 +32,7 @@ enumeration or brute force.
 from .compress import latent_compress, softmax_rows
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
+from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
 from .accept import (
     spec_accept,
     spec_accept_one,

@@ -677,3 +677,110 @@ def test_sample_tokens_one_hot_and_degenerate():
     p[1, 4] = 5e-13
     u = np.array([0.9, 0.1, 0.3], dtype=np.float32)
     assert list(oracle.sample_tokens(p, u)) == [3, 4, 0]
+
+
+# ------------------------------------------------- acceptance from logits
+
+def _numpy_philox_block(counter, key):
+    """The block numpy's independent Philox-4x64 implementation produces at
+    256-bit counter `counter` (numpy advances its counter before each block,
+    so it is started one below)."""
+    c = sum(int(x) << (64 * i) for i, x in enumerate(counter)) - 1
+    c %= 1 << 256
+    start = np.array([(c >> (64 * i)) & ((1 << 64) - 1) for i in range(4)], dtype=np.uint64)
+    g = np.random.Philox(key=np.array(key, dtype=np.uint64), counter=start)
+    return [int(x) for x in g.random_raw(4)]
+
+
+def test_philox_matches_numpy_implementation():
+    cases = [((0, 0, 0, 0), (0, 0)), ((1, 2, 3, 4), (5, 6)), ((0, 7, 1, 0), (123456789, 0)),
+             ((2 ** 64 - 1, 3, 0, 0), (2 ** 63 + 11, 99)), ((5, 0, 2 ** 40, 0), (2 ** 64 - 1, 2 ** 64 - 1))]
+    for ctr, key in cases:
+        assert oracle.philox4x64(ctr, key) == _numpy_philox_block(ctr, key), (ctr, key)
+
+
+def test_philox_uniforms_layout_and_grid():
+    seed, offset, B, n = 0x1234ABCD, 77, 3, 9
+    u = oracle.philox_uniforms(seed, offset, B, n)
+    assert u.shape == (B, n) and u.dtype == np.float32
+    a = u.astype(np.float64) * 2.0 ** 24
+    assert np.all(a == np.floor(a)) and np.all((a >= 0) & (a < 2 ** 24))
+    for b in range(B):
+        for i in range(n):
+            word = _numpy_philox_block((i // 4, b, offset, 0), (seed, 0))[i % 4]
+            assert int(a[b, i]) == word >> 40
+    # different seeds, offsets and sequences give different streams
+    assert not np.array_equal(u, oracle.philox_uniforms(seed + 1, offset, B, n))
+    assert not np.array_equal(u, oracle.philox_uniforms(seed, offset + 1, B, n))
+    assert not np.array_equal(u[0], u[1])
+
+
+def _logit_case(seed, B=2, k=3, V=11, scale=3.0, integer=False):
+    rng = np.random.default_rng(seed)
+    z = rng.normal(size=(B, k + 1, V)) * scale
+    zd = z[:, :k] + rng.normal(size=(B, k, V))
+    if integer:
+        z, zd = np.round(z), np.round(zd)
+    draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    return z, zd, draft
+
+
+def test_accept_logits_scale_and_shift_invariance():
+    # softmax(z / tau) is unchanged (exactly, in binary floating point) by a
+    # power-of-two scale of both z and tau, and by integer shifts of a row of
+    # integer-valued logits
+    z, zd, draft = _logit_case(5, integer=True)
+    ref = oracle.spec_accept_logits(z, zd, draft, 9, 1, 0.75, oracle.ACCEPT_SAMPLED)
+    scaled = oracle.spec_accept_logits(4 * z, 4 * zd, draft, 9, 1, 3.0, oracle.ACCEPT_SAMPLED)
+    shift = np.arange(z.shape[1])[None, :, None] * 7.0
+    shifted = oracle.spec_accept_logits(z + shift, zd - shift[:, :-1], draft, 9, 1, 0.75,
+                                        oracle.ACCEPT_SAMPLED)
+    for got in (scaled, shifted):
+        assert np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1])
+
+
+def test_accept_logits_cold_limit_is_greedy():
+    # as tau -> 0, p and q become one-hot at the argmaxes: a draft equal to
+    # the target argmax is accepted (u q = u < 1 = p), any other is rejected
+    # (p = 0) and the residual is one-hot at the target argmax
+    z, zd, _ = _logit_case(11, B=4, k=4, V=13)
+    draft = np.argmax(zd, axis=-1).astype(np.int32)
+    draft[1, 0] = np.argmax(z[1, 0])                     # plant agreements
+    draft[2, :2] = np.argmax(z[2, :2], axis=-1)
+    cold = oracle.spec_accept_logits(z, zd, draft, 3, 0, 1e-4, oracle.ACCEPT_SAMPLED)
+    greedy = oracle.spec_accept_logits(z, None, draft, 0, 0, 0.0, oracle.ACCEPT_GREEDY)
+    assert np.array_equal(cold[0], greedy[0]) and np.array_equal(cold[1], greedy[1])
+
+
+def test_accept_logits_greedy_ignores_temperature_and_seed():
+    z, zd, _ = _logit_case(2, B=3, k=3, V=9)
+    draft = np.argmax(z[:, :3], axis=-1).astype(np.int32)
+    draft[0, 1] = (draft[0, 1] + 1) % 9                  # mismatch at position 1
+    a = oracle.spec_accept_logits(z, zd, draft, 1, 2, 0.3, oracle.ACCEPT_GREEDY)
+    b = oracle.spec_accept_logits(z, None, draft, 8, 5, 2.0, oracle.ACCEPT_GREEDY)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert a[0].tolist() == [1, 3, 3]
+    assert a[1][0].tolist()[:2] == [draft[0, 0], int(np.argmax(z[0, 1]))]
+
+
+def test_accept_logits_first_token_follows_target_law():
+    # speculative sampling emits its first token with the target law p_0
+    # whatever the draft does; over many (seed, offset) streams the counts
+    # pass a chi-square test against softmax(z_0 / tau)
+    V, k, tau = 6, 2, 1.3
+    rng = np.random.default_rng(4)
+    z = rng.normal(size=(1, k + 1, V)) * 1.5
+    zd = rng.normal(size=(1, k, V)) * 1.5
+    q = oracle.softmax_temperature(zd, tau)
+    p0 = oracle.softmax_temperature(z, tau)[0, 0]
+    counts = np.zeros(V)
+    trials = 6000
+    for s in range(trials):
+        # the drafts follow q (drawn from an unrelated generator)
+        d = np.array([[rng.choice(V, p=q[0, i]) for i in range(k)]], dtype=np.int32)
+        n, toks = oracle.spec_accept_logits(z, zd, d, 1000 + s, s, tau, oracle.ACCEPT_SAMPLED)
+        counts[toks[0, 0]] += 1
+    expected = p0 * trials
+    chi2 = float(np.sum((counts - expected) ** 2 / expected))
+    # 5 degrees of freedom: P(chi2 > 20.5) ~ 0.001
+    assert chi2 < 20.5, (counts, expected)

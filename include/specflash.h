@@ -194,6 +194,54 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Speculative acceptance from logits (the same rule as sd_spec_accept,
+ * Sec. 3.1 and Sec. 3.3, with the temperature softmax of Sec. 4.2 and the
+ * uniforms produced on the device).
+ *
+ * SD_ACCEPT_SAMPLED: p = softmax(target_logits / tau) and q =
+ *   softmax(draft_logits / tau) per row, in float32 (p(v) = 2^(z(v) s - M)
+ *   / L with s = log2(e) / tau and the row's max M and sum L), and u[b, i] =
+ *   the Philox uniform of sd_philox_uniforms(seed, offset); then the rule
+ *   of sd_spec_accept exactly as stated there, applied to these float32
+ *   values.
+ * SD_ACCEPT_GREEDY: g_i = argmax_v target_logits[b, i, v] (lowest index on
+ *   ties); temperature, seed, offset and draft_logits are not used
+ *   (draft_logits may be NULL).
+ *
+ *   target_logits [B, k+1, V] dtype (SD_F32 or SD_BF16)
+ *   draft_logits  [B, k, V]   dtype (sampled mode)
+ *   draft         [B, k]      int32 drafted ids
+ *   seed, offset              key and stream offset of the uniforms
+ *   temperature               tau > 0, finite (sampled mode)
+ *   n_accepted, tokens        as for sd_spec_accept
+ *   workspace   sd_spec_accept_logits_workspace_size(B, k, V, mode) bytes
+ *               (row statistics of the logits, then the rule's partials)
+ * Requirements: as for sd_spec_accept; logits finite (others give an
+ * unspecified result, never an out-of-bounds access).
+ * ---------------------------------------------------------------------- */
+size_t sd_spec_accept_logits_workspace_size(int B, int k, int V, int mode);
+
+int sd_spec_accept_logits(const void* target_logits, const void* draft_logits,
+                          const int32_t* draft, uint64_t seed, uint64_t offset,
+                          float temperature, int32_t* n_accepted,
+                          int32_t* tokens, int B, int k, int V, int dtype,
+                          int mode, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/* ------------------------------------------------------------------------
+ * Counter-based uniforms for the acceptance (Philox-4x64-10 of Salmon,
+ * Moraes, Dror and Shaw, SC'11).  u[b, i] for b < B, i < n: the block
+ * at counter (i / 4, b, offset, 0) under key (seed, 0), its word i % 4
+ * as (word >> 40) * 2^-24, a multiple of 2^-24 in [0, 1).  Any (b, i) is
+ * computed alone, so the same values arise wherever they are needed.
+ *
+ *   u   [B, n] float32, device, out
+ * Requirements: B >= 1, 1 <= n <= 2^16, B * n <= 2^31 - 1.
+ * ---------------------------------------------------------------------- */
+int sd_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B,
+                       int n, void* stream);
+
+/* ------------------------------------------------------------------------
  * LM head with temperature softmax (Sec. 3.1: the head maps a feature to a
  * distribution over the vocabulary; Sec. 3.3 and Algorithm 1: the draft's K
  * hidden states go through the target's frozen head to give P'; Sec. 4.2:

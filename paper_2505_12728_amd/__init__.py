@@ -27,6 +27,7 @@ __all__ = [
     "sd_spec_accept_workspace_size", "sd_spec_accept",
     "sd_lm_head_workspace_size", "sd_lm_head_probs",
     "sd_sample_workspace_size", "sd_sample_tokens",
+    "sd_spec_accept_logits_workspace_size", "sd_spec_accept_logits", "sd_philox_uniforms",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -49,6 +50,10 @@ _SIGNATURES = {
                                  _i, _i, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
     "sd_spec_accept_workspace_size": (_sz, [_i, _i, _i, _i]),
     "sd_spec_accept": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "sd_spec_accept_logits_workspace_size": (_sz, [_i, _i, _i, _i]),
+    "sd_spec_accept_logits": (_i, [_vp, _vp, _vp, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_float,
+                                   _vp, _vp, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "sd_philox_uniforms": (_i, [ctypes.c_uint64, ctypes.c_uint64, _vp, _i, _i, _vp]),
     "sd_lm_head_workspace_size": (_sz, [_i, _i, _i, _i]),
     "sd_lm_head_probs": (_i, [_vp, _vp, _vp, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
     "sd_sample_workspace_size": (_sz, [_i, _i]),
@@ -262,6 +267,53 @@ def sd_spec_accept(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, toke
                                   _stream(stream))
     _raise(st, "sd_spec_accept")
     return n_accepted, tokens
+
+
+def sd_spec_accept_logits_workspace_size(B, k, V, mode):
+    return library().sd_spec_accept_logits_workspace_size(B, k, V, mode)
+
+
+def sd_spec_accept_logits(target_logits, draft_logits, draft, seed, offset, temperature,
+                          mode=SD_ACCEPT_SAMPLED, n_accepted=None, tokens=None, workspace=None,
+                          stream=None):
+    """Acceptance from logits: target_logits [B, k+1, V], draft_logits [B, k, V]
+    (fp32 or bf16, same dtype), draft [B, k] int32; uniforms from Philox(seed,
+    offset).  Returns (n_accepted [B] int32, tokens [B, k+1] int32)."""
+    torch = _torch()
+    _check(target_logits, "target_logits", ndim=3)
+    _check(draft, "draft", dtype=torch.int32, ndim=2)
+    B, kp1, V = target_logits.shape
+    k = kp1 - 1
+    if tuple(draft.shape) != (B, k):
+        raise ValueError("draft must be [B, k]")
+    if mode == SD_ACCEPT_SAMPLED:
+        _check(draft_logits, "draft_logits", dtype=target_logits.dtype, ndim=3)
+        if tuple(draft_logits.shape) != (B, k, V):
+            raise ValueError("draft_logits must be [B, k, V]")
+    dt = _dtype_code(target_logits)
+    if n_accepted is None:
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=target_logits.device)
+    if tokens is None:
+        tokens = torch.empty((B, k + 1), dtype=torch.int32, device=target_logits.device)
+    ws_bytes = sd_spec_accept_logits_workspace_size(B, k, V, mode)
+    ws, ws_len = _workspace(ws_bytes, target_logits.device, workspace)
+    st = library().sd_spec_accept_logits(_ptr(target_logits), _ptr(draft_logits), _ptr(draft),
+                                         int(seed), int(offset), float(temperature),
+                                         _ptr(n_accepted), _ptr(tokens), B, k, V, dt, int(mode),
+                                         _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_spec_accept_logits")
+    return n_accepted, tokens
+
+
+def sd_philox_uniforms(seed, offset, B, n, out=None, device=None, stream=None):
+    """u [B, n] float32 on the device: the acceptance uniforms of (seed, offset)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty((B, n), dtype=torch.float32, device=device or "cuda")
+    _check(out, "out", dtype=torch.float32, ndim=2)
+    st = library().sd_philox_uniforms(int(seed), int(offset), _ptr(out), B, n, _stream(stream))
+    _raise(st, "sd_philox_uniforms")
+    return out
 
 
 def sd_lm_head_workspace_size(R, d, V, dtype):

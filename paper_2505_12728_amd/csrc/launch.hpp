@@ -100,4 +100,18 @@ struct AcceptArgs {
 size_t accept_workspace_bytes(int B, int k, int V, int mode);
 hipError_t launch_accept(const AcceptArgs& a, void* workspace, hipStream_t s);
 
+// acceptance from logits: the rule's fields (p, q, u unused) plus the logits,
+// log2(e) / tau and the Philox key / offset of the uniforms
+struct AcceptLogitsArgs {
+  AcceptArgs rule;
+  const void* target_logits;   // [B, k+1, V]
+  const void* draft_logits;    // [B, k, V] (sampled mode)
+  float scale_log2;
+  uint64_t seed, offset;
+};
+
+size_t accept_logits_workspace_bytes(int B, int k, int V, int mode);
+hipError_t launch_accept_logits(const AcceptLogitsArgs& a, int dtype, void* workspace, hipStream_t s);
+hipError_t launch_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B, int n, hipStream_t s);
+
 }  // namespace sd

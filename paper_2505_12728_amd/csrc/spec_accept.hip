@@ -59,16 +59,94 @@ __device__ __forceinline__ uint64_t fixed_weight(float r) {
   return s >= 1.0f ? (uint64_t)s : 0ull;
 }
 
-// Sampled weight of entry v: residual (use_q) or p alone.
-__device__ __forceinline__ uint64_t weight_at(const float* prow, const float* qrow, int v, int use_q) {
-  float r = prow[v];
-  if (use_q) r = fmaxf(0.0f, r - qrow[v]);
+// Where the rule's inputs come from.  A source gives, for sequence b,
+// position i and token v: target(b, i, v) = p_i(v), drafted(b, i, v) =
+// q_i(v), greedy(b, i, v) = the value whose row maximum is the greedy token,
+// and uniform(b, i) = u_i.
+
+// p, q and u handed over as float32 arrays
+struct ProbSrc {
+  const float* p;
+  const float* q;
+  const float* u;
+  int k, V;
+  __device__ __forceinline__ float target(int b, int i, int v) const {
+    return p[((size_t)b * (k + 1) + i) * V + v];
+  }
+  __device__ __forceinline__ float drafted(int b, int i, int v) const {
+    return q[((size_t)b * k + i) * V + v];
+  }
+  __device__ __forceinline__ float greedy(int b, int i, int v) const { return target(b, i, v); }
+  __device__ __forceinline__ float uniform(int b, int i) const { return u[(size_t)b * (k + 1) + i]; }
+};
+
+// Philox-4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 64 x 64 -> 128-bit products, the high halves mixed with the other words
+// and the key, the key bumped by the Weyl increments.  Uniform i of sequence
+// b is word i % 4 of the block at counter (i / 4, b, offset, 0) under key
+// (seed, 0), as a multiple of 2^-24: (word >> 40) * 2^-24.
+__device__ __forceinline__ float philox_uniform(uint64_t seed, uint64_t offset, int b, int i) {
+  uint64_t c0 = (uint64_t)(i >> 2), c1 = (uint64_t)b, c2 = offset, c3 = 0;
+  uint64_t k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t lo0 = 0xD2E7470EE14C6C93ull * c0, hi0 = __umul64hi(0xD2E7470EE14C6C93ull, c0);
+    const uint64_t lo1 = 0xCA5A826395121157ull * c2, hi1 = __umul64hi(0xCA5A826395121157ull, c2);
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+  const int wsel = i & 3;
+  const uint64_t word = wsel == 0 ? c0 : (wsel == 1 ? c1 : (wsel == 2 ? c2 : c3));
+  return (float)(word >> 40) * 5.9604644775390625e-08f;   // 2^-24
+}
+
+__device__ __forceinline__ float load_logit(const float* z, size_t i) { return z[i]; }
+__device__ __forceinline__ float load_logit(const uint16_t* z, size_t i) { return bf16_bits_to_float(z[i]); }
+
+// p and q from logits at temperature tau: p_i(v) = 2^(z_i(v) s - M_i) / L_i
+// with s = log2(e) / tau and the row statistics (M_i, 1 / L_i) in `rows`
+// (target rows b (k+1) + i, then draft rows B (k+1) + b k + i); u from
+// Philox.  Greedy compares the target logits themselves.
+template <typename T>
+struct LogitSrc {
+  const T* zt;
+  const T* zd;
+  const float2* rows;
+  float s;
+  uint64_t seed, offset;
+  int B, k, V;
+  __device__ __forceinline__ float target(int b, int i, int v) const {
+    const size_t r = (size_t)b * (k + 1) + i;
+    const float2 st = rows[r];
+    return fast_exp2(load_logit(zt, r * V + v) * s - st.x) * st.y;
+  }
+  __device__ __forceinline__ float drafted(int b, int i, int v) const {
+    const size_t r = (size_t)b * k + i;
+    const float2 st = rows[(size_t)B * (k + 1) + r];
+    return fast_exp2(load_logit(zd, r * V + v) * s - st.x) * st.y;
+  }
+  __device__ __forceinline__ float greedy(int b, int i, int v) const {
+    return load_logit(zt, ((size_t)b * (k + 1) + i) * V + v);
+  }
+  __device__ __forceinline__ float uniform(int b, int i) const { return philox_uniform(seed, offset, b, i); }
+};
+
+// Sampled weight of entry v of row n: residual (use_q) or p alone.
+template <typename Src>
+__device__ __forceinline__ uint64_t weight_at(const Src& src, int b, int n, int v, int use_q) {
+  float r = src.target(b, n, v);
+  if (use_q) r = fmaxf(0.0f, r - src.drafted(b, n, v));
   return fixed_weight(r);
 }
 
 // n for one sequence: leading accepted drafts.  Uses lanes 0..63 of wave 0;
 // the result is returned to every thread through `slot`.
-__device__ int accepted_prefix(const AcceptArgs& a, int b, int* slot) {
+template <typename Src>
+__device__ int accepted_prefix(const AcceptArgs& a, const Src& src, int b, int* slot) {
   const int k = a.k, V = a.V;
   if (threadIdx.x < 64) {
     const int i = threadIdx.x;
@@ -76,9 +154,8 @@ __device__ int accepted_prefix(const AcceptArgs& a, int b, int* slot) {
     if (i < k) {
       const int x = a.draft[(size_t)b * k + i];
       if (x >= 0 && x < V) {
-        const double pu = (double)a.u[(size_t)b * (k + 1) + i] *
-                          (double)a.q[((size_t)b * k + i) * V + x];
-        acc = pu < (double)a.p[((size_t)b * (k + 1) + i) * V + x];
+        const double pu = (double)src.uniform(b, i) * (double)src.drafted(b, i, x);
+        acc = pu < (double)src.target(b, i, x);
       }
     }
     // bit i set where position i rejects; position k always "rejects"
@@ -102,11 +179,13 @@ __device__ __forceinline__ ArgMax better(ArgMax x, ArgMax y) {
   return x;
 }
 
-__device__ ArgMax block_argmax_range(const float* row, int v0, int v1, ArgMax* sm) {
+// (value, lowest index) maximum of value(v) over [v0, v1)
+template <typename F>
+__device__ ArgMax block_argmax_range(F&& value, int v0, int v1, ArgMax* sm) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   ArgMax best{-INFINITY, -1};
   for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
-    const float x = row[v];
+    const float x = value(v);
     if (best.i < 0 || x > best.v) best = ArgMax{x, v};   // indices increase: ties keep the first
   }
 #pragma unroll
@@ -125,7 +204,8 @@ __device__ ArgMax block_argmax_range(const float* row, int v0, int v1, ArgMax* s
 // workspace layout (per sequence b, chunk c):
 //   sampled: uint64 sums[B][C][2]  (residual / p-only)
 //   greedy:  ArgMax best[B][k+1][C]
-__global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, void* ws, int nchunks) {
+template <typename Src>
+__global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, Src src, void* ws, int nchunks) {
   __shared__ uint64_t wsum[kWaves][2];
   __shared__ ArgMax sm[kWaves];
   __shared__ int s_n;
@@ -135,20 +215,18 @@ __global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, void* ws
   if (a.mode == 0) {
     ArgMax* out = static_cast<ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
     for (int i = 0; i <= k; ++i) {
-      const ArgMax r = block_argmax_range(a.p + ((size_t)b * (k + 1) + i) * V, v0, v1, sm);
+      const ArgMax r = block_argmax_range([&](int v) { return src.greedy(b, i, v); }, v0, v1, sm);
       if (threadIdx.x == 0) out[(size_t)i * nchunks + chunk] = r;
     }
     return;
   }
-  const int n = accepted_prefix(a, b, &s_n);
-  const float* prow = a.p + ((size_t)b * (k + 1) + n) * V;
-  const float* qrow = n < k ? a.q + ((size_t)b * k + n) * V : nullptr;
+  const int n = accepted_prefix(a, src, b, &s_n);
   const int use_q = n < k ? 1 : 0;
   uint64_t sr = 0, sp = 0;
   for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
-    const float pv = prow[v];
+    const float pv = src.target(b, n, v);
     sp += fixed_weight(pv);
-    sr += use_q ? fixed_weight(fmaxf(0.0f, pv - qrow[v])) : fixed_weight(pv);
+    sr += use_q ? fixed_weight(fmaxf(0.0f, pv - src.drafted(b, n, v))) : fixed_weight(pv);
   }
   sr = wave_sum_u64(sr);
   sp = wave_sum_u64(sp);
@@ -192,7 +270,8 @@ __device__ uint64_t block_exclusive_scan(uint64_t x, uint64_t* tot, uint64_t* to
   return before + inc - x;
 }
 
-__global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const void* ws, int nchunks) {
+template <typename Src>
+__global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src, const void* ws, int nchunks) {
   __shared__ ArgMax sm[kWaves];
   __shared__ uint64_t tot[kWaves];
   __shared__ int s_n;
@@ -229,10 +308,8 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const vo
     }
     n = nn;
   } else {
-    n = accepted_prefix(a, b, &s_n);
+    n = accepted_prefix(a, src, b, &s_n);
     const uint64_t* sums = static_cast<const uint64_t*>(ws) + (size_t)b * nchunks * 2;
-    const float* prow = a.p + ((size_t)b * (k + 1) + n) * V;
-    const float* qrow = n < k ? a.q + ((size_t)b * k + n) * V : nullptr;
     // residual weights, else p-only weights, else argmax
     uint64_t S;
     uint64_t x = c < nchunks ? sums[2 * c] : 0ull;
@@ -244,10 +321,10 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const vo
       before = block_exclusive_scan(x, tot, &S);
     }
     if (S == 0) {
-      token = block_argmax_range(prow, 0, V, sm).i;
+      token = block_argmax_range([&](int v) { return src.target(b, n, v); }, 0, V, sm).i;
     } else {
       const int use_q = (sel == 0 && n < k) ? 1 : 0;
-      float uf = a.u[(size_t)b * (k + 1) + k] * 16777216.0f;   // exact: u is a float32
+      float uf = src.uniform(b, k) * 16777216.0f;   // exact: u is a float32
       uf = fminf(fmaxf(floorf(uf), 0.0f), 16777215.0f);
       const uint64_t av = (uint64_t)uf;
       const uint64_t T = av * (S >> 24) + ((av * (S & 0xffffffull)) >> 24);
@@ -266,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const vo
       uint64_t running = s_before;
       for (int base = c0; base < c1; base += kThreads) {
         const int v = base + 64 * w + lane;
-        uint64_t y = v < c1 ? weight_at(prow, qrow, v, use_q) : 0ull;
+        uint64_t y = v < c1 ? weight_at(src, b, n, v, use_q) : 0ull;
 #pragma unroll
         for (int d = 1; d < 64; d <<= 1) {
           const uint64_t z = shfl_up_u64(y, d);
@@ -294,7 +371,128 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, const vo
   if (threadIdx.x == 0) a.n_accepted[b] = n;
 }
 
+// Row statistics of the logits at temperature: grid (vocabulary chunk, row)
+// with rows b (k+1) + i of the target logits, then B (k+1) + b k + i of the
+// draft logits; each work-group writes (max, sum 2^(z s - max)) of its chunk.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void logit_stats_chunks(const T* zt, const T* zd, float s, int B,
+                                                               int k, int V, float2* part, int nchunks) {
+  __shared__ float2 sm[kWaves];
+  const int chunk = blockIdx.x, r = blockIdx.y;
+  const int rt = B * (k + 1);
+  const T* row = r < rt ? zt + (size_t)r * V : zd + (size_t)(r - rt) * V;
+  const int v0 = chunk * kChunk, v1 = min(V, v0 + kChunk);
+  float x[kChunk / kThreads];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kChunk / kThreads; ++j) {
+    const int v = v0 + j * kThreads + threadIdx.x;
+    x[j] = v < v1 ? load_logit(row, v) * s : -INFINITY;
+    m = fmaxf(m, x[j]);
+  }
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  if (lane == 0) sm[w].x = m;
+  __syncthreads();
+  float M = sm[0].x;
+  for (int i = 1; i < kWaves; ++i) M = fmaxf(M, sm[i].x);
+  float l = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int j = 0; j < kChunk / kThreads; ++j) l += fast_exp2(x[j] - M);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+  __syncthreads();
+  if (lane == 0) sm[w].y = l;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float L = 0.f;
+    for (int i = 0; i < kWaves; ++i) L += sm[i].y;
+    part[(size_t)r * nchunks + chunk] = make_float2(M, L);
+  }
+}
+
+// One wave per row: the chunk statistics merged into (M, 1 / L).
+__global__ __launch_bounds__(kThreads) void logit_stats_rows(const float2* part, float2* rows, int nrows,
+                                                             int nchunks) {
+  const int r = blockIdx.x * kWaves + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (r >= nrows) return;
+  float m = -INFINITY;
+  for (int c = lane; c < nchunks; c += 64) m = fmaxf(m, part[(size_t)r * nchunks + c].x);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  float l = 0.f;
+  for (int c = lane; c < nchunks; c += 64) {
+    const float2 st = part[(size_t)r * nchunks + c];
+    if (st.x != -INFINITY) l += st.y * fast_exp2(st.x - m);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+  if (lane == 0) rows[r] = make_float2(m, 1.f / l);
+}
+
+__global__ __launch_bounds__(kThreads) void philox_uniforms_kernel(uint64_t seed, uint64_t offset, float* u,
+                                                                   int B, int n) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t < B * n) u[t] = philox_uniform(seed, offset, t / n, t % n);
+}
+
+template <typename Src>
+hipError_t launch_rule(const AcceptArgs& a, const Src& src, void* ws, hipStream_t st) {
+  const int nchunks = (a.V + kChunk - 1) / kChunk;
+  hipLaunchKernelGGL((accept_chunks<Src>), dim3(nchunks, a.B), dim3(kThreads), 0, st, a, src, ws, nchunks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((accept_finish<Src>), dim3(a.B), dim3(kThreads), 0, st, a, src, ws, nchunks);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_logits(const AcceptLogitsArgs& la, void* ws, hipStream_t st) {
+  const AcceptArgs& a = la.rule;
+  const int nchunks = (a.V + kChunk - 1) / kChunk;
+  const int nrows = a.B * (2 * a.k + 1);
+  LogitSrc<T> src{static_cast<const T*>(la.target_logits), static_cast<const T*>(la.draft_logits), nullptr,
+                  la.scale_log2, la.seed, la.offset, a.B, a.k, a.V};
+  unsigned char* base = static_cast<unsigned char*>(ws);
+  if (a.mode != 0) {
+    float2* part = reinterpret_cast<float2*>(base);
+    float2* rows = part + (size_t)nrows * nchunks;
+    hipLaunchKernelGGL((logit_stats_chunks<T>), dim3(nchunks, nrows), dim3(kThreads), 0, st, src.zt, src.zd,
+                       la.scale_log2, a.B, a.k, a.V, part, nchunks);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(logit_stats_rows, dim3((nrows + kWaves - 1) / kWaves), dim3(kThreads), 0, st, part, rows,
+                       nrows, nchunks);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    src.rows = rows;
+    base += ((size_t)nrows * (nchunks + 1) * sizeof(float2) + 255) / 256 * 256;
+  }
+  return launch_rule(a, src, base, st);
+}
+
 }  // namespace
+
+size_t accept_logits_workspace_bytes(int B, int k, int V, int mode) {
+  const int nchunks = (V + kChunk - 1) / kChunk;
+  size_t stats = 0;
+  if (mode != 0) stats = ((size_t)B * (2 * k + 1) * (nchunks + 1) * sizeof(float2) + 255) / 256 * 256;
+  return stats + accept_workspace_bytes(B, k, V, mode);
+}
+
+hipError_t launch_accept_logits(const AcceptLogitsArgs& la, int dtype, void* ws, hipStream_t st) {
+  return dtype == 0 ? launch_logits<float>(la, ws, st) : launch_logits<uint16_t>(la, ws, st);
+}
+
+hipError_t launch_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B, int n, hipStream_t st) {
+  const long long total = (long long)B * n;
+  hipLaunchKernelGGL(philox_uniforms_kernel, dim3((unsigned)((total + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     st, seed, offset, u, B, n);
+  return hipGetLastError();
+}
 
 size_t accept_workspace_bytes(int B, int k, int V, int mode) {
   const int nchunks = (V + kChunk - 1) / kChunk;
@@ -303,12 +501,7 @@ size_t accept_workspace_bytes(int B, int k, int V, int mode) {
 }
 
 hipError_t launch_accept(const AcceptArgs& a, void* ws, hipStream_t st) {
-  const int nchunks = (a.V + kChunk - 1) / kChunk;
-  hipLaunchKernelGGL(accept_chunks, dim3(nchunks, a.B), dim3(kThreads), 0, st, a, ws, nchunks);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_finish, dim3(a.B), dim3(kThreads), 0, st, a, ws, nchunks);
-  return hipGetLastError();
+  return launch_rule(a, ProbSrc{a.p, a.q, a.u, a.k, a.V}, ws, st);
 }
 
 }  // namespace sd

@@ -203,6 +203,53 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const f
   return status_from(sd::launch_accept(a, workspace, static_cast<hipStream_t>(stream)));
 }
 
+// ------------------------------------------------------ accept (logits)
+size_t sd_spec_accept_logits_workspace_size(int B, int k, int V, int mode) {
+  if (B < 1 || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
+      (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
+    return 0;
+  return sd::accept_logits_workspace_bytes(B, k, V, mode);
+}
+
+int sd_spec_accept_logits(const void* target_logits, const void* draft_logits, const int32_t* draft,
+                          uint64_t seed, uint64_t offset, float temperature, int32_t* n_accepted,
+                          int32_t* tokens, int B, int k, int V, int dtype, int mode, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED) ||
+      (dtype != SD_F32 && dtype != SD_BF16))
+    return SD_ERR_INVALID_ARG;
+  if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (!target_logits || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
+  if (mode == SD_ACCEPT_SAMPLED && (!draft_logits || !isfinite(temperature) || !(temperature > 0.f)))
+    return SD_ERR_INVALID_ARG;
+  const size_t al = dtype == SD_F32 ? 4 : 2;
+  if (!aligned(target_logits, al) || (draft_logits && !aligned(draft_logits, al)) || !aligned(draft, 4) ||
+      !aligned(n_accepted, 4) || !aligned(tokens, 4))
+    return SD_ERR_INVALID_ARG;
+  const size_t need = sd::accept_logits_workspace_bytes(B, k, V, mode);
+  if (!workspace || workspace_bytes < need || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
+  sd::AcceptLogitsArgs la{};
+  la.rule.draft = draft;
+  la.rule.n_accepted = n_accepted;
+  la.rule.tokens = tokens;
+  la.rule.B = B;
+  la.rule.k = k;
+  la.rule.V = V;
+  la.rule.mode = mode;
+  la.target_logits = target_logits;
+  la.draft_logits = draft_logits;
+  la.scale_log2 = mode == SD_ACCEPT_SAMPLED ? 1.4426950408889634f / temperature : 0.f;
+  la.seed = seed;
+  la.offset = offset;
+  return status_from(sd::launch_accept_logits(la, dtype, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int sd_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B, int n, void* stream) {
+  if (!u || B < 1 || n < 1 || !aligned(u, 4)) return SD_ERR_INVALID_ARG;
+  if (n > (1 << 16) || (long long)B * n > 2147483647LL) return SD_ERR_UNSUPPORTED;
+  return status_from(sd::launch_philox_uniforms(seed, offset, u, B, n, static_cast<hipStream_t>(stream)));
+}
+
 // -------------------------------------------------------------- LM head
 size_t sd_lm_head_workspace_size(int R, int d, int V, int dtype) {
   if (R < 1 || d < 1 || V < 1 || R > 4096 || V > (1 << 24) || (dtype != SD_F32 && dtype != SD_BF16))

@@ -308,19 +308,14 @@ def _probs(z, tau):
     return (e / e.sum(axis=-1, keepdims=True)).astype(np.float32)
 
 
-def accept_inputs(w, mode, seed=None, batch=None):
-    """Target / draft probabilities, drafted ids and uniforms.
-
-    Returns a dict with p [B, k+1, V] float32, q [B, k, V] float32,
-    draft [B, k] int32 and u [B, k+1] float32 (multiples of 2^-24).
-    """
+def _accept_draws(w, mode, seed, batch):
+    """Target / draft logits (float64), temperature and drafted ids."""
     rs = streams(w.seed if seed is None else seed)
     B = w.batch if batch is None else batch
     k, V = w.block, w.vocab
     tau = w.temperature if mode == "sampled" else 1.0
     z = 3.0 * normal(rs["target_logits"], (B, k + 1, V)).astype(np.float64)
     zd = z[:, :k] + normal(rs["draft_noise"], (B, k, V)).astype(np.float64)
-    p = _probs(z, tau)
     q = _probs(zd, tau)
     if mode == "greedy":
         draft = np.argmax(q, axis=-1).astype(np.int32)
@@ -332,6 +327,18 @@ def accept_inputs(w, mode, seed=None, batch=None):
                 c = np.cumsum(q[b, i].astype(np.float64))
                 draft[b, i] = min(V - 1, int(np.searchsorted(c, du[b, i] * c[-1],
                                                              side="right")))
+    return z, zd, q, tau, draft
+
+
+def accept_inputs(w, mode, seed=None, batch=None):
+    """Target / draft probabilities, drafted ids and uniforms.
+
+    Returns a dict with p [B, k+1, V] float32, q [B, k, V] float32,
+    draft [B, k] int32 and u [B, k+1] float32 (multiples of 2^-24).
+    """
+    z, _, q, tau, draft = _accept_draws(w, mode, seed, batch)
+    B, k = draft.shape
+    p = _probs(z, tau)
     # one independent uniform stream per sequence
     base = w.seed if seed is None else seed
     ui = _STREAMS.index("accept_uniforms")
@@ -342,6 +349,17 @@ def accept_inputs(w, mode, seed=None, batch=None):
         u[b] = (g.integers(0, 1 << 24, size=k + 1).astype(np.float64)
                 * 2.0 ** -24).astype(np.float32)
     return {"p": p, "q": q, "draft": draft, "u": u, "temperature": tau}
+
+
+def accept_logits_inputs(w, mode, seed=None, batch=None):
+    """The same draws handed over as logits: target_logits [B, k+1, V] and
+    draft_logits [B, k, V] (float32), draft [B, k] int32, the temperature and
+    a key / offset for the device-side uniforms."""
+    z, zd, _, tau, draft = _accept_draws(w, mode, seed, batch)
+    base = w.seed if seed is None else seed
+    return {"target_logits": z.astype(np.float32), "draft_logits": zd.astype(np.float32),
+            "draft": draft, "temperature": tau,
+            "philox_seed": (0x5EED0000 + 7919 * base) & ((1 << 64) - 1), "philox_offset": 3}
 
 
 # --------------------------------------------------------- byte / flop counts

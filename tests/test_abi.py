@@ -181,3 +181,35 @@ def test_sample_validation_errors(lib):
     assert call(ws=None) == sd.SD_ERR_WORKSPACE
     assert call(wsb=lib.sd_sample_workspace_size(3, 100) - 1) == sd.SD_ERR_WORKSPACE
     assert lib.sd_sample_workspace_size(3, 100) >= 3 * 4
+
+
+def test_accept_logits_validation_errors(lib):
+    keep, (zt, zd, d, n, t, ws) = _fake(6)
+    f = lib.sd_spec_accept_logits
+
+    def call(zt=zt, zd=zd, d=d, n=n, t=t, tau=0.7, B=1, k=4, V=100, dt=0, mode=1, ws=ws, wsb=1 << 30):
+        return f(zt, zd, d, 1, 2, tau, n, t, B, k, V, dt, mode, ws, wsb, None)
+
+    assert call(zt=None) == sd.SD_ERR_INVALID_ARG
+    assert call(zd=None) == sd.SD_ERR_INVALID_ARG         # sampled needs draft logits
+    assert call(tau=0.0) == sd.SD_ERR_INVALID_ARG
+    assert call(tau=float("nan")) == sd.SD_ERR_INVALID_ARG
+    assert call(dt=3) == sd.SD_ERR_INVALID_ARG
+    assert call(mode=4) == sd.SD_ERR_INVALID_ARG
+    assert call(B=0) == sd.SD_ERR_INVALID_ARG
+    assert call(k=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=16) == sd.SD_ERR_WORKSPACE
+    # the sampled workspace adds the logits' row statistics to the rule's
+    greedy = lib.sd_spec_accept_logits_workspace_size(4, 8, 152064, 0)
+    sampled = lib.sd_spec_accept_logits_workspace_size(4, 8, 152064, 1)
+    assert sampled >= lib.sd_spec_accept_workspace_size(4, 8, 152064, 1) + 4 * 17 * 149 * 8
+    assert greedy == lib.sd_spec_accept_workspace_size(4, 8, 152064, 0)
+    assert lib.sd_spec_accept_logits_workspace_size(4, 17, 100, 1) == 0
+
+    g = lib.sd_philox_uniforms
+    assert g(1, 2, None, 1, 4, None) == sd.SD_ERR_INVALID_ARG
+    assert g(1, 2, n, 0, 4, None) == sd.SD_ERR_INVALID_ARG
+    assert g(1, 2, n, 1, 0, None) == sd.SD_ERR_INVALID_ARG
+    assert g(1, 2, n, 1, (1 << 16) + 1, None) == sd.SD_ERR_UNSUPPORTED

@@ -5,19 +5,21 @@
 One step is one pass of the whole hot path over one batch of synthetic
 input with every tensor already resident in HBM:
     sd_latent_compress (Eq. 3) -> sd_verify_attention -> sd_lm_head_probs
-    (the k+1 target rows) -> sd_spec_accept
+    (the k+1 target rows) -> sd_spec_accept -> sd_spec_accept_logits
 Default workload: "long-video" (batch 4, GQA 64/8 heads, head dim 128, KV
 length 65536, block k = 8; compression of 16384 tokens of width 8192 to 512
 latents over 64 heads; an LM head of width 8192 over a 152064-token
 vocabulary for the 36 target rows; sampled acceptance over that vocabulary
 at temperature 0.7).  The acceptance consumes synthetic p and q with
-realistic acceptance rates, not the head's output (its weights are random).
+realistic acceptance rates, not the head's output (its weights are random);
+the acceptance from logits runs on the logits of the same draws (temperature
+softmax and Philox uniforms on the device).
 
 Prints one JSON line.  `value` is the verify step's KV-read rate: bytes of
 K and V the step must read once, divided by the time of verification
 attention plus acceptance, in TB/s.  Per-kernel times come from HIP events
 on the stream the kernels run on.  `roofline` describes the dominant kernel
-(the longest per step); `rooflines` lists all four.  `traffic` is the HBM
+(the longest per step); `rooflines` lists all five.  `traffic` is the HBM
 bytes per launch measured with rocprofv3 counters (profiles/), or null when
 the kernel's sources changed since they were taken.  `cpu_baseline` times
 the plain CPU oracle on a bounded sample of the same workload and scales it
@@ -76,7 +78,18 @@ def accept_bytes(p, n):
     return total
 
 
-def cpu_baseline(w, comp, ver, acc, mode, lm):
+def accept_logits_bytes(w, n):
+    """Algorithmic bytes of one acceptance from float32 logits: every target
+    and draft row once (the softmax statistics), then the sampled row pass
+    over p_n and q_n (p_k alone after full acceptance)."""
+    k, V = w.block, w.vocab
+    total = 0
+    for nb in n:
+        total += (2 * k + 1) * V * 4 + (2 * V if nb < k else V) * 4
+    return total
+
+
+def cpu_baseline(w, comp, ver, acc, mode, lm, accl):
     """Time the oracle on a bounded sample and scale it to one whole step."""
     import numpy as np
     import oracle
@@ -114,6 +127,10 @@ def cpu_baseline(w, comp, ver, acc, mode, lm):
     t0 = time.perf_counter()
     oracle.spec_accept(acc["p"], acc["q"], acc["draft"], acc["u"], mode)
     ta = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.spec_accept_logits(accl["target_logits"], accl["draft_logits"], accl["draft"],
+                              accl["philox_seed"], accl["philox_offset"], accl["temperature"], mode)
+    tal = time.perf_counter() - t0
     # LM head: one row over the whole vocabulary (logits 8192 entries at a time)
     R = lm["hidden"].shape[0]
     t0 = time.perf_counter()
@@ -121,10 +138,12 @@ def cpu_baseline(w, comp, ver, acc, mode, lm):
                         for v in range(0, w.vocab, 8192)], axis=1)
     oracle.softmax_temperature(z, lm["temperature"])
     tl = (time.perf_counter() - t0) * R
-    return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "lm_head_s": tl, "threads": threads,
+    return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "lm_head_s": tl, "accept_logits_s": tal,
+            "threads": threads,
             "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
                       f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
-                      f"pairs, acceptance of all {w.batch} sequences, LM head 1 of {R} rows; "
+                      f"pairs, acceptance (from p, q and from logits) of all {w.batch} sequences, "
+                      f"LM head 1 of {R} rows; "
                       f"scaled linearly"}
 
 
@@ -178,6 +197,7 @@ def main():
     comp = synth.compress_inputs(w)
     ver = synth.verify_inputs(w)
     acc = synth.accept_inputs(w, mode)
+    accl = synth.accept_logits_inputs(w, mode)
     lm = synth.lm_inputs(w)
 
     lat_d, feats_d = to_dev(comp[0], dev), to_dev(comp[1], dev)
@@ -188,6 +208,9 @@ def main():
     qq_d = torch.from_numpy(acc["q"]).to(dev)
     dr_d = torch.from_numpy(acc["draft"]).to(dev)
     u_d = torch.from_numpy(acc["u"]).to(dev)
+    zt_d = torch.from_numpy(accl["target_logits"]).to(dev)
+    zd_d = torch.from_numpy(accl["draft_logits"]).to(dev)
+    drl_d = torch.from_numpy(accl["draft"]).to(dev)
     h_d, wt_d = to_dev(lm["hidden"], dev), to_dev(lm["weight"], dev)
     dt_code = sd.SD_BF16 if w.dtype == "bf16" else sd.SD_F32
     amode = sd.SD_ACCEPT_SAMPLED if mode == "sampled" else sd.SD_ACCEPT_GREEDY
@@ -210,6 +233,10 @@ def main():
                         dtype=torch.uint8, device=dev)
     n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
+    al_ws = torch.empty(sd.sd_spec_accept_logits_workspace_size(w.batch, w.block, w.vocab, amode),
+                        dtype=torch.uint8, device=dev)
+    nl_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
+    tl_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
     scale = 1.0 / math.sqrt(w.head_dim)
 
     def step(ev=None):
@@ -229,6 +256,11 @@ def main():
                           workspace=a_ws)
         if ev is not None:
             ev[4].record()
+        sd.sd_spec_accept_logits(zt_d, zd_d, drl_d, accl["philox_seed"], accl["philox_offset"],
+                                 accl["temperature"], amode, n_accepted=nl_out, tokens=tl_out,
+                                 workspace=al_ws)
+        if ev is not None:
+            ev[5].record()
 
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
@@ -239,7 +271,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -251,6 +283,7 @@ def main():
     ver_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
     lm_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
     acc_ms = np.array([e[3].elapsed_time(e[4]) for e in events])
+    accl_ms = np.array([e[4].elapsed_time(e[5]) for e in events])
 
     kv_bytes = synth.verify_kv_bytes(w, ver["kv_len"])
     flops = synth.compress_flops(w)
@@ -259,6 +292,8 @@ def main():
     a_bytes = accept_bytes(acc["p"], n_host)
     t_c, t_v, t_a = float(comp_ms.mean()), float(ver_ms.mean()), float(acc_ms.mean())
     t_l = float(lm_ms.mean())
+    t_al = float(accl_ms.mean())
+    al_bytes = accept_logits_bytes(w, nl_out.cpu().numpy())
     l_bytes = synth.lm_bytes(w, lm_rows)
     verify_step_ms = t_v + t_a
     value = kv_bytes / (verify_step_ms * 1e-3) / 1e12
@@ -278,6 +313,9 @@ def main():
         "lm_head": {"bound": "hbm", "achieved": l_bytes / (t_l * 1e-3) / 1e9,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
                     "algorithmic": l_bytes, "us": t_l * 1e3},
+        "spec_accept_logits": {"bound": "hbm", "achieved": al_bytes / (t_al * 1e-3) / 1e9,
+                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
+                               "algorithmic": al_bytes, "us": t_al * 1e3},
     }
     traffic = counter_traffic(w.name)
     for name_, r in rl.items():
@@ -316,6 +354,7 @@ def main():
         "latent_compress_us": t_c * 1e3,
         "lm_head_us": t_l * 1e3,
         "lm_head_tbps": l_bytes / (t_l * 1e-3) / 1e12,
+        "spec_accept_logits_us": t_al * 1e3,
         "latent_compress_tflops": rl["latent_compress"]["achieved"],
         "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
         "accepted_mean": float(n_host.mean()),
@@ -324,14 +363,14 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        cb = cpu_baseline(w, comp, ver, acc, 0 if mode == "greedy" else 1, lm)
+        cb = cpu_baseline(w, comp, ver, acc, 0 if mode == "greedy" else 1, lm, accl)
         cpu_step = cb["verify_s"] + cb["accept_s"]
         result["cpu_baseline"] = {
             "value": kv_bytes / cpu_step / 1e12, "unit": "TB/s", "cores": cb["threads"],
             "kind": "oracle", "sample": cb["sample"],
             "verify_step_s": cpu_step, "latent_compress_s": cb["compress_s"],
-            "lm_head_s": cb["lm_head_s"],
-            "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"],
+            "lm_head_s": cb["lm_head_s"], "accept_logits_s": cb["accept_logits_s"],
+            "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"] + cb["accept_logits_s"],
         }
     print(json.dumps(result), flush=True)
 

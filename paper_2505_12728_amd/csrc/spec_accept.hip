@@ -21,6 +21,15 @@
 //    exceeds T (64-wide wave prefix sums).  Greedy: argmax per row from the
 //    chunk maxima, then the longest matching prefix.
 // Every vocabulary access is a coalesced stream.
+//
+// From logits (the target's k + 1 and the draft's k rows per sequence), the
+// same two kernels read p and q on demand as a temperature softmax of the
+// logits, after a statistics pass, grid (4096-entry chunk, row), that writes
+// each chunk's (max, sum of 2^(z s - max)) with s = log2(e) / tau.  Each
+// work-group of the rule first merges its sequence's 2k + 1 rows of chunk
+// statistics into (M, 1 / L) in LDS.  The uniforms come from Philox-4x64-10
+// on the device.  Greedy mode skips the statistics and compares the target
+// logits directly.
 #include <math.h>
 
 #include "device_common.hpp"
@@ -32,6 +41,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 1024;     // vocabulary entries per chunk (<= 256 chunks for V <= 2^18)
+constexpr int kStatChunk = 4096;
+constexpr int kMaxStatParts = (1 << 18) / kStatChunk;   // statistics chunks of a row at most
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
   const uint32_t lo = __shfl_xor((uint32_t)v, m, 64);
@@ -78,6 +89,7 @@ struct ProbSrc {
   }
   __device__ __forceinline__ float greedy(int b, int i, int v) const { return target(b, i, v); }
   __device__ __forceinline__ float uniform(int b, int i) const { return u[(size_t)b * (k + 1) + i]; }
+  __device__ __forceinline__ void prepare(int, float2*) {}
 };
 
 // Philox-4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
@@ -108,26 +120,61 @@ __device__ __forceinline__ float load_logit(const float* z, size_t i) { return z
 __device__ __forceinline__ float load_logit(const uint16_t* z, size_t i) { return bf16_bits_to_float(z[i]); }
 
 // p and q from logits at temperature tau: p_i(v) = 2^(z_i(v) s - M_i) / L_i
-// with s = log2(e) / tau and the row statistics (M_i, 1 / L_i) in `rows`
-// (target rows b (k+1) + i, then draft rows B (k+1) + b k + i); u from
-// Philox.  Greedy compares the target logits themselves.
+// with s = log2(e) / tau; u from Philox.  Greedy compares the target logits
+// themselves.  `part` holds the chunk statistics (max, sum) of every row
+// (target rows b (k+1) + i, then draft rows B (k+1) + b k + i);
+// prepare(b) merges the 2k + 1 rows of sequence b into (M, 1 / L) in the
+// work-group's LDS array `rows` (target rows 0..k, then draft rows), which
+// target() and drafted() read.
 template <typename T>
 struct LogitSrc {
   const T* zt;
   const T* zd;
-  const float2* rows;
+  const float2* part;
+  int nparts;
+  float2* rows;
   float s;
   uint64_t seed, offset;
   int B, k, V;
   __device__ __forceinline__ float target(int b, int i, int v) const {
-    const size_t r = (size_t)b * (k + 1) + i;
-    const float2 st = rows[r];
-    return fast_exp2(load_logit(zt, r * V + v) * s - st.x) * st.y;
+    const float2 st = rows[i];
+    return fast_exp2(load_logit(zt, ((size_t)b * (k + 1) + i) * V + v) * s - st.x) * st.y;
   }
   __device__ __forceinline__ float drafted(int b, int i, int v) const {
-    const size_t r = (size_t)b * k + i;
-    const float2 st = rows[(size_t)B * (k + 1) + r];
-    return fast_exp2(load_logit(zd, r * V + v) * s - st.x) * st.y;
+    const float2 st = rows[k + 1 + i];
+    return fast_exp2(load_logit(zd, ((size_t)b * k + i) * V + v) * s - st.x) * st.y;
+  }
+  // Eight lanes per row, up to eight chunk partials each (nparts <= 64):
+  // all loads issue at once, then a max and a rescaled sum over the eight
+  // lanes.  The caller synchronises before reading `rows`.
+  __device__ void prepare(int b, float2* lds) {
+    rows = lds;
+    if (part == nullptr) return;               // greedy: no statistics
+    const int sub = threadIdx.x & 7;
+    for (int j0 = 0; j0 <= 2 * k; j0 += kThreads / 8) {
+      const int j = j0 + (int)(threadIdx.x >> 3);
+      const bool live = j <= 2 * k;
+      const size_t r = j <= k ? (size_t)b * (k + 1) + j : (size_t)B * (k + 1) + (size_t)b * k + (j - k - 1);
+      const float2* pr = part + r * nparts;
+      float2 v[kMaxStatParts / 8];
+#pragma unroll
+      for (int i = 0; i < kMaxStatParts / 8; ++i) {
+        const int c = sub + 8 * i;
+        v[i] = live && c < nparts ? pr[c] : make_float2(-INFINITY, 0.f);
+      }
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < kMaxStatParts / 8; ++i) m = fmaxf(m, v[i].x);
+#pragma unroll
+      for (int o = 4; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+      float l = 0.f;
+#pragma unroll
+      for (int i = 0; i < kMaxStatParts / 8; ++i)
+        if (v[i].x != -INFINITY) l += v[i].y * fast_exp2(v[i].x - m);
+#pragma unroll
+      for (int o = 4; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+      if (live && sub == 0) lds[j] = make_float2(m, 1.f / l);
+    }
   }
   __device__ __forceinline__ float greedy(int b, int i, int v) const {
     return load_logit(zt, ((size_t)b * (k + 1) + i) * V + v);
@@ -209,7 +256,10 @@ __global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, Src src,
   __shared__ uint64_t wsum[kWaves][2];
   __shared__ ArgMax sm[kWaves];
   __shared__ int s_n;
+  __shared__ float2 s_rows[33];
   const int chunk = blockIdx.x, b = blockIdx.y;
+  src.prepare(b, s_rows);
+  __syncthreads();
   const int k = a.k, V = a.V;
   const int v0 = chunk * kChunk, v1 = min(V, v0 + kChunk);
   if (a.mode == 0) {
@@ -278,7 +328,10 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
   __shared__ int s_tok;
   __shared__ int s_chunk;
   __shared__ uint64_t s_before;
+  __shared__ float2 s_rows[33];
   const int b = blockIdx.x;
+  src.prepare(b, s_rows);
+  __syncthreads();
   const int k = a.k, V = a.V;
   const int32_t* draft = a.draft + (size_t)b * k;
   const int c = threadIdx.x;                   // one thread per chunk (nchunks <= 256)
@@ -371,23 +424,53 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
   if (threadIdx.x == 0) a.n_accepted[b] = n;
 }
 
-// Row statistics of the logits at temperature: grid (vocabulary chunk, row)
+// Row statistics of the logits at temperature: grid (4096-entry chunk, row)
 // with rows b (k+1) + i of the target logits, then B (k+1) + b k + i of the
 // draft logits; each work-group writes (max, sum 2^(z s - max)) of its chunk.
+// Rows whose start is 16-byte aligned are read with 16-byte loads (4 fp32 or
+// 8 bf16 logits per load), others one logit at a time.
+
+__device__ __forceinline__ void load16(const float* p, float* x) {
+  const floatx4 v = *reinterpret_cast<const floatx4*>(p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = v[e];
+}
+__device__ __forceinline__ void load16(const uint16_t* p, float* x) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(v[e] << 16);
+    x[2 * e + 1] = __uint_as_float(v[e] & 0xffff0000u);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads) void logit_stats_chunks(const T* zt, const T* zd, float s, int B,
                                                                int k, int V, float2* part, int nchunks) {
+  constexpr int PER = 16 / sizeof(T);                    // logits per 16-byte load
+  constexpr int NX = kStatChunk / kThreads;              // logits per thread
   __shared__ float2 sm[kWaves];
   const int chunk = blockIdx.x, r = blockIdx.y;
   const int rt = B * (k + 1);
   const T* row = r < rt ? zt + (size_t)r * V : zd + (size_t)(r - rt) * V;
-  const int v0 = chunk * kChunk, v1 = min(V, v0 + kChunk);
-  float x[kChunk / kThreads];
+  const int v0 = chunk * kStatChunk, v1 = min(V, v0 + kStatChunk);
+  float x[NX];
+  if ((reinterpret_cast<uintptr_t>(row) & 15) == 0 && v1 - v0 == kStatChunk) {
+#pragma unroll
+    for (int j = 0; j < NX / PER; ++j) load16(row + v0 + (j * kThreads + threadIdx.x) * PER, x + j * PER);
+  } else {
+#pragma unroll
+    for (int j = 0; j < NX / PER; ++j)
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int v = v0 + (j * kThreads + threadIdx.x) * PER + e;
+        x[j * PER + e] = v < v1 ? load_logit(row, v) : -INFINITY;
+      }
+  }
   float m = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < kChunk / kThreads; ++j) {
-    const int v = v0 + j * kThreads + threadIdx.x;
-    x[j] = v < v1 ? load_logit(row, v) * s : -INFINITY;
+  for (int j = 0; j < NX; ++j) {
+    x[j] *= s;
     m = fmaxf(m, x[j]);
   }
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -400,11 +483,10 @@ __global__ __launch_bounds__(kThreads) void logit_stats_chunks(const T* zt, cons
   float l = 0.f;
   if (M != -INFINITY) {
 #pragma unroll
-    for (int j = 0; j < kChunk / kThreads; ++j) l += fast_exp2(x[j] - M);
+    for (int j = 0; j < NX; ++j) l += fast_exp2(x[j] - M);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
-  __syncthreads();
   if (lane == 0) sm[w].y = l;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -412,25 +494,6 @@ __global__ __launch_bounds__(kThreads) void logit_stats_chunks(const T* zt, cons
     for (int i = 0; i < kWaves; ++i) L += sm[i].y;
     part[(size_t)r * nchunks + chunk] = make_float2(M, L);
   }
-}
-
-// One wave per row: the chunk statistics merged into (M, 1 / L).
-__global__ __launch_bounds__(kThreads) void logit_stats_rows(const float2* part, float2* rows, int nrows,
-                                                             int nchunks) {
-  const int r = blockIdx.x * kWaves + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (r >= nrows) return;
-  float m = -INFINITY;
-  for (int c = lane; c < nchunks; c += 64) m = fmaxf(m, part[(size_t)r * nchunks + c].x);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-  float l = 0.f;
-  for (int c = lane; c < nchunks; c += 64) {
-    const float2 st = part[(size_t)r * nchunks + c];
-    if (st.x != -INFINITY) l += st.y * fast_exp2(st.x - m);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
-  if (lane == 0) rows[r] = make_float2(m, 1.f / l);
 }
 
 __global__ __launch_bounds__(kThreads) void philox_uniforms_kernel(uint64_t seed, uint64_t offset, float* u,
@@ -452,24 +515,19 @@ hipError_t launch_rule(const AcceptArgs& a, const Src& src, void* ws, hipStream_
 template <typename T>
 hipError_t launch_logits(const AcceptLogitsArgs& la, void* ws, hipStream_t st) {
   const AcceptArgs& a = la.rule;
-  const int nchunks = (a.V + kChunk - 1) / kChunk;
+  const int nchunks = (a.V + kStatChunk - 1) / kStatChunk;
   const int nrows = a.B * (2 * a.k + 1);
   LogitSrc<T> src{static_cast<const T*>(la.target_logits), static_cast<const T*>(la.draft_logits), nullptr,
-                  la.scale_log2, la.seed, la.offset, a.B, a.k, a.V};
+                  nchunks, nullptr, la.scale_log2, la.seed, la.offset, a.B, a.k, a.V};
   unsigned char* base = static_cast<unsigned char*>(ws);
   if (a.mode != 0) {
     float2* part = reinterpret_cast<float2*>(base);
-    float2* rows = part + (size_t)nrows * nchunks;
     hipLaunchKernelGGL((logit_stats_chunks<T>), dim3(nchunks, nrows), dim3(kThreads), 0, st, src.zt, src.zd,
                        la.scale_log2, a.B, a.k, a.V, part, nchunks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(logit_stats_rows, dim3((nrows + kWaves - 1) / kWaves), dim3(kThreads), 0, st, part, rows,
-                       nrows, nchunks);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    src.rows = rows;
-    base += ((size_t)nrows * (nchunks + 1) * sizeof(float2) + 255) / 256 * 256;
+    src.part = part;
+    base += ((size_t)nrows * nchunks * sizeof(float2) + 255) / 256 * 256;
   }
   return launch_rule(a, src, base, st);
 }
@@ -477,9 +535,9 @@ hipError_t launch_logits(const AcceptLogitsArgs& la, void* ws, hipStream_t st) {
 }  // namespace
 
 size_t accept_logits_workspace_bytes(int B, int k, int V, int mode) {
-  const int nchunks = (V + kChunk - 1) / kChunk;
+  const int nchunks = (V + kStatChunk - 1) / kStatChunk;
   size_t stats = 0;
-  if (mode != 0) stats = ((size_t)B * (2 * k + 1) * (nchunks + 1) * sizeof(float2) + 255) / 256 * 256;
+  if (mode != 0) stats = ((size_t)B * (2 * k + 1) * nchunks * sizeof(float2) + 255) / 256 * 256;
   return stats + accept_workspace_bytes(B, k, V, mode);
 }
 

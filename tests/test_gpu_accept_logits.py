@@ -123,9 +123,11 @@ def test_accept_logits_many_streams_bf16():
                       max_borderline=1)
 
 
-@pytest.mark.parametrize("B,k,V,tau", [(1, 1, 1, 1.0), (3, 2, 7, 0.05), (2, 16, 1025, 20.0),
-                                       (5, 5, 4097, 0.7), (1, 8, 262144, 1.0)])
-def test_accept_logits_edge_shapes(B, k, V, tau):
+@pytest.mark.parametrize("B,k,V,tau,dtype", [(1, 1, 1, 1.0, "f32"), (3, 2, 7, 0.05, "f32"),
+                                             (2, 16, 1025, 20.0, "f32"), (5, 5, 4097, 0.7, "f32"),
+                                             (1, 8, 262144, 1.0, "f32"), (2, 3, 12288, 0.8, "bf16"),
+                                             (3, 4, 8195, 1.5, "bf16")])
+def test_accept_logits_edge_shapes(B, k, V, tau, dtype):
     rng = np.random.default_rng(B * 1000 + V)
     zt = (rng.normal(size=(B, k + 1, V)) * 3).astype(np.float32)
     zd = (zt[:, :k] + rng.normal(size=(B, k, V))).astype(np.float32)
@@ -133,7 +135,7 @@ def test_accept_logits_edge_shapes(B, k, V, tau):
     draft[0, 0] = int(np.argmax(zt[0, 0]))               # a likely acceptance
     if B > 1:
         draft[1, 0] = V + 3                              # an id outside the vocabulary: rejected
-    check_sampled(zt, zd, draft, 5 + B, V, tau)
+    check_sampled(zt, zd, draft, 5 + B, V, tau, dtype)
 
 
 def test_accept_logits_first_token_law():

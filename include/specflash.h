@@ -98,6 +98,11 @@ int sd_version(void);
  * For SD_BF16 the value aggregation runs on float16 matrix cores, so
  * |feats| must stay below 65504 (larger magnitudes are a precondition
  * violation).
+ * When the tokens are split across work-groups, the workspace holds one
+ * partial result per split; for SD_BF16 the split count follows the
+ * compute units of the current device, so query
+ * sd_latent_compress_workspace_size with the device the call will run on
+ * current (a smaller workspace is rejected with SD_ERR_WORKSPACE).
  * ---------------------------------------------------------------------- */
 size_t sd_latent_compress_workspace_size(int B, int N, int C, int d,
                                          int num_heads, int dtype);

@@ -81,7 +81,8 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // The loop is software-pipelined across tiles (scores of the next tile under
 // the exponentials of the current one) and split into groups whose LDS
 // reads are issued one group ahead.  The running maximum is raised (O, l
-// rescaled) only when a row's scores exceed it by 2^8, and the token mask
+// rescaled) only when a row's scores exceed it by 2^8, which each lane
+// checks on its own scores against a per-row threshold, and the token mask
 // is applied only on the tail tile.  Tile reads and the in-place conversion
 // are inline asm, and each step has one counted wait and one fence-free
 // barrier.
@@ -248,6 +249,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       }
     }
   };
+  // Steady-state check of a tile: each lane compares the 16 scores it holds
+  // of each row block with the row's threshold thr = (m + kRescale) / sl2 in
+  // score units (+inf for sl2 = 0), without the cross-lane maxima; only when
+  // some lane exceeds it does the step take the exact maxima and raise m.
+  float thr[2];
+  auto set_thresholds = [&]() {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) thr[rb] = sl2 > 0.f ? (m[rb] + kRescale) / sl2 : INFINITY;
+  };
+  auto tile_exceeds = [&](const floatx4 (&s)[4][2]) {
+    bool hit = false;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      float ext = s[0][rb][0];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ext = fmaxf(ext, s[kb][rb][i]);
+      hit = hit || ext > thr[rb];
+    }
+    return hit;
+  };
   // tokens at or past the end of the split get score -inf (last tile only)
   auto mask_tail = [&](floatx4 (&s)[4][2], int t0) {
 #pragma unroll
@@ -303,9 +326,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   //     accumulated over dc (8 independent ops per group) | exponentials of
   //     tile it (one quarter of them per group for DH = 128)
   //   PV groups (4 value blocks of one half each): P V of tile it | in-place
-  //     conversion of tile it+2 (first half), row maxima of tile it+1
-  //     (second half)
-  // and raises the maxima (rare rescale) for the next step, while tile it+3
+  //     conversion of tile it+2 (first half), the lane-local threshold check
+  //     of tile it+1 (second half)
+  // and, when some lane's scores passed its threshold, takes the exact row
+  // maxima and raises them (rare rescale) for the next step, while tile it+3
   // is in flight.  Every step issues one tile (re-reading the last past the
   // end) and converts one buffer (past the end one that is never read
   // again), so the wait counts are the same at every step and the groups
@@ -340,6 +364,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     float tmax[2];
     tile_max(scur, tmax);
     raise_max(tmax);
+    set_thresholds();
   }
 
   // LDS reads of group g into the alternating register sets xr / vr (and
@@ -400,7 +425,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     u32x4 cv[CVT_PER_THREAD];
     floatx4 snext[4][2];
     f16x8 pf[2][2];
-    float tmax[2];
+    bool exceed = false;
     reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
     issue(min(it + 3, last), ring[(it + 3) % NBUF]);
     static_for<0, NG>([&](auto gtag) {
@@ -458,13 +483,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
             for (int e = 0; e < 4; ++e) cv[i][e] = bf16x2_to_f16x2(cv[i][e]);
         } else if constexpr (pb == NPVH - 1) {
-          tile_max(snext, tmax);
+          exceed = tile_exceeds(snext);
         }
         SD_INTERLEAVE(8 + (pb == NPVH - 1 ? 2 : 0), 3, g + 1)
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-    raise_max(tmax);
+    if (__ballot(exceed) != 0ull) {            // rare: exact maxima, raise, new thresholds
+      float tmax[2];
+      tile_max(snext, tmax);
+      raise_max(tmax);
+      set_thresholds();
+    }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -593,29 +623,51 @@ __global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int 
   }
 }
 
-// Combine token splits: grid (latent block of 64, sequence x head).
+// Combine token splits: one thread per (sequence x head, latent, 4
+// channels).  Up to 16 splits are loaded at once; a running maximum
+// rescales the sums between rounds as in the online softmax.
+constexpr int kMergeRound = 16;
 __global__ __launch_bounds__(256) void compress_merge(CompressArgs a, int dh, int nsplit) {
-  const int bh = blockIdx.y;
-  const int b = bh / a.H, h = bh % a.H;
-  const int r0 = blockIdx.x * 64;
   const int d4n = dh / 4;
-  const int nr = min(64, a.C - r0);
-  for (int i = threadIdx.x; i < nr * d4n; i += blockDim.x) {
-    const int r = r0 + i / d4n, d4 = i % d4n;
-    float mx = -INFINITY;
-    for (int s = 0; s < nsplit; ++s)
-      mx = fmaxf(mx, a.part_lse[((size_t)bh * nsplit + s) * a.C + r]);
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const size_t pr = ((size_t)bh * nsplit + s) * a.C + r;
-      const float wgt = exp2f(a.part_lse[pr] - mx);
-      wsum += wgt;
-      acc += wgt * *reinterpret_cast<const floatx4*>(a.part_o + pr * dh + d4 * 4);
+  const long long item = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long rows = (long long)a.B * a.H * a.C;
+  if (item >= rows * d4n) return;
+  const long long row = item / d4n;
+  const int d4 = (int)(item - row * d4n);
+  const int bh = (int)(row / a.C), r = (int)(row - (long long)bh * a.C);
+  const int b = bh / a.H, h = bh - b * a.H;
+  const float* lse = a.part_lse + (size_t)bh * nsplit * a.C + r;
+  const float* po = a.part_o + ((size_t)bh * nsplit * a.C + r) * dh + d4 * 4;
+  const size_t ostride = (size_t)a.C * dh;     // elements between splits
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  float mx = -INFINITY, wsum = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kMergeRound) {
+    float l[kMergeRound];
+    floatx4 v[kMergeRound];
+#pragma unroll
+    for (int i = 0; i < kMergeRound; ++i) {
+      const int s = s0 + i;
+      l[i] = s < nsplit ? lse[(size_t)s * a.C] : -INFINITY;
+      v[i] = s < nsplit ? *reinterpret_cast<const floatx4*>(po + s * ostride) : floatx4{0.f, 0.f, 0.f, 0.f};
     }
-    *reinterpret_cast<floatx4*>(a.out + ((size_t)b * a.C + r) * a.d + h * dh + d4 * 4) =
-        acc * (1.f / wsum);
+    float cm = l[0];
+#pragma unroll
+    for (int i = 1; i < kMergeRound; ++i) cm = fmaxf(cm, l[i]);
+    const float nm = fmaxf(mx, cm);
+    if (nm == -INFINITY) continue;
+    const float keep = mx == -INFINITY ? 0.f : exp2f(mx - nm);
+    acc = acc * keep;
+    wsum *= keep;
+#pragma unroll
+    for (int i = 0; i < kMergeRound; ++i) {
+      const float wgt = l[i] == -INFINITY ? 0.f : exp2f(l[i] - nm);
+      wsum += wgt;
+      acc += wgt * v[i];
+    }
+    mx = nm;
   }
+  *reinterpret_cast<floatx4*>(a.out + ((size_t)b * a.C + r) * a.d + h * dh + d4 * 4) =
+      acc * (wsum > 0.f ? 1.f / wsum : 0.f);
 }
 
 template <int NW, int DH>
@@ -639,7 +691,7 @@ hipError_t dispatch_nw(const CompressArgs& a, const CompressPlan& p, hipStream_t
 
 }  // namespace
 
-CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype) {
+CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus) {
   CompressPlan p{};
   p.dh = d / H;
   const long long n_bh = (long long)B * H;
@@ -650,17 +702,19 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype) {
     const long long cap = (65536 - 4LL * kF32Rows * p.dh - 16 * kF32Rows) / (8 * kF32Rows);
     p.tokens_per_split = (int)std::max(64LL, std::min(2048LL, cap / 64 * 64));
   } else {
-    // 32 latents per wave; eight-wave groups (F_V tiles shared by 256
-    // latents) when that still gives a full grid without token splits
-    int waves = C <= 32 ? 1 : (C <= 64 ? 2 : 4);
-    if (C > 128 && (long long)n_bh * ((C + 255) / 256) >= 256) waves = 8;
+    // 32 latents per wave; eight-wave groups (each F_V tile copied and
+    // converted once for 256 latents) whenever there are more than 128
+    int waves = C <= 32 ? 1 : (C <= 64 ? 2 : (C <= 128 ? 4 : 8));
     p.lat_tile = waves * 32;
     p.lat_tiles = (C + p.lat_tile - 1) / p.lat_tile;
-    // split the tokens until about 512 work-groups exist, keeping >= 256 tokens each
+    // split the tokens so that the grid fills the device in one round:
+    // two work-groups per compute unit (one of eight waves), keeping at
+    // least 128 tokens per split
     const long long groups = n_bh * p.lat_tiles;
-    long long nsplit = std::max(1LL, (512 + groups - 1) / groups);
+    const long long resident = (long long)std::max(cus, 1) * (waves == 8 ? 1 : 2);
+    long long nsplit = std::max(1LL, resident / groups);
     long long tps = (N + nsplit - 1) / nsplit;
-    tps = std::max(256LL, (tps + kTok - 1) / kTok * kTok);
+    tps = std::max(128LL, (tps + kTok - 1) / kTok * kTok);
     p.tokens_per_split = (int)tps;
   }
   p.nsplit = std::max(1, (N + p.tokens_per_split - 1) / p.tokens_per_split);
@@ -682,7 +736,8 @@ hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dty
     e = p.dh == 128 ? dispatch_nw<128>(a, p, st) : dispatch_nw<64>(a, p, st);
   }
   if (e != hipSuccess || p.nsplit == 1) return e;
-  hipLaunchKernelGGL(compress_merge, dim3((a.C + 63) / 64, a.B * a.H), dim3(256), 0, st, a, p.dh,
+  const long long items = (long long)a.B * a.H * a.C * (p.dh / 4);
+  hipLaunchKernelGGL(compress_merge, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a, p.dh,
                      p.nsplit);
   return hipGetLastError();
 }

@@ -58,7 +58,7 @@ struct CompressPlan {
   size_t workspace_bytes;
 };
 
-CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype);
+CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus);
 
 struct CompressArgs {
   const void* latents;

@@ -62,11 +62,25 @@ const char* sd_status_string(int status) {
 
 int sd_version(void) { return (1 << 16) | 0; }
 
+// Compute units of the current device (cached per device; 256 when no
+// device can be queried, e.g. for sizing on a host without a GPU).
+static int device_cus() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    return 256;
+  if (dev < 64) cached[dev] = n;
+  return n;
+}
+
 // ------------------------------------------------------------- compress
 size_t sd_latent_compress_workspace_size(int B, int N, int C, int d, int num_heads, int dtype) {
   int st;
   if (!compress_shape_ok(B, N, C, d, num_heads, dtype, &st)) return 0;
-  return sd::plan_compress(B, N, C, d, num_heads, dtype).workspace_bytes;
+  return sd::plan_compress(B, N, C, d, num_heads, dtype, device_cus()).workspace_bytes;
 }
 
 int sd_latent_compress(const void* latents, const void* feats, float* out, int B, int N, int C,
@@ -76,7 +90,7 @@ int sd_latent_compress(const void* latents, const void* feats, float* out, int B
   if (!compress_shape_ok(B, N, C, d, num_heads, dtype, &st)) return st;
   if (!latents || !feats || !out || !isfinite(scale)) return SD_ERR_INVALID_ARG;
   if (!aligned(latents, 16) || !aligned(feats, 16) || !aligned(out, 16)) return SD_ERR_INVALID_ARG;
-  const sd::CompressPlan plan = sd::plan_compress(B, N, C, d, num_heads, dtype);
+  const sd::CompressPlan plan = sd::plan_compress(B, N, C, d, num_heads, dtype, device_cus());
   if (plan.workspace_bytes > 0 && (!workspace || workspace_bytes < plan.workspace_bytes ||
                                    !aligned(workspace, 16)))
     return SD_ERR_WORKSPACE;
@@ -99,20 +113,6 @@ int sd_latent_compress(const void* latents, const void* feats, float* out, int B
 }
 
 // --------------------------------------------------------------- verify
-// Compute units of the current device (cached per device; 256 when no
-// device can be queried, e.g. for sizing on a host without a GPU).
-static int device_cus() {
-  static int cached[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
-  if (dev < 64 && cached[dev] > 0) return cached[dev];
-  int n = 0;
-  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-    return 256;
-  if (dev < 64) cached[dev] = n;
-  return n;
-}
-
 size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype) {
   int st;
   if (!verify_shape_ok(B, k, Hq, Hkv, D, dtype, &st) || capacity < 1) return 0;

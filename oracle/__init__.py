@@ -22,6 +22,11 @@ reader can check it against the paper by eye:
 * ``spec_accept_logits`` / ``philox_uniforms`` -- acceptance from logits: the
   temperature softmax in front of the rule and counter-based uniforms
   (Philox-4x64-10, Salmon et al., SC'11).
+* ``semi_ar_layer`` (with ``rms_norm``, ``rope``, ``linear``, ``swiglu``) --
+  one step of the draft's semi-autoregressive layer over its cached context:
+  the fully connected fusion of feature and embedding, then one pre-norm
+  decoder layer whose placeholder rows give the next K draft states
+  (Sec. 3.1, Sec. 3.3, Algorithm 1, Sec. 4.4).
 
 Readings of points the paper leaves open are stated in each module.  No
 function here is "parity unpinned": every one is checked in
@@ -33,6 +38,7 @@ from .compress import latent_compress, softmax_rows
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
+from .draft_layer import rms_norm, rope, linear, silu, swiglu, semi_ar_layer
 from .accept import (
     spec_accept,
     spec_accept_one,
@@ -64,4 +70,13 @@ __all__ = [
     "softmax_temperature",
     "lm_head_probs",
     "sample_tokens",
+    "philox4x64",
+    "philox_uniforms",
+    "spec_accept_logits",
+    "rms_norm",
+    "rope",
+    "linear",
+    "silu",
+    "swiglu",
+    "semi_ar_layer",
 ]

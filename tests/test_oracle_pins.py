@@ -784,3 +784,156 @@ def test_accept_logits_first_token_follows_target_law():
     chi2 = float(np.sum((counts - expected) ** 2 / expected))
     # 5 degrees of freedom: P(chi2 > 20.5) ~ 0.001
     assert chi2 < 20.5, (counts, expected)
+
+
+# ---------------------------------------------------------------- draft layer
+def test_rms_norm_closed_forms():
+    w = np.array([0.5, -2.0, 3.0, 1.0])
+    # a constant row c * 1 has rms |c|: the output is sign(c) * w (eps = 0)
+    assert np.allclose(oracle.rms_norm(np.full(4, -7.0), w, 0.0), -w, rtol=0, atol=1e-15)
+    # [3, 4] has mean square 12.5
+    r = math.sqrt(12.5)
+    assert np.allclose(oracle.rms_norm(np.array([3.0, 4.0]), np.ones(2), 0.0), [3 / r, 4 / r], atol=1e-15)
+    # eps enters under the root: [1, 1] with eps = 3 is divided by 2
+    assert np.allclose(oracle.rms_norm(np.array([1.0, 1.0]), np.ones(2), 3.0), [0.5, 0.5], atol=1e-15)
+    # invariant under positive scaling (eps = 0), rows independent
+    x = np.random.default_rng(0).normal(size=(3, 8))
+    assert np.allclose(oracle.rms_norm(x * 9.5, np.ones(8), 0.0), oracle.rms_norm(x, np.ones(8), 0.0))
+
+
+def test_rope_closed_forms_and_relative_position():
+    # D = 2: (1, 0) at position p becomes (cos p, sin p)
+    for p in [0, 1, 5, 37]:
+        assert np.allclose(oracle.rope(np.array([[1.0, 0.0]]), np.array([p]), 10000.0),
+                           [[math.cos(p), math.sin(p)]], atol=1e-14)
+    # D = 4, theta = 10000: pair 1 turns at 10000^(-1/2) = 0.01 rad per position
+    y = oracle.rope(np.array([[0.0, 1.0, 0.0, 0.0]]), np.array([50]), 10000.0)
+    assert np.allclose(y, [[0.0, math.cos(0.5), 0.0, math.sin(0.5)]], atol=1e-14)
+    rng = np.random.default_rng(1)
+    x = rng.normal(size=(6, 8))
+    # position 0 is the identity; every pair keeps its length
+    assert np.allclose(oracle.rope(x, np.zeros(6), 500.0), x, atol=0)
+    y = oracle.rope(x, np.arange(6) * 3, 500.0)
+    assert np.allclose(y[:, :4] ** 2 + y[:, 4:] ** 2, x[:, :4] ** 2 + x[:, 4:] ** 2)
+    # scores depend on positions only through their difference
+    q, k = rng.normal(size=8), rng.normal(size=8)
+    s = lambda m, n: float(oracle.rope(q[None], np.array([m]), 500.0)[0] @ oracle.rope(k[None], np.array([n]), 500.0)[0])
+    assert abs(s(9, 4) - s(15, 10)) < 1e-12 and abs(s(3, 3) - float(q @ k)) < 1e-12
+    # a heads axis: [n, H, D] with one position per row rotates every head alike
+    xh = rng.normal(size=(4, 3, 8))
+    yh = oracle.rope(xh, np.arange(4), 500.0)
+    for h in range(3):
+        assert np.allclose(yh[:, h], oracle.rope(xh[:, h], np.arange(4), 500.0))
+
+
+def test_linear_and_swiglu_closed_forms():
+    rng = np.random.default_rng(2)
+    x = rng.normal(size=(3, 5))
+    assert np.array_equal(oracle.linear(x, np.eye(5)), x)
+    assert np.allclose(oracle.linear(x, np.eye(5)[[4, 0]], bias=[1.0, 2.0], residual=np.ones((3, 2))),
+                       np.stack([x[:, 4] + 2.0, x[:, 0] + 3.0], axis=1))
+    # silu(0) = 0; silu(x) - silu(-x) = x; sigmoid(log 3) = 3/4
+    assert oracle.silu(0.0) == 0.0
+    z = rng.normal(size=7) * 4
+    assert np.allclose(oracle.silu(z) - oracle.silu(-z), z)
+    assert abs(float(oracle.swiglu(np.array([math.log(3.0), 2.0]))[0]) - 0.75 * math.log(3.0) * 2.0) < 1e-15
+
+
+def _draft_case(seed, B=2, r=3, d=8, hq=2, hkv=1, I=6, ctx=(4, 2), Lmax=10):
+    rng = np.random.default_rng(seed)
+    D = d // hq
+    W = {"fc_w": rng.normal(size=(d, 2 * d)) / 4, "fc_b": rng.normal(size=d),
+         "ln1": 1 + rng.normal(size=d) / 5, "wqkv": rng.normal(size=((hq + 2 * hkv) * D, d)) / 3,
+         "wo": rng.normal(size=(d, hq * D)) / 3, "ln2": 1 + rng.normal(size=d) / 5,
+         "wgu": rng.normal(size=(2 * I, d)) / 3, "wdown": rng.normal(size=(d, I)) / 3}
+    u = rng.normal(size=(B, r, 2 * d))
+    kc = rng.normal(size=(B, Lmax, hkv, D))
+    vc = rng.normal(size=(B, Lmax, hkv, D))
+    return u, W, kc, vc, np.array(ctx[:B])
+
+
+def test_draft_layer_without_branches_is_the_fc_map():
+    # Wo = Wdown = 0: the output is FC(u) and the caches gain RoPE(k), v of
+    # the normed rows at positions pos .. pos + r - 1, nothing else changes
+    u, W, kc, vc, pos = _draft_case(3)
+    W0 = dict(W, wo=np.zeros_like(W["wo"]), wdown=np.zeros_like(W["wdown"]))
+    out, kc2, vc2 = oracle.semi_ar_layer(u, W0, kc, vc, pos, 2, 1, 1e-6, 10000.0)
+    x0 = u @ W["fc_w"].T + W["fc_b"]
+    assert np.allclose(out, x0)
+    h = x0 / np.sqrt(np.mean(x0 ** 2, axis=-1, keepdims=True) + 1e-6) * W["ln1"]
+    kv = h @ W["wqkv"].T                                   # [B, r, 4 * D], D = 4
+    for b in range(2):
+        p = pos[b]
+        assert np.allclose(vc2[b, p:p + 3, 0], kv[b, :, 12:16])
+        assert np.allclose(kc2[b, p:p + 3, 0], oracle.rope(kv[b, :, 8:12], p + np.arange(3), 10000.0))
+        assert np.array_equal(kc2[b, :p], kc[b, :p]) and np.array_equal(vc2[b, p + 3:], vc[b, p + 3:])
+
+
+def test_draft_layer_is_causal_inside_the_new_rows():
+    # changing row j's input leaves rows < j and other sequences unchanged
+    u, W, kc, vc, pos = _draft_case(4)
+    ref, _, _ = oracle.semi_ar_layer(u, W, kc, vc, pos, 2, 1, 1e-6, 10000.0)
+    u2 = u.copy()
+    u2[0, 1] += 1.0
+    out, _, _ = oracle.semi_ar_layer(u2, W, kc, vc, pos, 2, 1, 1e-6, 10000.0)
+    assert np.allclose(out[0, 0], ref[0, 0]) and np.allclose(out[1], ref[1])
+    assert not np.allclose(out[0, 1], ref[0, 1]) and not np.allclose(out[0, 2], ref[0, 2])
+    # context entries at or past pos + r are never read
+    kc3, vc3 = kc.copy(), vc.copy()
+    kc3[0, pos[0] + 3:] = 1e6
+    vc3[0, pos[0] + 3:] = -1e6
+    out3, _, _ = oracle.semi_ar_layer(u, W, kc3, vc3, pos, 2, 1, 1e-6, 10000.0)
+    assert np.allclose(out3, ref)
+
+
+def test_draft_layer_gqa_equals_repeated_heads():
+    # Hkv = 1 shared by 2 query heads equals Hkv = 2 with the KV head repeated
+    u, W, kc, vc, pos = _draft_case(5)
+    ref, _, _ = oracle.semi_ar_layer(u, W, kc, vc, pos, 2, 1, 1e-6, 10000.0)
+    D = 4
+    wq, wk, wv = W["wqkv"][:2 * D], W["wqkv"][2 * D:3 * D], W["wqkv"][3 * D:]
+    W2 = dict(W, wqkv=np.concatenate([wq, wk, wk, wv, wv]))
+    out, _, _ = oracle.semi_ar_layer(u, W2, np.repeat(kc, 2, axis=2), np.repeat(vc, 2, axis=2), pos, 2, 2,
+                                     1e-6, 10000.0)
+    assert np.allclose(out, ref)
+
+
+def test_draft_layer_brute_force():
+    # pure-Python loops on a tiny case: d = 4, 2 heads of D = 2, I = 3
+    u, W, kc, vc, pos = _draft_case(6, B=1, r=2, d=4, hq=2, hkv=2, I=3, ctx=(3,), Lmax=6)
+    out, _, _ = oracle.semi_ar_layer(u, W, kc, vc, pos, 2, 2, 1e-5, 100.0)
+    d, D, I, eps, theta = 4, 2, 3, 1e-5, 100.0
+    L = W["wqkv"].tolist()
+
+    def mv(m, x):
+        return [sum(m[i][j] * x[j] for j in range(len(x))) for i in range(len(m))]
+
+    def norm(x, w):
+        r = math.sqrt(sum(v * v for v in x) / len(x) + eps)
+        return [x[i] / r * w[i] for i in range(len(x))]
+
+    def rot(x, p):                             # D = 2: one pair, frequency 1
+        return [x[0] * math.cos(p) - x[1] * math.sin(p), x[1] * math.cos(p) + x[0] * math.sin(p)]
+
+    keys = {t: [list(kc[0, t, h]) for h in range(2)] for t in range(pos[0])}
+    vals = {t: [list(vc[0, t, h]) for h in range(2)] for t in range(pos[0])}
+    xs = []
+    for j in range(2):
+        x0 = [v + b for v, b in zip(mv(W["fc_w"].tolist(), u[0, j].tolist()), W["fc_b"].tolist())]
+        qkv = mv(L, norm(x0, W["ln1"].tolist()))
+        p = pos[0] + j
+        keys[p] = [rot(qkv[4 + 2 * h:6 + 2 * h], p) for h in range(2)]
+        vals[p] = [qkv[8 + 2 * h:10 + 2 * h] for h in range(2)]
+        xs.append((x0, [rot(qkv[2 * h:2 * h + 2], p) for h in range(2)], p))
+    for j, (x0, qs, p) in enumerate(xs):
+        att = []
+        for h in range(2):
+            s = [(qs[h][0] * keys[t][h][0] + qs[h][1] * keys[t][h][1]) / math.sqrt(D) for t in range(p + 1)]
+            m = max(s)
+            e = [math.exp(v - m) for v in s]
+            att += [sum(e[t] * vals[t][h][c] for t in range(p + 1)) / sum(e) for c in range(2)]
+        x1 = [a + b for a, b in zip(x0, mv(W["wo"].tolist(), att))]
+        gu = mv(W["wgu"].tolist(), norm(x1, W["ln2"].tolist()))
+        act = [gu[i] / (1 + math.exp(-gu[i])) * gu[I + i] for i in range(I)]
+        x2 = [a + b for a, b in zip(x1, mv(W["wdown"].tolist(), act))]
+        assert np.allclose(out[0, j], x2, rtol=1e-12, atol=1e-12), j

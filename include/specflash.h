@@ -295,6 +295,81 @@ size_t sd_sample_workspace_size(int R, int V);
 int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R, int V,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Skinny projection y = x W^T (+ bias) (+ residual) for few input rows, the
+ * shape of every projection of a drafting step (Sec. 3.1: the fully
+ * connected fusion of feature and embedding; Sec. 3.3: the draft layer).
+ *
+ *   x         [R, K] bf16     input rows (row-major)
+ *   w         [N, K] bf16     weight (row n holds output column n)
+ *   bias      [N]    float32  or NULL
+ *   residual  [R, N] float32  or NULL (may alias y)
+ *   y         [R, N] float32  out
+ *   workspace sd_linear_workspace_size(R, K, N) bytes (fp32 partial sums of
+ *             the reduction splits; the split count follows the compute units
+ *             of the current device, so size it on the device of the call)
+ * Accumulation in fp32 on bf16 matrix cores; the weight is read once per
+ * pass of up to 128 input rows.
+ * Requirements: R >= 1; K a multiple of 256 (at most 2^20); N >= 1; R * N
+ * <= 2^31; x and w 16-byte aligned.  Errors: SD_ERR_INVALID_ARG (NULL or
+ * misaligned pointers), SD_ERR_UNSUPPORTED (shape outside the
+ * requirements), SD_ERR_WORKSPACE (missing or short workspace).
+ * ---------------------------------------------------------------------- */
+size_t sd_linear_workspace_size(int R, int K, int N);
+
+int sd_linear(const void* x, const void* w, const float* bias, const float* residual, float* y,
+              int R, int K, int N, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * One step of the draft's semi-autoregressive layer over its cached context
+ * (Sec. 3.1 and Algorithm 1: textual input FC(concat(F_T, E)); Sec. 3.3:
+ * one pass of the layer gives the states of the K placeholder positions;
+ * Sec. 4.4: one layer, 32 heads).  For the r new rows of each sequence b
+ * (the last K of them placeholders), at positions pos[b] .. pos[b] + r - 1:
+ *
+ *   x0  = u W_fc^T + b_fc
+ *   q, k, v = RoPE(RMSNorm(x0; ln1) Wqkv^T)     (k, v written to the cache)
+ *   x1  = x0 + Attn(q; cache positions 0 .. pos[b] + r - 1) Wo^T
+ *   out = x1 + (silu(h Wg^T) * (h Wu^T)) Wdown^T,  h = RMSNorm(x1; ln2)
+ *
+ * RMSNorm(x; w) = x / sqrt(mean(x^2) + eps) * w.  RoPE turns the pairs
+ * (i, i + D/2) of every head by the angle p * theta^(-2i/D).  Attention:
+ * scale 1/sqrt(D), query head h reads KV head h / (Hq / Hkv), row j of a
+ * sequence sees cache positions 0 .. pos[b] + j (causal inside the new
+ * rows); D = d / Hq.
+ *
+ *   u        [B r, 2d] bf16     concat(F_T, E) of the new rows (a
+ *                                placeholder row carries its own input)
+ *   fc_w     [d, 2d] bf16, fc_b [d] float32
+ *   ln1, ln2 [d] float32        RMSNorm weights
+ *   wqkv     [(Hq + 2 Hkv) D, d] bf16   query heads, key heads, value heads
+ *   wo       [d, Hq D] bf16
+ *   wgu      [2I, d] bf16       gate rows, then up rows
+ *   wdown    [d, I] bf16
+ *   k_cache, v_cache [B, Lmax, Hkv, D] bf16  the draft cache (post-RoPE
+ *            keys); positions pos[b] .. pos[b] + r - 1 are overwritten
+ *   pos      [B] int32 (device)  first new position of each sequence; rows
+ *            whose position falls outside 0 .. Lmax - 1 are not written to
+ *            the cache and attend over what the cache holds (unspecified
+ *            output, no out-of-range access)
+ *   out      [B r, d] float32   the layer's outputs (placeholder rows: the
+ *            draft states for the LM head)
+ *   workspace  sd_semi_ar_layer_workspace_size(...) bytes, 256-byte aligned
+ *            (device-dependent like sd_linear's)
+ * Requirements: d = Hq * D with D in {64, 128}; Hq % Hkv == 0; 1 <= r <= 16;
+ * r * (Hq / Hkv) <= 256; d and I multiples of 256; Lmax >= r; eps >= 0;
+ * theta > 0.  Errors as for sd_linear.
+ * ---------------------------------------------------------------------- */
+size_t sd_semi_ar_layer_workspace_size(int B, int r, int d, int num_q_heads, int num_kv_heads,
+                                       int I, int Lmax);
+
+int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const float* ln1,
+                     const void* wqkv, const void* wo, const float* ln2, const void* wgu,
+                     const void* wdown, void* k_cache, void* v_cache, const int32_t* pos,
+                     float* out, int B, int r, int d, int num_q_heads, int num_kv_heads, int I,
+                     int Lmax, float eps, float theta, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,6 +28,8 @@ __all__ = [
     "sd_lm_head_workspace_size", "sd_lm_head_probs",
     "sd_sample_workspace_size", "sd_sample_tokens",
     "sd_spec_accept_logits_workspace_size", "sd_spec_accept_logits", "sd_philox_uniforms",
+    "sd_linear_workspace_size", "sd_linear",
+    "sd_semi_ar_layer_workspace_size", "sd_semi_ar_layer",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -58,6 +60,11 @@ _SIGNATURES = {
     "sd_lm_head_probs": (_i, [_vp, _vp, _vp, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
     "sd_sample_workspace_size": (_sz, [_i, _i]),
     "sd_sample_tokens": (_i, [_vp, _vp, _vp, _i, _i, _vp, _sz, _vp]),
+    "sd_linear_workspace_size": (_sz, [_i, _i, _i]),
+    "sd_linear": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _vp, _sz, _vp]),
+    "sd_semi_ar_layer_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
+    "sd_semi_ar_layer": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                              _i, _i, _i, _i, _i, _i, _i, _f, _f, _vp, _sz, _vp]),
 }
 
 
@@ -361,4 +368,86 @@ def sd_sample_tokens(probs, u, out=None, workspace=None, stream=None):
     st = library().sd_sample_tokens(_ptr(probs), _ptr(u), _ptr(out), R, V, _ptr(ws), ws_len,
                                     _stream(stream))
     _raise(st, "sd_sample_tokens")
+    return out
+
+
+def sd_linear_workspace_size(R, K, N):
+    return library().sd_linear_workspace_size(R, K, N)
+
+
+def sd_linear(x, w, bias=None, residual=None, out=None, workspace=None, stream=None):
+    """y = x W^T (+ bias) (+ residual): x [R, K] bf16, w [N, K] bf16, bias [N]
+    fp32, residual [R, N] fp32.  Returns y [R, N] fp32."""
+    torch = _torch()
+    _check(x, "x", dtype=torch.bfloat16, ndim=2)
+    _check(w, "w", dtype=torch.bfloat16, ndim=2)
+    R, K = x.shape
+    N = w.shape[0]
+    if w.shape[1] != K:
+        raise ValueError("w must be [N, K] with the width K of x")
+    if bias is not None:
+        _check(bias, "bias", dtype=torch.float32, ndim=1)
+        if bias.shape[0] != N:
+            raise ValueError("bias must be [N]")
+    if residual is not None:
+        _check(residual, "residual", dtype=torch.float32, ndim=2)
+        if tuple(residual.shape) != (R, N):
+            raise ValueError("residual must be [R, N]")
+    if out is None:
+        out = torch.empty((R, N), dtype=torch.float32, device=x.device)
+    ws_bytes = sd_linear_workspace_size(R, K, N)
+    ws, ws_len = _workspace(ws_bytes, x.device, workspace)
+    st = library().sd_linear(_ptr(x), _ptr(w), _ptr(bias), _ptr(residual), _ptr(out), R, K, N,
+                             _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_linear")
+    return out
+
+
+def sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax):
+    return library().sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax)
+
+
+SEMI_AR_WEIGHTS = ("fc_w", "fc_b", "ln1", "wqkv", "wo", "ln2", "wgu", "wdown")
+
+
+def sd_semi_ar_layer(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, out=None,
+                     workspace=None, stream=None):
+    """One draft step of the semi-autoregressive layer.  u [B, r, 2d] bf16;
+    weights: dict of fc_w [d, 2d], wqkv [(hq + 2 hkv) D, d], wo [d, hq D],
+    wgu [2I, d], wdown [d, I] (bf16) and fc_b, ln1, ln2 [d] (fp32); caches
+    [B, Lmax, hkv, D] bf16 (updated in place at positions pos[b] ..
+    pos[b] + r - 1); pos [B] int32.  Returns out [B, r, d] fp32."""
+    torch = _torch()
+    _check(u, "u", dtype=torch.bfloat16, ndim=3)
+    B, r, d2 = u.shape
+    d = d2 // 2
+    for name in SEMI_AR_WEIGHTS:
+        t = weights[name]
+        _check(t, name, dtype=torch.float32 if name in ("fc_b", "ln1", "ln2") else torch.bfloat16)
+    _check(k_cache, "k_cache", dtype=torch.bfloat16, ndim=4)
+    _check(v_cache, "v_cache", dtype=torch.bfloat16, ndim=4)
+    _check(pos, "pos", dtype=torch.int32, ndim=1)
+    Lmax = k_cache.shape[1]
+    I = weights["wdown"].shape[1]
+    D = d // hq
+    shapes = {"fc_w": (d, 2 * d), "fc_b": (d,), "ln1": (d,), "wqkv": ((hq + 2 * hkv) * D, d),
+              "wo": (d, hq * D), "ln2": (d,), "wgu": (2 * I, d), "wdown": (d, I)}
+    for name, shp in shapes.items():
+        if tuple(weights[name].shape) != shp:
+            raise ValueError(f"{name} must be {shp}, got {tuple(weights[name].shape)}")
+    if tuple(k_cache.shape) != (B, Lmax, hkv, D) or tuple(v_cache.shape) != (B, Lmax, hkv, D):
+        raise ValueError("caches must be [B, Lmax, hkv, d / hq]")
+    if pos.shape[0] != B:
+        raise ValueError("pos must be [B]")
+    if out is None:
+        out = torch.empty((B, r, d), dtype=torch.float32, device=u.device)
+    ws_bytes = sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax)
+    ws, ws_len = _workspace(ws_bytes, u.device, workspace)
+    W = weights
+    st = library().sd_semi_ar_layer(_ptr(u), _ptr(W["fc_w"]), _ptr(W["fc_b"]), _ptr(W["ln1"]),
+                                    _ptr(W["wqkv"]), _ptr(W["wo"]), _ptr(W["ln2"]), _ptr(W["wgu"]),
+                                    _ptr(W["wdown"]), _ptr(k_cache), _ptr(v_cache), _ptr(pos),
+                                    _ptr(out), B, r, d, hq, hkv, I, Lmax, float(eps), float(theta),
+                                    _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_semi_ar_layer")
     return out

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspecflash.so")
 SOURCES = ["specflash_api.hip", "verify_attention.hip", "spec_accept.hip", "latent_compress.hip",
-           "lm_head.hip"]
+           "lm_head.hip", "draft_layer.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -1,0 +1,374 @@
+// One step of the draft's semi-autoregressive layer (SpecFLASH Sec. 3.1
+// and Algorithm 1: the textual input FC(concat(F_T, E)); Sec. 3.3: one pass
+// of one transformer layer gives the K placeholder states; Sec. 4.4: one
+// layer of 32 heads):
+//   x0 = [F_T, E] W_fc^T + b_fc
+//   x1 = x0 + Attn(RoPE(RMSNorm(x0) Wqkv^T)) Wo^T      (cached context)
+//   out = x1 + (silu(h Wg^T) * (h Wu^T)) Wdown^T,  h = RMSNorm(x1)
+// for the r new rows of each sequence, over the draft's KV cache.
+//
+// A drafting step has few rows (R = B r <= 128 per pass), so every
+// projection streams its weight once and is bound by HBM.  One kernel
+// serves all five: work-groups of NW waves own NW * 16 output columns and
+// a range of 256-channel chunks of the reduction; lane (c, G) of a wave
+// reads 128 contiguous bytes of weight row c per chunk (every row in
+// 512-byte runs) straight into registers, the chunk of all input rows is
+// copied into LDS by the global_load_lds DMA, and z^T = W x^T runs on bf16
+// matrix cores.  The reduction is split across work-groups until the grid
+// fills the device; each split writes fp32 partial sums, and one epilogue
+// kernel per projection adds the splits and applies what follows it:
+// bias + RMSNorm, RoPE + cache append, residual + RMSNorm, SwiGLU, or the
+// final residual.  The attention is the verification kernel: the new rows
+// are a block of r queries, causal inside the block, over the cache.
+#include <math.h>
+
+#include <algorithm>
+
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace sd {
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_cvoid;
+
+constexpr int kChunkK = 256;    // reduction channels per step
+constexpr int kEpiThreads = 256;
+
+// part[ks][r][n] = sum over split ks's chunks of x[r][k] w[n][k], for the
+// rows r0 .. r0 + 16 RB - 1 of this pass.  Matrix-core product i of a chunk
+// takes the i-th 16-byte load of every lane (channels 64 G + 8 i .. +7 of
+// the chunk), a fixed permutation of the chunk's channels that the input
+// fragments follow; the input chunk's 16-byte pieces of row t sit at slot
+// piece ^ (t & 15), so the fragment reads are free of bank conflicts.
+template <int RB, int NW>
+__global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
+  constexpr int HROWS = RB * 16;
+  constexpr int HPIECES = HROWS * 32;          // 16-byte pieces of one input chunk
+  constexpr int DMA = HPIECES / (NW * 64);     // copies per thread and chunk
+  static_assert(HPIECES % (NW * 64) == 0, "whole copies per thread");
+  __shared__ __align__(16) unsigned char hbuf[2][HPIECES * 16];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, G = lane >> 4, c = lane & 15;
+  const int n0 = blockIdx.x * (NW * 16) + w * 16;
+  const int ks = blockIdx.y;
+  const int r0 = blockIdx.z * HROWS;
+  const int K = a.K, N = a.N, R = a.R;
+  const int nch = K / kChunkK;
+  const int ch0 = (int)((long long)nch * ks / a.ksplit);
+  const int ch1 = (int)((long long)nch * (ks + 1) / a.ksplit);
+  const uint16_t* W = static_cast<const uint16_t*>(a.w);
+  const uint16_t* X = static_cast<const uint16_t*>(a.x);
+  // weight row n0 + c (clamped; columns >= N are not written)
+  const u32x4* wsrc = reinterpret_cast<const u32x4*>(W + (size_t)min(n0 + c, N - 1) * K + 64 * G);
+  // copy j of this thread moves piece P = (w DMA + j) 64 + lane of a chunk:
+  // input row P / 32 of the pass (clamped; padded rows are not written)
+  const uint16_t* hsrc[DMA];
+#pragma unroll
+  for (int j = 0; j < DMA; ++j) {
+    const int P = (w * DMA + j) * 64 + lane;
+    const int row = P >> 5, slot = P & 31;
+    hsrc[j] = X + (size_t)min(r0 + row, R - 1) * K + ((slot ^ (row & 15)) * 8);
+  }
+  auto issue = [&](int n, int buf) {
+#pragma unroll
+    for (int j = 0; j < DMA; ++j)
+      __builtin_amdgcn_global_load_lds((gbl_cvoid*)(hsrc[j] + (size_t)n * kChunkK),
+                                       (lds_void*)(&hbuf[buf][(w * DMA + j) * 1024]), 16, 0, 0);
+  };
+
+  floatx4 acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (ch0 < ch1) issue(ch0, 0);
+#pragma unroll 1
+  for (int n = ch0; n < ch1; ++n) {
+    const int buf = (n - ch0) & 1;
+    u32x4 wf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) wf[i] = wsrc[(size_t)n * 32 + i];
+    // the weight loads are the newest: this thread's copies of chunk n have
+    // landed; after the barrier every wave's have, and every wave is done
+    // reading the other buffer
+    wait_vm_then_barrier<8>();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      Pack8 x;
+      x.u = wf[i];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = rb * 16 + c;
+        Pack8 y;
+        y.u = *reinterpret_cast<const u32x4*>(&hbuf[buf][(row * 32 + ((8 * G + i) ^ c)) * 16]);
+        acc[rb] = mfma_bf16(x.b, y.b, acc[rb]);
+      }
+    }
+    if (n + 1 < ch1) issue(n + 1, buf ^ 1);
+  }
+  // accumulator element i of lane (c, G): input row rb*16 + c, column n0 + 4G + i
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = r0 + rb * 16 + c;
+    if (r >= R || n0 + 4 * G >= N) continue;
+    float* dst = a.part + ((size_t)ks * R + r) * N + n0 + 4 * G;
+    if (n0 + 4 * G + 3 < N && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+      *reinterpret_cast<floatx4*>(dst) = acc[rb];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (n0 + 4 * G + i < N) dst[i] = acc[rb][i];
+    }
+  }
+}
+
+__device__ __forceinline__ float split_sum(const float* part, int ksplit, size_t stride, size_t idx) {
+  float s = 0.f;
+  for (int ks = 0; ks < ksplit; ++ks) s += part[(size_t)ks * stride + idx];
+  return s;
+}
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += red[i];
+  return t;
+}
+
+// y = sum of splits (+ bias) (+ residual), written as fp32 `out` [R, N].
+// With `norm_w`, also h = y / sqrt(mean(y^2) + eps) * norm_w in bf16.
+// One work-group per row.
+__global__ __launch_bounds__(kEpiThreads) void epi_add_norm(const float* part, int ksplit, int R, int N,
+                                                            const float* bias, const float* residual,
+                                                            float* out, const float* norm_w, float eps,
+                                                            __bf16* h) {
+  __shared__ float red[kEpiThreads / 64];
+  const int r = blockIdx.x;
+  const size_t stride = (size_t)R * N;
+  float ss = 0.f;
+  for (int n = threadIdx.x; n < N; n += kEpiThreads) {
+    const size_t idx = (size_t)r * N + n;
+    float y = split_sum(part, ksplit, stride, idx);
+    if (bias) y += bias[n];
+    if (residual) y += residual[idx];
+    out[idx] = y;
+    ss += y * y;
+  }
+  if (norm_w == nullptr) return;
+  const float inv = 1.f / sqrtf(block_sum(ss, red) / (float)N + eps);
+  for (int n = threadIdx.x; n < N; n += kEpiThreads) {
+    const size_t idx = (size_t)r * N + n;
+    h[idx] = float_to_bf16(out[idx] * inv * norm_w[n]);
+  }
+}
+
+// Fused projection output of row r (sequence b = r / rows, j = r % rows,
+// position p = pos[b] + j): query heads rotated into q [R, Hq, D] (bf16),
+// key heads rotated and value heads copied into the caches at position p
+// (skipped when p is outside 0 .. Lmax - 1).  Half-split pairs (i, i + D/2)
+// turn by p theta^(-2i/D), the angle formed in float64.  Row 0 of each
+// sequence also writes kv_len[b] = pos[b] + rows for the attention.
+__global__ __launch_bounds__(kEpiThreads) void epi_rope_qkv(const float* part, int ksplit, int R, int N,
+                                                            const int32_t* pos, int rows, int Hq, int Hkv,
+                                                            int D, double log_theta, int Lmax, __bf16* q,
+                                                            __bf16* kc, __bf16* vc, int32_t* kv_len) {
+  const int r = blockIdx.x;
+  const int b = r / rows, j = r - b * rows;
+  const int p = pos[b] + j;
+  const bool store = p >= 0 && p < Lmax;
+  if (j == 0 && threadIdx.x == 0) kv_len[b] = pos[b] + rows;
+  const size_t stride = (size_t)R * N;
+  const int half = D / 2;
+  const int pairs = (Hq + Hkv) * half;
+  for (int t = threadIdx.x; t < pairs; t += kEpiThreads) {
+    const int hh = t / half, i = t - hh * half;
+    const size_t base = (size_t)r * N + (size_t)hh * D;
+    const float x0 = split_sum(part, ksplit, stride, base + i);
+    const float x1 = split_sum(part, ksplit, stride, base + i + half);
+    const double ang = (double)p * exp(-2.0 * (double)i / (double)D * log_theta);
+    const float cs = (float)cos(ang), sn = (float)sin(ang);
+    const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
+    if (hh < Hq) {
+      __bf16* dst = q + ((size_t)r * Hq + hh) * D;
+      dst[i] = float_to_bf16(y0);
+      dst[i + half] = float_to_bf16(y1);
+    } else if (store) {
+      __bf16* dst = kc + (((size_t)b * Lmax + p) * Hkv + (hh - Hq)) * D;
+      dst[i] = float_to_bf16(y0);
+      dst[i + half] = float_to_bf16(y1);
+    }
+  }
+  if (!store) return;
+  for (int t = threadIdx.x; t < Hkv * D; t += kEpiThreads) {
+    const int hv = t / D, e = t - hv * D;
+    const float v = split_sum(part, ksplit, stride, (size_t)r * N + (size_t)(Hq + Hkv + hv) * D + e);
+    vc[(((size_t)b * Lmax + p) * Hkv + hv) * D + e] = float_to_bf16(v);
+  }
+}
+
+// act[r][i] = silu(g) * u with g, u the split sums of columns i and I + i
+__global__ __launch_bounds__(kEpiThreads) void epi_swiglu(const float* part, int ksplit, int R, int I,
+                                                          __bf16* act) {
+  const int r = blockIdx.y;
+  const int i = blockIdx.x * kEpiThreads + threadIdx.x;
+  if (i >= I) return;
+  const size_t N = 2 * (size_t)I;
+  const size_t stride = (size_t)R * N;
+  const float g = split_sum(part, ksplit, stride, (size_t)r * N + i);
+  const float u = split_sum(part, ksplit, stride, (size_t)r * N + I + i);
+  act[(size_t)r * I + i] = float_to_bf16(g / (1.f + expf(-g)) * u);
+}
+
+__global__ __launch_bounds__(kEpiThreads) void to_bf16(const float* x, __bf16* y, size_t n) {
+  const size_t i = (size_t)blockIdx.x * kEpiThreads + threadIdx.x;
+  if (i < n) y[i] = float_to_bf16(x[i]);
+}
+
+template <int NW>
+hipError_t launch_partial_nw(const LinearArgs& a, int rb, int passes, hipStream_t st) {
+  const dim3 grid((a.N + NW * 16 - 1) / (NW * 16), a.ksplit, passes);
+  const dim3 block(NW * 64);
+  switch (rb) {
+    case 1: hipLaunchKernelGGL((linear_partial<1, NW>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((linear_partial<2, NW>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((linear_partial<3, NW>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((linear_partial<4, NW>), grid, block, 0, st, a); break;
+    case 5: hipLaunchKernelGGL((linear_partial<5, NW>), grid, block, 0, st, a); break;
+    case 6: hipLaunchKernelGGL((linear_partial<6, NW>), grid, block, 0, st, a); break;
+    case 7: hipLaunchKernelGGL((linear_partial<7, NW>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((linear_partial<8, NW>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+LinearPlan plan_linear(int R, int K, int N, int cus) {
+  LinearPlan p{};
+  const int rows = std::min(R, kLinearRowsPerPass);
+  p.row_blocks = (rows + 15) / 16;
+  p.passes = (R + kLinearRowsPerPass - 1) / kLinearRowsPerPass;
+  p.waves = 4;
+  const long long groups = (long long)((N + p.waves * 16 - 1) / (p.waves * 16)) * p.passes;
+  const int nch = K / kChunkK;
+  // split the reduction until about two work-groups per compute unit exist,
+  // keeping at least four chunks per split
+  long long ks = (2LL * std::max(cus, 1) + groups - 1) / groups;
+  ks = std::min<long long>(ks, std::max(1, nch / 4));
+  p.ksplit = (int)std::max(1LL, std::min<long long>(ks, kLinearMaxSplits));
+  p.part_bytes = (size_t)p.ksplit * R * N * sizeof(float);
+  return p;
+}
+
+hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipStream_t st) {
+  return launch_partial_nw<4>(a, p.row_blocks, p.passes, st);
+}
+
+hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias, const float* residual,
+                          float* out, hipStream_t st) {
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, ksplit, R, N, bias, residual, out,
+                     nullptr, 0.f, nullptr);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- the whole layer
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+SemiArPlan plan_semi_ar(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, int cus) {
+  SemiArPlan p{};
+  const int R = B * r, D = d / Hq;
+  const int nqkv = (Hq + 2 * Hkv) * D;
+  p.fc = plan_linear(R, 2 * d, d, cus);
+  p.qkv = plan_linear(R, d, nqkv, cus);
+  p.o = plan_linear(R, Hq * D, d, cus);
+  p.gu = plan_linear(R, d, 2 * I, cus);
+  p.down = plan_linear(R, I, d, cus);
+  p.verify = plan_verify(B, r, Hq, Hkv, D, Lmax, 1, cus);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += align256(bytes); return o; };
+  const size_t part = std::max({p.fc.part_bytes, p.qkv.part_bytes, p.o.part_bytes, p.gu.part_bytes,
+                                p.down.part_bytes});
+  p.off_part = take(part);
+  p.off_x0 = take((size_t)R * d * 4);
+  p.off_h = take((size_t)R * d * 2);
+  p.off_q = take((size_t)R * Hq * D * 2);
+  p.off_attn = take((size_t)R * Hq * D * 4);
+  p.off_attn16 = take((size_t)R * Hq * D * 2);
+  p.off_x1 = take((size_t)R * d * 4);
+  p.off_act = take((size_t)R * I * 2);
+  p.off_kvlen = take((size_t)B * 4);
+  p.off_verify = take(p.verify.workspace_bytes);
+  p.workspace_bytes = off;
+  p.ok = p.verify.ok;
+  return p;
+}
+
+hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t st) {
+  unsigned char* ws = static_cast<unsigned char*>(a.workspace);
+  float* part = reinterpret_cast<float*>(ws + p.off_part);
+  float* x0 = reinterpret_cast<float*>(ws + p.off_x0);
+  __bf16* h = reinterpret_cast<__bf16*>(ws + p.off_h);
+  __bf16* q = reinterpret_cast<__bf16*>(ws + p.off_q);
+  float* attn = reinterpret_cast<float*>(ws + p.off_attn);
+  __bf16* attn16 = reinterpret_cast<__bf16*>(ws + p.off_attn16);
+  float* x1 = reinterpret_cast<float*>(ws + p.off_x1);
+  __bf16* act = reinterpret_cast<__bf16*>(ws + p.off_act);
+  int32_t* kv_len = reinterpret_cast<int32_t*>(ws + p.off_kvlen);
+  const int R = a.B * a.r, d = a.d, D = d / a.Hq;
+  const int nqkv = (a.Hq + 2 * a.Hkv) * D;
+  hipError_t e;
+  auto lin = [&](const void* x, const void* w, int K, int N, const LinearPlan& lp) {
+    LinearArgs la{x, w, part, R, K, N, lp.ksplit};
+    return launch_linear_partial(la, lp, st);
+  };
+  // x0 = FC(u), h = RMSNorm(x0)
+  if ((e = lin(a.u, a.fc_w, 2 * d, d, p.fc)) != hipSuccess) return e;
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
+                     (const float*)nullptr, x0, a.ln1, a.eps, h);
+  // q, k, v with RoPE; k, v appended to the cache
+  if ((e = lin(h, a.wqkv, d, nqkv, p.qkv)) != hipSuccess) return e;
+  hipLaunchKernelGGL(epi_rope_qkv, dim3(R), dim3(kEpiThreads), 0, st, part, p.qkv.ksplit, R, nqkv, a.pos, a.r,
+                     a.Hq, a.Hkv, D, log((double)a.theta), a.Lmax, q,
+                     static_cast<__bf16*>(a.k_cache), static_cast<__bf16*>(a.v_cache), kv_len);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // attention of the r new rows over the cache, causal inside them
+  VerifyArgs va{};
+  va.q = q;
+  va.kc = a.k_cache;
+  va.vc = a.v_cache;
+  va.kv_len = kv_len;
+  va.page_table = nullptr;
+  va.Lmax = a.Lmax;
+  va.out = attn;
+  va.lse = nullptr;
+  va.B = a.B;
+  va.k = a.r;
+  va.Hq = a.Hq;
+  va.Hkv = a.Hkv;
+  va.D = D;
+  va.scale = 1.f / sqrtf((float)D);
+  va.scale_log2 = va.scale * kLog2e;
+  va.part_o = reinterpret_cast<float*>(ws + p.off_verify);
+  va.part_lse = va.part_o + p.verify.part_rows * D;
+  if ((e = launch_verify(va, p.verify, 1, st)) != hipSuccess) return e;
+  const size_t na = (size_t)R * a.Hq * D;
+  hipLaunchKernelGGL(to_bf16, dim3((unsigned)((na + kEpiThreads - 1) / kEpiThreads)), dim3(kEpiThreads), 0, st,
+                     attn, attn16, na);
+  // x1 = x0 + attn Wo^T, h = RMSNorm(x1)
+  if ((e = lin(attn16, a.wo, a.Hq * D, d, p.o)) != hipSuccess) return e;
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, p.o.ksplit, R, d,
+                     (const float*)nullptr, x0, x1, a.ln2, a.eps, h);
+  // act = SwiGLU(h), out = x1 + act Wdown^T
+  if ((e = lin(h, a.wgu, d, 2 * a.I, p.gu)) != hipSuccess) return e;
+  hipLaunchKernelGGL(epi_swiglu, dim3((a.I + kEpiThreads - 1) / kEpiThreads, R), dim3(kEpiThreads), 0, st, part,
+                     p.gu.ksplit, R, a.I, act);
+  if ((e = lin(act, a.wdown, a.I, d, p.down)) != hipSuccess) return e;
+  return launch_epi_add(part, p.down.ksplit, R, d, nullptr, x1, a.out, st);
+}
+
+}  // namespace sd

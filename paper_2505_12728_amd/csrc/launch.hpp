@@ -114,4 +114,60 @@ size_t accept_logits_workspace_bytes(int B, int k, int V, int mode);
 hipError_t launch_accept_logits(const AcceptLogitsArgs& a, int dtype, void* workspace, hipStream_t s);
 hipError_t launch_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B, int n, hipStream_t s);
 
+// ------------------------------------------------- draft semi-AR layer
+constexpr int kLinearRowsPerPass = 128;   // input rows per pass of the weight stream
+constexpr int kLinearMaxSplits = 16;      // reduction splits at most
+
+struct LinearArgs {
+  const void* x;   // [R, K] bf16
+  const void* w;   // [N, K] bf16
+  float* part;     // [ksplit, R, N] fp32 partial sums
+  int R, K, N;
+  int ksplit;
+};
+
+struct LinearPlan {
+  int row_blocks;  // 16-row blocks per pass (1..8)
+  int passes;      // passes over the weight (ceil(R / 128))
+  int waves;       // waves per work-group (16 output columns each)
+  int ksplit;      // splits of the reduction
+  size_t part_bytes;
+};
+
+LinearPlan plan_linear(int R, int K, int N, int cus);
+hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipStream_t s);
+// out = sum of the ksplit partials (+ bias [N]) (+ residual [R, N]), fp32
+hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias,
+                          const float* residual, float* out, hipStream_t s);
+
+struct SemiArArgs {
+  const void* u;       // [B r, 2d] bf16: concat(F_T, E) of the new rows
+  const void* fc_w;    // [d, 2d] bf16
+  const float* fc_b;   // [d]
+  const float* ln1;    // [d]
+  const void* wqkv;    // [(Hq + 2 Hkv) D, d] bf16
+  const void* wo;      // [d, Hq D] bf16
+  const float* ln2;    // [d]
+  const void* wgu;     // [2I, d] bf16
+  const void* wdown;   // [d, I] bf16
+  void* k_cache;       // [B, Lmax, Hkv, D] bf16
+  void* v_cache;
+  const int32_t* pos;  // [B] first new position of each sequence
+  float* out;          // [B r, d]
+  int B, r, d, Hq, Hkv, I, Lmax;
+  float eps, theta;
+  void* workspace;
+};
+
+struct SemiArPlan {
+  LinearPlan fc, qkv, o, gu, down;
+  VerifyPlan verify;
+  size_t off_part, off_x0, off_h, off_q, off_attn, off_attn16, off_x1, off_act, off_kvlen, off_verify;
+  size_t workspace_bytes;
+  bool ok;
+};
+
+SemiArPlan plan_semi_ar(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, int cus);
+hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t s);
+
 }  // namespace sd

@@ -317,3 +317,96 @@ int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R,
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ draft layer
+static bool linear_shape_ok(int R, int K, int N) {
+  return R >= 1 && R <= (1 << 20) && K >= 256 && K % 256 == 0 && K <= (1 << 20) && N >= 1 && N <= (1 << 24) &&
+         (long long)R * N <= (1LL << 31);
+}
+
+size_t sd_linear_workspace_size(int R, int K, int N) {
+  if (!linear_shape_ok(R, K, N)) return 0;
+  return sd::plan_linear(R, K, N, device_cus()).part_bytes;
+}
+
+int sd_linear(const void* x, const void* w, const float* bias, const float* residual, float* y, int R, int K,
+              int N, void* workspace, size_t workspace_bytes, void* stream) {
+  if (R < 1 || K < 1 || N < 1 || !x || !w || !y) return SD_ERR_INVALID_ARG;
+  if (!linear_shape_ok(R, K, N)) return SD_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 4) || (bias && !aligned(bias, 4)) ||
+      (residual && !aligned(residual, 4)))
+    return SD_ERR_INVALID_ARG;
+  const sd::LinearPlan plan = sd::plan_linear(R, K, N, device_cus());
+  if (!workspace || workspace_bytes < plan.part_bytes || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  sd::LinearArgs a{x, w, static_cast<float*>(workspace), R, K, N, plan.ksplit};
+  hipError_t e = sd::launch_linear_partial(a, plan, st);
+  if (e != hipSuccess) return status_from(e);
+  return status_from(sd::launch_epi_add(a.part, plan.ksplit, R, N, bias, residual, y, st));
+}
+
+static bool semi_ar_shape_ok(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, int* status) {
+  *status = SD_ERR_INVALID_ARG;
+  if (B < 1 || r < 1 || d < 1 || Hq < 1 || Hkv < 1 || I < 1 || Lmax < 1 || d % Hq != 0 || Hq % Hkv != 0)
+    return false;
+  *status = SD_ERR_UNSUPPORTED;
+  const int D = d / Hq;
+  if (r > 16 || (D != 64 && D != 128) || r * (Hq / Hkv) > 256 || d % 256 != 0 || I % 256 != 0 ||
+      Lmax < r || (long long)B * r > (1 << 16) || (long long)B * Lmax * Hkv * D > (1LL << 40))
+    return false;
+  *status = SD_OK;
+  return true;
+}
+
+size_t sd_semi_ar_layer_workspace_size(int B, int r, int d, int num_q_heads, int num_kv_heads, int I,
+                                       int Lmax) {
+  int st;
+  if (!semi_ar_shape_ok(B, r, d, num_q_heads, num_kv_heads, I, Lmax, &st)) return 0;
+  const sd::SemiArPlan plan = sd::plan_semi_ar(B, r, d, num_q_heads, num_kv_heads, I, Lmax, device_cus());
+  return plan.ok ? plan.workspace_bytes : 0;
+}
+
+int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const float* ln1, const void* wqkv,
+                     const void* wo, const float* ln2, const void* wgu, const void* wdown, void* k_cache,
+                     void* v_cache, const int32_t* pos, float* out, int B, int r, int d, int num_q_heads,
+                     int num_kv_heads, int I, int Lmax, float eps, float theta, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  int st = SD_OK;
+  if (!semi_ar_shape_ok(B, r, d, num_q_heads, num_kv_heads, I, Lmax, &st)) return st;
+  if (!u || !fc_w || !fc_b || !ln1 || !wqkv || !wo || !ln2 || !wgu || !wdown || !k_cache || !v_cache || !pos ||
+      !out || !isfinite(eps) || eps < 0.f || !isfinite(theta) || theta <= 0.f)
+    return SD_ERR_INVALID_ARG;
+  const void* a16[] = {u, fc_w, wqkv, wo, wgu, wdown, k_cache, v_cache};
+  for (const void* p : a16)
+    if (!aligned(p, 16)) return SD_ERR_INVALID_ARG;
+  if (!aligned(fc_b, 4) || !aligned(ln1, 4) || !aligned(ln2, 4) || !aligned(pos, 4) || !aligned(out, 16))
+    return SD_ERR_INVALID_ARG;
+  const sd::SemiArPlan plan = sd::plan_semi_ar(B, r, d, num_q_heads, num_kv_heads, I, Lmax, device_cus());
+  if (!plan.ok) return SD_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned(workspace, 256)) return SD_ERR_WORKSPACE;
+  sd::SemiArArgs a{};
+  a.u = u;
+  a.fc_w = fc_w;
+  a.fc_b = fc_b;
+  a.ln1 = ln1;
+  a.wqkv = wqkv;
+  a.wo = wo;
+  a.ln2 = ln2;
+  a.wgu = wgu;
+  a.wdown = wdown;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.pos = pos;
+  a.out = out;
+  a.B = B;
+  a.r = r;
+  a.d = d;
+  a.Hq = num_q_heads;
+  a.Hkv = num_kv_heads;
+  a.I = I;
+  a.Lmax = Lmax;
+  a.eps = eps;
+  a.theta = theta;
+  a.workspace = workspace;
+  return status_from(sd::launch_semi_ar(a, plan, static_cast<hipStream_t>(stream)));
+}

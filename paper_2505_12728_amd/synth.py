@@ -39,7 +39,8 @@ POISON = 8192.0          # exact in bfloat16 and float32
 # stream order for SeedSequence.spawn; never reorder (it changes every value)
 _STREAMS = ("latents", "feats", "q", "k", "v", "target_logits", "draft_noise",
             "draft_uniforms", "accept_uniforms", "kv_lens", "page_perm",
-            "lm_hidden", "lm_weight", "sample_uniforms")
+            "lm_hidden", "lm_weight", "sample_uniforms", "draft_u", "draft_w",
+            "draft_cache")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -69,6 +70,12 @@ class Workload:
     # LM head (hidden width d of the head; its rows are the batch's k+1
     # target positions)
     lm_width: int = 0
+    # draft semi-AR layer: the target layer's heads and width (d = hq *
+    # head_dim), MLP width I, cached context length before the step (the
+    # compressed visual rows plus earlier text); the step's rows per
+    # sequence are one accepted token and the k placeholders
+    draft_ffn: int = 0
+    draft_ctx: int = 0
 
     @property
     def seed(self):
@@ -79,23 +86,25 @@ WORKLOADS = [
     Workload("tiny-f32", "f32", batch=1, hq=4, hkv=1, head_dim=64, kv_len=608,
              block=4, c_batch=1, c_tokens=576, c_width=256, c_latents=16,
              c_heads=1, vocab=1024, modes=("sampled", "greedy"),
-             temperature=1.0, lm_width=256),
+             temperature=1.0, lm_width=256, draft_ffn=512, draft_ctx=24),
     Workload("llava-7b-image", "bf16", batch=1, hq=32, hkv=32, head_dim=128,
              kv_len=1200, block=5, c_batch=1, c_tokens=576, c_width=4096,
              c_latents=64, c_heads=32, vocab=32000, modes=("sampled",),
-             temperature=1.0, lm_width=4096),
+             temperature=1.0, lm_width=4096, draft_ffn=11008, draft_ctx=96),
     Workload("qwen2vl-7b-video", "bf16", batch=1, hq=28, hkv=4, head_dim=128,
              kv_len=6528, block=8, c_batch=1, c_tokens=6272, c_width=3584,
              c_latents=256, c_heads=28, vocab=152064,
-             modes=("greedy", "sampled"), temperature=1.0, lm_width=3584),
+             modes=("greedy", "sampled"), temperature=1.0, lm_width=3584,
+             draft_ffn=18944, draft_ctx=288),
     Workload("batched-paged", "bf16", batch=16, hq=32, hkv=8, head_dim=128,
              kv_len=16384, kv_len_min=2048, block=6, paged=True, c_batch=16,
              c_tokens=1024, c_width=4096, c_latents=128, c_heads=32,
-             vocab=32000, modes=("sampled",), temperature=1.0, lm_width=4096),
+             vocab=32000, modes=("sampled",), temperature=1.0, lm_width=4096,
+             draft_ffn=14336, draft_ctx=160),
     Workload("long-video", "bf16", batch=4, hq=64, hkv=8, head_dim=128,
              kv_len=65536, block=8, c_batch=4, c_tokens=16384, c_width=8192,
              c_latents=512, c_heads=64, vocab=152064, modes=("sampled",),
-             temperature=0.7, lm_width=8192),
+             temperature=0.7, lm_width=8192, draft_ffn=28672, draft_ctx=544),
 ]
 
 
@@ -406,3 +415,65 @@ def compress_bytes(w):
     es = 4 if w.dtype == "f32" else 2
     return (w.c_batch * w.c_tokens * w.c_width * es + w.c_latents * w.c_width * es
             + w.c_batch * w.c_latents * w.c_width * 4)
+
+
+DRAFT_EPS = 1e-6
+DRAFT_THETA = 10000.0
+
+
+def draft_dims(w):
+    """(B, r, d, hq, hkv, I, Lmax) of the workload's draft step."""
+    d = w.hq * w.head_dim
+    r = w.block + 1
+    Lmax = (w.draft_ctx + 3 * (w.batch - 1) + r + 15) // 16 * 16 + 16
+    return w.batch, r, d, w.hq, w.hkv, w.draft_ffn, Lmax
+
+
+def draft_inputs(w, seed=None, batch=None):
+    """Inputs of one draft step, always in bfloat16 (weights, u, caches):
+    u = concat(F_T, E) ~ N(0, 1) of shape [B, r, 2d]; projection weights
+    ~ N(0, 1 / fan_in), so every projection maps unit-variance rows to
+    unit-variance rows; RMSNorm weights 1 + N(0, 0.1^2) and the FC bias
+    N(0, 0.1^2) in float32; the caches hold N(0, 1) context keys and values
+    at positions 0 .. pos[b] - 1 and the poison value elsewhere; pos[b] =
+    draft_ctx + 3 b (ragged contexts)."""
+    rs = streams(w.seed if seed is None else seed)
+    B, r, d, hq, hkv, I, Lmax = draft_dims(w)
+    B = B if batch is None else batch
+    D = d // hq
+
+    def weight(shape, fan_in):
+        x = normal(rs["draft_w"], shape)
+        _parallel_map(lambda v: v * np.float32(1.0 / math.sqrt(fan_in)), x, x)
+        t = Tensor(x, "bf16")
+        del x
+        return t
+
+    u = Tensor(normal(rs["draft_u"], (B, r, 2 * d)), "bf16")
+    W = {"fc_w": weight((d, 2 * d), 2 * d),
+         "fc_b": (normal(rs["draft_w"], (d,)) * np.float32(0.1)).astype(np.float32),
+         "ln1": (1.0 + normal(rs["draft_w"], (d,)) * np.float32(0.1)).astype(np.float32),
+         "wqkv": weight(((hq + 2 * hkv) * D, d), d),
+         "wo": weight((d, hq * D), hq * D),
+         "ln2": (1.0 + normal(rs["draft_w"], (d,)) * np.float32(0.1)).astype(np.float32),
+         "wgu": weight((2 * I, d), d),
+         "wdown": weight((d, I), I)}
+    pos = (w.draft_ctx + 3 * np.arange(B)).astype(np.int32)
+    kc = normal(rs["draft_cache"], (B, Lmax, hkv, D))
+    vc = normal(rs["draft_cache"], (B, Lmax, hkv, D))
+    for b in range(B):
+        kc[b, pos[b]:] = POISON
+        vc[b, pos[b]:] = POISON
+    return {"u": u, "weights": W, "k_cache": Tensor(kc, "bf16"), "v_cache": Tensor(vc, "bf16"),
+            "pos": pos, "eps": DRAFT_EPS, "theta": DRAFT_THETA, "hq": hq, "hkv": hkv}
+
+
+def draft_bytes(w):
+    """Algorithmic HBM bytes of one draft step: every weight once (bf16),
+    the rows' input and output, and the cache entries the attention reads
+    (keys and values of positions 0 .. pos[b] + r - 1) and writes."""
+    B, r, d, hq, hkv, I, Lmax = draft_dims(w)
+    D = d // hq
+    params = d * 2 * d + (hq + 2 * hkv) * D * d + d * hq * D + 2 * I * d + d * I
+    ctx = sum(w.draft_ctx + 3 * b + r for b in range(B))
+    return 2 * params + B * r * (2 * d * 2 + d * 4) + ctx * 2 * hkv * D * 2

@@ -213,3 +213,57 @@ def test_accept_logits_validation_errors(lib):
     assert g(1, 2, n, 0, 4, None) == sd.SD_ERR_INVALID_ARG
     assert g(1, 2, n, 1, 0, None) == sd.SD_ERR_INVALID_ARG
     assert g(1, 2, n, 1, (1 << 16) + 1, None) == sd.SD_ERR_UNSUPPORTED
+
+
+def test_linear_validation_errors(lib):
+    # every call below fails validation, so nothing is launched
+    keep, (x, w, b, r, y, ws) = _fake(6)
+    f = lib.sd_linear
+
+    def call(x=x, w=w, b=None, r=None, y=y, R=4, K=512, N=100, ws=ws, wsb=0):
+        return f(x, w, b, r, y, R, K, N, ws, wsb, None)
+
+    assert call(x=None) == sd.SD_ERR_INVALID_ARG
+    assert call(y=None) == sd.SD_ERR_INVALID_ARG
+    assert call(R=0) == sd.SD_ERR_INVALID_ARG
+    assert call(N=0) == sd.SD_ERR_INVALID_ARG
+    assert call(K=300) == sd.SD_ERR_UNSUPPORTED                # K % 256
+    assert call(K=128) == sd.SD_ERR_UNSUPPORTED
+    assert call(R=1 << 16, N=1 << 16) == sd.SD_ERR_UNSUPPORTED  # R * N > 2^31
+    assert call(x=ctypes.c_void_p(x.value + 8)) == sd.SD_ERR_INVALID_ARG
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=8) == sd.SD_ERR_WORKSPACE
+    # one fp32 partial per reduction split; at most 16 splits
+    n = lib.sd_linear_workspace_size(36, 8192, 8192)
+    assert n >= 36 * 8192 * 4 and n % (36 * 8192 * 4) == 0 and n <= 16 * 36 * 8192 * 4
+    assert lib.sd_linear_workspace_size(36, 300, 10) == 0
+
+
+def test_semi_ar_layer_validation_errors(lib):
+    keep, ptrs = _fake(14)
+    f = lib.sd_semi_ar_layer
+    P = dict(zip(["u", "fcw", "fcb", "ln1", "wqkv", "wo", "ln2", "wgu", "wdown", "kc", "vc", "pos", "out",
+                  "ws"], ptrs))
+
+    def call(B=2, r=9, d=1024, hq=8, hkv=2, I=2048, L=64, eps=1e-6, theta=1e4, wsb=0, **kw):
+        p = dict(P, **kw)
+        return f(p["u"], p["fcw"], p["fcb"], p["ln1"], p["wqkv"], p["wo"], p["ln2"], p["wgu"], p["wdown"],
+                 p["kc"], p["vc"], p["pos"], p["out"], B, r, d, hq, hkv, I, L, eps, theta, p["ws"], wsb, None)
+
+    assert call(u=None) == sd.SD_ERR_INVALID_ARG
+    assert call(pos=None) == sd.SD_ERR_INVALID_ARG
+    assert call(B=0) == sd.SD_ERR_INVALID_ARG
+    assert call(hq=3) == sd.SD_ERR_INVALID_ARG                  # d % hq
+    assert call(hkv=3) == sd.SD_ERR_INVALID_ARG                 # hq % hkv
+    assert call(r=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(d=1024, hq=4) == sd.SD_ERR_UNSUPPORTED          # D = 256
+    assert call(I=1000) == sd.SD_ERR_UNSUPPORTED                # I % 256
+    assert call(L=8) == sd.SD_ERR_UNSUPPORTED                   # Lmax < r
+    assert call(eps=-1.0) == sd.SD_ERR_INVALID_ARG
+    assert call(theta=0.0) == sd.SD_ERR_INVALID_ARG
+    assert call(theta=float("nan")) == sd.SD_ERR_INVALID_ARG
+    assert call(wgu=ctypes.c_void_p(ptrs[7].value + 8)) == sd.SD_ERR_INVALID_ARG
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert call(wsb=64) == sd.SD_ERR_WORKSPACE
+    assert lib.sd_semi_ar_layer_workspace_size(2, 9, 1024, 8, 2, 2048, 64) > 2 * 9 * 2048 * 2
+    assert lib.sd_semi_ar_layer_workspace_size(2, 17, 1024, 8, 2, 2048, 64) == 0

@@ -6,6 +6,8 @@ One step is one pass of the whole hot path over one batch of synthetic
 input with every tensor already resident in HBM:
     sd_latent_compress (Eq. 3) -> sd_verify_attention -> sd_lm_head_probs
     (the k+1 target rows) -> sd_spec_accept -> sd_spec_accept_logits
+    -> sd_semi_ar_layer (the draft's step for one accepted token and the k
+    placeholders of each sequence)
 Default workload: "long-video" (batch 4, GQA 64/8 heads, head dim 128, KV
 length 65536, block k = 8; compression of 16384 tokens of width 8192 to 512
 latents over 64 heads; an LM head of width 8192 over a 152064-token
@@ -13,13 +15,15 @@ vocabulary for the 36 target rows; sampled acceptance over that vocabulary
 at temperature 0.7).  The acceptance consumes synthetic p and q with
 realistic acceptance rates, not the head's output (its weights are random);
 the acceptance from logits runs on the logits of the same draws (temperature
-softmax and Philox uniforms on the device).
+softmax and Philox uniforms on the device).  The draft layer has the
+target's width and heads (8192, 64 / 8) with a SwiGLU MLP of width 28672,
+over a cached context of 544 + 3 b positions.
 
 Prints one JSON line.  `value` is the verify step's KV-read rate: bytes of
 K and V the step must read once, divided by the time of verification
 attention plus acceptance, in TB/s.  Per-kernel times come from HIP events
 on the stream the kernels run on.  `roofline` describes the dominant kernel
-(the longest per step); `rooflines` lists all five.  `traffic` is the HBM
+(the longest per step); `rooflines` lists all six.  `traffic` is the HBM
 bytes per launch measured with rocprofv3 counters (profiles/), or null when
 the kernel's sources changed since they were taken.  `cpu_baseline` times
 the plain CPU oracle on a bounded sample of the same workload and scales it
@@ -89,7 +93,7 @@ def accept_logits_bytes(w, n):
     return total
 
 
-def cpu_baseline(w, comp, ver, acc, mode, lm, accl):
+def cpu_baseline(w, comp, ver, acc, mode, lm, accl, dr):
     """Time the oracle on a bounded sample and scale it to one whole step."""
     import numpy as np
     import oracle
@@ -138,12 +142,19 @@ def cpu_baseline(w, comp, ver, acc, mode, lm, accl):
                         for v in range(0, w.vocab, 8192)], axis=1)
     oracle.softmax_temperature(z, lm["temperature"])
     tl = (time.perf_counter() - t0) * R
+    # draft layer step: the first sequence's rows (the oracle's cost grows
+    # with the rows), scaled to the batch
+    Wd = {k: (v.values if hasattr(v, "values") else v) for k, v in dr["weights"].items()}
+    t0 = time.perf_counter()
+    oracle.semi_ar_layer(dr["u"].values[:1], Wd, dr["k_cache"].values[:1], dr["v_cache"].values[:1],
+                         dr["pos"][:1], dr["hq"], dr["hkv"], dr["eps"], dr["theta"])
+    td = (time.perf_counter() - t0) * dr["u"].shape[0]
     return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "lm_head_s": tl, "accept_logits_s": tal,
-            "threads": threads,
+            "draft_layer_s": td, "threads": threads,
             "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
                       f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
                       f"pairs, acceptance (from p, q and from logits) of all {w.batch} sequences, "
-                      f"LM head 1 of {R} rows; "
+                      f"LM head 1 of {R} rows, draft layer 1 of {dr['u'].shape[0]} sequences; "
                       f"scaled linearly"}
 
 
@@ -199,6 +210,7 @@ def main():
     acc = synth.accept_inputs(w, mode)
     accl = synth.accept_logits_inputs(w, mode)
     lm = synth.lm_inputs(w)
+    dr = synth.draft_inputs(w)
 
     lat_d, feats_d = to_dev(comp[0], dev), to_dev(comp[1], dev)
     q_d, k_d, v_d = to_dev(ver["q"], dev), to_dev(ver["k_cache"], dev), to_dev(ver["v_cache"], dev)
@@ -212,6 +224,11 @@ def main():
     zd_d = torch.from_numpy(accl["draft_logits"]).to(dev)
     drl_d = torch.from_numpy(accl["draft"]).to(dev)
     h_d, wt_d = to_dev(lm["hidden"], dev), to_dev(lm["weight"], dev)
+    du_d = to_dev(dr["u"], dev)
+    dw_d = {k: (to_dev(v, dev) if hasattr(v, "bits") else torch.from_numpy(v).to(dev))
+            for k, v in dr["weights"].items()}
+    dkc_d, dvc_d = to_dev(dr["k_cache"], dev), to_dev(dr["v_cache"], dev)
+    dpos_d = torch.from_numpy(dr["pos"]).to(dev)
     dt_code = sd.SD_BF16 if w.dtype == "bf16" else sd.SD_F32
     amode = sd.SD_ACCEPT_SAMPLED if mode == "sampled" else sd.SD_ACCEPT_GREEDY
 
@@ -236,6 +253,10 @@ def main():
     al_ws = torch.empty(sd.sd_spec_accept_logits_workspace_size(w.batch, w.block, w.vocab, amode),
                         dtype=torch.uint8, device=dev)
     nl_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
+    dB, dr_rows, dd, _, _, dI, dL = synth.draft_dims(w)
+    d_out = torch.empty((dB, dr_rows, dd), dtype=torch.float32, device=dev)
+    d_ws = torch.empty(sd.sd_semi_ar_layer_workspace_size(dB, dr_rows, dd, dr["hq"], dr["hkv"], dI, dL),
+                       dtype=torch.uint8, device=dev)
     tl_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
     scale = 1.0 / math.sqrt(w.head_dim)
 
@@ -261,6 +282,11 @@ def main():
                                  workspace=al_ws)
         if ev is not None:
             ev[5].record()
+        # the draft step writes the same cache slots every time (same positions)
+        sd.sd_semi_ar_layer(du_d, dw_d, dkc_d, dvc_d, dpos_d, dr["hq"], dr["hkv"], dr["eps"],
+                            dr["theta"], out=d_out, workspace=d_ws)
+        if ev is not None:
+            ev[6].record()
 
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
@@ -271,7 +297,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -284,6 +310,7 @@ def main():
     lm_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
     acc_ms = np.array([e[3].elapsed_time(e[4]) for e in events])
     accl_ms = np.array([e[4].elapsed_time(e[5]) for e in events])
+    draft_ms = np.array([e[5].elapsed_time(e[6]) for e in events])
 
     kv_bytes = synth.verify_kv_bytes(w, ver["kv_len"])
     flops = synth.compress_flops(w)
@@ -293,6 +320,8 @@ def main():
     t_c, t_v, t_a = float(comp_ms.mean()), float(ver_ms.mean()), float(acc_ms.mean())
     t_l = float(lm_ms.mean())
     t_al = float(accl_ms.mean())
+    t_d = float(draft_ms.mean())
+    d_bytes = synth.draft_bytes(w)
     al_bytes = accept_logits_bytes(w, nl_out.cpu().numpy())
     l_bytes = synth.lm_bytes(w, lm_rows)
     verify_step_ms = t_v + t_a
@@ -316,6 +345,9 @@ def main():
         "spec_accept_logits": {"bound": "hbm", "achieved": al_bytes / (t_al * 1e-3) / 1e9,
                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
                                "algorithmic": al_bytes, "us": t_al * 1e3},
+        "semi_ar_layer": {"bound": "hbm", "achieved": d_bytes / (t_d * 1e-3) / 1e9,
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "traffic": None,
+                          "algorithmic": d_bytes, "us": t_d * 1e3},
     }
     traffic = counter_traffic(w.name)
     for name_, r in rl.items():
@@ -347,6 +379,7 @@ def main():
             "latents": w.c_latents, "compress_heads": w.c_heads,
             "vocab": w.vocab, "accept_mode": mode, "temperature": acc["temperature"],
             "lm_rows": lm_rows, "lm_width": w.lm_width,
+            "draft_rows": dB * dr_rows, "draft_ffn": dI, "draft_ctx": w.draft_ctx,
         },
         "verify_step_us": verify_step_ms * 1e3,
         "verify_attention_us": t_v * 1e3,
@@ -355,6 +388,8 @@ def main():
         "lm_head_us": t_l * 1e3,
         "lm_head_tbps": l_bytes / (t_l * 1e-3) / 1e12,
         "spec_accept_logits_us": t_al * 1e3,
+        "semi_ar_layer_us": t_d * 1e3,
+        "semi_ar_layer_tbps": d_bytes / (t_d * 1e-3) / 1e12,
         "latent_compress_tflops": rl["latent_compress"]["achieved"],
         "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
         "accepted_mean": float(n_host.mean()),
@@ -363,14 +398,16 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        cb = cpu_baseline(w, comp, ver, acc, 0 if mode == "greedy" else 1, lm, accl)
+        cb = cpu_baseline(w, comp, ver, acc, 0 if mode == "greedy" else 1, lm, accl, dr)
         cpu_step = cb["verify_s"] + cb["accept_s"]
         result["cpu_baseline"] = {
             "value": kv_bytes / cpu_step / 1e12, "unit": "TB/s", "cores": cb["threads"],
             "kind": "oracle", "sample": cb["sample"],
             "verify_step_s": cpu_step, "latent_compress_s": cb["compress_s"],
             "lm_head_s": cb["lm_head_s"], "accept_logits_s": cb["accept_logits_s"],
-            "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"] + cb["accept_logits_s"],
+            "draft_layer_s": cb["draft_layer_s"],
+            "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"] + cb["accept_logits_s"]
+                            + cb["draft_layer_s"],
         }
     print(json.dumps(result), flush=True)
 

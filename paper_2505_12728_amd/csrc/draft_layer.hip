@@ -81,17 +81,23 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   floatx4 acc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = floatx4{0.f, 0.f, 0.f, 0.f};
-  if (ch0 < ch1) issue(ch0, 0);
-#pragma unroll 1
-  for (int n = ch0; n < ch1; ++n) {
-    const int buf = (n - ch0) & 1;
-    u32x4 wf[8];
+  // the weights of chunk n + 1 are loaded before chunk n is multiplied, so
+  // two chunks of every lane's row are in flight
+  auto wload = [&](u32x4 (&wf)[8], int n) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) wf[i] = wsrc[(size_t)n * 32 + i];
-    // the weight loads are the newest: this thread's copies of chunk n have
-    // landed; after the barrier every wave's have, and every wave is done
-    // reading the other buffer
-    wait_vm_then_barrier<8>();
+  };
+  auto step = [&](const u32x4 (&wf)[8], u32x4 (&wnext)[8], int n) {
+    const int buf = (n - ch0) & 1;
+    if (n + 1 < ch1) {
+      wload(wnext, n + 1);
+      // the next weights are the 8 newest loads: this thread's copies of
+      // chunk n (and its weights) have landed; after the barrier every
+      // wave's have, and every wave is done reading the other buffer
+      wait_vm_then_barrier<8>();
+    } else {
+      wait_vm_then_barrier<0>();
+    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       Pack8 x;
@@ -105,6 +111,16 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
       }
     }
     if (n + 1 < ch1) issue(n + 1, buf ^ 1);
+  };
+  u32x4 wa[8], wb[8];
+  if (ch0 < ch1) {
+    wload(wa, ch0);
+    issue(ch0, 0);
+  }
+#pragma unroll 1
+  for (int n = ch0; n < ch1; n += 2) {
+    step(wa, wb, n);
+    if (n + 1 < ch1) step(wb, wa, n + 1);
   }
   // accumulator element i of lane (c, G): input row rb*16 + c, column n0 + 4G + i
 #pragma unroll
@@ -142,56 +158,85 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 
 // y = sum of splits (+ bias) (+ residual), written as fp32 `out` [R, N].
 // With `norm_w`, also h = y / sqrt(mean(y^2) + eps) * norm_w in bf16.
-// One work-group per row.
-__global__ __launch_bounds__(kEpiThreads) void epi_add_norm(const float* part, int ksplit, int R, int N,
+// One work-group of 1024 threads per row, four columns per access when the
+// row allows (N % 4 == 0 and 16-byte aligned bias, residual and out).
+constexpr int kRowThreads = 1024;
+__global__ __launch_bounds__(kRowThreads) void epi_add_norm(const float* part, int ksplit, int R, int N,
                                                             const float* bias, const float* residual,
                                                             float* out, const float* norm_w, float eps,
                                                             __bf16* h) {
-  __shared__ float red[kEpiThreads / 64];
+  __shared__ float red[kRowThreads / 64];
   const int r = blockIdx.x;
   const size_t stride = (size_t)R * N;
+  const size_t row = (size_t)r * N;
   float ss = 0.f;
-  for (int n = threadIdx.x; n < N; n += kEpiThreads) {
-    const size_t idx = (size_t)r * N + n;
-    float y = split_sum(part, ksplit, stride, idx);
-    if (bias) y += bias[n];
-    if (residual) y += residual[idx];
-    out[idx] = y;
-    ss += y * y;
+  auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  const bool vec = (N & 3) == 0 && a16(part) && a16(out) && (!bias || a16(bias)) && (!residual || a16(residual));
+  if (vec) {
+    for (int n = threadIdx.x * 4; n < N; n += kRowThreads * 4) {
+      floatx4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+      for (int ks = 0; ks < ksplit; ++ks) y += *reinterpret_cast<const floatx4*>(part + ks * stride + row + n);
+      if (bias) y += *reinterpret_cast<const floatx4*>(bias + n);
+      if (residual) y += *reinterpret_cast<const floatx4*>(residual + row + n);
+      *reinterpret_cast<floatx4*>(out + row + n) = y;
+      ss += y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+    }
+  } else {
+    for (int n = threadIdx.x; n < N; n += kRowThreads) {
+      float y = split_sum(part, ksplit, stride, row + n);
+      if (bias) y += bias[n];
+      if (residual) y += residual[row + n];
+      out[row + n] = y;
+      ss += y * y;
+    }
   }
   if (norm_w == nullptr) return;
   const float inv = 1.f / sqrtf(block_sum(ss, red) / (float)N + eps);
-  for (int n = threadIdx.x; n < N; n += kEpiThreads) {
-    const size_t idx = (size_t)r * N + n;
-    h[idx] = float_to_bf16(out[idx] * inv * norm_w[n]);
-  }
+  for (int n = threadIdx.x; n < N; n += kRowThreads) h[row + n] = float_to_bf16(out[row + n] * inv * norm_w[n]);
 }
 
 // Fused projection output of row r (sequence b = r / rows, j = r % rows,
 // position p = pos[b] + j): query heads rotated into q [R, Hq, D] (bf16),
 // key heads rotated and value heads copied into the caches at position p
 // (skipped when p is outside 0 .. Lmax - 1).  Half-split pairs (i, i + D/2)
-// turn by p theta^(-2i/D), the angle formed in float64.  Row 0 of each
-// sequence also writes kv_len[b] = pos[b] + rows for the attention.
+// turn by p theta^(-2i/D): the frequencies are formed once per work-group
+// in float64, the angle p f in float64 is reduced to [-pi, pi] in float64,
+// and only the sine and cosine of the reduced angle are taken in float32
+// (an error of a few float32 ulp at any position).  Row 0 of each sequence
+// also writes kv_len[b] = pos[b] + rows for the attention.
 __global__ __launch_bounds__(kEpiThreads) void epi_rope_qkv(const float* part, int ksplit, int R, int N,
                                                             const int32_t* pos, int rows, int Hq, int Hkv,
                                                             int D, double log_theta, int Lmax, __bf16* q,
                                                             __bf16* kc, __bf16* vc, int32_t* kv_len) {
-  const int r = blockIdx.x;
+  __shared__ float2 rot[64];                   // (cos, sin) of each pair's angle
+  const int r = blockIdx.y;
   const int b = r / rows, j = r - b * rows;
   const int p = pos[b] + j;
   const bool store = p >= 0 && p < Lmax;
-  if (j == 0 && threadIdx.x == 0) kv_len[b] = pos[b] + rows;
+  if (j == 0 && blockIdx.x == 0 && threadIdx.x == 0) kv_len[b] = pos[b] + rows;
   const size_t stride = (size_t)R * N;
   const int half = D / 2;
+  if (threadIdx.x < half) {
+    const double f = exp(-2.0 * (double)threadIdx.x / (double)D * log_theta);
+    const double ang = (double)p * f;
+    const double twopi = 6.283185307179586476925286766559;
+    const float red = (float)(ang - twopi * rint(ang / twopi));
+    float sn, cs;
+    sincosf(red, &sn, &cs);
+    rot[threadIdx.x] = make_float2(cs, sn);
+  }
+  __syncthreads();
+  // thread t of the row: pair t (query and key heads), then value element
+  // t - pairs
   const int pairs = (Hq + Hkv) * half;
-  for (int t = threadIdx.x; t < pairs; t += kEpiThreads) {
+  const int t = blockIdx.x * kEpiThreads + threadIdx.x;
+  if (t < pairs) {
     const int hh = t / half, i = t - hh * half;
     const size_t base = (size_t)r * N + (size_t)hh * D;
     const float x0 = split_sum(part, ksplit, stride, base + i);
     const float x1 = split_sum(part, ksplit, stride, base + i + half);
-    const double ang = (double)p * exp(-2.0 * (double)i / (double)D * log_theta);
-    const float cs = (float)cos(ang), sn = (float)sin(ang);
+    const float cs = rot[i].x, sn = rot[i].y;
     const float y0 = x0 * cs - x1 * sn, y1 = x1 * cs + x0 * sn;
     if (hh < Hq) {
       __bf16* dst = q + ((size_t)r * Hq + hh) * D;
@@ -202,10 +247,8 @@ __global__ __launch_bounds__(kEpiThreads) void epi_rope_qkv(const float* part, i
       dst[i] = float_to_bf16(y0);
       dst[i + half] = float_to_bf16(y1);
     }
-  }
-  if (!store) return;
-  for (int t = threadIdx.x; t < Hkv * D; t += kEpiThreads) {
-    const int hv = t / D, e = t - hv * D;
+  } else if (store && t < pairs + Hkv * D) {
+    const int hv = (t - pairs) / D, e = (t - pairs) - hv * D;
     const float v = split_sum(part, ksplit, stride, (size_t)r * N + (size_t)(Hq + Hkv + hv) * D + e);
     vc[(((size_t)b * Lmax + p) * Hkv + hv) * D + e] = float_to_bf16(v);
   }
@@ -253,12 +296,21 @@ LinearPlan plan_linear(int R, int K, int N, int cus) {
   const int rows = std::min(R, kLinearRowsPerPass);
   p.row_blocks = (rows + 15) / 16;
   p.passes = (R + kLinearRowsPerPass - 1) / kLinearRowsPerPass;
-  p.waves = 4;
-  const long long groups = (long long)((N + p.waves * 16 - 1) / (p.waves * 16)) * p.passes;
+  // work-groups resident per compute unit: LDS (two input chunks of
+  // row_blocks * 8 KB) and 32 waves
+  const int lds_fit = (160 * 1024) / (p.row_blocks * 16 * 1024);
+  auto resident = [&](int waves) {
+    return (long long)std::max(cus, 1) * std::max(1, std::min(lds_fit, 32 / waves));
+  };
+  auto groups = [&](int waves) { return (long long)((N + waves * 16 - 1) / (waves * 16)) * p.passes; };
+  // eight waves per work-group (128 output columns), each chunk of the
+  // inputs copied once for all of them
+  p.waves = 8;
+  const long long g = groups(p.waves), cap = resident(p.waves);
   const int nch = K / kChunkK;
-  // split the reduction until about two work-groups per compute unit exist,
-  // keeping at least four chunks per split
-  long long ks = (2LL * std::max(cus, 1) + groups - 1) / groups;
+  // split the reduction to fill the resident slots in one round, keeping
+  // at least four chunks per split
+  long long ks = std::max(1LL, cap / g);
   ks = std::min<long long>(ks, std::max(1, nch / 4));
   p.ksplit = (int)std::max(1LL, std::min<long long>(ks, kLinearMaxSplits));
   p.part_bytes = (size_t)p.ksplit * R * N * sizeof(float);
@@ -266,12 +318,13 @@ LinearPlan plan_linear(int R, int K, int N, int cus) {
 }
 
 hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipStream_t st) {
-  return launch_partial_nw<4>(a, p.row_blocks, p.passes, st);
+  return p.waves == 8 ? launch_partial_nw<8>(a, p.row_blocks, p.passes, st)
+                      : launch_partial_nw<4>(a, p.row_blocks, p.passes, st);
 }
 
 hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias, const float* residual,
                           float* out, hipStream_t st) {
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, ksplit, R, N, bias, residual, out,
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, ksplit, R, N, bias, residual, out,
                      nullptr, 0.f, nullptr);
   return hipGetLastError();
 }
@@ -328,11 +381,12 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   };
   // x0 = FC(u), h = RMSNorm(x0)
   if ((e = lin(a.u, a.fc_w, 2 * d, d, p.fc)) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
                      (const float*)nullptr, x0, a.ln1, a.eps, h);
   // q, k, v with RoPE; k, v appended to the cache
   if ((e = lin(h, a.wqkv, d, nqkv, p.qkv)) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_rope_qkv, dim3(R), dim3(kEpiThreads), 0, st, part, p.qkv.ksplit, R, nqkv, a.pos, a.r,
+  const int rope_threads = (a.Hq + a.Hkv) * (D / 2) + a.Hkv * D;
+  hipLaunchKernelGGL(epi_rope_qkv, dim3((rope_threads + kEpiThreads - 1) / kEpiThreads, R), dim3(kEpiThreads), 0, st, part, p.qkv.ksplit, R, nqkv, a.pos, a.r,
                      a.Hq, a.Hkv, D, log((double)a.theta), a.Lmax, q,
                      static_cast<__bf16*>(a.k_cache), static_cast<__bf16*>(a.v_cache), kv_len);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -361,7 +415,7 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
                      attn, attn16, na);
   // x1 = x0 + attn Wo^T, h = RMSNorm(x1)
   if ((e = lin(attn16, a.wo, a.Hq * D, d, p.o)) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kEpiThreads), 0, st, part, p.o.ksplit, R, d,
+  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.o.ksplit, R, d,
                      (const float*)nullptr, x0, x1, a.ln2, a.eps, h);
   // act = SwiGLU(h), out = x1 + act Wdown^T
   if ((e = lin(h, a.wgu, d, 2 * a.I, p.gu)) != hipSuccess) return e;

@@ -26,7 +26,8 @@ reader can check it against the paper by eye:
   one step of the draft's semi-autoregressive layer over its cached context:
   the fully connected fusion of feature and embedding, then one pre-norm
   decoder layer whose placeholder rows give the next K draft states
-  (Sec. 3.1, Sec. 3.3, Algorithm 1, Sec. 4.4).
+  (Sec. 3.1, Sec. 3.3, Algorithm 1, Sec. 4.4); ``semi_ar_draft`` runs K
+  drafts in K / k' passes of k' (the group size of the paper's ablation).
 
 Readings of points the paper leaves open are stated in each module.  No
 function here is "parity unpinned": every one is checked in
@@ -38,7 +39,7 @@ from .compress import latent_compress, softmax_rows
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
-from .draft_layer import rms_norm, rope, linear, silu, swiglu, semi_ar_layer
+from .draft_layer import rms_norm, rope, linear, silu, swiglu, semi_ar_layer, semi_ar_draft, bf16_round
 from .accept import (
     spec_accept,
     spec_accept_one,
@@ -79,4 +80,6 @@ __all__ = [
     "silu",
     "swiglu",
     "semi_ar_layer",
+    "semi_ar_draft",
+    "bf16_round",
 ]

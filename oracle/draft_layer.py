@@ -118,3 +118,58 @@ def semi_ar_layer(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta):
     x1 = linear(attn.reshape(B * r, hq * D), W["wo"], residual=x0)
     out = linear(swiglu(linear(rms_norm(x1, W["ln2"], eps), W["wgu"])), W["wdown"], residual=x1)
     return out.reshape(B, r, d), kc, vc
+
+
+def bf16_round(x):
+    """Round float64 values to the nearest bfloat16 value (ties to even),
+    returned as float64: the precision the layer's inputs are stored in."""
+    f = np.asarray(x, dtype=np.float32)
+    bits = f.view(np.uint32).astype(np.uint64)
+    bits = (bits + 0x7FFF + ((bits >> 16) & 1)) >> 16 << 16
+    return bits.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, hq, hkv, eps, theta, tau,
+                  uniforms, K, kp, tokens=None):
+    """K drafts in K / k' passes of the semi-AR layer, k' per pass (the group
+    size k' of the paper's ablation, Appendix).
+
+    Pass 0 runs the layer on u0 [B, r0, 2d], whose last k' rows are
+    placeholders, at positions pos .. pos + r0 - 1.  After each pass the
+    LM head gives the k' placeholder rows' distributions at temperature tau
+    (their states rounded to bf16, the head's input precision)
+    and one token is drawn per row (``sample_tokens`` with the uniforms of
+    those positions, uniforms [B, K]).  The next pass takes 2k' rows: the k'
+    drafted tokens, each with input concat(F', E[token]) where F' is the
+    output state of the placeholder that drafted it (rounded to bf16, the
+    layer's input precision), at that placeholder's position, followed by
+    k' placeholder rows (input ph [2d]).  With ``tokens`` [B, K] given, those
+    tokens are fed back instead of the drawn ones (the distributions are
+    still those of the pass).  Returns (tokens [B, K], q [B, K, V]).
+    """
+    from .lm_head import lm_head_probs, sample_tokens
+    u = np.asarray(u0, dtype=np.float64)
+    B, r, _ = u.shape
+    d = u.shape[2] // 2
+    emb = np.asarray(emb, dtype=np.float64)
+    ph = np.asarray(ph, dtype=np.float64)
+    uniforms = np.asarray(uniforms, dtype=np.float32)
+    V = np.asarray(lm_w).shape[0]
+    kc, vc = k_cache, v_cache
+    p = np.asarray(pos, dtype=np.int64).copy()
+    out_tok = np.zeros((B, K), dtype=np.int32)
+    out_q = np.zeros((B, K, V), dtype=np.float64)
+    for t in range(K // kp):
+        out, kc, vc = semi_ar_layer(u, weights, kc, vc, p, hq, hkv, eps, theta)
+        hid = bf16_round(out[:, r - kp:]).reshape(B * kp, d)   # the head's input precision
+        q = lm_head_probs(hid, lm_w, tau).reshape(B, kp, V)
+        drawn = sample_tokens(q.reshape(B * kp, V).astype(np.float32),
+                              uniforms[:, t * kp:(t + 1) * kp].reshape(-1)).reshape(B, kp)
+        tok = drawn if tokens is None else np.asarray(tokens)[:, t * kp:(t + 1) * kp]
+        out_tok[:, t * kp:(t + 1) * kp] = tok
+        out_q[:, t * kp:(t + 1) * kp] = q
+        text = np.concatenate([bf16_round(out[:, r - kp:]), emb[tok]], axis=-1)
+        u = np.concatenate([text, np.broadcast_to(ph, (B, kp, 2 * d))], axis=1)
+        p = p + (r - kp)
+        r = 2 * kp
+    return out_tok, out_q

@@ -937,3 +937,65 @@ def test_draft_layer_brute_force():
         act = [gu[i] / (1 + math.exp(-gu[i])) * gu[I + i] for i in range(I)]
         x2 = [a + b for a, b in zip(x1, mv(W["wdown"].tolist(), act))]
         assert np.allclose(out[0, j], x2, rtol=1e-12, atol=1e-12), j
+
+
+def _kp_case(seed, B=2, r0=3, kp=2, d=8, V=11):
+    u0, W, kc, vc, pos = _draft_case(seed, B=B, r=r0, Lmax=16)
+    rng = np.random.default_rng(seed + 100)
+    u0 = u0.copy()
+    ph = rng.normal(size=2 * d)
+    u0[:, r0 - kp:] = ph                                   # the last k' rows are placeholders
+    lm_w = rng.normal(size=(V, d)) * 3 / np.sqrt(d)
+    emb = rng.normal(size=(V, d))
+    return u0, W, kc, vc, pos, ph, lm_w, emb
+
+
+def test_bf16_round_matches_hand_values():
+    # 1 + 2^-8 is a tie between 1 and 1 + 2^-7: ties go to the even mantissa (1)
+    assert oracle.bf16_round(np.array([1.0 + 2.0 ** -8]))[0] == 1.0
+    assert oracle.bf16_round(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6
+    assert oracle.bf16_round(np.array([-2.5]))[0] == -2.5            # exact
+    assert oracle.bf16_round(np.array([1.0 + 2.0 ** -9]))[0] == 1.0  # below half an ulp
+
+
+def test_kp_draft_single_pass_is_layer_head_and_draw():
+    # k' = K: one pass; the drafts are the head's draws from the placeholder rows
+    u0, W, kc, vc, pos, ph, lm_w, emb = _kp_case(7, r0=3, kp=2)
+    uni = (np.arange(4).reshape(2, 2) * 2 ** 21 * 2.0 ** -24 + 0.1).astype(np.float32)
+    tok, q = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 0.8, uni, 2, 2)
+    out, _, _ = oracle.semi_ar_layer(u0, W, kc, vc, pos, 2, 1, 1e-6, 1e4)
+    p = oracle.lm_head_probs(oracle.bf16_round(out[:, 1:]).reshape(4, 8), lm_w, 0.8)
+    assert np.allclose(q.reshape(4, -1), p)
+    assert np.array_equal(tok.reshape(-1), oracle.sample_tokens(p.astype(np.float32), uni.reshape(-1)))
+
+
+def test_kp_draft_first_draft_independent_of_group_size():
+    # the first placeholder sees only the rows before it (causal), so its
+    # distribution is the same for every k'
+    u0, W, kc, vc, pos, ph, lm_w, emb = _kp_case(8, r0=5, kp=4)
+    uni = np.full((2, 4), 0.37, dtype=np.float32)
+    qs = []
+    for kp in (1, 2, 4):
+        u = u0[:, :1 + kp].copy()                          # one text row + k' placeholders
+        _, q = oracle.semi_ar_draft(u, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni, 4, kp)
+        qs.append(q)
+    assert np.allclose(qs[0][:, 0], qs[1][:, 0]) and np.allclose(qs[0][:, 0], qs[2][:, 0])
+    assert not np.allclose(qs[0][:, 1], qs[2][:, 1])       # later drafts do depend on k'
+
+
+def test_kp_draft_feeds_drafts_back_in_order():
+    # forced tokens: the distributions of pass t depend on the tokens of
+    # passes < t only; a later pass's uniforms never change earlier drafts
+    u0, W, kc, vc, pos, ph, lm_w, emb = _kp_case(9, r0=3, kp=2)
+    uni = np.full((2, 6), 0.5, dtype=np.float32)
+    forced = np.array([[1, 2, 3, 4, 5, 6], [7, 8, 9, 10, 0, 1]], dtype=np.int32)
+    _, qa = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni, 6, 2, forced)
+    f2 = forced.copy()
+    f2[:, 2] = (f2[:, 2] + 1) % 11                          # change a draft of pass 1
+    _, qb = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni, 6, 2, f2)
+    assert np.allclose(qa[:, :4], qb[:, :4]) and not np.allclose(qa[:, 4:], qb[:, 4:])
+    uni2 = uni.copy()
+    uni2[:, 4:] = 0.99
+    ta, _ = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni, 6, 2)
+    tb, _ = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni2, 6, 2)
+    assert np.array_equal(ta[:, :4], tb[:, :4])

@@ -370,6 +370,48 @@ int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const f
                      int Lmax, float eps, float theta, void* workspace, size_t workspace_bytes,
                      void* stream);
 
+/* ------------------------------------------------------------------------
+ * K drafts in K / k' passes of the semi-autoregressive layer, k' per pass
+ * (the group size k' of the paper's ablation, Appendix: the draft emits k'
+ * tokens per forward pass and feeds them back for the next k').
+ *
+ * Pass 0 is sd_semi_ar_layer on u0 [B, r0, 2d] at positions pos[b] ..
+ * pos[b] + r0 - 1, the last k' rows being placeholders.  After each pass the
+ * placeholder rows' states, rounded to bf16, go through the frozen LM head
+ * (softmax(h lm_w^T / temperature)) and one token per row is drawn with
+ * sd_sample_tokens' exact inverse CDF and the uniform u[b][t k' + j] (pass t,
+ * row j).  Pass t + 1 runs on 2k' rows: the k' drafted tokens, with input
+ * concat(bf16(state of the placeholder that drafted it), emb[token]), at
+ * that placeholder's position, then k' placeholder rows with input ph.
+ *
+ *   u0       [B, r0, 2d] bf16; weights as for sd_semi_ar_layer
+ *   lm_w     [V, d] bf16     frozen LM head
+ *   emb      [V, d] bf16     token embeddings
+ *   ph       [2d] bf16       input of a placeholder row
+ *   k_cache, v_cache, pos    as for sd_semi_ar_layer (the caches gain every
+ *            pass's rows; pos is not modified)
+ *   u        [B, K] float32  uniforms in [0, 1) (multiples of 2^-24)
+ *   tokens   [B, K] int32    out: the drafts
+ *   q        [B, K, V] float32  out: their distributions (the q of the
+ *            acceptance rule)
+ *   workspace  sd_semi_ar_draft_workspace_size(...) bytes, 256-byte aligned
+ *            (device-dependent)
+ * Requirements: those of sd_semi_ar_layer for r0 and, when K > k', for
+ * 2k' rows; 1 <= k' <= min(r0, 8); K % k' == 0; B * k' <= 256;
+ * 1 <= V <= 2^18; temperature > 0.  Errors as for sd_linear.
+ * ---------------------------------------------------------------------- */
+size_t sd_semi_ar_draft_workspace_size(int B, int r0, int d, int num_q_heads, int num_kv_heads,
+                                       int I, int Lmax, int V, int K, int k_prime);
+
+int sd_semi_ar_draft(const void* u0, const void* fc_w, const float* fc_b, const float* ln1,
+                     const void* wqkv, const void* wo, const float* ln2, const void* wgu,
+                     const void* wdown, const void* lm_w, const void* emb, const void* ph,
+                     void* k_cache, void* v_cache, const int32_t* pos, const float* u,
+                     int32_t* tokens, float* q, int B, int r0, int d, int num_q_heads,
+                     int num_kv_heads, int I, int Lmax, int V, int K, int k_prime, float eps,
+                     float theta, float temperature, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,6 +30,7 @@ __all__ = [
     "sd_spec_accept_logits_workspace_size", "sd_spec_accept_logits", "sd_philox_uniforms",
     "sd_linear_workspace_size", "sd_linear",
     "sd_semi_ar_layer_workspace_size", "sd_semi_ar_layer",
+    "sd_semi_ar_draft_workspace_size", "sd_semi_ar_draft",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -65,6 +66,8 @@ _SIGNATURES = {
     "sd_semi_ar_layer_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
     "sd_semi_ar_layer": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                               _i, _i, _i, _i, _i, _i, _i, _f, _f, _vp, _sz, _vp]),
+    "sd_semi_ar_draft_workspace_size": (_sz, [_i] * 10),
+    "sd_semi_ar_draft": (_i, [_vp] * 18 + [_i] * 10 + [_f, _f, _f, _vp, _sz, _vp]),
 }
 
 
@@ -451,3 +454,50 @@ def sd_semi_ar_layer(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, out
                                     _ptr(ws), ws_len, _stream(stream))
     _raise(st, "sd_semi_ar_layer")
     return out
+
+
+def sd_semi_ar_draft_workspace_size(B, r0, d, hq, hkv, I, Lmax, V, K, kp):
+    return library().sd_semi_ar_draft_workspace_size(B, r0, d, hq, hkv, I, Lmax, V, K, kp)
+
+
+def sd_semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, u, K, kp, hq, hkv, eps, theta,
+                     temperature, tokens=None, q=None, workspace=None, stream=None):
+    """K drafts in K / kp passes of the semi-AR layer.  u0 [B, r0, 2d] bf16
+    (last kp rows placeholders); weights as for sd_semi_ar_layer; lm_w and
+    emb [V, d] bf16; ph [2d] bf16; u [B, K] fp32 uniforms.  The caches are
+    updated in place.  Returns (tokens [B, K] int32, q [B, K, V] fp32)."""
+    torch = _torch()
+    _check(u0, "u0", dtype=torch.bfloat16, ndim=3)
+    B, r0, d2 = u0.shape
+    d = d2 // 2
+    _check(lm_w, "lm_w", dtype=torch.bfloat16, ndim=2)
+    _check(emb, "emb", dtype=torch.bfloat16, ndim=2)
+    _check(ph, "ph", dtype=torch.bfloat16, ndim=1)
+    _check(u, "u", dtype=torch.float32, ndim=2)
+    V = lm_w.shape[0]
+    if lm_w.shape[1] != d or tuple(emb.shape) != (V, d) or ph.shape[0] != 2 * d:
+        raise ValueError("lm_w and emb must be [V, d], ph [2d]")
+    if tuple(u.shape) != (B, K):
+        raise ValueError("u must be [B, K]")
+    for name in SEMI_AR_WEIGHTS:
+        _check(weights[name], name, dtype=torch.float32 if name in ("fc_b", "ln1", "ln2") else torch.bfloat16)
+    _check(k_cache, "k_cache", dtype=torch.bfloat16, ndim=4)
+    _check(v_cache, "v_cache", dtype=torch.bfloat16, ndim=4)
+    _check(pos, "pos", dtype=torch.int32, ndim=1)
+    Lmax = k_cache.shape[1]
+    I = weights["wdown"].shape[1]
+    if tokens is None:
+        tokens = torch.empty((B, K), dtype=torch.int32, device=u0.device)
+    if q is None:
+        q = torch.empty((B, K, V), dtype=torch.float32, device=u0.device)
+    ws_bytes = sd_semi_ar_draft_workspace_size(B, r0, d, hq, hkv, I, Lmax, V, K, kp)
+    ws, ws_len = _workspace(ws_bytes, u0.device, workspace)
+    W = weights
+    st = library().sd_semi_ar_draft(_ptr(u0), _ptr(W["fc_w"]), _ptr(W["fc_b"]), _ptr(W["ln1"]),
+                                    _ptr(W["wqkv"]), _ptr(W["wo"]), _ptr(W["ln2"]), _ptr(W["wgu"]),
+                                    _ptr(W["wdown"]), _ptr(lm_w), _ptr(emb), _ptr(ph), _ptr(k_cache),
+                                    _ptr(v_cache), _ptr(pos), _ptr(u), _ptr(tokens), _ptr(q),
+                                    B, r0, d, hq, hkv, I, Lmax, V, K, kp, float(eps), float(theta),
+                                    float(temperature), _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_semi_ar_draft")
+    return tokens, q

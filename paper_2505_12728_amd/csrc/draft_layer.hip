@@ -272,6 +272,49 @@ __global__ __launch_bounds__(kEpiThreads) void to_bf16(const float* x, __bf16* y
   if (i < n) y[i] = float_to_bf16(x[i]);
 }
 
+// ------------------------------------------------- K drafts in K / k' passes
+// Before the head: the k' placeholder rows of a pass's output (rows
+// r - k' .. r - 1 of each sequence) rounded to bf16 as the LM head's input
+// rows (b, j), and this pass's uniforms u[b][t k' + j] gathered.
+__global__ __launch_bounds__(kEpiThreads) void kp_prep(const float* out, int r, int kp, int d, const float* u,
+                                                       int K, int t, __bf16* hid, float* ut) {
+  const int row = blockIdx.x;
+  const int b = row / kp, j = row - b * kp;
+  const float* src = out + ((size_t)b * r + (r - kp + j)) * d;
+  for (int e = threadIdx.x; e < d; e += kEpiThreads) hid[(size_t)row * d + e] = float_to_bf16(src[e]);
+  if (threadIdx.x == 0) ut[row] = u[(size_t)b * K + (size_t)t * kp + j];
+}
+
+// After the draw: row (b, j)'s token and distribution to the outputs at
+// draft t k' + j; with another pass to come, the next pass's rows of
+// sequence b (the drafted token, concat(bf16(F'), E[token]), then a
+// placeholder row) and its positions pos_out[b] = pos_in[b] + advance.
+// Token ids outside the vocabulary read the nearest embedding row.
+__global__ __launch_bounds__(kEpiThreads) void kp_post(const float* probs, const int32_t* tok, int kp, int K,
+                                                       int t, int V, int d, const __bf16* hid, const __bf16* emb,
+                                                       const __bf16* ph, int32_t* tokens, float* q, __bf16* unext,
+                                                       const int32_t* pos_in, int advance, int32_t* pos_out,
+                                                       int more) {
+  const int row = blockIdx.x;
+  const int b = row / kp, j = row - b * kp;
+  const int token = tok[row];
+  const size_t dst = (size_t)b * K + (size_t)t * kp + j;
+  if (threadIdx.x == 0) tokens[dst] = token;
+  const float* src = probs + (size_t)row * V;
+  float* qd = q + dst * V;
+  for (int v = threadIdx.x; v < V; v += kEpiThreads) qd[v] = src[v];
+  if (!more) return;
+  const int tk = min(max(token, 0), V - 1);
+  __bf16* text = unext + ((size_t)b * 2 * kp + j) * 2 * d;
+  __bf16* place = unext + ((size_t)b * 2 * kp + kp + j) * 2 * d;
+  for (int e = threadIdx.x; e < d; e += kEpiThreads) {
+    text[e] = hid[(size_t)row * d + e];
+    text[d + e] = emb[(size_t)tk * d + e];
+  }
+  for (int e = threadIdx.x; e < 2 * d; e += kEpiThreads) place[e] = ph[e];
+  if (j == 0 && threadIdx.x == 0) pos_out[b] = pos_in[b] + advance;
+}
+
 template <int NW>
 hipError_t launch_partial_nw(const LinearArgs& a, int rb, int passes, hipStream_t st) {
   const dim3 grid((a.N + NW * 16 - 1) / (NW * 16), a.ksplit, passes);
@@ -423,6 +466,84 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
                      p.gu.ksplit, R, a.I, act);
   if ((e = lin(act, a.wdown, a.I, d, p.down)) != hipSuccess) return e;
   return launch_epi_add(part, p.down.ksplit, R, d, nullptr, x1, a.out, st);
+}
+
+}  // namespace sd
+
+namespace sd {
+
+SemiArDraftPlan plan_semi_ar_draft(int B, int r0, int d, int Hq, int Hkv, int I, int Lmax, int V, int K, int kp,
+                                   int cus) {
+  SemiArDraftPlan p{};
+  p.first = plan_semi_ar(B, r0, d, Hq, Hkv, I, Lmax, cus);
+  p.later = K > kp ? plan_semi_ar(B, 2 * kp, d, Hq, Hkv, I, Lmax, cus) : p.first;
+  const int rmax = std::max(r0, 2 * kp), R = B * kp;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += align256(bytes); return o; };
+  p.off_layer = take(std::max(p.first.workspace_bytes, p.later.workspace_bytes));
+  p.off_out = take((size_t)B * rmax * d * 4);
+  p.off_unext = take((size_t)B * 2 * kp * 2 * d * 2);
+  p.off_hid = take((size_t)R * d * 2);
+  p.off_probs = take((size_t)R * V * 4);
+  p.off_lmstats = take(lm_head_workspace_bytes(R, V));
+  p.off_sample = take(accept_workspace_bytes(R, 0, V, 1));
+  p.off_nacc = take((size_t)R * 4);
+  p.off_ut = take((size_t)R * 4);
+  p.off_tok = take((size_t)R * 4);
+  p.off_pos = take((size_t)2 * B * 4);
+  p.workspace_bytes = off;
+  p.ok = p.first.ok && p.later.ok;
+  return p;
+}
+
+hipError_t launch_semi_ar_draft(const SemiArDraftArgs& a, const SemiArDraftPlan& p, hipStream_t st) {
+  unsigned char* ws = static_cast<unsigned char*>(a.workspace);
+  float* out = reinterpret_cast<float*>(ws + p.off_out);
+  __bf16* unext = reinterpret_cast<__bf16*>(ws + p.off_unext);
+  __bf16* hid = reinterpret_cast<__bf16*>(ws + p.off_hid);
+  float* probs = reinterpret_cast<float*>(ws + p.off_probs);
+  float* ut = reinterpret_cast<float*>(ws + p.off_ut);
+  int32_t* tok = reinterpret_cast<int32_t*>(ws + p.off_tok);
+  int32_t* posbuf = reinterpret_cast<int32_t*>(ws + p.off_pos);
+  const int B = a.layer.B, d = a.layer.d, kp = a.kp, R = B * kp;
+  const int passes = a.K / kp;
+  hipError_t e;
+  for (int t = 0; t < passes; ++t) {
+    SemiArArgs la = a.layer;
+    la.r = t == 0 ? a.layer.r : 2 * kp;
+    la.u = t == 0 ? a.layer.u : unext;
+    la.pos = t == 0 ? a.layer.pos : posbuf + (t & 1) * B;
+    la.out = out;
+    la.workspace = ws + p.off_layer;
+    if ((e = launch_semi_ar(la, t == 0 ? p.first : p.later, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(kp_prep, dim3(R), dim3(kEpiThreads), 0, st, out, la.r, kp, d, a.u, a.K, t, hid, ut);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    LmHeadArgs lh{};
+    lh.hidden = hid;
+    lh.weight = a.lm_w;
+    lh.probs = probs;
+    lh.R = R;
+    lh.d = d;
+    lh.V = a.V;
+    lh.scale_log2 = kLog2e / a.temperature;
+    lh.stats = reinterpret_cast<float*>(ws + p.off_lmstats);
+    if ((e = launch_lm_head(lh, 1, st)) != hipSuccess) return e;
+    AcceptArgs sa{};
+    sa.p = probs;
+    sa.u = ut;
+    sa.n_accepted = reinterpret_cast<int32_t*>(ws + p.off_nacc);
+    sa.tokens = tok;
+    sa.B = R;
+    sa.k = 0;
+    sa.V = a.V;
+    sa.mode = 1;
+    if ((e = launch_accept(sa, ws + p.off_sample, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(kp_post, dim3(R), dim3(kEpiThreads), 0, st, probs, tok, kp, a.K, t, a.V, d, hid,
+                       static_cast<const __bf16*>(a.emb), static_cast<const __bf16*>(a.ph), a.tokens, a.q, unext,
+                       la.pos, la.r - kp, posbuf + ((t + 1) & 1) * B, (int)(t + 1 < passes));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace sd

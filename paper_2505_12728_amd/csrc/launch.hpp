@@ -170,4 +170,31 @@ struct SemiArPlan {
 SemiArPlan plan_semi_ar(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, int cus);
 hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t s);
 
+// K drafts in K / kp passes: pass 0 on layer.u (layer.r rows, the last kp
+// placeholders), later passes on 2 kp rows built on the device
+struct SemiArDraftArgs {
+  SemiArArgs layer;      // layer.out and layer.workspace are set per pass
+  const void* lm_w;      // [V, d] bf16
+  const void* emb;       // [V, d] bf16
+  const void* ph;        // [2d] bf16 placeholder input
+  const float* u;        // [B, K]
+  int32_t* tokens;       // [B, K]
+  float* q;              // [B, K, V]
+  int V, K, kp;
+  float temperature;
+  void* workspace;
+};
+
+struct SemiArDraftPlan {
+  SemiArPlan first, later;
+  size_t off_layer, off_out, off_unext, off_hid, off_probs, off_lmstats, off_sample, off_nacc, off_ut, off_tok,
+      off_pos;
+  size_t workspace_bytes;
+  bool ok;
+};
+
+SemiArDraftPlan plan_semi_ar_draft(int B, int r0, int d, int Hq, int Hkv, int I, int Lmax, int V, int K, int kp,
+                                   int cus);
+hipError_t launch_semi_ar_draft(const SemiArDraftArgs& a, const SemiArDraftPlan& p, hipStream_t s);
+
 }  // namespace sd

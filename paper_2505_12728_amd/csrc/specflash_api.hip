@@ -410,3 +410,83 @@ int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const f
   a.workspace = workspace;
   return status_from(sd::launch_semi_ar(a, plan, static_cast<hipStream_t>(stream)));
 }
+
+static bool semi_ar_draft_ok(int B, int r0, int d, int Hq, int Hkv, int I, int Lmax, int V, int K, int kp,
+                             int* status) {
+  if (!semi_ar_shape_ok(B, r0, d, Hq, Hkv, I, Lmax, status)) return false;
+  *status = SD_ERR_INVALID_ARG;
+  if (V < 1 || K < 1 || kp < 1 || kp > r0 || K % kp != 0) return false;
+  *status = SD_ERR_UNSUPPORTED;
+  if (kp > 8 || V > (1 << 18) || (long long)B * kp > 256 || (long long)B * K * V > (1LL << 40)) return false;
+  if (K > kp && !semi_ar_shape_ok(B, 2 * kp, d, Hq, Hkv, I, Lmax, status)) return false;
+  *status = SD_OK;
+  return true;
+}
+
+size_t sd_semi_ar_draft_workspace_size(int B, int r0, int d, int num_q_heads, int num_kv_heads, int I, int Lmax,
+                                       int V, int K, int k_prime) {
+  int st;
+  if (!semi_ar_draft_ok(B, r0, d, num_q_heads, num_kv_heads, I, Lmax, V, K, k_prime, &st)) return 0;
+  const sd::SemiArDraftPlan plan =
+      sd::plan_semi_ar_draft(B, r0, d, num_q_heads, num_kv_heads, I, Lmax, V, K, k_prime, device_cus());
+  return plan.ok ? plan.workspace_bytes : 0;
+}
+
+int sd_semi_ar_draft(const void* u0, const void* fc_w, const float* fc_b, const float* ln1, const void* wqkv,
+                     const void* wo, const float* ln2, const void* wgu, const void* wdown, const void* lm_w,
+                     const void* emb, const void* ph, void* k_cache, void* v_cache, const int32_t* pos,
+                     const float* u, int32_t* tokens, float* q, int B, int r0, int d, int num_q_heads,
+                     int num_kv_heads, int I, int Lmax, int V, int K, int k_prime, float eps, float theta,
+                     float temperature, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = SD_OK;
+  if (!semi_ar_draft_ok(B, r0, d, num_q_heads, num_kv_heads, I, Lmax, V, K, k_prime, &st)) return st;
+  if (!u0 || !fc_w || !fc_b || !ln1 || !wqkv || !wo || !ln2 || !wgu || !wdown || !lm_w || !emb || !ph ||
+      !k_cache || !v_cache || !pos || !u || !tokens || !q || !isfinite(eps) || eps < 0.f || !isfinite(theta) ||
+      theta <= 0.f || !isfinite(temperature) || !(temperature > 0.f))
+    return SD_ERR_INVALID_ARG;
+  const void* a16[] = {u0, fc_w, wqkv, wo, wgu, wdown, lm_w, emb, k_cache, v_cache};
+  for (const void* p : a16)
+    if (!aligned(p, 16)) return SD_ERR_INVALID_ARG;
+  const void* a4[] = {fc_b, ln1, ln2, pos, u, tokens, q};
+  for (const void* p : a4)
+    if (!aligned(p, 4)) return SD_ERR_INVALID_ARG;
+  if (!aligned(ph, 2)) return SD_ERR_INVALID_ARG;
+  const sd::SemiArDraftPlan plan =
+      sd::plan_semi_ar_draft(B, r0, d, num_q_heads, num_kv_heads, I, Lmax, V, K, k_prime, device_cus());
+  if (!plan.ok) return SD_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned(workspace, 256)) return SD_ERR_WORKSPACE;
+  sd::SemiArDraftArgs a{};
+  a.layer.u = u0;
+  a.layer.fc_w = fc_w;
+  a.layer.fc_b = fc_b;
+  a.layer.ln1 = ln1;
+  a.layer.wqkv = wqkv;
+  a.layer.wo = wo;
+  a.layer.ln2 = ln2;
+  a.layer.wgu = wgu;
+  a.layer.wdown = wdown;
+  a.layer.k_cache = k_cache;
+  a.layer.v_cache = v_cache;
+  a.layer.pos = pos;
+  a.layer.B = B;
+  a.layer.r = r0;
+  a.layer.d = d;
+  a.layer.Hq = num_q_heads;
+  a.layer.Hkv = num_kv_heads;
+  a.layer.I = I;
+  a.layer.Lmax = Lmax;
+  a.layer.eps = eps;
+  a.layer.theta = theta;
+  a.lm_w = lm_w;
+  a.emb = emb;
+  a.ph = ph;
+  a.u = u;
+  a.tokens = tokens;
+  a.q = q;
+  a.V = V;
+  a.K = K;
+  a.kp = k_prime;
+  a.temperature = temperature;
+  a.workspace = workspace;
+  return status_from(sd::launch_semi_ar_draft(a, plan, static_cast<hipStream_t>(stream)));
+}

@@ -477,3 +477,16 @@ def draft_bytes(w):
     params = d * 2 * d + (hq + 2 * hkv) * D * d + d * hq * D + 2 * I * d + d * I
     ctx = sum(w.draft_ctx + 3 * b + r for b in range(B))
     return 2 * params + B * r * (2 * d * 2 + d * 4) + ctx * 2 * hkv * D * 2
+
+
+def draft_kp_bytes(w, kp):
+    """Algorithmic HBM bytes of K = block drafts in K / kp passes: per pass
+    the draft layer's weights once (and its rows and cache traffic), the
+    LM head weight once and the kp rows' distributions written once."""
+    B, r, d, hq, hkv, I, Lmax = draft_dims(w)
+    D = d // hq
+    passes = w.block // kp
+    params = d * 2 * d + (hq + 2 * hkv) * D * d + d * hq * D + 2 * I * d + d * I
+    per_pass = 2 * params + 2 * w.vocab * d + B * kp * w.vocab * 4
+    ctx = sum(w.draft_ctx + 3 * b + r for b in range(B))
+    return passes * per_pass + ctx * 2 * hkv * D * 2

@@ -267,3 +267,32 @@ def test_semi_ar_layer_validation_errors(lib):
     assert call(wsb=64) == sd.SD_ERR_WORKSPACE
     assert lib.sd_semi_ar_layer_workspace_size(2, 9, 1024, 8, 2, 2048, 64) > 2 * 9 * 2048 * 2
     assert lib.sd_semi_ar_layer_workspace_size(2, 17, 1024, 8, 2, 2048, 64) == 0
+
+
+def test_semi_ar_draft_validation_errors(lib):
+    keep, ptrs = _fake(15)
+    f = lib.sd_semi_ar_draft
+    names = ["u0", "fcw", "fcb", "ln1", "wqkv", "wo", "ln2", "wgu", "wdown", "lmw", "emb", "ph", "kc", "vc",
+             "pos"]
+    P = dict(zip(names, ptrs))
+    keep2, (uu, tok, q, ws) = _fake(4)
+    P.update(u=uu, tok=tok, q=q, ws=ws)
+
+    def call(B=2, r0=3, d=1024, hq=8, hkv=2, I=2048, L=64, V=1000, K=6, kp=2, eps=1e-6, theta=1e4, tau=0.8,
+             wsb=0, **kw):
+        p = dict(P, **kw)
+        return f(*[p[n] for n in names], p["u"], p["tok"], p["q"], B, r0, d, hq, hkv, I, L, V, K, kp, eps, theta,
+                 tau, p["ws"], wsb, None)
+
+    assert call(lmw=None) == sd.SD_ERR_INVALID_ARG
+    assert call(q=None) == sd.SD_ERR_INVALID_ARG
+    assert call(K=5) == sd.SD_ERR_INVALID_ARG                  # K % k'
+    assert call(kp=4) == sd.SD_ERR_INVALID_ARG                 # k' > r0
+    assert call(kp=0) == sd.SD_ERR_INVALID_ARG
+    assert call(r0=12, kp=9, K=9) == sd.SD_ERR_UNSUPPORTED     # k' > 8
+    assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
+    assert call(B=200, kp=2) == sd.SD_ERR_UNSUPPORTED          # B k' > 256
+    assert call(tau=0.0) == sd.SD_ERR_INVALID_ARG
+    assert call(ws=None) == sd.SD_ERR_WORKSPACE
+    assert lib.sd_semi_ar_draft_workspace_size(2, 3, 1024, 8, 2, 2048, 64, 1000, 6, 2) > 0
+    assert lib.sd_semi_ar_draft_workspace_size(2, 3, 1024, 8, 2, 2048, 64, 1000, 5, 2) == 0

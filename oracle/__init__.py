@@ -39,7 +39,8 @@ from .compress import latent_compress, softmax_rows
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
-from .draft_layer import rms_norm, rope, linear, silu, swiglu, semi_ar_layer, semi_ar_draft, bf16_round
+from .draft_layer import (rms_norm, rope, linear, silu, swiglu, semi_ar_layer, semi_ar_draft, bf16_round,
+                          dequantize_rows, linear_q8, semi_ar_layer_q8)
 from .accept import (
     spec_accept,
     spec_accept_one,
@@ -82,4 +83,7 @@ __all__ = [
     "semi_ar_layer",
     "semi_ar_draft",
     "bf16_round",
+    "dequantize_rows",
+    "linear_q8",
+    "semi_ar_layer_q8",
 ]

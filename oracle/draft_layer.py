@@ -33,6 +33,10 @@ Readings (the paper names the parts, not their formulas):
 * The fused projection weight Wqkv stacks the Hq query heads, then the Hkv
   key heads, then the Hkv value heads, each D rows; Wgu stacks the gate
   rows over the up rows.
+* The int8 draft (the paper's quantised-draft ablation names int8 without
+  a scheme) is weight-only: every projection row n holds int8 values wq
+  and one scale, W[n, :] = scale[n] * wq[n, :]; activations, norms and the
+  FC bias stay as in the bf16 draft.
 """
 
 import numpy as np
@@ -173,3 +177,27 @@ def semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, hq, hkv, ep
         p = p + (r - kp)
         r = 2 * kp
     return out_tok, out_q
+
+
+def dequantize_rows(wq, scale):
+    """The weight an int8 row-quantised projection stands for: W[n, k] =
+    scale[n] * wq[n, k] (one scale per output row)."""
+    return np.asarray(scale, dtype=np.float64)[:, None] * np.asarray(wq, dtype=np.float64)
+
+
+def linear_q8(x, wq, scale, bias=None, residual=None):
+    """x W^T (+ bias) (+ residual) with W = dequantize_rows(wq, scale)."""
+    return linear(x, dequantize_rows(wq, scale), bias, residual)
+
+
+Q8_WEIGHTS = ("fc_w", "wqkv", "wo", "wgu", "wdown")
+
+
+def semi_ar_layer_q8(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta):
+    """``semi_ar_layer`` of the int8 draft: weights holds, for each projection
+    name in Q8_WEIGHTS, the int8 rows under that name and their scales under
+    name + "_s"; the layer is the one of the dequantised weights."""
+    W = {k: v for k, v in weights.items() if not k.endswith("_s")}
+    for name in Q8_WEIGHTS:
+        W[name] = dequantize_rows(weights[name], weights[name + "_s"])
+    return semi_ar_layer(u, W, k_cache, v_cache, pos, hq, hkv, eps, theta)

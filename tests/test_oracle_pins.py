@@ -999,3 +999,32 @@ def test_kp_draft_feeds_drafts_back_in_order():
     ta, _ = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni, 6, 2)
     tb, _ = oracle.semi_ar_draft(u0, W, lm_w, emb, ph, kc, vc, pos, 2, 1, 1e-6, 1e4, 1.0, uni2, 6, 2)
     assert np.array_equal(ta[:, :4], tb[:, :4])
+
+
+def test_int8_rows_dequantise_and_project():
+    # W = scale[n] * wq[n, :]: unit scales give the int8 matrix itself; a
+    # row of scale 1/2 halves its output column; one-hot int8 rows pick inputs
+    wq = np.array([[1, -2, 0], [127, -128, 3]], dtype=np.int8)
+    assert np.array_equal(oracle.dequantize_rows(wq, [1.0, 1.0]), wq.astype(np.float64))
+    assert np.array_equal(oracle.dequantize_rows(wq, [0.5, 2.0]), [[0.5, -1.0, 0.0], [254.0, -256.0, 6.0]])
+    x = np.array([[2.0, 3.0, 5.0]])
+    onehot = np.array([[0, 0, 1], [1, 0, 0]], dtype=np.int8)
+    assert np.array_equal(oracle.linear_q8(x, onehot, [1.0, 0.25]), [[5.0, 0.5]])
+    assert np.array_equal(oracle.linear_q8(x, onehot, [1.0, 1.0], bias=[1.0, -1.0]), [[6.0, 1.0]])
+
+
+def test_int8_layer_equals_layer_of_dequantised_weights():
+    # an int8 draft whose rows are exactly representable equals the float
+    # draft with those weights
+    u, W, kc, vc, pos = _draft_case(12)
+    rng = np.random.default_rng(12)
+    Wq = dict(W)
+    Wf = dict(W)
+    for name in oracle.draft_layer.Q8_WEIGHTS:
+        q = rng.integers(-127, 128, size=W[name].shape).astype(np.int8)
+        s = rng.uniform(0.001, 0.02, size=W[name].shape[0])
+        Wq[name], Wq[name + "_s"] = q, s
+        Wf[name] = s[:, None] * q.astype(np.float64)
+    a, ka, va = oracle.semi_ar_layer_q8(u, Wq, kc, vc, pos, 2, 1, 1e-6, 1e4)
+    b, kb, vb = oracle.semi_ar_layer(u, Wf, kc, vc, pos, 2, 1, 1e-6, 1e4)
+    assert np.array_equal(a, b) and np.array_equal(ka, kb) and np.array_equal(va, vb)

@@ -324,7 +324,7 @@ int sd_linear(const void* x, const void* w, const float* bias, const float* resi
  * One step of the draft's semi-autoregressive layer over its cached context
  * (Sec. 3.1 and Algorithm 1: textual input FC(concat(F_T, E)); Sec. 3.3:
  * one pass of the layer gives the states of the K placeholder positions;
- * Sec. 4.4: one layer, 32 heads).  For the r new rows of each sequence b
+ * Sec. 4.3: one layer, 32 heads).  For the r new rows of each sequence b
  * (the last K of them placeholders), at positions pos[b] .. pos[b] + r - 1:
  *
  *   x0  = u W_fc^T + b_fc
@@ -372,7 +372,7 @@ int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const f
 
 /* ------------------------------------------------------------------------
  * K drafts in K / k' passes of the semi-autoregressive layer, k' per pass
- * (the group size k' of the paper's ablation, Appendix: the draft emits k'
+ * (the group size k' of the paper's ablation, Appendix E: the draft emits k'
  * tokens per forward pass and feeds them back for the next k').
  *
  * Pass 0 is sd_semi_ar_layer on u0 [B, r0, 2d] at positions pos[b] ..

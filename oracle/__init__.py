@@ -26,7 +26,7 @@ reader can check it against the paper by eye:
   one step of the draft's semi-autoregressive layer over its cached context:
   the fully connected fusion of feature and embedding, then one pre-norm
   decoder layer whose placeholder rows give the next K draft states
-  (Sec. 3.1, Sec. 3.3, Algorithm 1, Sec. 4.4); ``semi_ar_draft`` runs K
+  (Sec. 3.1, Sec. 3.3, Algorithm 1, Sec. 4.3); ``semi_ar_draft`` runs K
   drafts in K / k' passes of k' (the group size of the paper's ablation).
 
 Readings of points the paper leaves open are stated in each module.  No

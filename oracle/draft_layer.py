@@ -1,12 +1,12 @@
 """Oracle for one step of the draft's semi-autoregressive layer (Sec. 3.1;
-Sec. 3.3; Algorithm 1 of Appendix B; the draft size of Sec. 4.4).
+Sec. 3.3; Algorithm 1 of Appendix B; the draft size of Sec. 4.3).
 
 Test infrastructure only (see the package docstring).
 
 The draft builds its textual input by a fully connected map of the
 concatenated target feature and token embedding (following EAGLE, Sec. 3.1
 and Algorithm 1), joins it to the compressed visual features, and runs one
-transformer layer with 32 heads (the draft size the paper keeps, Sec. 4.4)
+transformer layer with 32 heads (the draft size the paper keeps, Sec. 4.3)
 whose outputs at K placeholder positions are the hidden states of the next
 K drafts, all in one pass (Sec. 3.3).  This module states one such pass for
 the rows that are new in a drafting round, over the draft's cached context.
@@ -33,7 +33,7 @@ Readings (the paper names the parts, not their formulas):
 * The fused projection weight Wqkv stacks the Hq query heads, then the Hkv
   key heads, then the Hkv value heads, each D rows; Wgu stacks the gate
   rows over the up rows.
-* The int8 draft (the paper's quantised-draft ablation names int8 without
+* The int8 draft (the quantised drafts of Appendix A name int8 without
   a scheme) is weight-only: every projection row n holds int8 values wq
   and one scale, W[n, :] = scale[n] * wq[n, :]; activations, norms and the
   FC bias stay as in the bf16 draft.
@@ -136,7 +136,7 @@ def bf16_round(x):
 def semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, hq, hkv, eps, theta, tau,
                   uniforms, K, kp, tokens=None):
     """K drafts in K / k' passes of the semi-AR layer, k' per pass (the group
-    size k' of the paper's ablation, Appendix).
+    size k' of the paper's ablation in Appendix E).
 
     Pass 0 runs the layer on u0 [B, r0, 2d], whose last k' rows are
     placeholders, at positions pos .. pos + r0 - 1.  After each pass the

@@ -1,6 +1,6 @@
 // One step of the draft's semi-autoregressive layer (SpecFLASH Sec. 3.1
 // and Algorithm 1: the textual input FC(concat(F_T, E)); Sec. 3.3: one pass
-// of one transformer layer gives the K placeholder states; Sec. 4.4: one
+// of one transformer layer gives the K placeholder states; Sec. 4.3: one
 // layer of 32 heads):
 //   x0 = [F_T, E] W_fc^T + b_fc
 //   x1 = x0 + Attn(RoPE(RMSNorm(x0) Wqkv^T)) Wo^T      (cached context)

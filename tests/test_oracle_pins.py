@@ -28,7 +28,7 @@ def rng(seed=0):
 @pytest.mark.parametrize("heads,scale", [(1, 1.0), (4, 0.5), (2, 1 / math.sqrt(8))])
 def test_compress_zero_queries_is_average_pooling(heads, scale):
     # Cq = 0 makes every score equal, so each latent averages all N tokens:
-    # global average pooling (the pooling compressor of Sec. 4.4, Tab. 4).
+    # global average pooling (the pooling compressor of the compression ablation in Sec. 4.3).
     r = rng(1)
     feats = r.standard_normal((3, 7, 16))
     out = oracle.latent_compress(np.zeros((5, 16)), feats, heads, scale)

@@ -341,6 +341,28 @@ def main():
     t_kp = float(np.mean([e[0].elapsed_time(e[1]) for e in kp_ev]))
     kp_bytes = synth.draft_kp_bytes(w, kp)
 
+    # the int8 draft's step (weight-only int8 rows), also timed on its own
+    dq = synth.draft_inputs(w, q8=True)
+    dq_w = {k: (to_dev(v, dev) if hasattr(v, "bits") else torch.from_numpy(v).to(dev))
+            for k, v in dq["weights"].items()}
+    dq_out = torch.empty_like(d_out)
+
+    def q8_call():
+        sd.sd_semi_ar_layer_q8(du_d, dq_w, dkc_d, dvc_d, dpos_d, dr["hq"], dr["hkv"], dr["eps"], dr["theta"],
+                               out=dq_out, workspace=d_ws)
+
+    for _ in range(2):
+        q8_call()
+    q8_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
+    for e in q8_ev:
+        e[0].record()
+        q8_call()
+        e[1].record()
+    torch.cuda.synchronize()
+    t_q8 = float(np.mean([e[0].elapsed_time(e[1]) for e in q8_ev]))
+    q8_bytes = synth.draft_q8_bytes(w)
+    del dq_w
+
     comp_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     ver_ms = np.array([e[6].elapsed_time(e[2]) for e in events])
     lm_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -394,6 +416,9 @@ def main():
                               "unit": "GB/s", "traffic": None, "algorithmic": kp_bytes, "us": t_kp * 1e3,
                               "frac": kp_bytes / (t_kp * 1e-3) / 1e9 / HBM_PEAK_GBS, "k_prime": kp,
                               "drafts": w.block, "outside_step": True}
+    rl["semi_ar_layer_q8"] = {"bound": "hbm", "achieved": q8_bytes / (t_q8 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "traffic": None, "algorithmic": q8_bytes, "us": t_q8 * 1e3,
+                              "frac": q8_bytes / (t_q8 * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
     roof = {k_: rl[dominant][k_] for k_ in ("bound", "achieved", "peak", "unit", "frac",
                                              "traffic")}
     roof["kernel"] = dominant
@@ -431,6 +456,7 @@ def main():
         "semi_ar_layer_us": t_d * 1e3,
         "semi_ar_layer_tbps": d_bytes / (t_d * 1e-3) / 1e12,
         "semi_ar_draft_kp_us": t_kp * 1e3,
+        "semi_ar_layer_q8_us": t_q8 * 1e3,
         "latent_compress_tflops": rl["latent_compress"]["achieved"],
         "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
         "accepted_mean": float(n_host.mean()),

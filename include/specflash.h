@@ -371,6 +371,35 @@ int sd_semi_ar_layer(const void* u, const void* fc_w, const float* fc_b, const f
                      void* stream);
 
 /* ------------------------------------------------------------------------
+ * The int8 draft (the quantised drafts of Appendix A; weight-only): every
+ * projection row n holds int8 values wq[n, :] and one fp32 scale, the
+ * weight it stands for being scale[n] * wq[n, :].  Activations, norms and
+ * the FC bias are as in the bf16 draft; the int8 x bf16 products are exact
+ * in the fp32 accumulation and each output is scaled once, so the results
+ * match the bf16 path on the dequantised weights to the same tolerance
+ * while every weight byte read is halved.
+ *
+ * sd_linear_q8: y = x (scale * wq)^T (+ bias) (+ residual); wq [N, K] int8,
+ *   scale [N] float32; other arguments, requirements, errors and workspace
+ *   (sd_linear_workspace_size) as for sd_linear.
+ * sd_semi_ar_layer_q8: sd_semi_ar_layer with int8 fc_w, wqkv, wo, wgu,
+ *   wdown and their scales fc_s [d], wqkv_s [(Hq + 2 Hkv) D], wo_s [d],
+ *   wgu_s [2I], wdown_s [d]; workspace sd_semi_ar_layer_workspace_size.
+ * ---------------------------------------------------------------------- */
+int sd_linear_q8(const void* x, const int8_t* wq, const float* scale, const float* bias,
+                 const float* residual, float* y, int R, int K, int N, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+int sd_semi_ar_layer_q8(const void* u, const int8_t* fc_w, const float* fc_s, const float* fc_b,
+                        const float* ln1, const int8_t* wqkv, const float* wqkv_s,
+                        const int8_t* wo, const float* wo_s, const float* ln2,
+                        const int8_t* wgu, const float* wgu_s, const int8_t* wdown,
+                        const float* wdown_s, void* k_cache, void* v_cache, const int32_t* pos,
+                        float* out, int B, int r, int d, int num_q_heads, int num_kv_heads, int I,
+                        int Lmax, float eps, float theta, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/* ------------------------------------------------------------------------
  * K drafts in K / k' passes of the semi-autoregressive layer, k' per pass
  * (the group size k' of the paper's ablation, Appendix E: the draft emits k'
  * tokens per forward pass and feeds them back for the next k').

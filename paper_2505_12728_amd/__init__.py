@@ -31,6 +31,7 @@ __all__ = [
     "sd_linear_workspace_size", "sd_linear",
     "sd_semi_ar_layer_workspace_size", "sd_semi_ar_layer",
     "sd_semi_ar_draft_workspace_size", "sd_semi_ar_draft",
+    "sd_linear_q8", "sd_semi_ar_layer_q8",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -67,6 +68,8 @@ _SIGNATURES = {
     "sd_semi_ar_layer": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                               _i, _i, _i, _i, _i, _i, _i, _f, _f, _vp, _sz, _vp]),
     "sd_semi_ar_draft_workspace_size": (_sz, [_i] * 10),
+    "sd_linear_q8": (_i, [_vp] * 6 + [_i, _i, _i, _vp, _sz, _vp]),
+    "sd_semi_ar_layer_q8": (_i, [_vp] * 18 + [_i] * 7 + [_f, _f, _vp, _sz, _vp]),
     "sd_semi_ar_draft": (_i, [_vp] * 18 + [_i] * 10 + [_f, _f, _f, _vp, _sz, _vp]),
 }
 
@@ -501,3 +504,72 @@ def sd_semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, u, K, kp
                                     float(temperature), _ptr(ws), ws_len, _stream(stream))
     _raise(st, "sd_semi_ar_draft")
     return tokens, q
+
+
+def sd_linear_q8(x, wq, scale, bias=None, residual=None, out=None, workspace=None, stream=None):
+    """y = x (scale * wq)^T (+ bias) (+ residual): x [R, K] bf16, wq [N, K]
+    int8, scale [N] fp32.  Returns y [R, N] fp32."""
+    torch = _torch()
+    _check(x, "x", dtype=torch.bfloat16, ndim=2)
+    _check(wq, "wq", dtype=torch.int8, ndim=2)
+    _check(scale, "scale", dtype=torch.float32, ndim=1)
+    R, K = x.shape
+    N = wq.shape[0]
+    if wq.shape[1] != K or scale.shape[0] != N:
+        raise ValueError("wq must be [N, K] and scale [N]")
+    if bias is not None:
+        _check(bias, "bias", dtype=torch.float32, ndim=1)
+    if residual is not None:
+        _check(residual, "residual", dtype=torch.float32, ndim=2)
+    if out is None:
+        out = torch.empty((R, N), dtype=torch.float32, device=x.device)
+    ws_bytes = sd_linear_workspace_size(R, K, N)
+    ws, ws_len = _workspace(ws_bytes, x.device, workspace)
+    st = library().sd_linear_q8(_ptr(x), _ptr(wq), _ptr(scale), _ptr(bias), _ptr(residual), _ptr(out), R, K, N,
+                                _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_linear_q8")
+    return out
+
+
+Q8_WEIGHTS = ("fc_w", "wqkv", "wo", "wgu", "wdown")
+
+
+def sd_semi_ar_layer_q8(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, out=None, workspace=None,
+                        stream=None):
+    """sd_semi_ar_layer of the int8 draft: weights holds int8 fc_w, wqkv, wo,
+    wgu, wdown and their fp32 row scales under the names + "_s"."""
+    torch = _torch()
+    _check(u, "u", dtype=torch.bfloat16, ndim=3)
+    B, r, d2 = u.shape
+    d = d2 // 2
+    for name in Q8_WEIGHTS:
+        _check(weights[name], name, dtype=torch.int8, ndim=2)
+        _check(weights[name + "_s"], name + "_s", dtype=torch.float32, ndim=1)
+        if weights[name + "_s"].shape[0] != weights[name].shape[0]:
+            raise ValueError(f"{name}_s must hold one scale per row of {name}")
+    for name in ("fc_b", "ln1", "ln2"):
+        _check(weights[name], name, dtype=torch.float32, ndim=1)
+    _check(k_cache, "k_cache", dtype=torch.bfloat16, ndim=4)
+    _check(v_cache, "v_cache", dtype=torch.bfloat16, ndim=4)
+    _check(pos, "pos", dtype=torch.int32, ndim=1)
+    Lmax = k_cache.shape[1]
+    I = weights["wdown"].shape[1]
+    D = d // hq
+    shapes = {"fc_w": (d, 2 * d), "wqkv": ((hq + 2 * hkv) * D, d), "wo": (d, hq * D), "wgu": (2 * I, d),
+              "wdown": (d, I)}
+    for name, shp in shapes.items():
+        if tuple(weights[name].shape) != shp:
+            raise ValueError(f"{name} must be {shp}, got {tuple(weights[name].shape)}")
+    if out is None:
+        out = torch.empty((B, r, d), dtype=torch.float32, device=u.device)
+    ws_bytes = sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax)
+    ws, ws_len = _workspace(ws_bytes, u.device, workspace)
+    W = weights
+    st = library().sd_semi_ar_layer_q8(_ptr(u), _ptr(W["fc_w"]), _ptr(W["fc_w_s"]), _ptr(W["fc_b"]),
+                                       _ptr(W["ln1"]), _ptr(W["wqkv"]), _ptr(W["wqkv_s"]), _ptr(W["wo"]),
+                                       _ptr(W["wo_s"]), _ptr(W["ln2"]), _ptr(W["wgu"]), _ptr(W["wgu_s"]),
+                                       _ptr(W["wdown"]), _ptr(W["wdown_s"]), _ptr(k_cache), _ptr(v_cache),
+                                       _ptr(pos), _ptr(out), B, r, d, hq, hkv, I, Lmax, float(eps),
+                                       float(theta), _ptr(ws), ws_len, _stream(stream))
+    _raise(st, "sd_semi_ar_layer_q8")
+    return out

@@ -42,7 +42,19 @@ constexpr int kEpiThreads = 256;
 // the chunk), a fixed permutation of the chunk's channels that the input
 // fragments follow; the input chunk's 16-byte pieces of row t sit at slot
 // piece ^ (t & 15), so the fragment reads are free of bank conflicts.
-template <int RB, int NW>
+// Two int8 values (bytes k, k + 1 of v) as two bf16 values, exactly (every
+// int8 value has at most 8 significant bits): sign-extend, convert to
+// float32, keep the upper halves.
+__device__ __forceinline__ uint32_t i8x2_to_bf16x2(uint32_t v, int k) {
+  const float f0 = (float)(int)(int8_t)(v >> (8 * k));
+  const float f1 = (float)(int)(int8_t)(v >> (8 * k + 8));
+  return __builtin_amdgcn_perm(__float_as_uint(f1), __float_as_uint(f0), 0x07060302u);
+}
+
+// Q8: the weight holds int8 rows with one fp32 scale per row (output
+// column); each lane then loads 64 bytes of its row per chunk (4 loads),
+// widens them to bf16 in registers and scales the accumulators once.
+template <int RB, int NW, bool Q8>
 __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   constexpr int HROWS = RB * 16;
   constexpr int HPIECES = HROWS * 32;          // 16-byte pieces of one input chunk
@@ -61,7 +73,10 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   const uint16_t* W = static_cast<const uint16_t*>(a.w);
   const uint16_t* X = static_cast<const uint16_t*>(a.x);
   // weight row n0 + c (clamped; columns >= N are not written)
-  const u32x4* wsrc = reinterpret_cast<const u32x4*>(W + (size_t)min(n0 + c, N - 1) * K + 64 * G);
+  const u32x4* wsrc = Q8 ? reinterpret_cast<const u32x4*>(static_cast<const int8_t*>(a.w) +
+                                                          (size_t)min(n0 + c, N - 1) * K + 64 * G)
+                         : reinterpret_cast<const u32x4*>(W + (size_t)min(n0 + c, N - 1) * K + 64 * G);
+  constexpr int WL = Q8 ? 4 : 8;               // 16-byte weight loads per lane and chunk
   // copy j of this thread moves piece P = (w DMA + j) 64 + lane of a chunk:
   // input row P / 32 of the pass (clamped; padded rows are not written)
   const uint16_t* hsrc[DMA];
@@ -83,25 +98,33 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   for (int rb = 0; rb < RB; ++rb) acc[rb] = floatx4{0.f, 0.f, 0.f, 0.f};
   // the weights of chunk n + 1 are loaded before chunk n is multiplied, so
   // two chunks of every lane's row are in flight
-  auto wload = [&](u32x4 (&wf)[8], int n) {
+  auto wload = [&](u32x4 (&wf)[WL], int n) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) wf[i] = wsrc[(size_t)n * 32 + i];
+    for (int i = 0; i < WL; ++i) wf[i] = wsrc[(size_t)n * (4 * WL) + i];
   };
-  auto step = [&](const u32x4 (&wf)[8], u32x4 (&wnext)[8], int n) {
+  auto step = [&](const u32x4 (&wf)[WL], u32x4 (&wnext)[WL], int n) {
     const int buf = (n - ch0) & 1;
     if (n + 1 < ch1) {
       wload(wnext, n + 1);
-      // the next weights are the 8 newest loads: this thread's copies of
+      // the next weights are the WL newest loads: this thread's copies of
       // chunk n (and its weights) have landed; after the barrier every
       // wave's have, and every wave is done reading the other buffer
-      wait_vm_then_barrier<8>();
+      wait_vm_then_barrier<WL>();
     } else {
       wait_vm_then_barrier<0>();
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       Pack8 x;
-      x.u = wf[i];
+      if constexpr (Q8) {
+        // product i takes bytes 8 (i & 1) .. + 7 of load i / 2: channels
+        // 64 G + 8 i .. + 7 as in the bf16 layout
+        const u32x4& v = wf[i >> 1];
+        const uint32_t lo = v[(i & 1) * 2], hi = v[(i & 1) * 2 + 1];
+        x.u = u32x4{i8x2_to_bf16x2(lo, 0), i8x2_to_bf16x2(lo, 2), i8x2_to_bf16x2(hi, 0), i8x2_to_bf16x2(hi, 2)};
+      } else {
+        x.u = wf[i];
+      }
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const int row = rb * 16 + c;
@@ -112,7 +135,7 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
     }
     if (n + 1 < ch1) issue(n + 1, buf ^ 1);
   };
-  u32x4 wa[8], wb[8];
+  u32x4 wa[WL], wb[WL];
   if (ch0 < ch1) {
     wload(wa, ch0);
     issue(ch0, 0);
@@ -123,6 +146,13 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
     if (n + 1 < ch1) step(wb, wa, n + 1);
   }
   // accumulator element i of lane (c, G): input row rb*16 + c, column n0 + 4G + i
+  if constexpr (Q8) {
+    floatx4 sc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sc[i] = a.wscale[min(n0 + 4 * G + i, N - 1)];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] *= sc;
+  }
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int r = r0 + rb * 16 + c;
@@ -315,19 +345,19 @@ __global__ __launch_bounds__(kEpiThreads) void kp_post(const float* probs, const
   if (j == 0 && threadIdx.x == 0) pos_out[b] = pos_in[b] + advance;
 }
 
-template <int NW>
+template <int NW, bool Q8>
 hipError_t launch_partial_nw(const LinearArgs& a, int rb, int passes, hipStream_t st) {
   const dim3 grid((a.N + NW * 16 - 1) / (NW * 16), a.ksplit, passes);
   const dim3 block(NW * 64);
   switch (rb) {
-    case 1: hipLaunchKernelGGL((linear_partial<1, NW>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((linear_partial<2, NW>), grid, block, 0, st, a); break;
-    case 3: hipLaunchKernelGGL((linear_partial<3, NW>), grid, block, 0, st, a); break;
-    case 4: hipLaunchKernelGGL((linear_partial<4, NW>), grid, block, 0, st, a); break;
-    case 5: hipLaunchKernelGGL((linear_partial<5, NW>), grid, block, 0, st, a); break;
-    case 6: hipLaunchKernelGGL((linear_partial<6, NW>), grid, block, 0, st, a); break;
-    case 7: hipLaunchKernelGGL((linear_partial<7, NW>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((linear_partial<8, NW>), grid, block, 0, st, a); break;
+    case 1: hipLaunchKernelGGL((linear_partial<1, NW, Q8>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((linear_partial<2, NW, Q8>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((linear_partial<3, NW, Q8>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((linear_partial<4, NW, Q8>), grid, block, 0, st, a); break;
+    case 5: hipLaunchKernelGGL((linear_partial<5, NW, Q8>), grid, block, 0, st, a); break;
+    case 6: hipLaunchKernelGGL((linear_partial<6, NW, Q8>), grid, block, 0, st, a); break;
+    case 7: hipLaunchKernelGGL((linear_partial<7, NW, Q8>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((linear_partial<8, NW, Q8>), grid, block, 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -361,8 +391,9 @@ LinearPlan plan_linear(int R, int K, int N, int cus) {
 }
 
 hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipStream_t st) {
-  return p.waves == 8 ? launch_partial_nw<8>(a, p.row_blocks, p.passes, st)
-                      : launch_partial_nw<4>(a, p.row_blocks, p.passes, st);
+  if (a.wscale != nullptr) return launch_partial_nw<8, true>(a, p.row_blocks, p.passes, st);
+  return p.waves == 8 ? launch_partial_nw<8, false>(a, p.row_blocks, p.passes, st)
+                      : launch_partial_nw<4, false>(a, p.row_blocks, p.passes, st);
 }
 
 hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias, const float* residual,
@@ -418,16 +449,16 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   const int R = a.B * a.r, d = a.d, D = d / a.Hq;
   const int nqkv = (a.Hq + 2 * a.Hkv) * D;
   hipError_t e;
-  auto lin = [&](const void* x, const void* w, int K, int N, const LinearPlan& lp) {
-    LinearArgs la{x, w, part, R, K, N, lp.ksplit};
+  auto lin = [&](const void* x, const void* w, const float* scale, int K, int N, const LinearPlan& lp) {
+    LinearArgs la{x, w, part, R, K, N, lp.ksplit, scale};
     return launch_linear_partial(la, lp, st);
   };
   // x0 = FC(u), h = RMSNorm(x0)
-  if ((e = lin(a.u, a.fc_w, 2 * d, d, p.fc)) != hipSuccess) return e;
+  if ((e = lin(a.u, a.fc_w, a.fc_s, 2 * d, d, p.fc)) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
                      (const float*)nullptr, x0, a.ln1, a.eps, h);
   // q, k, v with RoPE; k, v appended to the cache
-  if ((e = lin(h, a.wqkv, d, nqkv, p.qkv)) != hipSuccess) return e;
+  if ((e = lin(h, a.wqkv, a.wqkv_s, d, nqkv, p.qkv)) != hipSuccess) return e;
   const int rope_threads = (a.Hq + a.Hkv) * (D / 2) + a.Hkv * D;
   hipLaunchKernelGGL(epi_rope_qkv, dim3((rope_threads + kEpiThreads - 1) / kEpiThreads, R), dim3(kEpiThreads), 0, st, part, p.qkv.ksplit, R, nqkv, a.pos, a.r,
                      a.Hq, a.Hkv, D, log((double)a.theta), a.Lmax, q,
@@ -457,14 +488,14 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   hipLaunchKernelGGL(to_bf16, dim3((unsigned)((na + kEpiThreads - 1) / kEpiThreads)), dim3(kEpiThreads), 0, st,
                      attn, attn16, na);
   // x1 = x0 + attn Wo^T, h = RMSNorm(x1)
-  if ((e = lin(attn16, a.wo, a.Hq * D, d, p.o)) != hipSuccess) return e;
+  if ((e = lin(attn16, a.wo, a.wo_s, a.Hq * D, d, p.o)) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.o.ksplit, R, d,
                      (const float*)nullptr, x0, x1, a.ln2, a.eps, h);
   // act = SwiGLU(h), out = x1 + act Wdown^T
-  if ((e = lin(h, a.wgu, d, 2 * a.I, p.gu)) != hipSuccess) return e;
+  if ((e = lin(h, a.wgu, a.wgu_s, d, 2 * a.I, p.gu)) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_swiglu, dim3((a.I + kEpiThreads - 1) / kEpiThreads, R), dim3(kEpiThreads), 0, st, part,
                      p.gu.ksplit, R, a.I, act);
-  if ((e = lin(act, a.wdown, a.I, d, p.down)) != hipSuccess) return e;
+  if ((e = lin(act, a.wdown, a.wdown_s, a.I, d, p.down)) != hipSuccess) return e;
   return launch_epi_add(part, p.down.ksplit, R, d, nullptr, x1, a.out, st);
 }
 

@@ -120,10 +120,11 @@ constexpr int kLinearMaxSplits = 16;      // reduction splits at most
 
 struct LinearArgs {
   const void* x;   // [R, K] bf16
-  const void* w;   // [N, K] bf16
+  const void* w;   // [N, K] bf16, or int8 when wscale is set
   float* part;     // [ksplit, R, N] fp32 partial sums
   int R, K, N;
   int ksplit;
+  const float* wscale;   // [N] scales of int8 rows, or NULL (bf16 weight)
 };
 
 struct LinearPlan {
@@ -150,6 +151,13 @@ struct SemiArArgs {
   const float* ln2;    // [d]
   const void* wgu;     // [2I, d] bf16
   const void* wdown;   // [d, I] bf16
+  // int8 draft: the five weights above hold int8 rows and these their
+  // per-row scales (all NULL for the bf16 draft)
+  const float* fc_s;
+  const float* wqkv_s;
+  const float* wo_s;
+  const float* wgu_s;
+  const float* wdown_s;
   void* k_cache;       // [B, Lmax, Hkv, D] bf16
   void* v_cache;
   const int32_t* pos;  // [B] first new position of each sequence

@@ -490,3 +490,74 @@ int sd_semi_ar_draft(const void* u0, const void* fc_w, const float* fc_b, const 
   a.workspace = workspace;
   return status_from(sd::launch_semi_ar_draft(a, plan, static_cast<hipStream_t>(stream)));
 }
+
+int sd_linear_q8(const void* x, const int8_t* wq, const float* scale, const float* bias, const float* residual,
+                 float* y, int R, int K, int N, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!scale || !aligned(scale, 4)) return SD_ERR_INVALID_ARG;
+  if (R < 1 || K < 1 || N < 1 || !x || !wq || !y) return SD_ERR_INVALID_ARG;
+  if (!linear_shape_ok(R, K, N)) return SD_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(wq, 16) || !aligned(y, 4) || (bias && !aligned(bias, 4)) ||
+      (residual && !aligned(residual, 4)))
+    return SD_ERR_INVALID_ARG;
+  const sd::LinearPlan plan = sd::plan_linear(R, K, N, device_cus());
+  if (!workspace || workspace_bytes < plan.part_bytes || !aligned(workspace, 16)) return SD_ERR_WORKSPACE;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  sd::LinearArgs a{x, wq, static_cast<float*>(workspace), R, K, N, plan.ksplit, scale};
+  hipError_t e = sd::launch_linear_partial(a, plan, st);
+  if (e != hipSuccess) return status_from(e);
+  return status_from(sd::launch_epi_add(a.part, plan.ksplit, R, N, bias, residual, y, st));
+}
+
+int sd_semi_ar_layer_q8(const void* u, const int8_t* fc_w, const float* fc_s, const float* fc_b, const float* ln1,
+                        const int8_t* wqkv, const float* wqkv_s, const int8_t* wo, const float* wo_s,
+                        const float* ln2, const int8_t* wgu, const float* wgu_s, const int8_t* wdown,
+                        const float* wdown_s, void* k_cache, void* v_cache, const int32_t* pos, float* out, int B,
+                        int r, int d, int num_q_heads, int num_kv_heads, int I, int Lmax, float eps, float theta,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  const float* sc[] = {fc_s, wqkv_s, wo_s, wgu_s, wdown_s};
+  int st = SD_OK;
+  if (!semi_ar_shape_ok(B, r, d, num_q_heads, num_kv_heads, I, Lmax, &st)) return st;
+  for (const float* p : sc)
+    if (!p || !aligned(p, 4)) return SD_ERR_INVALID_ARG;
+  if (!u || !fc_w || !fc_b || !ln1 || !wqkv || !wo || !ln2 || !wgu || !wdown || !k_cache || !v_cache || !pos ||
+      !out || !isfinite(eps) || eps < 0.f || !isfinite(theta) || theta <= 0.f)
+    return SD_ERR_INVALID_ARG;
+  const void* a16[] = {u, fc_w, wqkv, wo, wgu, wdown, k_cache, v_cache};
+  for (const void* p : a16)
+    if (!aligned(p, 16)) return SD_ERR_INVALID_ARG;
+  if (!aligned(fc_b, 4) || !aligned(ln1, 4) || !aligned(ln2, 4) || !aligned(pos, 4) || !aligned(out, 16))
+    return SD_ERR_INVALID_ARG;
+  const sd::SemiArPlan plan = sd::plan_semi_ar(B, r, d, num_q_heads, num_kv_heads, I, Lmax, device_cus());
+  if (!plan.ok) return SD_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < plan.workspace_bytes || !aligned(workspace, 256)) return SD_ERR_WORKSPACE;
+  sd::SemiArArgs a{};
+  a.u = u;
+  a.fc_w = fc_w;
+  a.fc_b = fc_b;
+  a.ln1 = ln1;
+  a.wqkv = wqkv;
+  a.wo = wo;
+  a.ln2 = ln2;
+  a.wgu = wgu;
+  a.wdown = wdown;
+  a.fc_s = fc_s;
+  a.wqkv_s = wqkv_s;
+  a.wo_s = wo_s;
+  a.wgu_s = wgu_s;
+  a.wdown_s = wdown_s;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.pos = pos;
+  a.out = out;
+  a.B = B;
+  a.r = r;
+  a.d = d;
+  a.Hq = num_q_heads;
+  a.Hkv = num_kv_heads;
+  a.I = I;
+  a.Lmax = Lmax;
+  a.eps = eps;
+  a.theta = theta;
+  a.workspace = workspace;
+  return status_from(sd::launch_semi_ar(a, plan, static_cast<hipStream_t>(stream)));
+}

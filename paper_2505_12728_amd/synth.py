@@ -429,21 +429,31 @@ def draft_dims(w):
     return w.batch, r, d, w.hq, w.hkv, w.draft_ffn, Lmax
 
 
-def draft_inputs(w, seed=None, batch=None):
+def draft_inputs(w, seed=None, batch=None, q8=False):
     """Inputs of one draft step, always in bfloat16 (weights, u, caches):
     u = concat(F_T, E) ~ N(0, 1) of shape [B, r, 2d]; projection weights
     ~ N(0, 1 / fan_in), so every projection maps unit-variance rows to
     unit-variance rows; RMSNorm weights 1 + N(0, 0.1^2) and the FC bias
     N(0, 0.1^2) in float32; the caches hold N(0, 1) context keys and values
     at positions 0 .. pos[b] - 1 and the poison value elsewhere; pos[b] =
-    draft_ctx + 3 b (ragged contexts)."""
+    draft_ctx + 3 b (ragged contexts).  With q8, every projection is int8
+    rows wq = clip(round(40 z), -127, 127), z ~ N(0, 1), under its name and
+    float32 row scales 1 / (40 sqrt(fan_in)) under name + "_s" (the same
+    N(0, 1 / fan_in) spread)."""
     rs = streams(w.seed if seed is None else seed)
     B, r, d, hq, hkv, I, Lmax = draft_dims(w)
     B = B if batch is None else batch
     D = d // hq
 
+    weights_q8 = {}
+
     def weight(shape, fan_in):
         x = normal(rs["draft_w"], shape)
+        if q8:
+            _parallel_map(lambda v: np.clip(np.rint(v * np.float32(40.0)), -127, 127), x, x)
+            wq = x.astype(np.int8)
+            del x
+            return wq, np.full(shape[0], 1.0 / (40.0 * math.sqrt(fan_in)), dtype=np.float32)
         _parallel_map(lambda v: v * np.float32(1.0 / math.sqrt(fan_in)), x, x)
         t = Tensor(x, "bf16")
         del x
@@ -458,6 +468,9 @@ def draft_inputs(w, seed=None, batch=None):
          "ln2": (1.0 + normal(rs["draft_w"], (d,)) * np.float32(0.1)).astype(np.float32),
          "wgu": weight((2 * I, d), d),
          "wdown": weight((d, I), I)}
+    if q8:
+        for name in ("fc_w", "wqkv", "wo", "wgu", "wdown"):
+            W[name], W[name + "_s"] = W[name]
     pos = (w.draft_ctx + 3 * np.arange(B)).astype(np.int32)
     kc = normal(rs["draft_cache"], (B, Lmax, hkv, D))
     vc = normal(rs["draft_cache"], (B, Lmax, hkv, D))
@@ -490,3 +503,13 @@ def draft_kp_bytes(w, kp):
     per_pass = 2 * params + 2 * w.vocab * d + B * kp * w.vocab * 4
     ctx = sum(w.draft_ctx + 3 * b + r for b in range(B))
     return passes * per_pass + ctx * 2 * hkv * D * 2
+
+
+def draft_q8_bytes(w):
+    """Algorithmic HBM bytes of one int8 draft step: every int8 weight once
+    and its row scales, plus the rows and cache traffic of draft_bytes."""
+    B, r, d, hq, hkv, I, Lmax = draft_dims(w)
+    D = d // hq
+    params = d * 2 * d + (hq + 2 * hkv) * D * d + d * hq * D + 2 * I * d + d * I
+    rows = d + (hq + 2 * hkv) * D + d + 2 * I + d
+    return draft_bytes(w) - 2 * params + params + 4 * rows

@@ -296,3 +296,30 @@ def test_semi_ar_draft_validation_errors(lib):
     assert call(ws=None) == sd.SD_ERR_WORKSPACE
     assert lib.sd_semi_ar_draft_workspace_size(2, 3, 1024, 8, 2, 2048, 64, 1000, 6, 2) > 0
     assert lib.sd_semi_ar_draft_workspace_size(2, 3, 1024, 8, 2, 2048, 64, 1000, 5, 2) == 0
+
+
+def test_q8_validation_errors(lib):
+    keep, (x, w, s, y, ws) = _fake(5)
+    f = lib.sd_linear_q8
+
+    def call(x=x, w=w, s=s, y=y, R=4, K=512, N=100, ws=ws, wsb=0):
+        return f(x, w, s, None, None, y, R, K, N, ws, wsb, None)
+
+    assert call(s=None) == sd.SD_ERR_INVALID_ARG
+    assert call(w=None) == sd.SD_ERR_INVALID_ARG
+    assert call(K=300) == sd.SD_ERR_UNSUPPORTED
+    assert call(w=ctypes.c_void_p(w.value + 8)) == sd.SD_ERR_INVALID_ARG
+    assert call(wsb=8) == sd.SD_ERR_WORKSPACE
+    keep2, ptrs = _fake(18)
+    g = lib.sd_semi_ar_layer_q8
+
+    def lcall(r=9, wgu_s=ptrs[11], ws=ptrs[17], wsb=0):
+        # u, fc_w, fc_s, fc_b, ln1, wqkv, wqkv_s, wo, wo_s, ln2, wgu, wgu_s,
+        # wdown, wdown_s, k_cache, v_cache, pos, out
+        p = list(ptrs[:18])
+        p[11] = wgu_s
+        return g(*p, 2, r, 1024, 8, 2, 2048, 64, 1e-6, 1e4, ws, wsb, None)
+
+    assert lcall(wgu_s=None) == sd.SD_ERR_INVALID_ARG
+    assert lcall(r=17) == sd.SD_ERR_UNSUPPORTED
+    assert lcall(ws=None) == sd.SD_ERR_WORKSPACE

@@ -35,7 +35,7 @@ function here is "parity unpinned": every one is checked in
 enumeration or brute force.
 """
 
-from .compress import latent_compress, softmax_rows
+from .compress import latent_compress, softmax_rows, avg_pool_compress
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
@@ -55,6 +55,7 @@ from .accept import (
 
 __all__ = [
     "latent_compress",
+    "avg_pool_compress",
     "softmax_rows",
     "verify_attention",
     "gather_paged",

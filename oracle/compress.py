@@ -67,3 +67,19 @@ def latent_compress(latents, feats, num_heads=1, scale=1.0, return_probs=False):
     if return_probs:
         return out, probs
     return out
+
+
+def avg_pool_compress(feats, C):
+    """Average pooling of the N visual tokens into C features, the
+    non-parametric compressor the compression ablation (Sec. 4.3) compares
+    against.  Reading (the paper gives no formula): group c holds the
+    contiguous tokens floor(c N / C) .. floor((c + 1) N / C) - 1 in the
+    encoder's order and its feature is their mean.  feats [B, N, d];
+    returns [B, C, d] float64 (1 <= C <= N)."""
+    F = np.asarray(feats, dtype=np.float64)
+    B, N, d = F.shape
+    out = np.zeros((B, C, d), dtype=np.float64)
+    for c in range(C):
+        lo, hi = (c * N) // C, ((c + 1) * N) // C
+        out[:, c] = F[:, lo:hi].mean(axis=1)
+    return out

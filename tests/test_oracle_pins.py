@@ -1028,3 +1028,17 @@ def test_int8_layer_equals_layer_of_dequantised_weights():
     a, ka, va = oracle.semi_ar_layer_q8(u, Wq, kc, vc, pos, 2, 1, 1e-6, 1e4)
     b, kb, vb = oracle.semi_ar_layer(u, Wf, kc, vc, pos, 2, 1, 1e-6, 1e4)
     assert np.array_equal(a, b) and np.array_equal(ka, kb) and np.array_equal(va, vb)
+
+
+def test_avg_pool_compress_closed_forms():
+    rng = np.random.default_rng(21)
+    F = rng.normal(size=(2, 7, 5))
+    # C = N is the identity, C = 1 the global mean, which is also Eq. 3 with
+    # zero queries (every token weighted 1/N)
+    assert np.allclose(oracle.avg_pool_compress(F, 7), F)
+    g = oracle.avg_pool_compress(F, 1)
+    assert np.allclose(g[:, 0], F.mean(axis=1))
+    assert np.allclose(np.repeat(g, 3, axis=1), oracle.latent_compress(np.zeros((3, 5)), F, 1, 1.0))
+    # N = 7, C = 3: groups floor(7c/3) .. -> tokens {0, 1}, {2, 3}, {4, 5, 6}
+    x = np.arange(7, dtype=np.float64).reshape(1, 7, 1)
+    assert np.array_equal(oracle.avg_pool_compress(x, 3)[0, :, 0], [0.5, 2.5, 5.0])

@@ -113,6 +113,25 @@ int sd_latent_compress(const void* latents, const void* feats, float* out,
                        void* stream);
 
 /* ------------------------------------------------------------------------
+ * Average pooling of the visual tokens, the non-parametric compressor the
+ * compression ablation compares against (Sec. 4.3): the N tokens of each
+ * sequence form C contiguous groups, group c holding tokens
+ * floor(c N / C) .. floor((c + 1) N / C) - 1, and
+ *
+ *   out[b, c, :] = mean of feats[b, t, :] over the tokens t of group c
+ *
+ * (summed in float64).  C = 1 is Eq. 3 with zero queries.
+ *
+ *   feats  [B, N, d]  dtype    visual features, token-major
+ *   out    [B, C, d]  float32  pooled features
+ * Requirements: 1 <= C <= N; B, C <= 65535; N <= 2^24; d <= 2^20.  No
+ * workspace.  Errors: SD_ERR_INVALID_ARG (sizes, NULL or misaligned
+ * pointers, dtype), SD_ERR_UNSUPPORTED (limits above).
+ * ---------------------------------------------------------------------- */
+int sd_avg_pool_compress(const void* feats, float* out, int B, int N, int C, int d, int dtype,
+                         void* stream);
+
+/* ------------------------------------------------------------------------
  * Verification attention of the drafted block (Sec. 3.1).
  *
  * The target scores the k drafted tokens in one pass; per layer that is

@@ -31,7 +31,7 @@ __all__ = [
     "sd_linear_workspace_size", "sd_linear",
     "sd_semi_ar_layer_workspace_size", "sd_semi_ar_layer",
     "sd_semi_ar_draft_workspace_size", "sd_semi_ar_draft",
-    "sd_linear_q8", "sd_semi_ar_layer_q8",
+    "sd_linear_q8", "sd_semi_ar_layer_q8", "sd_avg_pool_compress",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -69,6 +69,7 @@ _SIGNATURES = {
                               _i, _i, _i, _i, _i, _i, _i, _f, _f, _vp, _sz, _vp]),
     "sd_semi_ar_draft_workspace_size": (_sz, [_i] * 10),
     "sd_linear_q8": (_i, [_vp] * 6 + [_i, _i, _i, _vp, _sz, _vp]),
+    "sd_avg_pool_compress": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "sd_semi_ar_layer_q8": (_i, [_vp] * 18 + [_i] * 7 + [_f, _f, _vp, _sz, _vp]),
     "sd_semi_ar_draft": (_i, [_vp] * 18 + [_i] * 10 + [_f, _f, _f, _vp, _sz, _vp]),
 }
@@ -572,4 +573,17 @@ def sd_semi_ar_layer_q8(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, 
                                        _ptr(pos), _ptr(out), B, r, d, hq, hkv, I, Lmax, float(eps),
                                        float(theta), _ptr(ws), ws_len, _stream(stream))
     _raise(st, "sd_semi_ar_layer_q8")
+    return out
+
+
+def sd_avg_pool_compress(feats, C, out=None, stream=None):
+    """Average pooling of feats [B, N, d] (bf16 or fp32) into C contiguous
+    token groups.  Returns out [B, C, d] fp32."""
+    torch = _torch()
+    _check(feats, "feats", ndim=3)
+    B, N, d = feats.shape
+    if out is None:
+        out = torch.empty((B, C, d), dtype=torch.float32, device=feats.device)
+    st = library().sd_avg_pool_compress(_ptr(feats), _ptr(out), B, N, C, d, _dtype_code(feats), _stream(stream))
+    _raise(st, "sd_avg_pool_compress")
     return out

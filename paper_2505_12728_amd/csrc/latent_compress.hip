@@ -670,6 +670,52 @@ __global__ __launch_bounds__(256) void compress_merge(CompressArgs a, int dh, in
       acc * (wsum > 0.f ? 1.f / wsum : 0.f);
 }
 
+// Average pooling of the N tokens into C contiguous groups (the
+// non-parametric compressor of the compression ablation, Sec. 4.3): group c
+// holds tokens floor(c N / C) .. floor((c + 1) N / C) - 1, its feature is
+// their mean.  Grid (channel blocks of 2048, C, B); each thread sums 8
+// channels over the group's tokens in float64 (one 16-byte load per token
+// for bf16 rows when aligned), so F_V is read once.
+template <typename T>
+__global__ __launch_bounds__(256) void avg_pool(const T* feats, float* out, int N, int C, int d) {
+  const int c = blockIdx.y, b = blockIdx.z;
+  const int lo = (int)((long long)c * N / C), hi = (int)((long long)(c + 1) * N / C);
+  const int e0 = (blockIdx.x * 256 + threadIdx.x) * 8;
+  if (e0 >= d) return;
+  const T* src = feats + ((size_t)b * N + lo) * d + e0;
+  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const bool vec = sizeof(T) == 2 && e0 + 8 <= d && (d & 7) == 0 && (reinterpret_cast<uintptr_t>(feats) & 15) == 0;
+  if (vec) {
+#pragma unroll 4
+    for (int t = lo; t < hi; ++t, src += d) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += (double)__uint_as_float(v[i] << 16);
+        acc[2 * i + 1] += (double)__uint_as_float(v[i] & 0xffff0000u);
+      }
+    }
+  } else {
+    for (int t = lo; t < hi; ++t, src += d) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (e0 + i < d) {
+          if constexpr (sizeof(T) == 2) {
+            acc[i] += (double)bf16_bits_to_float(reinterpret_cast<const uint16_t*>(src)[i]);
+          } else {
+            acc[i] += (double)src[i];
+          }
+        }
+      }
+    }
+  }
+  const double inv = 1.0 / (double)(hi - lo);
+  float* dst = out + ((size_t)b * C + c) * d + e0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    if (e0 + i < d) dst[i] = (float)(acc[i] * inv);
+}
+
 template <int NW, int DH>
 hipError_t launch_bf16(const CompressArgs& a, const CompressPlan& p, hipStream_t st) {
   const int n_bh = a.B * a.H;
@@ -739,6 +785,17 @@ hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dty
   const long long items = (long long)a.B * a.H * a.C * (p.dh / 4);
   hipLaunchKernelGGL(compress_merge, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a, p.dh,
                      p.nsplit);
+  return hipGetLastError();
+}
+
+hipError_t launch_avg_pool(const void* feats, float* out, int B, int N, int C, int d, int dtype, hipStream_t st) {
+  const dim3 grid((d + 2047) / 2048, C, B);
+  if (dtype == 0) {
+    hipLaunchKernelGGL(avg_pool<float>, grid, dim3(256), 0, st, static_cast<const float*>(feats), out, N, C, d);
+  } else {
+    hipLaunchKernelGGL(avg_pool<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(feats), out, N, C,
+                       d);
+  }
   return hipGetLastError();
 }
 

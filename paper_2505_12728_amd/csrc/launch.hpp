@@ -72,6 +72,8 @@ struct CompressArgs {
 };
 
 hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dtype, hipStream_t s);
+// average pooling of N tokens into C contiguous groups (dtype 0 fp32, 1 bf16)
+hipError_t launch_avg_pool(const void* feats, float* out, int B, int N, int C, int d, int dtype, hipStream_t s);
 
 // --------------------------------------------------------------- LM head
 struct LmHeadArgs {

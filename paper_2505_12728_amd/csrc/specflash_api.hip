@@ -561,3 +561,10 @@ int sd_semi_ar_layer_q8(const void* u, const int8_t* fc_w, const float* fc_s, co
   a.workspace = workspace;
   return status_from(sd::launch_semi_ar(a, plan, static_cast<hipStream_t>(stream)));
 }
+
+int sd_avg_pool_compress(const void* feats, float* out, int B, int N, int C, int d, int dtype, void* stream) {
+  if (B < 1 || N < 1 || C < 1 || d < 1 || C > N || (dtype != SD_F32 && dtype != SD_BF16)) return SD_ERR_INVALID_ARG;
+  if (!feats || !out || !aligned(feats, dtype == SD_F32 ? 4 : 2) || !aligned(out, 4)) return SD_ERR_INVALID_ARG;
+  if (B > 65535 || C > 65535 || N > (1 << 24) || d > (1 << 20)) return SD_ERR_UNSUPPORTED;
+  return status_from(sd::launch_avg_pool(feats, out, B, N, C, d, dtype, static_cast<hipStream_t>(stream)));
+}

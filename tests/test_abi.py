@@ -323,3 +323,13 @@ def test_q8_validation_errors(lib):
     assert lcall(wgu_s=None) == sd.SD_ERR_INVALID_ARG
     assert lcall(r=17) == sd.SD_ERR_UNSUPPORTED
     assert lcall(ws=None) == sd.SD_ERR_WORKSPACE
+
+
+def test_avg_pool_validation_errors(lib):
+    keep, (f, o) = _fake(2)
+    call = lambda B=2, N=16, C=4, d=64, dt=1, f=f, o=o: lib.sd_avg_pool_compress(f, o, B, N, C, d, dt, None)
+    assert call(C=17) == sd.SD_ERR_INVALID_ARG                  # C > N
+    assert call(C=0) == sd.SD_ERR_INVALID_ARG
+    assert call(dt=2) == sd.SD_ERR_INVALID_ARG
+    assert call(f=None) == sd.SD_ERR_INVALID_ARG
+    assert call(N=1 << 25, C=70000) == sd.SD_ERR_UNSUPPORTED

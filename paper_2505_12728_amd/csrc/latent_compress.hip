@@ -13,7 +13,7 @@
 //   - each tile is converted in place bf16 -> fp16 once per work-group (exact
 //     for |F_V| in [2^-14, 65504]), so both products run on fp16 matrix
 //     cores: S^T = F_V Cq^T (lane = one latent row), online softmax in fp32
-//     with exp2, P (in [0, 256]) rounded to fp16, O^T += F_V^T P^T;
+//     with exp2, P (in [0, 2^15]) rounded to fp16, O^T += F_V^T P^T;
 //   - latent tiles of one (sequence, head) are placed on the same XCD
 //     (work-groups are dealt to the 8 XCDs round-robin) so their F_V reads
 //     hit the same L2.
@@ -76,12 +76,12 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // (each 16-byte piece once per work-group), so every wave then runs both
 // products on fp16 matrix cores with no per-wave conversion:
 //   S^T = F_V Cq^T   (lane = one latent row, 16 tokens per tile and row)
-//   O^T += F_V^T P^T (P = exp2(s - m) in [0, 256] rounded to fp16; F_V^T
+//   O^T += F_V^T P^T (P = exp2(s - m) in [0, 2^15] rounded to fp16; F_V^T
 //                     fragments via the transposing ds_read_b64_tr_b16)
 // The loop is software-pipelined across tiles (scores of the next tile under
 // the exponentials of the current one) and split into groups whose LDS
 // reads are issued one group ahead.  The running maximum is raised (O, l
-// rescaled) only when a row's scores exceed it by 2^8, which each lane
+// rescaled) only when a row's scores exceed it by 2^15, which each lane
 // checks on its own scores against a per-row threshold, and the token mask
 // is applied only on the tail tile.  Tile reads and the in-place conversion
 // are inline asm, and each step has one counted wait and one fence-free
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   constexpr int DMA_PER_WAVE = DMA / NW;
   constexpr int CVT_PER_THREAD = TT * PK / (NW * 64);   // pieces converted per thread
   constexpr int NBUF = 4;
-  constexpr float kRescale = 8.f;
+  constexpr float kRescale = 15.f;      // P = exp2(s - m) <= 2^15 < the fp16 maximum
   static_assert(DMA % NW == 0 && (TT * PK) % (NW * 64) == 0, "tile work must split evenly");
   __shared__ __align__(16) unsigned char ring[NBUF][TILE_BYTES];
 
@@ -251,12 +251,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   };
   // Steady-state check of a tile: each lane compares the 16 scores it holds
   // of each row block with the row's threshold thr = (m + kRescale) / sl2 in
-  // score units (+inf for sl2 = 0), without the cross-lane maxima; only when
-  // some lane exceeds it does the step take the exact maxima and raise m.
-  float thr[2];
+  // score units (+inf for sl2 = 0), without the cross-lane maxima, and keeps
+  // its own maxima (lmax); only when some lane exceeds the threshold does the
+  // step reduce lmax across the lanes and raise m.  A threshold off by an ulp
+  // only lets P reach 2^15 (1 + 2^-23), still far inside the fp16 range.
+  float thr[2], lmax[2];
+  const float inv_sl2 = sl2 > 0.f ? 1.f / sl2 : 0.f;
   auto set_thresholds = [&]() {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) thr[rb] = sl2 > 0.f ? (m[rb] + kRescale) / sl2 : INFINITY;
+    for (int rb = 0; rb < 2; ++rb) thr[rb] = sl2 > 0.f ? (m[rb] + kRescale) * inv_sl2 : INFINITY;
   };
   auto tile_exceeds = [&](const floatx4 (&s)[4][2]) {
     bool hit = false;
@@ -267,6 +270,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) ext = fmaxf(ext, s[kb][rb][i]);
+      lmax[rb] = ext;
       hit = hit || ext > thr[rb];
     }
     return hit;
@@ -491,7 +495,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     });
     if (__ballot(exceed) != 0ull) {            // rare: exact maxima, raise, new thresholds
       float tmax[2];
-      tile_max(snext, tmax);
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) tmax[rb] = wave_max_across_groups(lmax[rb] * sl2);
       raise_max(tmax);
       set_thresholds();
     }

@@ -116,6 +116,16 @@ __device__ __forceinline__ void lds_write_b128(uint32_t addr, const u32x4& v) {
 // Wait for every LDS operation of this wave (asm reads included).
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Wait until at most N of this wave's LDS operations are outstanding.  LDS
+// operations complete in issue order, so with the N most recent ones still
+// in flight every earlier one has finished (counts above the counter's
+// 4-bit range wait for 15, which is stricter).
+template <int N>
+__device__ __forceinline__ void lds_wait_n() {
+  static_assert(N >= 0, "count");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(N < 15 ? N : 15) : "memory");
+}
+
 // Make a register value depend on the preceding volatile asm (the wait), so
 // no use of it can be scheduled before the wait.
 template <typename T>

@@ -80,7 +80,8 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 //                     fragments via the transposing ds_read_b64_tr_b16)
 // The loop is software-pipelined across tiles (scores of the next tile under
 // the exponentials of the current one) and split into groups whose LDS
-// reads are issued one group ahead.  The running maximum is raised (O, l
+// reads are issued one group ahead (before the wait for the current
+// group's).  The running maximum is raised (O, l
 // rescaled) only when a row's scores exceed it by 2^15, which each lane
 // checks on its own scores against a per-row threshold, and the token mask
 // is applied only on the tail tile.  Tile reads and the in-place conversion
@@ -416,6 +417,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
   };
 
+  // LDS operations issued by reads() for group g
+  constexpr auto reads_in = [](int g) {
+    return g < NQK ? 4 : (g < NG ? 8 + (g == NQK ? CVT_PER_THREAD : 0) : 0);
+  };
+
   // one step; the mask flag (compile time) is set only for it = last - 1, so
   // the steady-state loop has no branch between its groups
   auto step = [&](int it, auto mask_tag) {
@@ -434,9 +440,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     issue(min(it + 3, last), ring[(it + 3) % NBUF]);
     static_for<0, NG>([&](auto gtag) {
       constexpr int g = decltype(gtag)::value;
-      lds_wait();
-      reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+      // issue the next group's reads, then wait for this group's (the
+      // next group's stay in flight)
       reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+      lds_wait_n<reads_in(g + 1)>();
+      reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
       if constexpr (g == NQK + NPVH) {
         // conversion finished in the first half: write it back
 #pragma unroll

@@ -80,13 +80,13 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 //                     fragments via the transposing ds_read_b64_tr_b16)
 // The loop is software-pipelined across tiles (scores of the next tile under
 // the exponentials of the current one) and split into groups whose LDS
-// reads are issued one group ahead (before the wait for the current
-// group's).  The running maximum is raised (O, l
+// reads are issued one group ahead.  The running maximum is raised (O, l
 // rescaled) only when a row's scores exceed it by 2^15, which each lane
 // checks on its own scores against a per-row threshold, and the token mask
 // is applied only on the tail tile.  Tile reads and the in-place conversion
-// are inline asm, and each step has one counted wait and one fence-free
-// barrier.
+// are inline asm, and each step has one counted wait for its copies and
+// one fence-free barrier (for eight-wave groups placed before the step's
+// last group, so the next step's first reads overlap that group's work).
 template <int NW, int DH>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
                                                          int tokens_per_split, int nsplit) {
@@ -422,29 +422,59 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     return g < NQK ? 4 : (g < NG ? 8 + (g == NQK ? CVT_PER_THREAD : 0) : 0);
   };
 
+  // Eight-wave groups (DH = 128) move the step's barrier from its start to
+  // the start of its last group: the conversion has been written back one
+  // group earlier, so after that barrier the next step's first reads and
+  // copy can be issued and overlap the last group's matrix-core work.
+  // Smaller groups keep the barrier at the step start and wait for a
+  // group's reads before issuing the next group's (they have no registers
+  // to spare for both in flight).
+  constexpr bool kRot = NW == 8 && NQK + NPVH < NG - 1;
+  u32x4 xr[2][4];
+
   // one step; the mask flag (compile time) is set only for it = last - 1, so
-  // the steady-state loop has no branch between its groups
+  // the steady-state loop has no branch between its groups.  Entering a
+  // step: tile it+1 converted by every wave, tile it+2 landed, the copy of
+  // tile it+3 issued and (kRot) the first group's reads done.
   auto step = [&](int it, auto mask_tag) {
-    // tile it+2 landed; tile it+1 converted by every wave; buffer it-1 free
-    wait_vm_then_barrier<0>();
     const uint32_t nb = lds_addr(ring[(it + 1) % NBUF]);
     const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);
     const uint32_t vb = lds_addr(ring[it % NBUF]);
-    u32x4 xr[2][4];
     u32x2 vr[2][4][2];
     u32x4 cv[CVT_PER_THREAD];
     floatx4 snext[4][2];
     f16x8 pf[2][2];
     bool exceed = false;
-    reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
-    issue(min(it + 3, last), ring[(it + 3) % NBUF]);
+    if constexpr (!kRot) {
+      // tile it+2 landed; tile it+1 converted by every wave; buffer it-1 free
+      wait_vm_then_barrier<0>();
+      reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+      issue(min(it + 3, last), ring[(it + 3) % NBUF]);
+    }
     static_for<0, NG>([&](auto gtag) {
       constexpr int g = decltype(gtag)::value;
       // issue the next group's reads, then wait for this group's (the
       // next group's stay in flight)
-      reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
-      lds_wait_n<reads_in(g + 1)>();
-      reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+      if constexpr (kRot) {
+        reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+        lds_wait_n<reads_in(g + 1)>();
+        reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+      } else {
+        lds_wait();
+        reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+        reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+      }
+      if constexpr (kRot && g == NG - 1) {
+        // tile it+2 converted by every wave, tile it+3 landed, buffer it
+        // read by every wave: start the next step's first group and copy
+        // tile it+4 into buffer it, under this group's matrix-core work
+        wait_vm_then_barrier<0>();
+        if constexpr (!decltype(mask_tag)::value) {
+          reads(std::integral_constant<int, 0>{}, lds_addr(ring[(it + 2) % NBUF]), vb, cb, xr, vr, cv,
+                std::false_type{});
+          issue(min(it + 4, last), ring[it % NBUF]);
+        }
+      }
       if constexpr (g == NQK + NPVH) {
         // conversion finished in the first half: write it back
 #pragma unroll
@@ -499,6 +529,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         }
         SD_INTERLEAVE(8 + (pb == NPVH - 1 ? 2 : 0), 3, g + 1)
       }
+      if constexpr (kRot && g == NG - 1 && !decltype(mask_tag)::value) {
+        // the next step's first group is complete before the loop edge
+        lds_wait();
+        reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::true_type{});
+      }
       __builtin_amdgcn_sched_barrier(0);
     });
     if (__ballot(exceed) != 0ull) {            // rare: exact maxima, raise, new thresholds
@@ -513,6 +548,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) scur[kb][rb] = snext[kb][rb];
   };
+  if (kRot && last >= 1) {
+    // tile 1 converted by every wave, tile 2 landed: the first group of step
+    // 0, and the copy of tile 3
+    wait_vm_then_barrier<0>();
+    u32x2 vr0[2][4][2];
+    u32x4 cv0[CVT_PER_THREAD];
+    const uint32_t nb0 = lds_addr(ring[1]);
+    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, std::false_type{});
+    issue(min(3, last), ring[3 % NBUF]);
+    lds_wait();
+    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, std::true_type{});
+  }
   for (int it = 0; it + 1 < last; ++it) step(it, std::false_type{});
   if (last >= 1) step(last - 1, std::true_type{});
   {

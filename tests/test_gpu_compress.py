@@ -58,6 +58,8 @@ CASES = [
     ("one-token", "bf16", 1, 1, 32, 128, 1, 1.0),
     ("many-latents", "bf16", 1, 300, 520, 128, 1, 1.0),
     ("split-tokens", "bf16", 1, 20000, 64, 128, 1, 1 / math.sqrt(128)),
+    ("eight-waves-ragged-splits", "bf16", 1, 20037, 260, 256, 2, 1 / math.sqrt(128)),
+    ("eight-waves-head-dim-64", "bf16", 1, 1500, 300, 128, 2, 1 / 8),
     ("f32-heads", "f32", 2, 333, 20, 256, 2, 0.5),
     ("f32-dh256", "f32", 1, 2000, 16, 256, 1, 1 / 16),
 ]

@@ -879,8 +879,9 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
   } else {
     // one wave per 16-row block, 1, 2 or 4 blocks per work-group.  Blocks
     // of 4 run as 8 waves in two key groups over a 128 KB ring, one work-
-    // group per compute unit; smaller ones hold a 48 KB ring, three per
-    // unit.  The grid is that many work-groups, whatever the lengths.
+    // group per compute unit; smaller ones hold a 64 KB ring, two per unit
+    // (stream_cfg).  The grid is that many work-groups, whatever the
+    // lengths.
     p.row_blocks = blocks16 <= 1 ? 1 : (blocks16 == 2 ? 2 : 4);
     p.row_groups = (blocks16 + p.row_blocks - 1) / p.row_blocks;
     p.rows_wg = p.row_blocks * 16;

@@ -186,45 +186,75 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
-// y = sum of splits (+ bias) (+ residual), written as fp32 `out` [R, N].
-// With `norm_w`, also h = y / sqrt(mean(y^2) + eps) * norm_w in bf16.
-// One work-group of 1024 threads per row, four columns per access when the
-// row allows (N % 4 == 0 and 16-byte aligned bias, residual and out).
-constexpr int kRowThreads = 1024;
-__global__ __launch_bounds__(kRowThreads) void epi_add_norm(const float* part, int ksplit, int R, int N,
+// y = sum of splits (+ bias) (+ residual), written as fp32 `out` [R, N];
+// grid (ceil(N / kEpiCols), R), kEpiThreads threads of four columns each.
+// Every split of a thread's columns is loaded before any is added (the
+// splits are added in split order), so a row's partials stream from many
+// compute units at once.  With `ss`, block x of row r also writes the sum
+// of squares of its columns to ss[r * gridDim.x + x] for epi_norm_cols.
+constexpr int kEpiCols = 4 * kEpiThreads;
+__global__ __launch_bounds__(kEpiThreads) void epi_add_cols(const float* part, int ksplit, int R, int N,
                                                             const float* bias, const float* residual,
-                                                            float* out, const float* norm_w, float eps,
-                                                            __bf16* h) {
-  __shared__ float red[kRowThreads / 64];
-  const int r = blockIdx.x;
+                                                            float* out, float* ss) {
+  __shared__ float red[kEpiThreads / 64];
+  const int r = blockIdx.y;
   const size_t stride = (size_t)R * N;
   const size_t row = (size_t)r * N;
-  float ss = 0.f;
+  const int n0 = blockIdx.x * kEpiCols + threadIdx.x * 4;
   auto a16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
   const bool vec = (N & 3) == 0 && a16(part) && a16(out) && (!bias || a16(bias)) && (!residual || a16(residual));
+  float s2 = 0.f;
   if (vec) {
-    for (int n = threadIdx.x * 4; n < N; n += kRowThreads * 4) {
+    if (n0 < N) {
+      floatx4 v[kLinearMaxSplits];
+#pragma unroll
+      for (int ks = 0; ks < kLinearMaxSplits; ++ks)
+        if (ks < ksplit) v[ks] = *reinterpret_cast<const floatx4*>(part + ks * stride + row + n0);
       floatx4 y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-      for (int ks = 0; ks < ksplit; ++ks) y += *reinterpret_cast<const floatx4*>(part + ks * stride + row + n);
-      if (bias) y += *reinterpret_cast<const floatx4*>(bias + n);
-      if (residual) y += *reinterpret_cast<const floatx4*>(residual + row + n);
-      *reinterpret_cast<floatx4*>(out + row + n) = y;
-      ss += y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+#pragma unroll
+      for (int ks = 0; ks < kLinearMaxSplits; ++ks)
+        if (ks < ksplit) y += v[ks];
+      if (bias) y += *reinterpret_cast<const floatx4*>(bias + n0);
+      if (residual) y += *reinterpret_cast<const floatx4*>(residual + row + n0);
+      *reinterpret_cast<floatx4*>(out + row + n0) = y;
+      s2 = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
     }
   } else {
-    for (int n = threadIdx.x; n < N; n += kRowThreads) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + j;
+      if (n >= N) break;
       float y = split_sum(part, ksplit, stride, row + n);
       if (bias) y += bias[n];
       if (residual) y += residual[row + n];
       out[row + n] = y;
-      ss += y * y;
+      s2 += y * y;
     }
   }
-  if (norm_w == nullptr) return;
-  const float inv = 1.f / sqrtf(block_sum(ss, red) / (float)N + eps);
-  for (int n = threadIdx.x; n < N; n += kRowThreads) h[row + n] = float_to_bf16(out[row + n] * inv * norm_w[n]);
+  if (ss == nullptr) return;
+  const float t = block_sum(s2, red);
+  if (threadIdx.x == 0) ss[(size_t)r * gridDim.x + blockIdx.x] = t;
 }
+
+// h = y / sqrt(mean(y^2) + eps) * norm_w in bf16, for the rows epi_add_cols
+// wrote with their block sums of squares (nblk per row, added in block
+// order); same grid as epi_add_cols.
+__global__ __launch_bounds__(kEpiThreads) void epi_norm_cols(const float* y, int N, const float* ss, int nblk,
+                                                             const float* norm_w, float eps, __bf16* h) {
+  const int r = blockIdx.y;
+  float t = 0.f;
+  for (int i = 0; i < nblk; ++i) t += ss[(size_t)r * nblk + i];
+  const float inv = 1.f / sqrtf(t / (float)N + eps);
+  const int n0 = blockIdx.x * kEpiCols + threadIdx.x * 4;
+  const size_t row = (size_t)r * N;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = n0 + j;
+    if (n < N) h[row + n] = float_to_bf16(y[row + n] * inv * norm_w[n]);
+  }
+}
+
+static int epi_blocks(int N) { return (N + kEpiCols - 1) / kEpiCols; }
 
 // Fused projection output of row r (sequence b = r / rows, j = r % rows,
 // position p = pos[b] + j): query heads rotated into q [R, Hq, D] (bf16),
@@ -398,8 +428,8 @@ hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipSt
 
 hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias, const float* residual,
                           float* out, hipStream_t st) {
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, ksplit, R, N, bias, residual, out,
-                     nullptr, 0.f, nullptr);
+  hipLaunchKernelGGL(epi_add_cols, dim3(epi_blocks(N), R), dim3(kEpiThreads), 0, st, part, ksplit, R, N, bias,
+                     residual, out, (float*)nullptr);
   return hipGetLastError();
 }
 
@@ -429,6 +459,7 @@ SemiArPlan plan_semi_ar(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, i
   p.off_x1 = take((size_t)R * d * 4);
   p.off_act = take((size_t)R * I * 2);
   p.off_kvlen = take((size_t)B * 4);
+  p.off_ss = take((size_t)R * epi_blocks(d) * 4);
   p.off_verify = take(p.verify.workspace_bytes);
   p.workspace_bytes = off;
   p.ok = p.verify.ok;
@@ -446,7 +477,9 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   float* x1 = reinterpret_cast<float*>(ws + p.off_x1);
   __bf16* act = reinterpret_cast<__bf16*>(ws + p.off_act);
   int32_t* kv_len = reinterpret_cast<int32_t*>(ws + p.off_kvlen);
+  float* ss = reinterpret_cast<float*>(ws + p.off_ss);
   const int R = a.B * a.r, d = a.d, D = d / a.Hq;
+  const dim3 eg(epi_blocks(d), R);
   const int nqkv = (a.Hq + 2 * a.Hkv) * D;
   hipError_t e;
   auto lin = [&](const void* x, const void* w, const float* scale, int K, int N, const LinearPlan& lp) {
@@ -455,8 +488,9 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   };
   // x0 = FC(u), h = RMSNorm(x0)
   if ((e = lin(a.u, a.fc_w, a.fc_s, 2 * d, d, p.fc)) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
-                     (const float*)nullptr, x0, a.ln1, a.eps, h);
+  hipLaunchKernelGGL(epi_add_cols, eg, dim3(kEpiThreads), 0, st, part, p.fc.ksplit, R, d, a.fc_b,
+                     (const float*)nullptr, x0, ss);
+  hipLaunchKernelGGL(epi_norm_cols, eg, dim3(kEpiThreads), 0, st, x0, d, ss, (int)eg.x, a.ln1, a.eps, h);
   // q, k, v with RoPE; k, v appended to the cache
   if ((e = lin(h, a.wqkv, a.wqkv_s, d, nqkv, p.qkv)) != hipSuccess) return e;
   const int rope_threads = (a.Hq + a.Hkv) * (D / 2) + a.Hkv * D;
@@ -489,8 +523,9 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
                      attn, attn16, na);
   // x1 = x0 + attn Wo^T, h = RMSNorm(x1)
   if ((e = lin(attn16, a.wo, a.wo_s, a.Hq * D, d, p.o)) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_add_norm, dim3(R), dim3(kRowThreads), 0, st, part, p.o.ksplit, R, d,
-                     (const float*)nullptr, x0, x1, a.ln2, a.eps, h);
+  hipLaunchKernelGGL(epi_add_cols, eg, dim3(kEpiThreads), 0, st, part, p.o.ksplit, R, d,
+                     (const float*)nullptr, x0, x1, ss);
+  hipLaunchKernelGGL(epi_norm_cols, eg, dim3(kEpiThreads), 0, st, x1, d, ss, (int)eg.x, a.ln2, a.eps, h);
   // act = SwiGLU(h), out = x1 + act Wdown^T
   if ((e = lin(h, a.wgu, a.wgu_s, d, 2 * a.I, p.gu)) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_swiglu, dim3((a.I + kEpiThreads - 1) / kEpiThreads, R), dim3(kEpiThreads), 0, st, part,

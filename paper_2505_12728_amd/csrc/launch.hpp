@@ -172,7 +172,7 @@ struct SemiArArgs {
 struct SemiArPlan {
   LinearPlan fc, qkv, o, gu, down;
   VerifyPlan verify;
-  size_t off_part, off_x0, off_h, off_q, off_attn, off_attn16, off_x1, off_act, off_kvlen, off_verify;
+  size_t off_part, off_x0, off_h, off_q, off_attn, off_attn16, off_x1, off_act, off_kvlen, off_ss, off_verify;
   size_t workspace_bytes;
   bool ok;
 };

@@ -18,8 +18,10 @@
 //    starting offset; T = floor(a S / 2^24) from a = u_k 2^24 (formed as
 //    a (S >> 24) + ((a (S mod 2^24)) >> 24) without overflow) picks the
 //    chunk, and inside it the first entry whose inclusive prefix sum
-//    exceeds T (64-wide wave prefix sums).  Greedy: argmax per row from the
-//    chunk maxima, then the longest matching prefix.
+//    exceeds T (the chunk's entries loaded in one round, four consecutive
+//    ones per thread, and a block prefix sum of the threads' totals).
+//    Greedy: argmax per row from the chunk maxima, then the longest
+//    matching prefix.
 // Every vocabulary access is a coalesced stream.
 //
 // From logits (the target's k + 1 and the draft's k rows per sequence), the
@@ -41,6 +43,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 1024;     // vocabulary entries per chunk (<= 256 chunks for V <= 2^18)
+static_assert(kChunk % kThreads == 0, "whole entries per thread in a chunk");
 constexpr int kStatChunk = 4096;
 constexpr int kMaxStatParts = (1 << 18) / kStatChunk;   // statistics chunks of a row at most
 
@@ -330,11 +333,19 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
   __shared__ uint64_t s_before;
   __shared__ float2 s_rows[33];
   const int b = blockIdx.x;
+  const int c = threadIdx.x;                   // one thread per chunk (nchunks <= 256)
+  // sampled: the chunk sums depend neither on n nor on the row statistics,
+  // so their loads are issued first and overlap both
+  uint64_t x_res = 0ull, x_p = 0ull;
+  if (a.mode != 0 && c < nchunks) {
+    const uint64_t* sums = static_cast<const uint64_t*>(ws) + (size_t)b * nchunks * 2;
+    x_res = sums[2 * c];
+    x_p = sums[2 * c + 1];
+  }
   src.prepare(b, s_rows);
   __syncthreads();
   const int k = a.k, V = a.V;
   const int32_t* draft = a.draft + (size_t)b * k;
-  const int c = threadIdx.x;                   // one thread per chunk (nchunks <= 256)
   int n = 0, token = 0;
   if (a.mode == 0) {
     const ArgMax* part = static_cast<const ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
@@ -362,15 +373,14 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
     n = nn;
   } else {
     n = accepted_prefix(a, src, b, &s_n);
-    const uint64_t* sums = static_cast<const uint64_t*>(ws) + (size_t)b * nchunks * 2;
     // residual weights, else p-only weights, else argmax
     uint64_t S;
-    uint64_t x = c < nchunks ? sums[2 * c] : 0ull;
+    uint64_t x = x_res;
     uint64_t before = block_exclusive_scan(x, tot, &S);
     int sel = 0;
     if (S == 0) {
       sel = 1;
-      x = c < nchunks ? sums[2 * c + 1] : 0ull;
+      x = x_p;
       before = block_exclusive_scan(x, tot, &S);
     }
     if (S == 0) {
@@ -388,34 +398,32 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
       }
       if (threadIdx.x == 0) s_tok = 0x7fffffff;
       __syncthreads();
-      const int cs = s_chunk;
-      // scan the chunk in 256-entry steps: wave w takes entries
-      // base + 64 w + lane, the waves' totals are prefix-summed in LDS
-      const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-      const int c0 = cs * kChunk, c1 = min(V, c0 + kChunk);
-      uint64_t running = s_before;
-      for (int base = c0; base < c1; base += kThreads) {
-        const int v = base + 64 * w + lane;
-        uint64_t y = v < c1 ? weight_at(src, b, n, v, use_q) : 0ull;
+      // inside the chunk, thread t takes the kPerThread consecutive entries
+      // from c0 + t kPerThread, all loaded at once; a block prefix sum of
+      // the threads' totals finds the thread whose range holds T, and that
+      // thread finds the first entry whose inclusive prefix sum exceeds T
+      constexpr int kPerThread = kChunk / kThreads;
+      const int c0 = s_chunk * kChunk, c1 = min(V, c0 + kChunk);
+      const int e0 = c0 + threadIdx.x * kPerThread;
+      uint64_t wv[kPerThread], mine = 0;
 #pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-          const uint64_t z = shfl_up_u64(y, d);
-          if (lane >= d) y += z;
-        }
-        if (lane == 63) tot[w] = y;
-        __syncthreads();
-        uint64_t off = running, step = 0;
-        for (int i = 0; i < kWaves; ++i) {
-          if (i < w) off += tot[i];
-          step += tot[i];
-        }
-        const uint64_t mask = __ballot(off + y > T);
-        // prefix sums rise with v, so the smallest hit is the token
-        if (mask != 0ull && lane == __builtin_ctzll(mask)) atomicMin(&s_tok, v);
-        __syncthreads();
-        if (s_tok != 0x7fffffff) break;
-        running += step;
+      for (int j = 0; j < kPerThread; ++j) {
+        wv[j] = e0 + j < c1 ? weight_at(src, b, n, e0 + j, use_q) : 0ull;
+        mine += wv[j];
       }
+      uint64_t chunk_total;
+      const uint64_t pre = s_before + block_exclusive_scan(mine, tot, &chunk_total);
+      if (mine != 0 && pre <= T && T < pre + mine) {
+        uint64_t incl = pre;
+        int hit = -1;
+#pragma unroll
+        for (int j = 0; j < kPerThread; ++j) {
+          incl += wv[j];
+          if (hit < 0 && incl > T) hit = e0 + j;
+        }
+        s_tok = hit;                           // found: T < pre + mine
+      }
+      __syncthreads();
       token = s_tok;
     }
   }

@@ -330,38 +330,42 @@ def main():
                             dr["hkv"], dr["eps"], dr["theta"], lm["temperature"], tokens=kp_tok, q=kp_q,
                             workspace=kp_ws)
 
-    for _ in range(2):
-        kp_call()
-    kp_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
-    for e in kp_ev:
-        e[0].record()
-        kp_call()
-        e[1].record()
-    torch.cuda.synchronize()
-    t_kp = float(np.mean([e[0].elapsed_time(e[1]) for e in kp_ev]))
-    kp_bytes = synth.draft_kp_bytes(w, kp)
+    # the K / k' drafts and the int8 draft take bf16 weights only
+    t_kp = t_q8 = None
+    if w.dtype == "bf16":
+        for _ in range(2):
+            kp_call()
+        kp_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
+        for e in kp_ev:
+            e[0].record()
+            kp_call()
+            e[1].record()
+        torch.cuda.synchronize()
+        t_kp = float(np.mean([e[0].elapsed_time(e[1]) for e in kp_ev]))
+        kp_bytes = synth.draft_kp_bytes(w, kp)
 
-    # the int8 draft's step (weight-only int8 rows), also timed on its own
-    dq = synth.draft_inputs(w, q8=True)
-    dq_w = {k: (to_dev(v, dev) if hasattr(v, "bits") else torch.from_numpy(v).to(dev))
-            for k, v in dq["weights"].items()}
-    dq_out = torch.empty_like(d_out)
+    if w.dtype == "bf16":
+        # the int8 draft's step (weight-only int8 rows), also timed on its own
+        dq = synth.draft_inputs(w, q8=True)
+        dq_w = {k: (to_dev(v, dev) if hasattr(v, "bits") else torch.from_numpy(v).to(dev))
+                for k, v in dq["weights"].items()}
+        dq_out = torch.empty_like(d_out)
 
-    def q8_call():
-        sd.sd_semi_ar_layer_q8(du_d, dq_w, dkc_d, dvc_d, dpos_d, dr["hq"], dr["hkv"], dr["eps"], dr["theta"],
-                               out=dq_out, workspace=d_ws)
+        def q8_call():
+            sd.sd_semi_ar_layer_q8(du_d, dq_w, dkc_d, dvc_d, dpos_d, dr["hq"], dr["hkv"], dr["eps"], dr["theta"],
+                                   out=dq_out, workspace=d_ws)
 
-    for _ in range(2):
-        q8_call()
-    q8_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
-    for e in q8_ev:
-        e[0].record()
-        q8_call()
-        e[1].record()
-    torch.cuda.synchronize()
-    t_q8 = float(np.mean([e[0].elapsed_time(e[1]) for e in q8_ev]))
-    q8_bytes = synth.draft_q8_bytes(w)
-    del dq_w
+        for _ in range(2):
+            q8_call()
+        q8_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
+        for e in q8_ev:
+            e[0].record()
+            q8_call()
+            e[1].record()
+        torch.cuda.synchronize()
+        t_q8 = float(np.mean([e[0].elapsed_time(e[1]) for e in q8_ev]))
+        q8_bytes = synth.draft_q8_bytes(w)
+        del dq_w
 
     # the average-pooling compressor on the compression's input, timed on its own
     ap_out = torch.empty_like(c_out)
@@ -426,13 +430,14 @@ def main():
         r["frac"] = r["achieved"] / r["peak"]
         r["traffic"] = traffic.get(name_)
     dominant = max(rl, key=lambda k_: rl[k_]["us"])     # the step's operations only
-    rl["semi_ar_draft_kp"] = {"bound": "hbm", "achieved": kp_bytes / (t_kp * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
-                              "unit": "GB/s", "traffic": None, "algorithmic": kp_bytes, "us": t_kp * 1e3,
-                              "frac": kp_bytes / (t_kp * 1e-3) / 1e9 / HBM_PEAK_GBS, "k_prime": kp,
-                              "drafts": w.block, "outside_step": True}
-    rl["semi_ar_layer_q8"] = {"bound": "hbm", "achieved": q8_bytes / (t_q8 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
-                              "unit": "GB/s", "traffic": None, "algorithmic": q8_bytes, "us": t_q8 * 1e3,
-                              "frac": q8_bytes / (t_q8 * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
+    if t_kp is not None:
+        rl["semi_ar_draft_kp"] = {"bound": "hbm", "achieved": kp_bytes / (t_kp * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "traffic": None, "algorithmic": kp_bytes, "us": t_kp * 1e3,
+                                  "frac": kp_bytes / (t_kp * 1e-3) / 1e9 / HBM_PEAK_GBS, "k_prime": kp,
+                                  "drafts": w.block, "outside_step": True}
+        rl["semi_ar_layer_q8"] = {"bound": "hbm", "achieved": q8_bytes / (t_q8 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "traffic": None, "algorithmic": q8_bytes, "us": t_q8 * 1e3,
+                                  "frac": q8_bytes / (t_q8 * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
     rl["avg_pool_compress"] = {"bound": "hbm", "achieved": ap_bytes / (t_ap * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
                                "unit": "GB/s", "traffic": None, "algorithmic": ap_bytes, "us": t_ap * 1e3,
                                "frac": ap_bytes / (t_ap * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
@@ -472,8 +477,8 @@ def main():
         "spec_accept_logits_us": t_al * 1e3,
         "semi_ar_layer_us": t_d * 1e3,
         "semi_ar_layer_tbps": d_bytes / (t_d * 1e-3) / 1e12,
-        "semi_ar_draft_kp_us": t_kp * 1e3,
-        "semi_ar_layer_q8_us": t_q8 * 1e3,
+        "semi_ar_draft_kp_us": t_kp * 1e3 if t_kp is not None else None,
+        "semi_ar_layer_q8_us": t_q8 * 1e3 if t_q8 is not None else None,
         "avg_pool_compress_us": t_ap * 1e3,
         "latent_compress_tflops": rl["latent_compress"]["achieved"],
         "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,

@@ -669,6 +669,7 @@ __global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int 
   for (int i = tid; i < nr * dh; i += blockDim.x) {
     const int r = i / dh, e = i % dh;
     double acc = 0.0;
+#pragma unroll 8
     for (int t = 0; t < nt; ++t)
       acc = fma(ss[(size_t)r * tokens_per_split + t], (double)F[(size_t)(tok0 + t) * a.d + e], acc);
     const double sum = st[2 * r + 1];

@@ -657,9 +657,14 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
     const int r = i / D, e = i % D;
     const double sum = st[2 * r + 1];
     double acc = 0.0;
+    // every load is issued regardless of p (keys k0 .. k0 + nk - 1 all lie
+    // inside the sequence), so the unrolled loads overlap; a zero weight
+    // still adds nothing, even against a non-finite value
+#pragma unroll 8
     for (int tt = 0; tt < nk; ++tt) {
       const double p = ss[(size_t)r * keys_per_split + tt];
-      if (p != 0.0) acc = fma(p, (double)vg[kv_offset<PAGED>(a, b, hk, k0 + tt, D) + e], acc);
+      const double v = (double)vg[kv_offset<PAGED>(a, b, hk, k0 + tt, D) + e];
+      acc = fma(p, p != 0.0 ? v : 0.0, acc);
     }
     a.part_o[(base + r) * D + e] = sum > 0.0 ? (float)(acc / sum) : 0.f;
     if (e == 0)

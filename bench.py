@@ -57,6 +57,10 @@ def parse():
     ap.add_argument("--workload", default="long-video")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip timing the other workloads' compression, verification and acceptance")
+    ap.add_argument("--workload-steps", type=int, default=30,
+                    help="timed calls per operation for each of the other workloads")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for counter scaling)")
     return ap.parse_args()
@@ -92,6 +96,123 @@ def accept_logits_bytes(w, n):
     for nb in n:
         total += (2 * k + 1) * V * 4 + (2 * V if nb < k else V) * 4
     return total
+
+
+def op_stats(ms):
+    """Per-call times (ms) -> median, p10, p90 and mean in microseconds."""
+    import numpy as np
+    us = np.asarray(ms, dtype=np.float64) * 1e3
+    return {"median_us": float(np.median(us)), "p10_us": float(np.percentile(us, 10)),
+            "p90_us": float(np.percentile(us, 90)), "mean_us": float(us.mean()), "calls": int(us.size)}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+# Targets on the roofline fraction of the gated operations, per workload:
+# verification attention >= 70% of HBM peak on the long-KV workloads and
+# latent compression >= 50% of the bf16 matrix-core peak where it is
+# matrix-core bound.
+GATES = {("batched-paged", "verify_attention"): 0.70, ("long-video", "verify_attention"): 0.70,
+         ("qwen2vl-7b-video", "latent_compress"): 0.50, ("long-video", "latent_compress"): 0.50}
+
+
+def time_workload_ops(w, dev, steps, warmup):
+    """Compression, verification attention and acceptance of one workload,
+    timed in pipeline order (the three operations of the metric) with HIP
+    events on the stream they run on; inputs resident in HBM.  Returns the
+    per-operation statistics with rates and roofline fractions."""
+    import numpy as np
+    import torch
+
+    import paper_2505_12728_amd as sd
+    from paper_2505_12728_amd import synth
+
+    mode = "sampled" if "sampled" in w.modes else "greedy"
+    comp = synth.compress_inputs(w)
+    ver = synth.verify_inputs(w)
+    acc = synth.accept_inputs(w, mode)
+    lat_d, feats_d = to_dev(comp[0], dev), to_dev(comp[1], dev)
+    q_d, k_d, v_d = to_dev(ver["q"], dev), to_dev(ver["k_cache"], dev), to_dev(ver["v_cache"], dev)
+    kl_d = torch.from_numpy(ver["kv_len"]).to(dev)
+    pt_d = None if ver["page_table"] is None else torch.from_numpy(ver["page_table"]).to(dev)
+    p_d, qq_d = torch.from_numpy(acc["p"]).to(dev), torch.from_numpy(acc["q"]).to(dev)
+    dr_d, u_d = torch.from_numpy(acc["draft"]).to(dev), torch.from_numpy(acc["u"]).to(dev)
+    dt_code = sd.SD_BF16 if w.dtype == "bf16" else sd.SD_F32
+    amode = sd.SD_ACCEPT_SAMPLED if mode == "sampled" else sd.SD_ACCEPT_GREEDY
+    c_out = torch.empty((w.c_batch, w.c_latents, w.c_width), dtype=torch.float32, device=dev)
+    c_ws_n = sd.sd_latent_compress_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width,
+                                                  w.c_heads, dt_code)
+    c_ws = torch.empty(c_ws_n, dtype=torch.uint8, device=dev) if c_ws_n else None
+    v_out = torch.empty((w.batch, w.block, w.hq, w.head_dim), dtype=torch.float32, device=dev)
+    v_lse = torch.empty((w.batch, w.block, w.hq), dtype=torch.float32, device=dev)
+    cap = w.kv_len if not w.paged else 16 * ver["max_pages"]
+    v_ws = torch.empty(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
+                                                   dt_code), dtype=torch.uint8, device=dev)
+    a_ws = torch.empty(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
+                       dtype=torch.uint8, device=dev)
+    n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
+    t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
+    scale = 1.0 / math.sqrt(w.head_dim)
+
+    def one(ev=None):
+        if ev is not None:
+            ev[0].record()
+        sd.sd_latent_compress(lat_d, feats_d, w.c_heads, 1.0, out=c_out, workspace=c_ws)
+        if ev is not None:
+            ev[1].record()
+        sd.sd_verify_attention(q_d, k_d, v_d, kl_d, scale=scale, page_table=pt_d, out=v_out,
+                               lse=v_lse, workspace=v_ws)
+        if ev is not None:
+            ev[2].record()
+        sd.sd_spec_accept(p_d, qq_d, dr_d, u_d, amode, n_accepted=n_out, tokens=t_out,
+                          workspace=a_ws)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for e in events:
+        one(e)
+    torch.cuda.synchronize()
+    comp_ms = [e[0].elapsed_time(e[1]) for e in events]
+    ver_ms = [e[1].elapsed_time(e[2]) for e in events]
+    acc_ms = [e[2].elapsed_time(e[3]) for e in events]
+    kv_bytes = synth.verify_kv_bytes(w, ver["kv_len"])
+    flops = synth.compress_flops(w)
+    a_bytes = accept_bytes(acc["p"], n_out.cpu().numpy())
+    peak_c = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_VALU_PEAK_TFLOPS
+    out = {"dtype": w.dtype, "accept_mode": mode}
+    for name, ms, work, peak, unit in (
+            ("latent_compress", comp_ms, flops, peak_c, "TFLOP/s"),
+            ("verify_attention", ver_ms, kv_bytes, HBM_PEAK_GBS, "GB/s"),
+            ("spec_accept", acc_ms, a_bytes, HBM_PEAK_GBS, "GB/s")):
+        st = op_stats(ms)
+        scale_ = 1e12 if unit == "TFLOP/s" else 1e9
+        rate = work / (st["median_us"] * 1e-6) / scale_
+        st.update({"algorithmic": work, "unit": unit, "achieved_at_median": rate, "peak": peak,
+                   "frac_at_median": rate / peak,
+                   "frac_at_p90": work / (st["p90_us"] * 1e-6) / scale_ / peak})
+        gate = GATES.get((w.name, name))
+        if gate is not None:
+            st["target_frac"] = gate
+            st["target_met_at_median"] = bool(st["frac_at_median"] >= gate)
+        out[name] = st
+    vs = [a + b for a, b in zip(ver_ms, acc_ms)]
+    out["verify_step"] = op_stats(vs)
+    out["verify_step"]["kv_read_tbps_at_median"] = kv_bytes / (out["verify_step"]["median_us"] * 1e-6) / 1e12
+    return out
 
 
 def cpu_baseline(w, comp, ver, acc, mode, lm, accl, dr):
@@ -151,7 +272,7 @@ def cpu_baseline(w, comp, ver, acc, mode, lm, accl, dr):
                          dr["pos"][:1], dr["hq"], dr["hkv"], dr["eps"], dr["theta"])
     td = (time.perf_counter() - t0) * dr["u"].shape[0]
     return {"compress_s": tc, "verify_s": tv, "accept_s": ta, "lm_head_s": tl, "accept_logits_s": tal,
-            "draft_layer_s": td, "threads": threads,
+            "draft_layer_s": td, "threads": threads, "cpu_model": cpu_model(),
             "sample": f"compress {len(pairs_c)} of {w.c_batch * w.c_heads} (sequence, head) "
                       f"pairs, verify {len(pairs_v)} of {w.batch * w.hkv} (sequence, KV head) "
                       f"pairs, acceptance (from p, q and from logits) of all {w.batch} sequences, "
@@ -393,14 +514,21 @@ def main():
     c_bytes = synth.compress_bytes(w)
     n_host = n_out.cpu().numpy()
     a_bytes = accept_bytes(acc["p"], n_host)
+    # Rooflines use each kernel's mean duration over the timed steps (the
+    # figure a rocprofv3 kernel trace averages); `ops` adds medians and the
+    # p10 / p90 spread, and `value` is taken at the medians.
     t_c, t_v, t_a = float(comp_ms.mean()), float(ver_ms.mean()), float(acc_ms.mean())
     t_l = float(lm_ms.mean())
     t_al = float(accl_ms.mean())
     t_d = float(draft_ms.mean())
+    ops = {"latent_compress": op_stats(comp_ms), "verify_attention": op_stats(ver_ms),
+           "spec_accept": op_stats(acc_ms), "lm_head": op_stats(lm_ms),
+           "spec_accept_logits": op_stats(accl_ms), "semi_ar_layer": op_stats(draft_ms),
+           "verify_step": op_stats(ver_ms + acc_ms)}
     d_bytes = synth.draft_bytes(w)
     al_bytes = accept_logits_bytes(w, nl_out.cpu().numpy())
     l_bytes = synth.lm_bytes(w, lm_rows)
-    verify_step_ms = t_v + t_a
+    verify_step_ms = ops["verify_step"]["median_us"] * 1e-3
     value = kv_bytes / (verify_step_ms * 1e-3) / 1e12
 
     peak_c = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_VALU_PEAK_TFLOPS
@@ -469,9 +597,9 @@ def main():
             "draft_rows": dB * dr_rows, "draft_ffn": dI, "draft_ctx": w.draft_ctx,
         },
         "verify_step_us": verify_step_ms * 1e3,
-        "verify_attention_us": t_v * 1e3,
-        "spec_accept_us": t_a * 1e3,
-        "latent_compress_us": t_c * 1e3,
+        "verify_attention_us": ops["verify_attention"]["median_us"],
+        "spec_accept_us": ops["spec_accept"]["median_us"],
+        "latent_compress_us": ops["latent_compress"]["median_us"],
         "lm_head_us": t_l * 1e3,
         "lm_head_tbps": l_bytes / (t_l * 1e-3) / 1e12,
         "spec_accept_logits_us": t_al * 1e3,
@@ -480,8 +608,11 @@ def main():
         "semi_ar_draft_kp_us": t_kp * 1e3 if t_kp is not None else None,
         "semi_ar_layer_q8_us": t_q8 * 1e3 if t_q8 is not None else None,
         "avg_pool_compress_us": t_ap * 1e3,
-        "latent_compress_tflops": rl["latent_compress"]["achieved"],
-        "kv_read_tbps_attention_only": kv_bytes / (t_v * 1e-3) / 1e12,
+        "latent_compress_tflops": flops / (ops["latent_compress"]["median_us"] * 1e-6) / 1e12,
+        "kv_read_tbps_attention_only": kv_bytes / (ops["verify_attention"]["median_us"] * 1e-6) / 1e12,
+        "ops": ops,
+        "timing": "value and the *_us figures: medians over the timed steps (HIP events on the "
+                  "kernels' stream); ops: median, p10, p90, mean; rooflines: mean launch duration",
         "accepted_mean": float(n_host.mean()),
         "roofline": roof,
         "rooflines": rl,
@@ -492,13 +623,41 @@ def main():
         cpu_step = cb["verify_s"] + cb["accept_s"]
         result["cpu_baseline"] = {
             "value": kv_bytes / cpu_step / 1e12, "unit": "TB/s", "cores": cb["threads"],
-            "kind": "oracle", "sample": cb["sample"],
+            "cpu_model": cb["cpu_model"], "kind": "oracle", "sample": cb["sample"],
             "verify_step_s": cpu_step, "latent_compress_s": cb["compress_s"],
             "lm_head_s": cb["lm_head_s"], "accept_logits_s": cb["accept_logits_s"],
             "draft_layer_s": cb["draft_layer_s"],
             "whole_step_s": cpu_step + cb["compress_s"] + cb["lm_head_s"] + cb["accept_logits_s"]
                             + cb["draft_layer_s"],
         }
+    if not args.no_workloads:
+        # the other workloads' compression, verification and acceptance in the
+        # same run (the main workload's operations are in `ops`)
+        wl = {}
+        for other in synth.WORKLOADS:
+            if other.name == w.name:
+                continue
+            print(f"[bench] timing workload {other.name}", file=sys.stderr, flush=True)
+            wl[other.name] = time_workload_ops(other, dev, args.workload_steps, args.warmup)
+        main_ = {"dtype": w.dtype, "accept_mode": mode}
+        for name_, work_, unit_, peak_ in (("latent_compress", flops, "TFLOP/s", peak_c),
+                                           ("verify_attention", kv_bytes, "GB/s", HBM_PEAK_GBS),
+                                           ("spec_accept", a_bytes, "GB/s", HBM_PEAK_GBS)):
+            st_ = dict(ops[name_])
+            sc_ = 1e12 if unit_ == "TFLOP/s" else 1e9
+            rate_ = work_ / (st_["median_us"] * 1e-6) / sc_
+            st_.update({"algorithmic": work_, "unit": unit_, "achieved_at_median": rate_, "peak": peak_,
+                        "frac_at_median": rate_ / peak_,
+                        "frac_at_p90": work_ / (st_["p90_us"] * 1e-6) / sc_ / peak_})
+            gate_ = GATES.get((w.name, name_))
+            if gate_ is not None:
+                st_["target_frac"] = gate_
+                st_["target_met_at_median"] = bool(st_["frac_at_median"] >= gate_)
+            main_[name_] = st_
+        main_["verify_step"] = dict(ops["verify_step"])
+        main_["verify_step"]["kv_read_tbps_at_median"] = value
+        wl[w.name] = main_
+        result["workloads"] = {o.name: wl[o.name] for o in synth.WORKLOADS if o.name in wl}
     print(json.dumps(result), flush=True)
 
 

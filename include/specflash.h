@@ -26,8 +26,10 @@
  * ---------------------------------------
  * - Every tensor pointer is DEVICE memory on the current HIP device, owned by
  *   the caller, dense and row-major in the layout given at each call.  The
- *   library never allocates, frees or keeps device memory and holds no
- *   global state; calls are thread-safe.
+ *   library never allocates, frees or keeps device memory.  Its only global
+ *   state is a per-device cache of the compute-unit count (filled on the
+ *   first call on a device with the value the runtime reports, never
+ *   changed afterwards); calls are thread-safe.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *   Work is enqueued asynchronously; no call synchronises the host.
  * - Return value: an sd_status.  Arguments are validated on the host before
@@ -329,8 +331,8 @@ int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R,
  *             of the current device, so size it on the device of the call)
  * Accumulation in fp32 on bf16 matrix cores; the weight is read once per
  * pass of up to 128 input rows.
- * Requirements: R >= 1; K a multiple of 256 (at most 2^20); N >= 1; R * N
- * <= 2^31; x and w 16-byte aligned.  Errors: SD_ERR_INVALID_ARG (NULL or
+ * Requirements: 1 <= R <= 65535; K a multiple of 256 (at most 2^20); N >= 1;
+ * R * N <= 2^31; x and w 16-byte aligned.  Errors: SD_ERR_INVALID_ARG (NULL or
  * misaligned pointers), SD_ERR_UNSUPPORTED (shape outside the
  * requirements), SD_ERR_WORKSPACE (missing or short workspace).
  * ---------------------------------------------------------------------- */
@@ -376,8 +378,8 @@ int sd_linear(const void* x, const void* w, const float* bias, const float* resi
  *   workspace  sd_semi_ar_layer_workspace_size(...) bytes, 256-byte aligned
  *            (device-dependent like sd_linear's)
  * Requirements: d = Hq * D with D in {64, 128}; Hq % Hkv == 0; 1 <= r <= 16;
- * r * (Hq / Hkv) <= 256; d and I multiples of 256; Lmax >= r; eps >= 0;
- * theta > 0.  Errors as for sd_linear.
+ * r * (Hq / Hkv) <= 256; d and I multiples of 256; Lmax >= r; B * r <=
+ * 65535; eps >= 0; theta > 0.  Errors as for sd_linear.
  * ---------------------------------------------------------------------- */
 size_t sd_semi_ar_layer_workspace_size(int B, int r, int d, int num_q_heads, int num_kv_heads,
                                        int I, int Lmax);

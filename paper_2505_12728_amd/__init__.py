@@ -134,6 +134,23 @@ def _check(t, name, dtype=None, ndim=None):
         raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
 
 
+def _out(t, name, shape, dtype, device):
+    """A caller-supplied output (or workspace) must be a contiguous tensor of
+    exactly the expected shape and dtype on the inputs' device: the kernels
+    write its whole extent, so a short buffer would be overrun on the device."""
+    _check(t, name, dtype=dtype)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    return t
+
+
+def _same_device(name, t, device):
+    if t is not None and t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+
+
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
@@ -148,6 +165,8 @@ def _workspace(nbytes, device, given):
     if nbytes == 0:
         return None, 0
     if given is not None:
+        _check(given, "workspace")
+        _same_device("workspace", given, device)
         return given, given.numel() * given.element_size()
     torch = _torch()
     return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
@@ -175,9 +194,10 @@ def sd_latent_compress(latents, feats, num_heads=1, scale=1.0, out=None, workspa
     if d2 != d:
         raise ValueError("latents and feats disagree on the feature width")
     dt = _dtype_code(latents)
+    _same_device("feats", feats, latents.device)
     if out is None:
         out = torch.empty((B, C, d), dtype=torch.float32, device=feats.device)
-    _check(out, "out", dtype=torch.float32)
+    _out(out, "out", (B, C, d), torch.float32, feats.device)
     ws_bytes = sd_latent_compress_workspace_size(B, N, C, d, num_heads, dt)
     ws, ws_len = _workspace(ws_bytes, feats.device, workspace)
     st = library().sd_latent_compress(_ptr(latents), _ptr(feats), _ptr(out), B, N, C, d,
@@ -200,6 +220,9 @@ def sd_verify_attention(q, k_cache, v_cache, kv_len, scale=None, page_table=None
     q [B, k, Hq, D]; caches [B, Lmax, Hkv, D], or page pools [P, Hkv, 16, D]
     with page_table [B, max_pages] int32; kv_len [B] int32 (block included).
     Returns (out [B, k, Hq, D] fp32, lse [B, k, Hq] fp32 or None).
+    ``scale`` multiplies q . k; the paper names no scale, and None passes the
+    standard attention scale 1 / sqrt(D) to the library explicitly (the C
+    entry point itself takes the scale as a required argument).
     """
     torch = _torch()
     _check(q, "q", ndim=4)
@@ -229,15 +252,17 @@ def sd_verify_attention(q, k_cache, v_cache, kv_len, scale=None, page_table=None
         num_pages_ = k_cache.shape[0] if num_pages is None else num_pages
         Lmax = 0
         capacity = 16 * max_pages
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("kv_len", kv_len),
+                    ("page_table", page_table)):
+        _same_device(name, t, q.device)
     if out is None:
         out = torch.empty((B, k, Hq, D), dtype=torch.float32, device=q.device)
-    _check(out, "out", dtype=torch.float32)
+    _out(out, "out", (B, k, Hq, D), torch.float32, q.device)
     lse_t = None
     if lse is True:
         lse_t = torch.empty((B, k, Hq), dtype=torch.float32, device=q.device)
     elif lse is not None and lse is not False:
-        lse_t = lse
-        _check(lse_t, "lse", dtype=torch.float32)
+        lse_t = _out(lse, "lse", (B, k, Hq), torch.float32, q.device)
     ws_bytes = sd_verify_workspace_size(B, k, Hq, Hkv, D, capacity, dt)
     ws, ws_len = _workspace(ws_bytes, q.device, workspace)
     st = library().sd_verify_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
@@ -270,10 +295,15 @@ def sd_spec_accept(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, toke
         _check(u, "u", dtype=torch.float32, ndim=2)
         if tuple(q.shape) != (B, k, V) or tuple(u.shape) != (B, k + 1):
             raise ValueError("q must be [B, k, V] and u [B, k+1]")
+    for name, t in (("q", q if mode == SD_ACCEPT_SAMPLED else None), ("draft", draft),
+                    ("u", u if mode == SD_ACCEPT_SAMPLED else None)):
+        _same_device(name, t, p.device)
     if n_accepted is None:
         n_accepted = torch.empty((B,), dtype=torch.int32, device=p.device)
     if tokens is None:
         tokens = torch.empty((B, k + 1), dtype=torch.int32, device=p.device)
+    _out(n_accepted, "n_accepted", (B,), torch.int32, p.device)
+    _out(tokens, "tokens", (B, k + 1), torch.int32, p.device)
     ws_bytes = sd_spec_accept_workspace_size(B, k, V, mode)
     ws, ws_len = _workspace(ws_bytes, p.device, workspace)
     st = library().sd_spec_accept(_ptr(p), _ptr(q), _ptr(draft), _ptr(u), _ptr(n_accepted),
@@ -305,10 +335,16 @@ def sd_spec_accept_logits(target_logits, draft_logits, draft, seed, offset, temp
         if tuple(draft_logits.shape) != (B, k, V):
             raise ValueError("draft_logits must be [B, k, V]")
     dt = _dtype_code(target_logits)
+    dev = target_logits.device
+    _same_device("draft", draft, dev)
+    if mode == SD_ACCEPT_SAMPLED:
+        _same_device("draft_logits", draft_logits, dev)
     if n_accepted is None:
-        n_accepted = torch.empty((B,), dtype=torch.int32, device=target_logits.device)
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=dev)
     if tokens is None:
-        tokens = torch.empty((B, k + 1), dtype=torch.int32, device=target_logits.device)
+        tokens = torch.empty((B, k + 1), dtype=torch.int32, device=dev)
+    _out(n_accepted, "n_accepted", (B,), torch.int32, dev)
+    _out(tokens, "tokens", (B, k + 1), torch.int32, dev)
     ws_bytes = sd_spec_accept_logits_workspace_size(B, k, V, mode)
     ws, ws_len = _workspace(ws_bytes, target_logits.device, workspace)
     st = library().sd_spec_accept_logits(_ptr(target_logits), _ptr(draft_logits), _ptr(draft),
@@ -324,7 +360,7 @@ def sd_philox_uniforms(seed, offset, B, n, out=None, device=None, stream=None):
     torch = _torch()
     if out is None:
         out = torch.empty((B, n), dtype=torch.float32, device=device or "cuda")
-    _check(out, "out", dtype=torch.float32, ndim=2)
+    _out(out, "out", (B, n), torch.float32, out.device)
     st = library().sd_philox_uniforms(int(seed), int(offset), _ptr(out), B, n, _stream(stream))
     _raise(st, "sd_philox_uniforms")
     return out
@@ -345,8 +381,10 @@ def sd_lm_head_probs(hidden, weight, temperature, out=None, workspace=None, stre
     if weight.shape[1] != d:
         raise ValueError("weight must be [V, d] with the hidden width d")
     dt = _dtype_code(hidden)
+    _same_device("weight", weight, hidden.device)
     if out is None:
         out = torch.empty((R, V), dtype=torch.float32, device=hidden.device)
+    _out(out, "out", (R, V), torch.float32, hidden.device)
     ws_bytes = sd_lm_head_workspace_size(R, d, V, dt)
     ws, ws_len = _workspace(ws_bytes, hidden.device, workspace)
     st = library().sd_lm_head_probs(_ptr(hidden), _ptr(weight), _ptr(out), R, d, V,
@@ -368,8 +406,10 @@ def sd_sample_tokens(probs, u, out=None, workspace=None, stream=None):
     R, V = probs.shape
     if u.shape[0] != R:
         raise ValueError("u must be [R]")
+    _same_device("u", u, probs.device)
     if out is None:
         out = torch.empty((R,), dtype=torch.int32, device=probs.device)
+    _out(out, "out", (R,), torch.int32, probs.device)
     ws_bytes = sd_sample_workspace_size(R, V)
     ws, ws_len = _workspace(ws_bytes, probs.device, workspace)
     st = library().sd_sample_tokens(_ptr(probs), _ptr(u), _ptr(out), R, V, _ptr(ws), ws_len,
@@ -400,8 +440,11 @@ def sd_linear(x, w, bias=None, residual=None, out=None, workspace=None, stream=N
         _check(residual, "residual", dtype=torch.float32, ndim=2)
         if tuple(residual.shape) != (R, N):
             raise ValueError("residual must be [R, N]")
+    for name, t in (("w", w), ("bias", bias), ("residual", residual)):
+        _same_device(name, t, x.device)
     if out is None:
         out = torch.empty((R, N), dtype=torch.float32, device=x.device)
+    _out(out, "out", (R, N), torch.float32, x.device)
     ws_bytes = sd_linear_workspace_size(R, K, N)
     ws, ws_len = _workspace(ws_bytes, x.device, workspace)
     st = library().sd_linear(_ptr(x), _ptr(w), _ptr(bias), _ptr(residual), _ptr(out), R, K, N,
@@ -446,8 +489,12 @@ def sd_semi_ar_layer(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, out
         raise ValueError("caches must be [B, Lmax, hkv, d / hq]")
     if pos.shape[0] != B:
         raise ValueError("pos must be [B]")
+    for name, t in [(n, weights[n]) for n in SEMI_AR_WEIGHTS] + [
+            ("k_cache", k_cache), ("v_cache", v_cache), ("pos", pos)]:
+        _same_device(name, t, u.device)
     if out is None:
         out = torch.empty((B, r, d), dtype=torch.float32, device=u.device)
+    _out(out, "out", (B, r, d), torch.float32, u.device)
     ws_bytes = sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax)
     ws, ws_len = _workspace(ws_bytes, u.device, workspace)
     W = weights
@@ -490,10 +537,26 @@ def sd_semi_ar_draft(u0, weights, lm_w, emb, ph, k_cache, v_cache, pos, u, K, kp
     _check(pos, "pos", dtype=torch.int32, ndim=1)
     Lmax = k_cache.shape[1]
     I = weights["wdown"].shape[1]
+    D = d // hq
+    shapes = {"fc_w": (d, 2 * d), "fc_b": (d,), "ln1": (d,), "wqkv": ((hq + 2 * hkv) * D, d),
+              "wo": (d, hq * D), "ln2": (d,), "wgu": (2 * I, d), "wdown": (d, I)}
+    for name, shp in shapes.items():
+        if tuple(weights[name].shape) != shp:
+            raise ValueError(f"{name} must be {shp}, got {tuple(weights[name].shape)}")
+    if tuple(k_cache.shape) != (B, Lmax, hkv, D) or tuple(v_cache.shape) != (B, Lmax, hkv, D):
+        raise ValueError("caches must be [B, Lmax, hkv, d / hq]")
+    if pos.shape[0] != B:
+        raise ValueError("pos must be [B]")
+    for name, t in [(n, weights[n]) for n in SEMI_AR_WEIGHTS] + [
+            ("lm_w", lm_w), ("emb", emb), ("ph", ph), ("k_cache", k_cache),
+            ("v_cache", v_cache), ("pos", pos), ("u", u)]:
+        _same_device(name, t, u0.device)
     if tokens is None:
         tokens = torch.empty((B, K), dtype=torch.int32, device=u0.device)
     if q is None:
         q = torch.empty((B, K, V), dtype=torch.float32, device=u0.device)
+    _out(tokens, "tokens", (B, K), torch.int32, u0.device)
+    _out(q, "q", (B, K, V), torch.float32, u0.device)
     ws_bytes = sd_semi_ar_draft_workspace_size(B, r0, d, hq, hkv, I, Lmax, V, K, kp)
     ws, ws_len = _workspace(ws_bytes, u0.device, workspace)
     W = weights
@@ -520,10 +583,17 @@ def sd_linear_q8(x, wq, scale, bias=None, residual=None, out=None, workspace=Non
         raise ValueError("wq must be [N, K] and scale [N]")
     if bias is not None:
         _check(bias, "bias", dtype=torch.float32, ndim=1)
+        if bias.shape[0] != N:
+            raise ValueError("bias must be [N]")
     if residual is not None:
         _check(residual, "residual", dtype=torch.float32, ndim=2)
+        if tuple(residual.shape) != (R, N):
+            raise ValueError("residual must be [R, N]")
+    for name, t in (("wq", wq), ("scale", scale), ("bias", bias), ("residual", residual)):
+        _same_device(name, t, x.device)
     if out is None:
         out = torch.empty((R, N), dtype=torch.float32, device=x.device)
+    _out(out, "out", (R, N), torch.float32, x.device)
     ws_bytes = sd_linear_workspace_size(R, K, N)
     ws, ws_len = _workspace(ws_bytes, x.device, workspace)
     st = library().sd_linear_q8(_ptr(x), _ptr(wq), _ptr(scale), _ptr(bias), _ptr(residual), _ptr(out), R, K, N,
@@ -561,8 +631,21 @@ def sd_semi_ar_layer_q8(u, weights, k_cache, v_cache, pos, hq, hkv, eps, theta, 
     for name, shp in shapes.items():
         if tuple(weights[name].shape) != shp:
             raise ValueError(f"{name} must be {shp}, got {tuple(weights[name].shape)}")
+    for name in ("fc_b", "ln1", "ln2"):
+        if tuple(weights[name].shape) != (d,):
+            raise ValueError(f"{name} must be ({d},)")
+    if tuple(k_cache.shape) != (B, Lmax, hkv, D) or tuple(v_cache.shape) != (B, Lmax, hkv, D):
+        raise ValueError("caches must be [B, Lmax, hkv, d / hq]")
+    if pos.shape[0] != B:
+        raise ValueError("pos must be [B]")
+    for name, t in [(n, weights[n]) for n in Q8_WEIGHTS] + [
+            (n + "_s", weights[n + "_s"]) for n in Q8_WEIGHTS] + [
+            (n, weights[n]) for n in ("fc_b", "ln1", "ln2")] + [
+            ("k_cache", k_cache), ("v_cache", v_cache), ("pos", pos)]:
+        _same_device(name, t, u.device)
     if out is None:
         out = torch.empty((B, r, d), dtype=torch.float32, device=u.device)
+    _out(out, "out", (B, r, d), torch.float32, u.device)
     ws_bytes = sd_semi_ar_layer_workspace_size(B, r, d, hq, hkv, I, Lmax)
     ws, ws_len = _workspace(ws_bytes, u.device, workspace)
     W = weights
@@ -584,6 +667,7 @@ def sd_avg_pool_compress(feats, C, out=None, stream=None):
     B, N, d = feats.shape
     if out is None:
         out = torch.empty((B, C, d), dtype=torch.float32, device=feats.device)
+    _out(out, "out", (B, C, d), torch.float32, feats.device)
     st = library().sd_avg_pool_compress(_ptr(feats), _ptr(out), B, N, C, d, _dtype_code(feats), _stream(stream))
     _raise(st, "sd_avg_pool_compress")
     return out

@@ -1,8 +1,11 @@
 // C ABI entry points: host-side validation, planning and launch.  Nothing is
 // enqueued unless every argument check passes; the library allocates no
-// device memory and keeps no state between calls.
+// device memory.  Its only state is the per-device cache of compute-unit
+// counts below (written once per device with the value the runtime reports).
 #include <math.h>
 #include <stdint.h>
+
+#include <atomic>
 
 #include "../../include/specflash.h"
 #include "launch.hpp"
@@ -63,16 +66,21 @@ const char* sd_status_string(int status) {
 int sd_version(void) { return (1 << 16) | 0; }
 
 // Compute units of the current device (cached per device; 256 when no
-// device can be queried, e.g. for sizing on a host without a GPU).
+// device can be queried, e.g. for sizing on a host without a GPU).  Every
+// writer stores the same value, and the atomics make concurrent first calls
+// from several host threads well defined.
 static int device_cus() {
-  static int cached[64];
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
-  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  if (dev < 64) {
+    const int c = cached[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
   int n = 0;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
     return 256;
-  if (dev < 64) cached[dev] = n;
+  if (dev < 64) cached[dev].store(n, std::memory_order_relaxed);
   return n;
 }
 
@@ -320,7 +328,7 @@ int sd_sample_tokens(const float* probs, const float* u, int32_t* tokens, int R,
 
 // ------------------------------------------------------------ draft layer
 static bool linear_shape_ok(int R, int K, int N) {
-  return R >= 1 && R <= (1 << 20) && K >= 256 && K % 256 == 0 && K <= (1 << 20) && N >= 1 && N <= (1 << 24) &&
+  return R >= 1 && R <= 65535 && K >= 256 && K % 256 == 0 && K <= (1 << 20) && N >= 1 && N <= (1 << 24) &&
          (long long)R * N <= (1LL << 31);
 }
 
@@ -352,7 +360,7 @@ static bool semi_ar_shape_ok(int B, int r, int d, int Hq, int Hkv, int I, int Lm
   *status = SD_ERR_UNSUPPORTED;
   const int D = d / Hq;
   if (r > 16 || (D != 64 && D != 128) || r * (Hq / Hkv) > 256 || d % 256 != 0 || I % 256 != 0 ||
-      Lmax < r || (long long)B * r > (1 << 16) || (long long)B * Lmax * Hkv * D > (1LL << 40))
+      Lmax < r || (long long)B * r > 65535 || (long long)B * Lmax * Hkv * D > (1LL << 40))
     return false;
   *status = SD_OK;
   return true;

@@ -49,16 +49,13 @@ def test_lm_head_workloads(name):
     check_probs(gpu, ref, z, w.dtype, name)
 
 
-def test_lm_head_long_video_sampled_rows():
-    # full size (36 rows, d 8192, V 152064, tau 0.7); the oracle checks a
-    # sample of rows, one from each 16-row block
+def test_lm_head_long_video_every_row():
+    # full size (36 rows, d 8192, V 152064, tau 0.7), every probability
     w = synth.workload("long-video")
     inp = synth.lm_inputs(w)
     gpu = run_probs(inp["hidden"], inp["weight"], inp["temperature"])
-    rows = [0, 17, 35]
-    ref, z = ref_probs(inp["hidden"], inp["weight"], inp["temperature"], rows)
-    check_probs(gpu[rows], ref, z, "bf16", "long-video")
-    assert np.allclose(gpu.sum(axis=1), 1.0, atol=1e-4)
+    ref, z = ref_probs(inp["hidden"], inp["weight"], inp["temperature"])
+    check_probs(gpu, ref, z, "bf16", "long-video")
 
 
 @pytest.mark.parametrize("R,d,V,tau", [(1, 64, 1, 1.0), (1, 64, 37, 0.5), (5, 128, 1000, 0.05),

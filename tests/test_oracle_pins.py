@@ -437,6 +437,37 @@ def test_residual_weights_fixed_point():
     assert list(R2) == [2 ** 40]
 
 
+def test_residual_weights_clamp_above_one():
+    # Probabilities lie in [0, 1]; a value above 1 (invalid input, used as
+    # given rather than renormalised) weighs exactly as 1, i.e. 2^40.  Hand
+    # values: residuals [3 - 1, 1.5 - 0, 0.5 - 0] = [2, 1.5, 0.5] give
+    # [2^40, 2^40, 2^39]; the bonus weights of [1.25, 0.5, 4.0] (no q) give
+    # [2^40, 2^39, 2^40].
+    p = np.array([3.0, 1.5, 0.5], np.float32)
+    q = np.array([1.0, 0.0, 0.0], np.float32)
+    assert list(oracle.residual_weights(p, q)) == [2 ** 40, 2 ** 40, 2 ** 39]
+    assert list(oracle.residual_weights(np.array([1.25, 0.5, 4.0], np.float32))) == \
+        [2 ** 40, 2 ** 39, 2 ** 40]
+    # A row [3, 1] then draws either token with probability exactly 1/2:
+    # S = 2^41, T = a * 2^17, token 0 iff T < 2^40 iff a < 2^23.
+    R = oracle.residual_weights(np.array([3.0, 1.0], np.float32))
+    assert oracle.fixed_point_sample(R, (1 << 23) - 1) == 0
+    assert oracle.fixed_point_sample(R, 1 << 23) == 1
+    # Through the whole rule: the draft (token 0, q = 1) is rejected by
+    # u = 0.75 only if 0.75 * 1 >= p = 3 -- it is accepted, so the final
+    # draw comes from the bonus row p_1 = [5, 0.25]: weights [2^40, 2^38],
+    # S = 1.25 * 2^40, u_1 = 0.5 gives T = 0.625 * 2^40 < 2^40: token 0.
+    pr = np.array([[[3.0, 0.0], [5.0, 0.25]]], np.float32)
+    qr = np.array([[[1.0, 0.0]]], np.float32)
+    n, tok = oracle.spec_accept(pr, qr, np.array([[0]], np.int32),
+                                np.array([[0.75, 0.5]], np.float32), oracle.ACCEPT_SAMPLED)
+    assert int(n[0]) == 1 and list(tok[0]) == [0, 0]
+    # u_1 = 0.9: T = floor(0.9 * 2^24) * 1.25 * 2^40 / 2^24 >= 2^40: token 1
+    n, tok = oracle.spec_accept(pr, qr, np.array([[0]], np.int32),
+                                np.array([[0.75, 0.9]], np.float32), oracle.ACCEPT_SAMPLED)
+    assert int(n[0]) == 1 and list(tok[0]) == [0, 1]
+
+
 def test_fixed_point_sample_matches_python_integers():
     r = rng(33)
     R = r.integers(0, 2 ** 40, size=300).astype(np.uint64)

@@ -152,13 +152,13 @@ def time_workload_ops(w, dev, steps, warmup):
     c_out = torch.empty((w.c_batch, w.c_latents, w.c_width), dtype=torch.float32, device=dev)
     c_ws_n = sd.sd_latent_compress_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width,
                                                   w.c_heads, dt_code)
-    c_ws = torch.empty(c_ws_n, dtype=torch.uint8, device=dev) if c_ws_n else None
+    c_ws = torch.zeros(c_ws_n, dtype=torch.uint8, device=dev) if c_ws_n else None
     v_out = torch.empty((w.batch, w.block, w.hq, w.head_dim), dtype=torch.float32, device=dev)
     v_lse = torch.empty((w.batch, w.block, w.hq), dtype=torch.float32, device=dev)
     cap = w.kv_len if not w.paged else 16 * ver["max_pages"]
-    v_ws = torch.empty(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
+    v_ws = torch.zeros(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
                                                    dt_code), dtype=torch.uint8, device=dev)
-    a_ws = torch.empty(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
+    a_ws = torch.zeros(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
                        dtype=torch.uint8, device=dev)
     n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
@@ -358,26 +358,26 @@ def main():
     c_out = torch.empty((w.c_batch, w.c_latents, w.c_width), dtype=torch.float32, device=dev)
     c_ws_n = sd.sd_latent_compress_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width,
                                                   w.c_heads, dt_code)
-    c_ws = torch.empty(max(c_ws_n, 1), dtype=torch.uint8, device=dev) if c_ws_n else None
+    c_ws = torch.zeros(max(c_ws_n, 1), dtype=torch.uint8, device=dev) if c_ws_n else None
     v_out = torch.empty((w.batch, w.block, w.hq, w.head_dim), dtype=torch.float32, device=dev)
     v_lse = torch.empty((w.batch, w.block, w.hq), dtype=torch.float32, device=dev)
     cap = w.kv_len if not w.paged else 16 * ver["max_pages"]
-    v_ws = torch.empty(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
+    v_ws = torch.zeros(sd.sd_verify_workspace_size(w.batch, w.block, w.hq, w.hkv, w.head_dim, cap,
                                                    dt_code), dtype=torch.uint8, device=dev)
-    a_ws = torch.empty(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
+    a_ws = torch.zeros(max(1, sd.sd_spec_accept_workspace_size(w.batch, w.block, w.vocab, amode)),
                        dtype=torch.uint8, device=dev)
     lm_rows = lm["hidden"].shape[0]
     lm_out = torch.empty((lm_rows, w.vocab), dtype=torch.float32, device=dev)
-    lm_ws = torch.empty(sd.sd_lm_head_workspace_size(lm_rows, w.lm_width, w.vocab, dt_code),
+    lm_ws = torch.zeros(sd.sd_lm_head_workspace_size(lm_rows, w.lm_width, w.vocab, dt_code),
                         dtype=torch.uint8, device=dev)
     n_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     t_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
-    al_ws = torch.empty(sd.sd_spec_accept_logits_workspace_size(w.batch, w.block, w.vocab, amode),
+    al_ws = torch.zeros(sd.sd_spec_accept_logits_workspace_size(w.batch, w.block, w.vocab, amode),
                         dtype=torch.uint8, device=dev)
     nl_out = torch.empty((w.batch,), dtype=torch.int32, device=dev)
     dB, dr_rows, dd, _, _, dI, dL = synth.draft_dims(w)
     d_out = torch.empty((dB, dr_rows, dd), dtype=torch.float32, device=dev)
-    d_ws = torch.empty(sd.sd_semi_ar_layer_workspace_size(dB, dr_rows, dd, dr["hq"], dr["hkv"], dI, dL),
+    d_ws = torch.zeros(sd.sd_semi_ar_layer_workspace_size(dB, dr_rows, dd, dr["hq"], dr["hkv"], dI, dL),
                        dtype=torch.uint8, device=dev)
     tl_out = torch.empty((w.batch, w.block + 1), dtype=torch.int32, device=dev)
     scale = 1.0 / math.sqrt(w.head_dim)
@@ -441,7 +441,7 @@ def main():
     u0_d = to_dev(synth.Tensor(u0_np, "bf16"), dev)
     ph_d = to_dev(synth.Tensor(ph_np, "bf16"), dev)
     uk_d = torch.from_numpy((rng.integers(0, 1 << 24, size=(dB, w.block)) * 2.0 ** -24).astype(np.float32)).to(dev)
-    kp_ws = torch.empty(sd.sd_semi_ar_draft_workspace_size(dB, 1 + kp, dd, dr["hq"], dr["hkv"], dI, dL, w.vocab,
+    kp_ws = torch.zeros(sd.sd_semi_ar_draft_workspace_size(dB, 1 + kp, dd, dr["hq"], dr["hkv"], dI, dL, w.vocab,
                                                            w.block, kp), dtype=torch.uint8, device=dev)
     kp_tok = torch.empty((dB, w.block), dtype=torch.int32, device=dev)
     kp_q = torch.empty((dB, w.block, w.vocab), dtype=torch.float32, device=dev)

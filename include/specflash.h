@@ -42,9 +42,15 @@
  *   arithmetic accumulates in float32 and all floating outputs are float32.
  * - Workspace: a caller-owned device buffer of at least the size returned by
  *   the matching *_workspace_size function for the same shape arguments
- *   (NULL is allowed when that size is 0).  Its contents need not be
- *   initialised and are garbage afterwards.  Two calls in flight at the
- *   same time must not share a workspace.
+ *   (NULL is allowed when that size is 0).  Two calls in flight at the
+ *   same time must not share a workspace.  Entry points marked "zeroed
+ *   workspace" below keep arrival counters in it (the last work-group of a
+ *   group of partial results to finish does the combining step, so no
+ *   second launch is needed): such a workspace must be all zero before its
+ *   first use and again whenever the shape arguments change; every call
+ *   returns the counters to zero, so later calls of the same shape reuse
+ *   it without clearing.  Other workspaces need no initialisation, and all
+ *   other workspace contents are garbage after a call.
  */
 #ifndef SPECFLASH_H
 #define SPECFLASH_H
@@ -207,8 +213,9 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
  *   n_accepted  [B]         int32    out: accepted drafts per sequence
  *   tokens      [B, k+1]    int32    out: draft[0..n-1], the extra token,
  *                                    then -1 padding
- *   workspace   sd_spec_accept_workspace_size(B, k, V, mode) bytes
- *               (per-chunk partial sums or maxima of the vocabulary pass)
+ *   workspace   sd_spec_accept_workspace_size(B, k, V, mode) bytes, zeroed
+ *               workspace (one arrival counter per sequence, then the
+ *               per-chunk partial sums or maxima of the vocabulary pass)
  * Requirements: B >= 1; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1]
  * (values outside are clamped when forming the weights).
  * ---------------------------------------------------------------------- */
@@ -240,8 +247,9 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
  *   seed, offset              key and stream offset of the uniforms
  *   temperature               tau > 0, finite (sampled mode)
  *   n_accepted, tokens        as for sd_spec_accept
- *   workspace   sd_spec_accept_logits_workspace_size(B, k, V, mode) bytes
- *               (row statistics of the logits, then the rule's partials)
+ *   workspace   sd_spec_accept_logits_workspace_size(B, k, V, mode) bytes,
+ *               zeroed workspace (row statistics of the logits, then the
+ *               rule's counters and partials)
  * Requirements: as for sd_spec_accept; logits finite (others give an
  * unspecified result, never an out-of-bounds access).
  * ---------------------------------------------------------------------- */
@@ -308,7 +316,7 @@ int sd_lm_head_probs(const void* hidden, const void* weight, float* probs,
  *   probs   [R, V] float32  distributions
  *   u       [R]    float32  uniforms in [0, 1) (multiples of 2^-24)
  *   tokens  [R]    int32    out
- *   workspace  sd_sample_workspace_size(R, V) bytes
+ *   workspace  sd_sample_workspace_size(R, V) bytes, zeroed workspace
  * Requirements: R >= 1; 1 <= V <= 2^18.
  * ---------------------------------------------------------------------- */
 size_t sd_sample_workspace_size(int R, int V);
@@ -445,7 +453,7 @@ int sd_semi_ar_layer_q8(const void* u, const int8_t* fc_w, const float* fc_s, co
  *   q        [B, K, V] float32  out: their distributions (the q of the
  *            acceptance rule)
  *   workspace  sd_semi_ar_draft_workspace_size(...) bytes, 256-byte aligned
- *            (device-dependent)
+ *            (device-dependent), zeroed workspace (the draws' counters)
  * Requirements: those of sd_semi_ar_layer for r0 and, when K > k', for
  * 2k' rows; 1 <= k' <= min(r0, 8); K % k' == 0; B * k' <= 256;
  * 1 <= V <= 2^18; temperature > 0.  Errors as for sd_linear.

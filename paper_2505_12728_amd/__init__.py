@@ -169,7 +169,9 @@ def _workspace(nbytes, device, given):
         _same_device("workspace", given, device)
         return given, given.numel() * given.element_size()
     torch = _torch()
-    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+    # zero-filled: some entry points keep arrival counters in the workspace
+    # that must start at zero (every call returns them to zero)
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device), nbytes
 
 
 def _raise(status, where):

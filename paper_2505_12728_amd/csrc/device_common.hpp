@@ -175,6 +175,43 @@ __device__ __forceinline__ void wait_vm_then_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Hand-off between work-groups of one launch (the last of a group of
+// work-groups to finish combines their partial results).  Partials are
+// written with device-scope stores, which write through to the level that
+// every XCD shares, and read back with device-scope loads, so neither side
+// needs a cache write-back or invalidate (an agent-scope fence costs both,
+// over the whole L2, in every work-group).  arrive_last() waits until this
+// wave's stores have completed, meets the work-group, counts its arrival
+// with a device-scope atomic and tells every thread whether it was the last
+// of `expected`; the last one resets the counter to zero for the next use.
+// No work-group ever waits for another, so the grid always drains.
+__device__ __forceinline__ void publish(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void publish(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t fetch_published(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float fetch_published(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected, int* lds_flag) {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));    // vmcnt(0): this wave's stores are done
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = prev + 1u == expected;
+    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *lds_flag = last;
+  }
+  __syncthreads();
+  return *lds_flag != 0;
+}
+
 // two bf16 -> two fp16 (exact inside the fp16 range; round toward zero
 // otherwise, so magnitudes beyond 65504 saturate at 65504)
 __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t v) {

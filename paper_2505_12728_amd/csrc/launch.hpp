@@ -101,6 +101,13 @@ struct AcceptArgs {
 
 size_t accept_workspace_bytes(int B, int k, int V, int mode);
 hipError_t launch_accept(const AcceptArgs& a, void* workspace, hipStream_t s);
+// the same rule with the arrival counters (one uint32 per sequence every
+// kCounterStride words, i.e. one per 128-byte line so that the sequences'
+// arrivals do not contend for one line; zero on entry, zero again on exit)
+// and the chunk partials (accept_partial_bytes) placed apart
+constexpr int kCounterStride = 32;
+size_t accept_partial_bytes(int B, int k, int V, int mode);
+hipError_t launch_accept_split(const AcceptArgs& a, unsigned* counters, void* partials, hipStream_t s);
 
 // acceptance from logits: the rule's fields (p, q, u unused) plus the logits,
 // log2(e) / tau and the Philox key / offset of the uniforms

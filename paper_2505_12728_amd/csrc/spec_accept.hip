@@ -1,9 +1,9 @@
 // Speculative acceptance with residual resampling (SpecFLASH Sec. 3.1 and
 // Sec. 3.3; greedy verification at temperature 0, Sec. 4.2).
 //
-// Two kernels, so that the vocabulary passes use the whole chip:
+// One kernel, grid (vocabulary chunk, sequence), 256 threads, in two phases:
 //
-// 1. chunk pass, grid (vocabulary chunk, sequence), 256 threads.
+// 1. chunk phase, every work-group.
 //    Sampled mode: every work-group of a sequence repeats the k acceptance
 //    tests u_i q_i(x_i) < p_i(x_i) (exact float64 products of 24-bit
 //    significands; a ballot and a count of trailing ones give n), then sums
@@ -13,7 +13,12 @@
 //    Integer sums are exact, so the order of additions does not matter.
 //    Greedy mode: the (value, lowest index) maximum of every target row
 //    over the chunk.
-// 2. finish pass, one work-group per sequence, one thread per chunk.
+// 2. finish phase, in the last work-group of each sequence to complete its
+//    chunk (an arrival counter per sequence in the workspace, counted with
+//    a device-scope atomic once the work-group's partials are written with
+//    device-scope stores; the last arrival resets it to zero, so a
+//    workspace that starts zeroed stays valid for the next call), one
+//    thread per chunk.
 //    Sampled: a block prefix sum of the chunk sums gives S and each chunk's
 //    starting offset; T = floor(a S / 2^24) from a = u_k 2^24 (formed as
 //    a (S >> 24) + ((a (S mod 2^24)) >> 24) without overflow) picks the
@@ -25,7 +30,7 @@
 // Every vocabulary access is a coalesced stream.
 //
 // From logits (the target's k + 1 and the draft's k rows per sequence), the
-// same two kernels read p and q on demand as a temperature softmax of the
+// same kernel reads p and q on demand as a temperature softmax of the
 // logits, after a statistics pass, grid (4096-entry chunk, row), that writes
 // each chunk's (max, sum of 2^(z s - max)) with s = log2(e) / tau.  Each
 // work-group of the rule first merges its sequence's 2k + 1 rows of chunk
@@ -196,15 +201,17 @@ __device__ __forceinline__ uint64_t weight_at(const Src& src, int b, int n, int 
 // n for one sequence: leading accepted drafts.  Uses lanes 0..63 of wave 0;
 // the result is returned to every thread through `slot`.
 template <typename Src>
-__device__ int accepted_prefix(const AcceptArgs& a, const Src& src, int b, int* slot) {
+__device__ int accepted_prefix(const AcceptArgs& a, const Src& src, int b, int* slot, int* drafts) {
   const int k = a.k, V = a.V;
   if (threadIdx.x < 64) {
     const int i = threadIdx.x;
     bool acc = false;
     if (i < k) {
+      const float ui = src.uniform(b, i);      // independent of the draft id: issued with it
       const int x = a.draft[(size_t)b * k + i];
+      drafts[i] = x;
       if (x >= 0 && x < V) {
-        const double pu = (double)src.uniform(b, i) * (double)src.drafted(b, i, x);
+        const double pu = (double)ui * (double)src.drafted(b, i, x);
         acc = pu < (double)src.target(b, i, x);
       }
     }
@@ -251,53 +258,130 @@ __device__ ArgMax block_argmax_range(F&& value, int v0, int v1, ArgMax* sm) {
   return r;
 }
 
-// workspace layout (per sequence b, chunk c):
+// workspace layout: arrival counters first, then the chunk partials
+//   uint32 count[B][kCounterStride] (one counter per 128-byte line)
 //   sampled: uint64 sums[B][C][2]  (residual / p-only)
 //   greedy:  ArgMax best[B][k+1][C]
+__host__ __device__ __forceinline__ size_t counter_bytes(int B) {
+  return ((size_t)B * kCounterStride * sizeof(unsigned) + 255) / 256 * 256;
+}
+
+// Partials cross work-groups (possibly on other XCDs, behind other L2
+// caches) as device-scope stores and loads of 64-bit words (publish /
+// fetch_published).
+__device__ __forceinline__ uint64_t load_partial(const uint64_t* p) { return fetch_published(p); }
+__device__ __forceinline__ ArgMax load_partial(const ArgMax* p) {
+  const uint64_t x = fetch_published(reinterpret_cast<const uint64_t*>(p));
+  return ArgMax{__uint_as_float((uint32_t)x), (int)(uint32_t)(x >> 32)};
+}
+__device__ __forceinline__ void store_partial(ArgMax* p, ArgMax r) {
+  publish(reinterpret_cast<uint64_t*>(p), ((uint64_t)(uint32_t)r.i << 32) | __float_as_uint(r.v));
+}
+
+constexpr int kMaxRows = 17;   // k + 1 rows at most (k <= 16)
+constexpr int kPer = kChunk / kThreads;
+constexpr int kRowGroup = 4;   // greedy rows reduced per barrier
+
+struct RuleShared {
+  uint64_t wsum[kWaves][2];
+  uint64_t tot[kWaves];
+  ArgMax sm[kWaves];
+  ArgMax gsm[kRowGroup][kWaves];
+  ArgMax gmax[kMaxRows];
+  int drafts[kMaxRows];
+  uint64_t before;
+  int n, tok, chunk, last;
+  float2 rows[33];
+};
+
+// Phase 1: this work-group's chunk partials of sequence b.  Thread t takes
+// entries v0 + j kThreads + t (j < kPer); every load of a row is issued
+// before any is used.
 template <typename Src>
-__global__ __launch_bounds__(kThreads) void accept_chunks(AcceptArgs a, Src src, void* ws, int nchunks) {
-  __shared__ uint64_t wsum[kWaves][2];
-  __shared__ ArgMax sm[kWaves];
-  __shared__ int s_n;
-  __shared__ float2 s_rows[33];
-  const int chunk = blockIdx.x, b = blockIdx.y;
-  src.prepare(b, s_rows);
-  __syncthreads();
+__device__ void chunk_phase(const AcceptArgs& a, const Src& src, unsigned char* parts, int nchunks, int chunk,
+                            int b, RuleShared& sh) {
   const int k = a.k, V = a.V;
   const int v0 = chunk * kChunk, v1 = min(V, v0 + kChunk);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (a.mode == 0) {
-    ArgMax* out = static_cast<ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
-    for (int i = 0; i <= k; ++i) {
-      const ArgMax r = block_argmax_range([&](int v) { return src.greedy(b, i, v); }, v0, v1, sm);
-      if (threadIdx.x == 0) out[(size_t)i * nchunks + chunk] = r;
+    // (value, lowest index) maximum of every target row over the chunk,
+    // kRowGroup rows at a time: all their loads in flight, wave maxima by
+    // shuffles, one barrier, then one thread per row merges the waves
+    ArgMax* out = reinterpret_cast<ArgMax*>(parts) + (size_t)b * (k + 1) * nchunks;
+    float x[kMaxRows][kPer];                   // every row's loads in flight at once
+#pragma unroll
+    for (int r = 0; r < kMaxRows; ++r)
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const int v = v0 + j * kThreads + threadIdx.x;
+        x[r][j] = (r <= k && v < v1) ? src.greedy(b, r, v) : 0.f;
+      }
+#pragma unroll
+    for (int i0 = 0; i0 < kMaxRows; i0 += kRowGroup) {
+      if (i0 > k) break;
+#pragma unroll
+      for (int r = 0; r < kRowGroup; ++r) {
+        if (i0 + r >= kMaxRows) break;
+        ArgMax best{-INFINITY, -1};
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+          const int v = v0 + j * kThreads + threadIdx.x;
+          if (v < v1 && (best.i < 0 || x[i0 + r][j] > best.v)) best = ArgMax{x[i0 + r][j], v};   // v grows with j
+        }
+#pragma unroll
+        for (int m = 32; m > 0; m >>= 1) {
+          ArgMax o{__shfl_xor(best.v, m, 64), __shfl_xor(best.i, m, 64)};
+          best = better(best, o);
+        }
+        if (lane == 0) sh.gsm[r][w] = best;
+      }
+      __syncthreads();
+      if (threadIdx.x < kRowGroup && i0 + (int)threadIdx.x <= k) {
+        const int r = threadIdx.x;
+        ArgMax g = sh.gsm[r][0];
+        for (int i = 1; i < kWaves; ++i) g = better(g, sh.gsm[r][i]);
+        store_partial(out + (size_t)(i0 + r) * nchunks + chunk, g);
+      }
+      __syncthreads();
     }
     return;
   }
-  const int n = accepted_prefix(a, src, b, &s_n);
+  const int n = accepted_prefix(a, src, b, &sh.n, sh.drafts);
   const int use_q = n < k ? 1 : 0;
+  float pv[kPer], qv[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int v = v0 + j * kThreads + threadIdx.x;
+    pv[j] = v < v1 ? src.target(b, n, v) : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int v = v0 + j * kThreads + threadIdx.x;
+    qv[j] = (use_q && v < v1) ? src.drafted(b, n, v) : 0.f;
+  }
   uint64_t sr = 0, sp = 0;
-  for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
-    const float pv = src.target(b, n, v);
-    sp += fixed_weight(pv);
-    sr += use_q ? fixed_weight(fmaxf(0.0f, pv - src.drafted(b, n, v))) : fixed_weight(pv);
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const uint64_t wp = fixed_weight(pv[j]);
+    sp += wp;
+    sr += use_q ? fixed_weight(fmaxf(0.0f, pv[j] - qv[j])) : wp;
   }
   sr = wave_sum_u64(sr);
   sp = wave_sum_u64(sp);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (lane == 0) {
-    wsum[w][0] = sr;
-    wsum[w][1] = sp;
+    sh.wsum[w][0] = sr;
+    sh.wsum[w][1] = sp;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     uint64_t tr = 0, tp = 0;
     for (int i = 0; i < kWaves; ++i) {
-      tr += wsum[i][0];
-      tp += wsum[i][1];
+      tr += sh.wsum[i][0];
+      tp += sh.wsum[i][1];
     }
-    uint64_t* out = static_cast<uint64_t*>(ws) + ((size_t)b * nchunks + chunk) * 2;
-    out[0] = tr;
-    out[1] = tp;
+    uint64_t* out = reinterpret_cast<uint64_t*>(parts) + ((size_t)b * nchunks + chunk) * 2;
+    publish(out, tr);
+    publish(out + 1, tp);
   }
 }
 
@@ -323,68 +407,72 @@ __device__ uint64_t block_exclusive_scan(uint64_t x, uint64_t* tot, uint64_t* to
   return before + inc - x;
 }
 
+// Phase 2, in the last work-group of sequence b: n and the final token
+// from every chunk's partials.
 template <typename Src>
-__global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src, const void* ws, int nchunks) {
-  __shared__ ArgMax sm[kWaves];
-  __shared__ uint64_t tot[kWaves];
-  __shared__ int s_n;
-  __shared__ int s_tok;
-  __shared__ int s_chunk;
-  __shared__ uint64_t s_before;
-  __shared__ float2 s_rows[33];
-  const int b = blockIdx.x;
+__device__ void finish_phase(const AcceptArgs& a, const Src& src, const unsigned char* parts, int nchunks, int b,
+                             RuleShared& sh) {
   const int c = threadIdx.x;                   // one thread per chunk (nchunks <= 256)
-  // sampled: the chunk sums depend neither on n nor on the row statistics,
-  // so their loads are issued first and overlap both
-  uint64_t x_res = 0ull, x_p = 0ull;
-  if (a.mode != 0 && c < nchunks) {
-    const uint64_t* sums = static_cast<const uint64_t*>(ws) + (size_t)b * nchunks * 2;
-    x_res = sums[2 * c];
-    x_p = sums[2 * c + 1];
-  }
-  src.prepare(b, s_rows);
-  __syncthreads();
   const int k = a.k, V = a.V;
   const int32_t* draft = a.draft + (size_t)b * k;
   int n = 0, token = 0;
   if (a.mode == 0) {
-    const ArgMax* part = static_cast<const ArgMax*>(ws) + (size_t)b * (k + 1) * nchunks;
+    // every row's chunk maxima loaded at once (one thread per chunk), the
+    // rows' argmaxes formed kRowGroup rows per barrier, then the longest
+    // prefix of drafts equal to them
+    const ArgMax* part = reinterpret_cast<const ArgMax*>(parts) + (size_t)b * (k + 1) * nchunks;
     const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    int nn = 0;
-    for (;;) {
-      ArgMax r = c < nchunks ? part[(size_t)nn * nchunks + c] : ArgMax{-INFINITY, -1};
+    if (c < k) sh.drafts[c] = draft[c];        // read by every thread after the barriers below
+    ArgMax r[kMaxRows];
 #pragma unroll
-      for (int m = 32; m > 0; m >>= 1) {
-        ArgMax o{__shfl_xor(r.v, m, 64), __shfl_xor(r.i, m, 64)};
-        r = better(r, o);
+    for (int i = 0; i < kMaxRows; ++i)
+      r[i] = (i <= k && c < nchunks) ? load_partial(part + (size_t)i * nchunks + c) : ArgMax{-INFINITY, -1};
+#pragma unroll
+    for (int i0 = 0; i0 < kMaxRows; i0 += kRowGroup) {
+      if (i0 > k) break;
+#pragma unroll
+      for (int rr = 0; rr < kRowGroup; ++rr) {
+        if (i0 + rr >= kMaxRows) break;
+        ArgMax x = r[i0 + rr];
+#pragma unroll
+        for (int m = 32; m > 0; m >>= 1) {
+          ArgMax o{__shfl_xor(x.v, m, 64), __shfl_xor(x.i, m, 64)};
+          x = better(x, o);
+        }
+        if (lane == 0) sh.gsm[rr][w] = x;
       }
-      if (lane == 0) sm[w] = r;
       __syncthreads();
-      ArgMax g = sm[0];
-      for (int i = 1; i < kWaves; ++i) g = better(g, sm[i]);
-      __syncthreads();
-      if (nn < k && draft[nn] == g.i) {
-        ++nn;
-        continue;
+      if (threadIdx.x < kRowGroup && i0 + (int)threadIdx.x <= k) {
+        ArgMax g = sh.gsm[threadIdx.x][0];
+        for (int i = 1; i < kWaves; ++i) g = better(g, sh.gsm[threadIdx.x][i]);
+        sh.gmax[i0 + threadIdx.x] = g;
       }
-      token = g.i;
-      break;
+      __syncthreads();
     }
+    int nn = 0;
+    while (nn < k && sh.drafts[nn] == sh.gmax[nn].i) ++nn;
     n = nn;
+    token = sh.gmax[nn].i;
   } else {
-    n = accepted_prefix(a, src, b, &s_n);
+    uint64_t x_res = 0ull, x_p = 0ull;
+    if (c < nchunks) {
+      const uint64_t* sums = reinterpret_cast<const uint64_t*>(parts) + (size_t)b * nchunks * 2;
+      x_res = load_partial(sums + 2 * c);
+      x_p = load_partial(sums + 2 * c + 1);
+    }
+    n = sh.n;                                  // the chunk phase's tests (same work-group)
     // residual weights, else p-only weights, else argmax
     uint64_t S;
     uint64_t x = x_res;
-    uint64_t before = block_exclusive_scan(x, tot, &S);
+    uint64_t before = block_exclusive_scan(x, sh.tot, &S);
     int sel = 0;
     if (S == 0) {
       sel = 1;
       x = x_p;
-      before = block_exclusive_scan(x, tot, &S);
+      before = block_exclusive_scan(x, sh.tot, &S);
     }
     if (S == 0) {
-      token = block_argmax_range([&](int v) { return src.target(b, n, v); }, 0, V, sm).i;
+      token = block_argmax_range([&](int v) { return src.target(b, n, v); }, 0, V, sh.sm).i;
     } else {
       const int use_q = (sel == 0 && n < k) ? 1 : 0;
       float uf = src.uniform(b, k) * 16777216.0f;   // exact: u is a float32
@@ -393,17 +481,17 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
       const uint64_t T = av * (S >> 24) + ((av * (S & 0xffffffull)) >> 24);
       // the chunk whose [before, before + x) range holds T (exactly one)
       if (x != 0 && before <= T && T < before + x) {
-        s_chunk = c;
-        s_before = before;
+        sh.chunk = c;
+        sh.before = before;
       }
-      if (threadIdx.x == 0) s_tok = 0x7fffffff;
+      if (threadIdx.x == 0) sh.tok = 0x7fffffff;
       __syncthreads();
       // inside the chunk, thread t takes the kPerThread consecutive entries
       // from c0 + t kPerThread, all loaded at once; a block prefix sum of
       // the threads' totals finds the thread whose range holds T, and that
       // thread finds the first entry whose inclusive prefix sum exceeds T
       constexpr int kPerThread = kChunk / kThreads;
-      const int c0 = s_chunk * kChunk, c1 = min(V, c0 + kChunk);
+      const int c0 = sh.chunk * kChunk, c1 = min(V, c0 + kChunk);
       const int e0 = c0 + threadIdx.x * kPerThread;
       uint64_t wv[kPerThread], mine = 0;
 #pragma unroll
@@ -412,7 +500,7 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
         mine += wv[j];
       }
       uint64_t chunk_total;
-      const uint64_t pre = s_before + block_exclusive_scan(mine, tot, &chunk_total);
+      const uint64_t pre = sh.before + block_exclusive_scan(mine, sh.tot, &chunk_total);
       if (mine != 0 && pre <= T && T < pre + mine) {
         uint64_t incl = pre;
         int hit = -1;
@@ -421,15 +509,32 @@ __global__ __launch_bounds__(kThreads) void accept_finish(AcceptArgs a, Src src,
           incl += wv[j];
           if (hit < 0 && incl > T) hit = e0 + j;
         }
-        s_tok = hit;                           // found: T < pre + mine
+        sh.tok = hit;                          // found: T < pre + mine
       }
       __syncthreads();
-      token = s_tok;
+      token = sh.tok;
     }
   }
   int32_t* tok = a.tokens + (size_t)b * (k + 1);
-  for (int i = threadIdx.x; i <= k; i += kThreads) tok[i] = i < n ? draft[i] : (i == n ? token : -1);
+  for (int i = threadIdx.x; i <= k; i += kThreads) tok[i] = i < n ? sh.drafts[i] : (i == n ? token : -1);
   if (threadIdx.x == 0) a.n_accepted[b] = n;
+}
+
+// The rule: grid (chunk, sequence).  Every work-group writes its chunk's
+// partials, publishes them (release fence) and counts its arrival; the one
+// that completes the count of its sequence runs the finish and resets the
+// counter.  Work-groups never wait for each other, so the grid always
+// drains.
+template <typename Src>
+__global__ __launch_bounds__(kThreads) void accept_rule(AcceptArgs a, Src src, unsigned* count, unsigned char* parts,
+                                                        int nchunks) {
+  __shared__ RuleShared sh;
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  src.prepare(b, sh.rows);
+  __syncthreads();
+  chunk_phase(a, src, parts, nchunks, chunk, b, sh);
+  if (!arrive_last(count + (size_t)b * kCounterStride, (unsigned)nchunks, &sh.last)) return;
+  finish_phase(a, src, parts, nchunks, b, sh);
 }
 
 // Row statistics of the logits at temperature: grid (4096-entry chunk, row)
@@ -511,13 +616,16 @@ __global__ __launch_bounds__(kThreads) void philox_uniforms_kernel(uint64_t seed
 }
 
 template <typename Src>
-hipError_t launch_rule(const AcceptArgs& a, const Src& src, void* ws, hipStream_t st) {
+hipError_t launch_rule(const AcceptArgs& a, const Src& src, unsigned* count, unsigned char* parts, hipStream_t st) {
   const int nchunks = (a.V + kChunk - 1) / kChunk;
-  hipLaunchKernelGGL((accept_chunks<Src>), dim3(nchunks, a.B), dim3(kThreads), 0, st, a, src, ws, nchunks);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((accept_finish<Src>), dim3(a.B), dim3(kThreads), 0, st, a, src, ws, nchunks);
+  hipLaunchKernelGGL((accept_rule<Src>), dim3(nchunks, a.B), dim3(kThreads), 0, st, a, src, count, parts, nchunks);
   return hipGetLastError();
+}
+
+template <typename Src>
+hipError_t launch_rule(const AcceptArgs& a, const Src& src, void* ws, hipStream_t st) {
+  unsigned char* base = static_cast<unsigned char*>(ws);
+  return launch_rule(a, src, reinterpret_cast<unsigned*>(base), base + counter_bytes(a.B), st);
 }
 
 template <typename T>
@@ -562,12 +670,20 @@ hipError_t launch_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int 
 
 size_t accept_workspace_bytes(int B, int k, int V, int mode) {
   const int nchunks = (V + kChunk - 1) / kChunk;
-  if (mode == 0) return (size_t)B * (k + 1) * nchunks * sizeof(ArgMax);
-  return (size_t)B * nchunks * 2 * sizeof(uint64_t);
+  if (mode == 0) return counter_bytes(B) + (size_t)B * (k + 1) * nchunks * sizeof(ArgMax);
+  return counter_bytes(B) + (size_t)B * nchunks * 2 * sizeof(uint64_t);
 }
 
 hipError_t launch_accept(const AcceptArgs& a, void* ws, hipStream_t st) {
   return launch_rule(a, ProbSrc{a.p, a.q, a.u, a.k, a.V}, ws, st);
+}
+
+size_t accept_partial_bytes(int B, int k, int V, int mode) {
+  return accept_workspace_bytes(B, k, V, mode) - counter_bytes(B);
+}
+
+hipError_t launch_accept_split(const AcceptArgs& a, unsigned* counters, void* partials, hipStream_t st) {
+  return launch_rule(a, ProbSrc{a.p, a.q, a.u, a.k, a.V}, counters, static_cast<unsigned char*>(partials), st);
 }
 
 }  // namespace sd

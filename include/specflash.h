@@ -227,6 +227,28 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * sd_spec_accept without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same rule, arguments, outputs and
+ * bit-exact results as sd_spec_accept; its counters and partials live in a
+ * fixed device array of the library (4 MiB on each device it runs on, held
+ * until the process ends): arrival counters of up to 1024 sequences, then
+ * the chunk partials.  It calls no allocating routine.  On its first call
+ * on a device it looks up that array's address and clears the counters (a
+ * kernel on `stream`); every call returns them to zero.
+ * All calls on one device share the array: calls that overlap in time on
+ * one device (different streams or host threads) race and give undefined
+ * results; calls ordered on one stream are safe.
+ * Requirements: those of sd_spec_accept, plus B <= 1024 and a partial size
+ * (per sequence 16 * ceil(V / 1024) bytes sampled, 8 * (k+1) * ceil(V /
+ * 1024) greedy) of at most 4 MiB - 4 KiB in total; larger calls return
+ * SD_ERR_WORKSPACE without launching anything.
+ * ---------------------------------------------------------------------- */
+int sd_spec_accept_noalloc(const float* p, const float* q, const int32_t* draft,
+                           const float* u, int32_t* n_accepted, int32_t* tokens,
+                           int B, int k, int V, int mode, void* stream);
+
+/* ------------------------------------------------------------------------
  * Speculative acceptance from logits (the same rule as sd_spec_accept,
  * Sec. 3.1 and Sec. 3.3, with the temperature softmax of Sec. 4.2 and the
  * uniforms produced on the device).

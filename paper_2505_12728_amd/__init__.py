@@ -24,7 +24,7 @@ __all__ = [
     "sd_status_string", "sd_version",
     "sd_latent_compress_workspace_size", "sd_latent_compress",
     "sd_verify_workspace_size", "sd_verify_attention",
-    "sd_spec_accept_workspace_size", "sd_spec_accept",
+    "sd_spec_accept_workspace_size", "sd_spec_accept", "sd_spec_accept_noalloc",
     "sd_lm_head_workspace_size", "sd_lm_head_probs",
     "sd_sample_workspace_size", "sd_sample_tokens",
     "sd_spec_accept_logits_workspace_size", "sd_spec_accept_logits", "sd_philox_uniforms",
@@ -54,6 +54,7 @@ _SIGNATURES = {
                                  _i, _i, _i, _i, _i, _f, _i, _vp, _sz, _vp]),
     "sd_spec_accept_workspace_size": (_sz, [_i, _i, _i, _i]),
     "sd_spec_accept": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _sz, _vp]),
+    "sd_spec_accept_noalloc": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
     "sd_spec_accept_logits_workspace_size": (_sz, [_i, _i, _i, _i]),
     "sd_spec_accept_logits": (_i, [_vp, _vp, _vp, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_float,
                                    _vp, _vp, _i, _i, _i, _i, _i, _vp, _sz, _vp]),
@@ -312,6 +313,38 @@ def sd_spec_accept(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, toke
                                   _ptr(tokens), B, k, V, int(mode), _ptr(ws), ws_len,
                                   _stream(stream))
     _raise(st, "sd_spec_accept")
+    return n_accepted, tokens
+
+
+def sd_spec_accept_noalloc(p, q, draft, u, mode=SD_ACCEPT_SAMPLED, n_accepted=None, tokens=None,
+                           stream=None):
+    """sd_spec_accept with the library's fixed device scratch instead of a
+    workspace (for callers that cannot allocate; pass n_accepted and tokens
+    to allocate nothing here either).  Same arguments and results."""
+    torch = _torch()
+    _check(p, "p", dtype=torch.float32, ndim=3)
+    _check(draft, "draft", dtype=torch.int32, ndim=2)
+    B, kp1, V = p.shape
+    k = kp1 - 1
+    if tuple(draft.shape) != (B, k):
+        raise ValueError("draft must be [B, k]")
+    if mode == SD_ACCEPT_SAMPLED:
+        _check(q, "q", dtype=torch.float32, ndim=3)
+        _check(u, "u", dtype=torch.float32, ndim=2)
+        if tuple(q.shape) != (B, k, V) or tuple(u.shape) != (B, k + 1):
+            raise ValueError("q must be [B, k, V] and u [B, k+1]")
+        _same_device("q", q, p.device)
+        _same_device("u", u, p.device)
+    _same_device("draft", draft, p.device)
+    if n_accepted is None:
+        n_accepted = torch.empty((B,), dtype=torch.int32, device=p.device)
+    if tokens is None:
+        tokens = torch.empty((B, k + 1), dtype=torch.int32, device=p.device)
+    _out(n_accepted, "n_accepted", (B,), torch.int32, p.device)
+    _out(tokens, "tokens", (B, k + 1), torch.int32, p.device)
+    st = library().sd_spec_accept_noalloc(_ptr(p), _ptr(q), _ptr(draft), _ptr(u), _ptr(n_accepted),
+                                          _ptr(tokens), B, k, V, int(mode), _stream(stream))
+    _raise(st, "sd_spec_accept_noalloc")
     return n_accepted, tokens
 
 

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "../../include/specflash.h"
 #include "launch.hpp"
@@ -48,6 +49,58 @@ bool compress_shape_ok(int B, int N, int C, int d, int H, int dtype, int* status
   return true;
 }
 
+}  // namespace
+
+// ------------------------------------------- scratch of the allocation-free entry point
+// sd_spec_accept_noalloc keeps its counters and partials in `scratch`, a
+// device array of fixed size: arrival counters of up to kScratchSeqs
+// sequences at offset 0 (their place never depends on the call's shape),
+// then the chunk partials.  Host code never uses the array's name as an
+// address: its device address comes from hipGetSymbolAddress, once per
+// device, and every use (kernel arguments, the clearing kernel) goes
+// through that pointer.
+namespace {
+constexpr size_t kScratchBytes = size_t(4) << 20;      // 4 MiB per device
+constexpr int kScratchSeqs = 1024;
+constexpr int kScratchCounterWords = kScratchSeqs * sd::kCounterStride;
+constexpr size_t kScratchCounterBytes = (size_t)kScratchCounterWords * sizeof(unsigned);
+static_assert(kScratchCounterBytes % 256 == 0, "partials start 256-byte aligned");
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+__global__ void zero_words(unsigned* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+struct ScratchSlot {
+  std::once_flag once;
+  unsigned char* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[64];
+
+// Device address of this device's scratch (set-up on its first use: the
+// address is looked up with the device current and the counters are
+// cleared on `st`, ahead of any kernel that reads them).
+hipError_t scratch_for_current_device(hipStream_t st, unsigned char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&] {
+    void* p = nullptr;
+    slot.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (slot.err != hipSuccess) return;
+    hipLaunchKernelGGL(zero_words, dim3((kScratchCounterWords + 255) / 256), dim3(256), 0, st,
+                       static_cast<unsigned*>(p), kScratchCounterWords);
+    slot.err = hipGetLastError();
+    if (slot.err == hipSuccess) slot.ptr = static_cast<unsigned char*>(p);
+  });
+  *out = slot.ptr;
+  return slot.err;
+}
 }  // namespace
 
 extern "C" {
@@ -209,6 +262,37 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const f
   a.V = V;
   a.mode = mode;
   return status_from(sd::launch_accept(a, workspace, static_cast<hipStream_t>(stream)));
+}
+
+// ------------------------------------------- accept without allocation
+int sd_spec_accept_noalloc(const float* p, const float* q, const int32_t* draft, const float* u,
+                           int32_t* n_accepted, int32_t* tokens, int B, int k, int V, int mode, void* stream) {
+  if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
+    return SD_ERR_INVALID_ARG;
+  if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (!p || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
+  if (mode == SD_ACCEPT_SAMPLED && (!q || !u)) return SD_ERR_INVALID_ARG;
+  if (!aligned(p, 4) || !aligned(draft, 4) || !aligned(n_accepted, 4) || !aligned(tokens, 4) ||
+      (q && !aligned(q, 4)) || (u && !aligned(u, 4)))
+    return SD_ERR_INVALID_ARG;
+  if (B > kScratchSeqs || sd::accept_partial_bytes(B, k, V, mode) > kScratchBytes - kScratchCounterBytes)
+    return SD_ERR_WORKSPACE;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  unsigned char* base = nullptr;
+  const hipError_t e = scratch_for_current_device(st, &base);
+  if (e != hipSuccess) return status_from(e);
+  sd::AcceptArgs a{};
+  a.p = p;
+  a.q = q;
+  a.draft = draft;
+  a.u = u;
+  a.n_accepted = n_accepted;
+  a.tokens = tokens;
+  a.B = B;
+  a.k = k;
+  a.V = V;
+  a.mode = mode;
+  return status_from(sd::launch_accept_split(a, reinterpret_cast<unsigned*>(base), base + kScratchCounterBytes, st));
 }
 
 // ------------------------------------------------------ accept (logits)

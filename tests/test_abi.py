@@ -124,6 +124,27 @@ def test_accept_validation_errors(lib):
     assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
 
 
+def test_accept_noalloc_validation_errors(lib):
+    # the allocation-free acceptance checks everything before touching HIP:
+    # invalid arguments, and shapes beyond its fixed 4 MiB scratch
+    keep, (p, q, d, u, n, t) = _fake(6)
+    f = lib.sd_spec_accept_noalloc
+
+    def call(p=p, q=q, d=d, u=u, n=n, t=t, B=1, k=4, V=100, mode=1):
+        return f(p, q, d, u, n, t, B, k, V, mode, None)
+
+    assert call(p=None) == sd.SD_ERR_INVALID_ARG
+    assert call(q=None) == sd.SD_ERR_INVALID_ARG
+    assert call(n=None) == sd.SD_ERR_INVALID_ARG
+    assert call(k=17) == sd.SD_ERR_UNSUPPORTED
+    assert call(B=1025) == sd.SD_ERR_WORKSPACE             # more sequences than counters
+    # greedy partials: 8 (k + 1) ceil(V / 1024) bytes per sequence, 34816 at
+    # k = 16, V = 2^18: 121 sequences exceed 4 MiB - 4 KiB (120 would fit)
+    assert call(B=121, k=16, V=1 << 18, mode=0) == sd.SD_ERR_WORKSPACE
+    # sampled: 16 ceil(V / 1024) bytes per sequence, at most 4096 per
+    # sequence, so 1024 sequences always fit
+
+
 def test_workspace_sizes_cover_the_partials(lib):
     # verify: one (D + 1)-float partial row per (sequence, KV head, split, row)
     for B, k, Hq, Hkv, D, cap in [(1, 4, 4, 1, 64, 608), (4, 8, 64, 8, 128, 65536),

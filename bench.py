@@ -61,6 +61,9 @@ def parse():
                     help="skip timing the other workloads' compression, verification and acceptance")
     ap.add_argument("--workload-steps", type=int, default=30,
                     help="timed calls per operation for each of the other workloads")
+    ap.add_argument("--core-only", action="store_true",
+                    help="time only the workload's compression, verification and acceptance "
+                         "(one JSON line of per-operation statistics; for profiling runs)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for counter scaling)")
     return ap.parse_args()
@@ -325,6 +328,16 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = synth.workload(args.workload)
+    if args.core_only:
+        if args.copy_calibration_mib:
+            src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
+            torch.empty_like(src).copy_(src)
+            torch.cuda.synchronize()
+        print(f"[bench] core operations of {w.name}", file=sys.stderr, flush=True)
+        ops_ = time_workload_ops(w, dev, args.steps, args.warmup)
+        print(json.dumps({"workload": w.name, "steps": args.steps, "warmup": args.warmup, "ops": ops_}),
+              flush=True)
+        return
     mode = "sampled" if "sampled" in w.modes else "greedy"
     print(f"[bench] generating workload {w.name}", file=sys.stderr, flush=True)
     comp = synth.compress_inputs(w)

@@ -10,7 +10,8 @@ defines (or, for acceptance, of the step-by-step rule the paper cites), so a
 reader can check it against the paper by eye:
 
 * ``latent_compress``  -- the visual-token compressor, Sec. 3.2, Eq. 3
-  (also Algorithm 1, Appendix B).
+  (also Algorithm 1, Appendix B); ``latent_compress_q8`` the same on the int8
+  draft's inputs (quantised drafts, Appendix A).
 * ``verify_attention`` -- attention of the K drafted positions over the
   target's KV cache during the single parallel verification pass, Sec. 3.1.
 * ``spec_accept``      -- token-wise acceptance / rejection with residual
@@ -35,7 +36,7 @@ function here is "parity unpinned": every one is checked in
 enumeration or brute force.
 """
 
-from .compress import latent_compress, softmax_rows, avg_pool_compress
+from .compress import latent_compress, softmax_rows, avg_pool_compress, latent_compress_q8, dequantize_pow2_rows
 from .verify import verify_attention, gather_paged, merge_partials
 from .lm_head import lm_head_logits, softmax_temperature, lm_head_probs, sample_tokens
 from .accept_logits import philox4x64, philox_uniforms, spec_accept_logits
@@ -56,6 +57,8 @@ from .accept import (
 __all__ = [
     "latent_compress",
     "avg_pool_compress",
+    "latent_compress_q8",
+    "dequantize_pow2_rows",
     "softmax_rows",
     "verify_attention",
     "gather_paged",

@@ -83,3 +83,29 @@ def avg_pool_compress(feats, C):
         lo, hi = (c * N) // C, ((c + 1) * N) // C
         out[:, c] = F[:, lo:hi].mean(axis=1)
     return out
+
+
+def dequantize_pow2_rows(q, e):
+    """The values an int8 row with a power-of-two scale stands for:
+    x[..., k] = q[..., k] * 2^e[...] (one exponent per row)."""
+    q = np.asarray(q, dtype=np.float64)
+    e = np.asarray(e, dtype=np.float64)
+    return q * np.exp2(e)[..., None]
+
+
+def latent_compress_q8(latents_q, latent_exp, feats_q, feat_exp, num_heads=1, scale=1.0):
+    """Eq. 3 for the int8 draft's compressor (quantised drafts, Appendix A).
+
+    Reading (the paper quantises the draft to int8 but names no scheme): the
+    learned queries and the visual features are stored as int8 rows, each row
+    (a latent, or a token of a sequence) with its own power-of-two scale 2^e,
+    and Eq. 3 is computed on the values they stand for, q * 2^e.
+
+    latents_q [C, d] int8, latent_exp [C] int; feats_q [B, N, d] int8,
+    feat_exp [B, N] int.  Returns out [B, C, d] float64 (``latent_compress``
+    of the dequantised inputs).
+    """
+    lat = dequantize_pow2_rows(latents_q, latent_exp)
+    F = dequantize_pow2_rows(feats_q, feat_exp)
+    return latent_compress(lat, F, num_heads, scale)
+

@@ -249,6 +249,41 @@ def compress_inputs(w, seed=None, batch=None, tokens=None):
     return latents, feats
 
 
+Q8_EXP_MIN, Q8_EXP_MAX = -14, 9    # every q * 2^e (|q| <= 127) a normal fp16 or zero
+
+
+def quantize_pow2_rows(x):
+    """int8 rows with one power-of-two scale each (the int8 compressor's
+    input format): e = ceil(log2(max|row| / 127)) clamped to [-14, 9],
+    q = clip(round(x / 2^e), -127, 127).  Returns (q int8, e int8)."""
+    x = np.asarray(x, dtype=np.float32)
+    amax = np.max(np.abs(x), axis=-1)
+    with np.errstate(divide="ignore"):
+        e = np.ceil(np.log2(np.maximum(amax, 1e-30) / 127.0))
+    e = np.clip(e, Q8_EXP_MIN, Q8_EXP_MAX).astype(np.int8)
+    q = np.empty(x.shape, dtype=np.int8)
+    scale = np.exp2(-e.astype(np.float32))[..., None]
+    q[...] = np.clip(np.rint(x * scale), -127, 127)
+    return q, e
+
+
+def compress_q8_inputs(w, seed=None, batch=None, tokens=None):
+    """The compression inputs of ``compress_inputs`` quantised to int8 rows
+    with power-of-two scales: latents_q [C, d], latent_exp [C], feats_q
+    [B, N, d], feat_exp [B, N] (int8 each)."""
+    lat, feats = compress_inputs(w, seed, batch, tokens)
+    lq, le = quantize_pow2_rows(lat.values)
+    fq, fe = quantize_pow2_rows(feats.values)
+    return {"latents_q": lq, "latent_exp": le, "feats_q": fq, "feat_exp": fe}
+
+
+def compress_q8_bytes(w):
+    """F_V's int8 rows and exponents once, the latents' likewise, the fp32
+    output once."""
+    return (w.c_batch * w.c_tokens * (w.c_width + 1) + w.c_latents * (w.c_width + 1)
+            + w.c_batch * w.c_latents * w.c_width * 4)
+
+
 def kv_lengths(w, seed=None):
     rs = streams(w.seed if seed is None else seed)
     if not w.paged:

@@ -1061,6 +1061,49 @@ def test_int8_layer_equals_layer_of_dequantised_weights():
     assert np.array_equal(a, b) and np.array_equal(ka, kb) and np.array_equal(va, vb)
 
 
+def test_compress_q8_dequantisation_hand_values():
+    # an int8 row stands for q * 2^e with its own exponent
+    q = np.array([[-127, 5, 0], [1, -2, 64]], np.int8)
+    e = np.array([-3, 2], np.int8)
+    x = oracle.dequantize_pow2_rows(q, e)
+    assert x.tolist() == [[-15.875, 0.625, 0.0], [4.0, -8.0, 256.0]]
+
+
+def test_compress_q8_two_token_closed_form():
+    # one latent [1, 0] (q [1, 0], e 0) over tokens [2, 0] (q [1, 0], e 1)
+    # and [0, 3] (q [0, 3], e 0), scale 1: scores [2, 0], so
+    # out = (e^2 [2, 0] + [0, 3]) / (e^2 + 1)
+    out = oracle.latent_compress_q8(np.array([[1, 0]], np.int8), np.array([0], np.int8),
+                                    np.array([[[1, 0], [0, 3]]], np.int8), np.array([[1, 0]], np.int8),
+                                    1, 1.0)
+    e2 = math.exp(2.0)
+    expect = np.array([2 * e2, 3.0]) / (e2 + 1.0)
+    assert np.allclose(out[0, 0], expect, rtol=1e-15, atol=0)
+
+
+def test_compress_q8_exponent_shift_doubles_the_output():
+    # moving one power of two from every latent row to every token row
+    # leaves the scores unchanged and doubles the values: out doubles exactly
+    r = rng(71)
+    lq = r.integers(-127, 128, size=(6, 16)).astype(np.int8)
+    fq = r.integers(-127, 128, size=(2, 9, 16)).astype(np.int8)
+    le = r.integers(-7, -3, size=6).astype(np.int8)
+    fe = r.integers(-7, -3, size=(2, 9)).astype(np.int8)
+    a = oracle.latent_compress_q8(lq, le, fq, fe, 2, 0.5)
+    b = oracle.latent_compress_q8(lq, (le - 1).astype(np.int8), fq, (fe + 1).astype(np.int8), 2, 0.5)
+    assert np.allclose(b, 2.0 * a, rtol=1e-13, atol=0)
+
+
+def test_compress_q8_zero_queries_average_the_dequantised_tokens():
+    r = rng(72)
+    fq = r.integers(-127, 128, size=(1, 5, 8)).astype(np.int8)
+    fe = np.array([[-2, 0, 1, -5, 3]], np.int8)
+    out = oracle.latent_compress_q8(np.zeros((3, 8), np.int8), np.zeros(3, np.int8), fq, fe, 1, 1.0)
+    mean = sum(fq[0, t].astype(np.float64) * 2.0 ** int(fe[0, t]) for t in range(5)) / 5.0
+    for c in range(3):
+        assert np.allclose(out[0, c], mean, rtol=1e-13, atol=1e-12)
+
+
 def test_avg_pool_compress_closed_forms():
     rng = np.random.default_rng(21)
     F = rng.normal(size=(2, 7, 5))

@@ -121,6 +121,33 @@ int sd_latent_compress(const void* latents, const void* feats, float* out,
                        void* stream);
 
 /* ------------------------------------------------------------------------
+ * Latent compression of the int8 draft (Eq. 3 with the draft quantised to
+ * int8, Appendix A; the paper names no scheme).  The learned queries and the
+ * visual features are int8 rows, each row with its own power-of-two scale:
+ * latent c stands for latents_q[c, :] * 2^latent_exp[c], token n of sequence
+ * b for feats_q[b, n, :] * 2^feat_exp[b, n].  The result is
+ * sd_latent_compress on those values (same heads, scale and output).
+ *
+ *   latents_q  [C, d]     int8     latent_exp [C]     int8
+ *   feats_q    [B, N, d]  int8     feat_exp   [B, N]  int8
+ *   out        [B, C, d]  float32
+ *   workspace  sd_latent_compress_q8_workspace_size(...) bytes (token-split
+ *              partials; depends on the current device like the bf16 path's)
+ * Every q * 2^e with |q| <= 127 and e in [-14, 9] is a normal fp16 (or
+ * zero), so the kernel forms the values exactly and runs both products on
+ * fp16 matrix cores; exponents outside [-14, 9] are clamped to it (a
+ * precondition).  Half the feature bytes of the bf16 path.
+ * Requirements: those of sd_latent_compress for SD_BF16 with dh = 128;
+ * latents_q, feats_q and out 16-byte aligned.  Errors as there.
+ * ---------------------------------------------------------------------- */
+size_t sd_latent_compress_q8_workspace_size(int B, int N, int C, int d, int num_heads);
+
+int sd_latent_compress_q8(const int8_t* latents_q, const int8_t* latent_exp,
+                          const int8_t* feats_q, const int8_t* feat_exp, float* out,
+                          int B, int N, int C, int d, int num_heads, float scale,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Average pooling of the visual tokens, the non-parametric compressor the
  * compression ablation compares against (Sec. 4.3): the N tokens of each
  * sequence form C contiguous groups, group c holding tokens

@@ -32,6 +32,7 @@ __all__ = [
     "sd_semi_ar_layer_workspace_size", "sd_semi_ar_layer",
     "sd_semi_ar_draft_workspace_size", "sd_semi_ar_draft",
     "sd_linear_q8", "sd_semi_ar_layer_q8", "sd_avg_pool_compress",
+    "sd_latent_compress_q8_workspace_size", "sd_latent_compress_q8",
 ]
 
 SD_OK, SD_ERR_INVALID_ARG, SD_ERR_UNSUPPORTED, SD_ERR_WORKSPACE, SD_ERR_HIP = 0, 1, 2, 3, 4
@@ -71,6 +72,8 @@ _SIGNATURES = {
     "sd_semi_ar_draft_workspace_size": (_sz, [_i] * 10),
     "sd_linear_q8": (_i, [_vp] * 6 + [_i, _i, _i, _vp, _sz, _vp]),
     "sd_avg_pool_compress": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "sd_latent_compress_q8_workspace_size": (_sz, [_i, _i, _i, _i, _i]),
+    "sd_latent_compress_q8": (_i, [_vp] * 5 + [_i] * 5 + [_f, _vp, _sz, _vp]),
     "sd_semi_ar_layer_q8": (_i, [_vp] * 18 + [_i] * 7 + [_f, _f, _vp, _sz, _vp]),
     "sd_semi_ar_draft": (_i, [_vp] * 18 + [_i] * 10 + [_f, _f, _f, _vp, _sz, _vp]),
 }
@@ -207,6 +210,39 @@ def sd_latent_compress(latents, feats, num_heads=1, scale=1.0, out=None, workspa
                                       num_heads, float(scale), dt, _ptr(ws), ws_len,
                                       _stream(stream))
     _raise(st, "sd_latent_compress")
+    return out
+
+
+def sd_latent_compress_q8_workspace_size(B, N, C, d, num_heads):
+    return library().sd_latent_compress_q8_workspace_size(B, N, C, d, num_heads)
+
+
+def sd_latent_compress_q8(latents_q, latent_exp, feats_q, feat_exp, num_heads=1, scale=1.0, out=None,
+                          workspace=None, stream=None):
+    """Eq. 3 on int8 rows with power-of-two row scales: latents_q [C, d] int8
+    with latent_exp [C] int8, feats_q [B, N, d] int8 with feat_exp [B, N]
+    int8 (row r stands for q[r] * 2^e[r]).  Returns out [B, C, d] fp32."""
+    torch = _torch()
+    _check(latents_q, "latents_q", dtype=torch.int8, ndim=2)
+    _check(feats_q, "feats_q", dtype=torch.int8, ndim=3)
+    _check(latent_exp, "latent_exp", dtype=torch.int8, ndim=1)
+    _check(feat_exp, "feat_exp", dtype=torch.int8, ndim=2)
+    C, d = latents_q.shape
+    B, N, d2 = feats_q.shape
+    if d2 != d or latent_exp.shape[0] != C or tuple(feat_exp.shape) != (B, N):
+        raise ValueError("latents_q [C, d], latent_exp [C], feats_q [B, N, d], feat_exp [B, N] expected")
+    dev = feats_q.device
+    for name, t in (("latents_q", latents_q), ("latent_exp", latent_exp), ("feat_exp", feat_exp)):
+        _same_device(name, t, dev)
+    if out is None:
+        out = torch.empty((B, C, d), dtype=torch.float32, device=dev)
+    _out(out, "out", (B, C, d), torch.float32, dev)
+    ws_bytes = sd_latent_compress_q8_workspace_size(B, N, C, d, num_heads)
+    ws, ws_len = _workspace(ws_bytes, dev, workspace)
+    st = library().sd_latent_compress_q8(_ptr(latents_q), _ptr(latent_exp), _ptr(feats_q), _ptr(feat_exp),
+                                         _ptr(out), B, N, C, d, num_heads, float(scale), _ptr(ws), ws_len,
+                                         _stream(stream))
+    _raise(st, "sd_latent_compress_q8")
     return out
 
 

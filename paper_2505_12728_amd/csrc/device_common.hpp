@@ -109,6 +109,13 @@ __device__ __forceinline__ u32x2 lds_read_tr16_b64(uint32_t addr) {
   return r;
 }
 
+// one signed byte, sign-extended
+__device__ __forceinline__ int lds_read_i8(uint32_t addr) {
+  int r;
+  asm volatile("ds_read_i8 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+
 __device__ __forceinline__ void lds_write_b128(uint32_t addr, const u32x4& v) {
   asm volatile("ds_write_b128 %0, %1" : : "v"(addr), "v"(v));
 }
@@ -221,6 +228,29 @@ __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t v) {
   uint32_t r;
   __builtin_memcpy(&r, &h2, 4);
   return r;
+}
+
+// 16 int8 values q (one 16-byte piece) to 16 fp16 values q * 2^e, exact
+// for e in [-14, 9] (|q| <= 127: every result is zero or a normal fp16).
+// Per 4 values: the bytes biased to u = q + 128, placed under the fp16
+// pattern of 1024 (0x64uu = 1024 + u) by byte permutes, then 1152
+// subtracted and 2^e applied with packed fp16 arithmetic (both exact).
+typedef _Float16 half2_ __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void i8x16_to_f16_pow2(const u32x4& q, int e, u32x4& lo, u32x4& hi) {
+  const uint32_t s_bits = (uint32_t)(e + 15) << 10;          // 2^e as fp16
+  const half2_ s2 = __builtin_bit_cast(half2_, s_bits | (s_bits << 16));
+  const half2_ off = {(_Float16)-1152.f, (_Float16)-1152.f};
+  uint32_t r[8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t u = q[k] ^ 0x80808080u;
+    const uint32_t p01 = __builtin_amdgcn_perm(0x64646464u, u, 0x04010400u);   // 0x64 u1 0x64 u0
+    const uint32_t p23 = __builtin_amdgcn_perm(0x64646464u, u, 0x04030402u);   // 0x64 u3 0x64 u2
+    r[2 * k] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(half2_, p01) + off) * s2);
+    r[2 * k + 1] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(half2_, p23) + off) * s2);
+  }
+  lo = u32x4{r[0], r[1], r[2], r[3]};
+  hi = u32x4{r[4], r[5], r[6], r[7]};
 }
 
 __device__ __forceinline__ float partner32(float v, float* other) {

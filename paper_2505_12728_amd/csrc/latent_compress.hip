@@ -34,6 +34,7 @@ namespace sd {
 namespace {
 
 constexpr int kTok = 64;   // tokens per LDS tile of the bf16 kernel
+constexpr int kQ8MaxSplit = 16384;   // tokens per split of the int8 kernel (their exponents sit in LDS)
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short shortx4;
 typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
@@ -87,22 +88,30 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // are inline asm, and each step has one counted wait for its copies and
 // one fence-free barrier (for eight-wave groups placed before the step's
 // last group, so the next step's first reads overlap that group's work).
-template <int NW, int DH>
+template <int NW, int DH, bool IN8>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
                                                          int tokens_per_split, int nsplit) {
   constexpr int TT = 64;                    // tokens per tile
   constexpr int DC = DH / 32;               // 32-channel slices (QK)
   constexpr int DB = DH / 16;               // 16-channel output blocks (PV)
-  constexpr int PK = DH / 8;                // 16-byte pieces per token
-  constexpr int ROW = DH * 2;               // bytes per token row
+  constexpr int PK = DH / 8;                // 16-byte fp16 pieces per token
+  constexpr int ROW = DH * 2;               // fp16 bytes per token row
   constexpr int TILE_BYTES = TT * ROW;
-  constexpr int DMA = TT * PK / 64;         // 64-lane copies per tile
+  constexpr int IN_ROW = IN8 ? DH : DH * 2; // input bytes per token row
+  constexpr int IN_PK = IN_ROW / 16;        // 16-byte input pieces per token
+  constexpr int IN_PIECES = TT * IN_PK;     // per tile
+  constexpr int DMA = IN_PIECES / 64;       // 64-lane copies per tile
   constexpr int DMA_PER_WAVE = DMA / NW;
-  constexpr int CVT_PER_THREAD = TT * PK / (NW * 64);   // pieces converted per thread
+  constexpr int CVT_PER_THREAD = IN_PIECES / (NW * 64);   // input pieces converted per thread
   constexpr int NBUF = 4;
   constexpr float kRescale = 15.f;      // P = exp2(s - m) <= 2^15 < the fp16 maximum
-  static_assert(DMA % NW == 0 && (TT * PK) % (NW * 64) == 0, "tile work must split evenly");
+  static_assert(DMA % NW == 0 && IN_PIECES % (NW * 64) == 0, "tile work must split evenly");
+  static_assert(!IN8 || DH == 128, "int8 input: 128-channel heads");
+  // fp16 tiles (bf16 input: the copy lands here and is converted in place;
+  // int8 input: converted here from the staging ring)
   __shared__ __align__(16) unsigned char ring[NBUF][TILE_BYTES];
+  __shared__ __align__(16) unsigned char stage[IN8 ? NBUF : 1][IN8 ? TT * IN_ROW : 16];
+  __shared__ int8_t sexp[IN8 ? kQ8MaxSplit : 4];   // int8 input: the split's token exponents
 
   int bh, lt;
   map_tile(blockIdx.x, n_bh, n_lt, bh, lt);
@@ -116,7 +125,24 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 
   // query fragments (fp16, B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..]
   f16x8 qf[2][DC];
-  {
+  if constexpr (IN8) {
+    const int8_t* lat = static_cast<const int8_t*>(a.latents);
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int r = lat0 + rb * 16 + c;
+      const int e = r < a.C ? min(max((int)a.latent_exp[r], -14), 9) : 0;
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) {
+        const u32x2 q = r < a.C ? *reinterpret_cast<const u32x2*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
+                                : u32x2{0u, 0u};
+        u32x4 lo, hi;
+        i8x16_to_f16_pow2(u32x4{q[0], q[1], 0u, 0u}, e, lo, hi);
+        Pack8 pk;
+        pk.u = lo;
+        qf[rb][dc] = pk.h;
+      }
+    }
+  } else {
     const uint16_t* lat = static_cast<const uint16_t*>(a.latents);
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
@@ -146,37 +172,84 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = (_Float16)(c == 0 ? 1.f : 0.f);
 
-  const uint16_t* fbase = static_cast<const uint16_t*>(a.feats) + (size_t)b * a.N * a.d + h * DH;
+  const unsigned char* fbase = static_cast<const unsigned char*>(a.feats) +
+                              ((size_t)b * a.N * a.d + h * DH) * (IN8 ? 1 : 2);
   const int ntiles = (tok1 - tok0 + TT - 1) / TT;
   const int last = ntiles - 1;
+  if constexpr (IN8) {
+    // the split's token exponents, once, before any copy is in flight
+    const int8_t* fe = a.feat_exp + (size_t)b * a.N + tok0;
+    for (int i = tid; i < tok1 - tok0; i += NW * 64) sexp[i] = fe[i];
+  }
 
-  // copy i of this wave moves pieces P = (w * DMA_PER_WAVE + i) * 64 + lane:
-  // token P / PK, LDS slot P % PK holding global piece slot ^ (token & 7)
-  auto issue = [&](int tile, unsigned char* buf) {
+  // copy i of this wave moves input pieces P = (w * DMA_PER_WAVE + i) * 64 +
+  // lane: token P / IN_PK.  bf16: LDS slot P % PK holds global piece
+  // slot ^ swizzle(token) of the fp16 tile; int8: the staging tile is plain
+  // token-major.  Tokens past the split re-read its last token.
+  auto issue = [&](int tile, int slot) {
     const int t0 = tok0 + tile * TT;
+    unsigned char* buf = IN8 ? stage[slot] : ring[slot];
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) {
       const int P = (w * DMA_PER_WAVE + i) * 64 + lane;
-      const int tk = P / PK, piece = P % PK;
+      const int tk = P / IN_PK, piece = P % IN_PK;
       const int tg = min(t0 + tk, tok1 - 1);
-      const uint16_t* src = fbase + (size_t)tg * a.d + ((piece ^ swz<DH>(tk)) * 8);
+      const int src_piece = IN8 ? piece : (piece ^ swz<DH>(tk));
+      const unsigned char* src = fbase + (size_t)tg * a.d * (IN8 ? 1 : 2) + src_piece * 16;
       __builtin_amdgcn_global_load_lds((gbl_cvoid*)src,
                                        (lds_void*)(buf + (w * DMA_PER_WAVE + i) * 1024), 16, 0, 0);
     }
   };
-  // in-place bf16 -> fp16 conversion of this thread's pieces of a tile
-  auto convert = [&](const unsigned char* buf) {
-    const uint32_t base = lds_addr(buf);
-    u32x4 v[CVT_PER_THREAD];
+  // int8 input: input piece i of this thread (token tk, channels 16 p8 ..)
+  // becomes fp16 pieces 2 p8 and 2 p8 + 1 of token tk (swizzled slots),
+  // written as soon as they are formed (the fp16 slot is not read before
+  // the next step's barrier)
+  auto piece_token = [&](int i) { return (i * NW * 64 + tid) / IN_PK; };
+  auto write_f16 = [&](uint32_t base, int i, const u32x4& lo, const u32x4& hi) {
+    const int tk = piece_token(i), p8 = (i * NW * 64 + tid) % IN_PK;
+    lds_write_b128(base + tk * ROW + (((2 * p8) ^ swz<DH>(tk)) * 16), lo);
+    lds_write_b128(base + tk * ROW + (((2 * p8 + 1) ^ swz<DH>(tk)) * 16), hi);
+  };
+  // LDS address of the exponent of input piece i of tile `tile` (the tile
+  // clamped as the copies are, the token clamped to the split)
+  const uint32_t sexp_base = lds_addr(sexp);
+  auto exp_addr = [&](int tile, int i) {
+    return sexp_base + (uint32_t)min(min(tile, last) * TT + piece_token(i), tok1 - tok0 - 1);
+  };
+  // conversion of this thread's pieces of a tile: bf16 in place, or int8
+  // from the staging slot into the fp16 slot
+  auto convert = [&](int slot, int tile) {
+    const uint32_t base = lds_addr(ring[slot]);
+    if constexpr (IN8) {
+      const uint32_t sbase = lds_addr(stage[slot]);
+      u32x4 v[CVT_PER_THREAD];
+      int e[CVT_PER_THREAD];
 #pragma unroll
-    for (int i = 0; i < CVT_PER_THREAD; ++i) v[i] = lds_read_b128(base + (i * NW * 64 + tid) * 16);
-    lds_wait();
+      for (int i = 0; i < CVT_PER_THREAD; ++i) {
+        v[i] = lds_read_b128(sbase + (i * NW * 64 + tid) * 16);
+        e[i] = lds_read_i8(exp_addr(tile, i));
+      }
+      lds_wait();
 #pragma unroll
-    for (int i = 0; i < CVT_PER_THREAD; ++i) {
-      tie(v[i]);
+      for (int i = 0; i < CVT_PER_THREAD; ++i) {
+        tie(v[i]);
+        tie(e[i]);
+        u32x4 lo, hi;
+        i8x16_to_f16_pow2(v[i], min(max(e[i], -14), 9), lo, hi);
+        write_f16(base, i, lo, hi);
+      }
+    } else {
+      u32x4 v[CVT_PER_THREAD];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[i][e] = bf16x2_to_f16x2(v[i][e]);
-      lds_write_b128(base + (i * NW * 64 + tid) * 16, v[i]);
+      for (int i = 0; i < CVT_PER_THREAD; ++i) v[i] = lds_read_b128(base + (i * NW * 64 + tid) * 16);
+      lds_wait();
+#pragma unroll
+      for (int i = 0; i < CVT_PER_THREAD; ++i) {
+        tie(v[i]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[i][e] = bf16x2_to_f16x2(v[i][e]);
+        lds_write_b128(base + (i * NW * 64 + tid) * 16, v[i]);
+      }
     }
   };
 
@@ -343,13 +416,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   constexpr int NPVH = DB / 4;         // PV read groups per half
   constexpr int NG = NQK + 2 * NPVH;
   constexpr int EPG = 4 / NQK;         // exponential quarters per QK group
-  issue(0, ring[0]);
-  issue(min(1, last), ring[1]);
-  issue(min(2, last), ring[2]);
+  issue(0, 0);
+  issue(min(1, last), 1);
+  issue(min(2, last), 2);
   wait_vm_then_barrier<2 * DMA_PER_WAVE>();           // tile 0 landed
-  convert(ring[0]);
+  convert(0, 0);
   wait_vm_then_barrier<DMA_PER_WAVE>();               // tile 1 landed, tile 0 converted
-  convert(ring[1]);
+  convert(1, 1);
   floatx4 scur[4][2];
   {
     const uint32_t sb = lds_addr(ring[0]);
@@ -375,7 +448,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // LDS reads of group g into the alternating register sets xr / vr (and
   // the conversion pieces cv with the first PV group)
   auto reads = [&](auto gtag, uint32_t nb, uint32_t vb, uint32_t cb, u32x4 (&xr)[2][4],
-                   u32x2 (&vr)[2][4][2], u32x4 (&cv)[CVT_PER_THREAD], auto tie_only) {
+                   u32x2 (&vr)[2][4][2], u32x4 (&cv)[CVT_PER_THREAD], int (&ce)[CVT_PER_THREAD], int etile,
+                   auto tie_only) {
     constexpr int g = decltype(gtag)::value;
     constexpr bool T = decltype(tie_only)::value;
     if constexpr (g < NQK) {
@@ -401,7 +475,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         }
         if constexpr (q == 0) {
 #pragma unroll
-          for (int i = 0; i < CVT_PER_THREAD; ++i) tie(cv[i]);
+          for (int i = 0; i < CVT_PER_THREAD; ++i) {
+            tie(cv[i]);
+            if constexpr (IN8) tie(ce[i]);
+          }
         }
       } else {
 #pragma unroll
@@ -411,7 +488,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         }
         if constexpr (q == 0) {
 #pragma unroll
-          for (int i = 0; i < CVT_PER_THREAD; ++i) cv[i] = lds_read_b128(cb + (i * NW * 64 + tid) * 16);
+          for (int i = 0; i < CVT_PER_THREAD; ++i) {
+            cv[i] = lds_read_b128(cb + (i * NW * 64 + tid) * 16);
+            if constexpr (IN8) ce[i] = lds_read_i8(exp_addr(etile, i));
+          }
         }
       }
     }
@@ -419,7 +499,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 
   // LDS operations issued by reads() for group g
   constexpr auto reads_in = [](int g) {
-    return g < NQK ? 4 : (g < NG ? 8 + (g == NQK ? CVT_PER_THREAD : 0) : 0);
+    return g < NQK ? 4 : (g < NG ? 8 + (g == NQK ? CVT_PER_THREAD * (IN8 ? 2 : 1) : 0) : 0);
   };
 
   // Eight-wave groups (DH = 128) move the step's barrier from its start to
@@ -438,31 +518,33 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   // tile it+3 issued and (kRot) the first group's reads done.
   auto step = [&](int it, auto mask_tag) {
     const uint32_t nb = lds_addr(ring[(it + 1) % NBUF]);
-    const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);
+    const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);          // converted tile it+2
+    const uint32_t ci = IN8 ? lds_addr(stage[(it + 2) % NBUF]) : cb;   // its input
     const uint32_t vb = lds_addr(ring[it % NBUF]);
     u32x2 vr[2][4][2];
     u32x4 cv[CVT_PER_THREAD];
+    int ce[CVT_PER_THREAD];
     floatx4 snext[4][2];
     f16x8 pf[2][2];
     bool exceed = false;
     if constexpr (!kRot) {
       // tile it+2 landed; tile it+1 converted by every wave; buffer it-1 free
       wait_vm_then_barrier<0>();
-      reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
-      issue(min(it + 3, last), ring[(it + 3) % NBUF]);
+      reads(std::integral_constant<int, 0>{}, nb, vb, ci, xr, vr, cv, ce, it + 2, std::false_type{});
+      issue(min(it + 3, last), (it + 3) % NBUF);
     }
     static_for<0, NG>([&](auto gtag) {
       constexpr int g = decltype(gtag)::value;
       // issue the next group's reads, then wait for this group's (the
       // next group's stay in flight)
       if constexpr (kRot) {
-        reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+        reads(std::integral_constant<int, g + 1>{}, nb, vb, ci, xr, vr, cv, ce, it + 2, std::false_type{});
         lds_wait_n<reads_in(g + 1)>();
-        reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
+        reads(gtag, nb, vb, ci, xr, vr, cv, ce, it + 2, std::true_type{});
       } else {
         lds_wait();
-        reads(gtag, nb, vb, cb, xr, vr, cv, std::true_type{});
-        reads(std::integral_constant<int, g + 1>{}, nb, vb, cb, xr, vr, cv, std::false_type{});
+        reads(gtag, nb, vb, ci, xr, vr, cv, ce, it + 2, std::true_type{});
+        reads(std::integral_constant<int, g + 1>{}, nb, vb, ci, xr, vr, cv, ce, it + 2, std::false_type{});
       }
       if constexpr (kRot && g == NG - 1) {
         // tile it+2 converted by every wave, tile it+3 landed, buffer it
@@ -470,15 +552,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         // tile it+4 into buffer it, under this group's matrix-core work
         wait_vm_then_barrier<0>();
         if constexpr (!decltype(mask_tag)::value) {
-          reads(std::integral_constant<int, 0>{}, lds_addr(ring[(it + 2) % NBUF]), vb, cb, xr, vr, cv,
-                std::false_type{});
-          issue(min(it + 4, last), ring[it % NBUF]);
+          reads(std::integral_constant<int, 0>{}, lds_addr(ring[(it + 2) % NBUF]), vb, ci, xr, vr, cv, ce,
+                it + 2, std::false_type{});
+          issue(min(it + 4, last), it % NBUF);
         }
       }
       if constexpr (g == NQK + NPVH) {
         // conversion finished in the first half: write it back
+        if constexpr (!IN8) {
 #pragma unroll
-        for (int i = 0; i < CVT_PER_THREAD; ++i) lds_write_b128(cb + (i * NW * 64 + tid) * 16, cv[i]);
+          for (int i = 0; i < CVT_PER_THREAD; ++i) lds_write_b128(cb + (i * NW * 64 + tid) * 16, cv[i]);
+        }
       }
       if constexpr (g < NQK) {
         // scores of tile it+1 for channel slice dc = g
@@ -519,11 +603,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           for (int rb = 0; rb < 2; ++rb) o[rb][DB] = mfma_f16(ones, pf[hf][rb], o[rb][DB]);
         }
         if constexpr (hf == 0) {
-          // in-place conversion of tile it+2, spread over the first half
+          // conversion of tile it+2, spread over the first half
 #pragma unroll
-          for (int i = pb; i < CVT_PER_THREAD; i += NPVH)
+          for (int i = pb; i < CVT_PER_THREAD; i += NPVH) {
+            if constexpr (IN8) {
+              u32x4 lo, hi;
+              i8x16_to_f16_pow2(cv[i], min(max(ce[i], -14), 9), lo, hi);
+              write_f16(cb, i, lo, hi);
+            } else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) cv[i][e] = bf16x2_to_f16x2(cv[i][e]);
+              for (int e = 0; e < 4; ++e) cv[i][e] = bf16x2_to_f16x2(cv[i][e]);
+            }
+          }
         } else if constexpr (pb == NPVH - 1) {
           exceed = tile_exceeds(snext);
         }
@@ -532,7 +623,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       if constexpr (kRot && g == NG - 1 && !decltype(mask_tag)::value) {
         // the next step's first group is complete before the loop edge
         lds_wait();
-        reads(std::integral_constant<int, 0>{}, nb, vb, cb, xr, vr, cv, std::true_type{});
+        reads(std::integral_constant<int, 0>{}, nb, vb, ci, xr, vr, cv, ce, it + 2, std::true_type{});
       }
       __builtin_amdgcn_sched_barrier(0);
     });
@@ -554,11 +645,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     wait_vm_then_barrier<0>();
     u32x2 vr0[2][4][2];
     u32x4 cv0[CVT_PER_THREAD];
+    int ce0[CVT_PER_THREAD];
     const uint32_t nb0 = lds_addr(ring[1]);
-    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, std::false_type{});
-    issue(min(3, last), ring[3 % NBUF]);
+    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, ce0, 0, std::false_type{});
+    issue(min(3, last), 3 % NBUF);
     lds_wait();
-    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, std::true_type{});
+    reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, ce0, 0, std::true_type{});
   }
   for (int it = 0; it + 1 < last; ++it) step(it, std::false_type{});
   if (last >= 1) step(last - 1, std::true_type{});
@@ -777,22 +869,22 @@ __global__ __launch_bounds__(256) void avg_pool(const T* feats, float* out, int 
     if (e0 + i < d) dst[i] = (float)(acc[i] * inv);
 }
 
-template <int NW, int DH>
+template <int NW, int DH, bool IN8>
 hipError_t launch_bf16(const CompressArgs& a, const CompressPlan& p, hipStream_t st) {
   const int n_bh = a.B * a.H;
   dim3 grid(n_bh * p.lat_tiles, p.nsplit);
-  hipLaunchKernelGGL((compress_bf16<NW, DH>), grid, dim3(NW * 64), 0, st, a, n_bh, p.lat_tiles,
+  hipLaunchKernelGGL((compress_bf16<NW, DH, IN8>), grid, dim3(NW * 64), 0, st, a, n_bh, p.lat_tiles,
                      p.tokens_per_split, p.nsplit);
   return hipGetLastError();
 }
 
-template <int DH>
+template <int DH, bool IN8>
 hipError_t dispatch_nw(const CompressArgs& a, const CompressPlan& p, hipStream_t st) {
   switch (p.lat_tile / 32) {
-    case 1: return launch_bf16<1, DH>(a, p, st);
-    case 2: return launch_bf16<2, DH>(a, p, st);
-    case 4: return launch_bf16<4, DH>(a, p, st);
-    default: return launch_bf16<8, DH>(a, p, st);
+    case 1: return launch_bf16<1, DH, IN8>(a, p, st);
+    case 2: return launch_bf16<2, DH, IN8>(a, p, st);
+    case 4: return launch_bf16<4, DH, IN8>(a, p, st);
+    default: return launch_bf16<8, DH, IN8>(a, p, st);
   }
 }
 
@@ -815,13 +907,16 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus
     p.lat_tile = waves * 32;
     p.lat_tiles = (C + p.lat_tile - 1) / p.lat_tile;
     // split the tokens so that the grid fills the device in one round:
-    // two work-groups per compute unit (one of eight waves), keeping at
-    // least 128 tokens per split
+    // two work-groups per compute unit (one of eight waves, or with int8
+    // input, whose staging ring doubles the LDS), keeping at least 128
+    // tokens per split; int8 splits hold at most kQ8MaxSplit tokens
     const long long groups = n_bh * p.lat_tiles;
-    const long long resident = (long long)std::max(cus, 1) * (waves == 8 ? 1 : 2);
+    const long long resident = (long long)std::max(cus, 1) * (waves == 8 || dtype == kCompressInt8 ? 1 : 2);
     long long nsplit = std::max(1LL, resident / groups);
+    if (dtype == kCompressInt8) nsplit = std::max(nsplit, ((long long)N + kQ8MaxSplit - 1) / kQ8MaxSplit);
     long long tps = (N + nsplit - 1) / nsplit;
     tps = std::max(128LL, (tps + kTok - 1) / kTok * kTok);
+    if (dtype == kCompressInt8) tps = std::min(tps, (long long)kQ8MaxSplit);
     p.tokens_per_split = (int)tps;
   }
   p.nsplit = std::max(1, (N + p.tokens_per_split - 1) / p.tokens_per_split);
@@ -839,8 +934,10 @@ hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dty
     hipLaunchKernelGGL(compress_f32, grid, dim3(256), lds, st, a, p.dh, p.tokens_per_split,
                        p.nsplit);
     e = hipGetLastError();
+  } else if (dtype == kCompressInt8) {
+    e = dispatch_nw<128, true>(a, p, st);
   } else {
-    e = p.dh == 128 ? dispatch_nw<128>(a, p, st) : dispatch_nw<64>(a, p, st);
+    e = p.dh == 128 ? dispatch_nw<128, false>(a, p, st) : dispatch_nw<64, false>(a, p, st);
   }
   if (e != hipSuccess || p.nsplit == 1) return e;
   const long long items = (long long)a.B * a.H * a.C * (p.dh / 4);

@@ -61,8 +61,10 @@ struct CompressPlan {
 CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus);
 
 struct CompressArgs {
-  const void* latents;
-  const void* feats;
+  const void* latents;          // [C, d] bf16 / fp32, or int8 rows (int8 input)
+  const void* feats;            // [B, N, d] likewise
+  const int8_t* latent_exp;     // int8 input: [C] exponents (row c stands for q * 2^e)
+  const int8_t* feat_exp;       // int8 input: [B, N] exponents
   float* out;
   int B, N, C, d, H;
   float scale;
@@ -71,6 +73,8 @@ struct CompressArgs {
   float* part_lse;     // [B, H, nsplit, C]
 };
 
+// dtype: 0 fp32, 1 bf16, 2 int8 rows with power-of-two row scales
+constexpr int kCompressInt8 = 2;
 hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dtype, hipStream_t s);
 // average pooling of N tokens into C contiguous groups (dtype 0 fp32, 1 bf16)
 hipError_t launch_avg_pool(const void* feats, float* out, int B, int N, int C, int d, int dtype, hipStream_t s);

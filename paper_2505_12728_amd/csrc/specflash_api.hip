@@ -173,6 +173,46 @@ int sd_latent_compress(const void* latents, const void* feats, float* out, int B
   return status_from(sd::launch_compress(a, plan, dtype, static_cast<hipStream_t>(stream)));
 }
 
+// ------------------------------------------------------ compress (int8)
+size_t sd_latent_compress_q8_workspace_size(int B, int N, int C, int d, int num_heads) {
+  int st = SD_OK;
+  if (!compress_shape_ok(B, N, C, d, num_heads, SD_BF16, &st) || d / num_heads != 128) return 0;
+  return sd::plan_compress(B, N, C, d, num_heads, sd::kCompressInt8, device_cus()).workspace_bytes;
+}
+
+int sd_latent_compress_q8(const int8_t* latents_q, const int8_t* latent_exp, const int8_t* feats_q,
+                          const int8_t* feat_exp, float* out, int B, int N, int C, int d, int num_heads,
+                          float scale, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = SD_OK;
+  if (!compress_shape_ok(B, N, C, d, num_heads, SD_BF16, &st)) return st;
+  if (d / num_heads != 128) return SD_ERR_UNSUPPORTED;
+  if (!latents_q || !latent_exp || !feats_q || !feat_exp || !out || !isfinite(scale))
+    return SD_ERR_INVALID_ARG;
+  if (!aligned(latents_q, 16) || !aligned(feats_q, 16) || !aligned(out, 16)) return SD_ERR_INVALID_ARG;
+  const sd::CompressPlan plan = sd::plan_compress(B, N, C, d, num_heads, sd::kCompressInt8, device_cus());
+  if (plan.workspace_bytes > 0 && (!workspace || workspace_bytes < plan.workspace_bytes ||
+                                   !aligned(workspace, 16)))
+    return SD_ERR_WORKSPACE;
+  sd::CompressArgs a{};
+  a.latents = latents_q;
+  a.feats = feats_q;
+  a.latent_exp = latent_exp;
+  a.feat_exp = feat_exp;
+  a.out = out;
+  a.B = B;
+  a.N = N;
+  a.C = C;
+  a.d = d;
+  a.H = num_heads;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  if (plan.workspace_bytes > 0) {
+    a.part_o = static_cast<float*>(workspace);
+    a.part_lse = a.part_o + (size_t)B * num_heads * plan.nsplit * C * plan.dh;
+  }
+  return status_from(sd::launch_compress(a, plan, sd::kCompressInt8, static_cast<hipStream_t>(stream)));
+}
+
 // --------------------------------------------------------------- verify
 size_t sd_verify_workspace_size(int B, int k, int Hq, int Hkv, int D, int capacity, int dtype) {
   int st;

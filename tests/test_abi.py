@@ -145,6 +145,22 @@ def test_accept_noalloc_validation_errors(lib):
     # sequence, so 1024 sequences always fit
 
 
+def test_compress_q8_validation_errors(lib):
+    keep, (lq, le, fq, fe, out, ws) = _fake(6)
+    f = lib.sd_latent_compress_q8
+
+    def call(lq=lq, le=le, fq=fq, fe=fe, out=out, B=1, N=64, C=32, d=256, H=2, scale=1.0):
+        return f(lq, le, fq, fe, out, B, N, C, d, H, scale, ws, 1 << 30, None)
+
+    assert call(lq=None) == sd.SD_ERR_INVALID_ARG
+    assert call(fe=None) == sd.SD_ERR_INVALID_ARG
+    assert call(N=0) == sd.SD_ERR_INVALID_ARG
+    assert call(d=255) == sd.SD_ERR_INVALID_ARG          # not a multiple of the heads
+    assert call(H=4) == sd.SD_ERR_UNSUPPORTED             # 64-channel heads
+    assert call(scale=float("nan")) == sd.SD_ERR_INVALID_ARG
+    assert lib.sd_latent_compress_q8_workspace_size(1, 64, 32, 256, 4) == 0
+
+
 def test_workspace_sizes_cover_the_partials(lib):
     # verify: one (D + 1)-float partial row per (sequence, KV head, split, row)
     for B, k, Hq, Hkv, D, cap in [(1, 4, 4, 1, 64, 608), (4, 8, 64, 8, 128, 65536),

@@ -212,6 +212,34 @@ def time_workload_ops(w, dev, steps, warmup):
             st["target_frac"] = gate
             st["target_met_at_median"] = bool(st["frac_at_median"] >= gate)
         out[name] = st
+    if w.dtype == "bf16":
+        # the int8 draft's compressor on the same inputs quantised to int8
+        # rows with power-of-two scales (same matrix-core work, half the
+        # feature bytes)
+        q = synth.compress_q8_inputs(w)
+        qd = {k_: torch.from_numpy(v_).to(dev) for k_, v_ in q.items()}
+        n8 = sd.sd_latent_compress_q8_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width, w.c_heads)
+        ws8 = torch.zeros(max(n8, 1), dtype=torch.uint8, device=dev)
+
+        def q8():
+            sd.sd_latent_compress_q8(qd["latents_q"], qd["latent_exp"], qd["feats_q"], qd["feat_exp"],
+                                     w.c_heads, 1.0, out=c_out, workspace=ws8)
+
+        for _ in range(warmup):
+            q8()
+        ev8 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for e in ev8:
+            e[0].record()
+            q8()
+            e[1].record()
+        torch.cuda.synchronize()
+        st = op_stats([e[0].elapsed_time(e[1]) for e in ev8])
+        rate = flops / (st["median_us"] * 1e-6) / 1e12
+        st.update({"algorithmic": flops, "unit": "TFLOP/s", "achieved_at_median": rate, "peak": BF16_PEAK_TFLOPS,
+                   "frac_at_median": rate / BF16_PEAK_TFLOPS, "bytes": synth.compress_q8_bytes(w),
+                   "outside_step": True})
+        out["latent_compress_q8"] = st
+        del qd, ws8
     vs = [a + b for a, b in zip(ver_ms, acc_ms)]
     out["verify_step"] = op_stats(vs)
     out["verify_step"]["kv_read_tbps_at_median"] = kv_bytes / (out["verify_step"]["median_us"] * 1e-6) / 1e12
@@ -515,6 +543,32 @@ def main():
     es = 2 if w.dtype == "bf16" else 4
     ap_bytes = w.c_batch * w.c_tokens * w.c_width * es + w.c_batch * w.c_latents * w.c_width * 4
 
+    # the int8 draft's compressor (int8 rows with power-of-two scales), timed
+    # on its own on the same features quantised
+    t_q8c = None
+    if w.dtype == "bf16":
+        qc = synth.compress_q8_inputs(w)
+        qcd = {k_: torch.from_numpy(v_).to(dev) for k_, v_ in qc.items()}
+        del qc
+        n8 = sd.sd_latent_compress_q8_workspace_size(w.c_batch, w.c_tokens, w.c_latents, w.c_width, w.c_heads)
+        ws8 = torch.zeros(max(n8, 1), dtype=torch.uint8, device=dev)
+        q8c_out = torch.empty_like(c_out)
+
+        def q8c_call():
+            sd.sd_latent_compress_q8(qcd["latents_q"], qcd["latent_exp"], qcd["feats_q"], qcd["feat_exp"],
+                                     w.c_heads, 1.0, out=q8c_out, workspace=ws8)
+
+        for _ in range(2):
+            q8c_call()
+        q8c_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
+        for e in q8c_ev:
+            e[0].record()
+            q8c_call()
+            e[1].record()
+        torch.cuda.synchronize()
+        t_q8c = float(np.mean([e[0].elapsed_time(e[1]) for e in q8c_ev]))
+        del qcd, ws8, q8c_out
+
     comp_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
     ver_ms = np.array([e[6].elapsed_time(e[2]) for e in events])
     lm_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
@@ -579,6 +633,14 @@ def main():
         rl["semi_ar_layer_q8"] = {"bound": "hbm", "achieved": q8_bytes / (t_q8 * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "traffic": None, "algorithmic": q8_bytes, "us": t_q8 * 1e3,
                                   "frac": q8_bytes / (t_q8 * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
+    if t_q8c is not None:
+        fq8 = synth.compress_flops(w)
+        rl["latent_compress_q8"] = {"bound": "mfma", "achieved": fq8 / (t_q8c * 1e-3) / 1e12,
+                                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "traffic": None,
+                                    "algorithmic": fq8, "us": t_q8c * 1e3,
+                                    "frac": fq8 / (t_q8c * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                                    "hbm_gbs": synth.compress_q8_bytes(w) / (t_q8c * 1e-3) / 1e9,
+                                    "outside_step": True}
     rl["avg_pool_compress"] = {"bound": "hbm", "achieved": ap_bytes / (t_ap * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
                                "unit": "GB/s", "traffic": None, "algorithmic": ap_bytes, "us": t_ap * 1e3,
                                "frac": ap_bytes / (t_ap * 1e-3) / 1e9 / HBM_PEAK_GBS, "outside_step": True}
@@ -621,6 +683,7 @@ def main():
         "semi_ar_draft_kp_us": t_kp * 1e3 if t_kp is not None else None,
         "semi_ar_layer_q8_us": t_q8 * 1e3 if t_q8 is not None else None,
         "avg_pool_compress_us": t_ap * 1e3,
+        "latent_compress_q8_us": t_q8c * 1e3 if t_q8c is not None else None,
         "latent_compress_tflops": flops / (ops["latent_compress"]["median_us"] * 1e-6) / 1e12,
         "kv_read_tbps_attention_only": kv_bytes / (ops["verify_attention"]["median_us"] * 1e-6) / 1e12,
         "ops": ops,

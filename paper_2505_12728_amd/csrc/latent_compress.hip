@@ -705,10 +705,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 }
 
 // ---------------------------------------------------------------- fp32
-// fp32 inputs: grid (8-latent block, token split, sequence x head).  Scores,
+// fp32 inputs: grid (8-latent block, token split, sequence x head) with
+// short token splits, so the work spreads over many compute units.  Scores,
 // softmax and P F_V run in float64 (literal Eq. 3 scores reach |s| ~ 60 for
 // unit-variance inputs, where fp32 rounding of s would already cost ~1e-5 of
-// relative accuracy in the weights).  Scores of the block live in LDS.
+// relative accuracy in the weights).  The block's queries and the split's
+// feature rows are staged in LDS with coalesced loads (rows padded by one
+// float so that lanes reading one channel of consecutive rows hit distinct
+// banks); the scores of the block live in LDS.
 constexpr int kF32Rows = 8;
 
 __global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int tokens_per_split,
@@ -721,20 +725,29 @@ __global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int 
   const int tok0 = split * tokens_per_split;
   const int nt = min(a.N, tok0 + tokens_per_split) - tok0;
   if (nt <= 0) return;
+  const int DS = dh + 1;
   double* ss = reinterpret_cast<double*>(smem);                // [8][tokens_per_split]
   double* st = ss + (size_t)kF32Rows * tokens_per_split;        // [8][2]
-  float* qs = reinterpret_cast<float*>(st + 2 * kF32Rows);      // [8][dh]
+  float* qs = reinterpret_cast<float*>(st + 2 * kF32Rows);      // [8][dh + 1]
+  float* fs = qs + (size_t)kF32Rows * DS;                        // [tokens_per_split][dh + 1]
   const float* lat = static_cast<const float*>(a.latents);
   const float* F = static_cast<const float*>(a.feats) + (size_t)b * a.N * a.d + h * dh;
   const int tid = threadIdx.x;
-  for (int i = tid; i < nr * dh; i += blockDim.x)
-    qs[i] = lat[(size_t)(r0 + i / dh) * a.d + h * dh + i % dh];
+  for (int i = tid; i < nr * dh; i += blockDim.x) {
+    const int r = i / dh, e = i - r * dh;
+    qs[r * DS + e] = lat[(size_t)(r0 + r) * a.d + h * dh + e];
+  }
+  for (int i = tid; i < nt * dh; i += blockDim.x) {
+    const int t = i / dh, e = i - t * dh;
+    fs[t * DS + e] = F[(size_t)(tok0 + t) * a.d + e];
+  }
   __syncthreads();
   const double scale = (double)a.scale;
+  // thread i: latent i / nt, token i % nt (consecutive lanes, consecutive tokens)
   for (int i = tid; i < nt * nr; i += blockDim.x) {
-    const int t = i / nr, r = i % nr;
-    const float* xr = F + (size_t)(tok0 + t) * a.d;
-    const float* qr = qs + r * dh;
+    const int r = i / nt, t = i - r * nt;
+    const float* xr = fs + t * DS;
+    const float* qr = qs + r * DS;
     double acc = 0.0;
     for (int e = 0; e < dh; ++e) acc = fma((double)qr[e], (double)xr[e], acc);
     ss[(size_t)r * tokens_per_split + t] = acc * scale;
@@ -759,19 +772,19 @@ __global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int 
   }
   __syncthreads();
   for (int i = tid; i < nr * dh; i += blockDim.x) {
-    const int r = i / dh, e = i % dh;
+    const int r = i / dh, e = i - r * dh;
+    const double* pr = ss + (size_t)r * tokens_per_split;
     double acc = 0.0;
 #pragma unroll 8
-    for (int t = 0; t < nt; ++t)
-      acc = fma(ss[(size_t)r * tokens_per_split + t], (double)F[(size_t)(tok0 + t) * a.d + e], acc);
+    for (int t = 0; t < nt; ++t) acc = fma(pr[t], (double)fs[t * DS + e], acc);
     const double sum = st[2 * r + 1];
     const float v = (float)(acc / sum);
     if (nsplit == 1) {
       a.out[((size_t)b * a.C + r0 + r) * a.d + h * dh + e] = v;
     } else {
-      const size_t pr = ((size_t)bh * nsplit + split) * a.C + r0 + r;
-      a.part_o[pr * dh + e] = v;
-      if (e == 0) a.part_lse[pr] = (float)((st[2 * r] + log(sum)) * 1.4426950408889634);
+      const size_t pr_ = ((size_t)bh * nsplit + split) * a.C + r0 + r;
+      a.part_o[pr_ * dh + e] = v;
+      if (e == 0) a.part_lse[pr_] = (float)((st[2 * r] + log(sum)) * 1.4426950408889634);
     }
   }
 }
@@ -897,9 +910,14 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus
   if (dtype == 0) {
     p.lat_tile = kF32Rows;
     p.lat_tiles = (C + kF32Rows - 1) / kF32Rows;
-    // fp64 scores of 8 latents + fp32 queries within 64 KB of LDS
-    const long long cap = (65536 - 4LL * kF32Rows * p.dh - 16 * kF32Rows) / (8 * kF32Rows);
-    p.tokens_per_split = (int)std::max(64LL, std::min(2048LL, cap / 64 * 64));
+    // short splits (64 tokens at most) so the grid spreads over the device;
+    // the split's fp32 feature rows and the 8 queries (rows padded by one
+    // float) and fp64 scores within 64 KB of LDS
+    long long tps = 64;
+    while (tps > 8 && (4LL * kF32Rows * (p.dh + 1) + 4LL * tps * (p.dh + 1) + 8LL * kF32Rows * tps +
+                       16 * kF32Rows) > 65536)
+      tps /= 2;
+    p.tokens_per_split = (int)tps;
   } else {
     // 32 latents per wave; eight-wave groups (each F_V tile copied and
     // converted once for 256 latents) whenever there are more than 128
@@ -929,7 +947,7 @@ hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dty
   hipError_t e;
   if (dtype == 0) {
     const size_t lds = (size_t)kF32Rows * p.tokens_per_split * 8 + 16 * kF32Rows +
-                       (size_t)kF32Rows * p.dh * 4;
+                       (size_t)kF32Rows * (p.dh + 1) * 4 + (size_t)p.tokens_per_split * (p.dh + 1) * 4;
     dim3 grid(p.lat_tiles, p.nsplit, a.B * a.H);
     hipLaunchKernelGGL(compress_f32, grid, dim3(256), lds, st, a, p.dh, p.tokens_per_split,
                        p.nsplit);

@@ -587,13 +587,18 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
 // ----------------------------------------------------------- fp32 split
 // fp32 inputs: scores, softmax and P V run in float64, so the result keeps
 // full fp32 accuracy even when large scores make the softmax sensitive to
-// rounding.  Queries and the split's scores sit in LDS; one wave per row
-// forms the softmax statistics; threads over (row, channel) accumulate P V.
+// rounding.  Grid (key split, KV head, sequence) with short splits, so the
+// work spreads over many compute units.  The block's queries and the
+// split's key and value rows are staged in LDS with coalesced loads (rows
+// padded by one float, so that lanes reading the same channel of
+// consecutive rows hit distinct banks); the split's scores sit in LDS; one
+// wave per row forms the softmax statistics; threads over (row, channel)
+// accumulate P V.
 template <bool PAGED>
 __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_per_split,
                                                         int nsplit, int rows_padded) {
   extern __shared__ __align__(16) unsigned char smem[];
-  const int D = a.D;
+  const int D = a.D, DS = D + 1;
   const int split = blockIdx.x;
   const int hk = blockIdx.y;
   const int b = blockIdx.z;
@@ -605,27 +610,35 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
   const int R = a.k * g;
   const int tid = threadIdx.x;
 
-  double* ss = reinterpret_cast<double*>(smem);        // [R][keys_per_split]
+  double* ss = reinterpret_cast<double*>(smem);         // [R][keys_per_split]
   double* st = ss + (size_t)R * keys_per_split;         // [R][2]: max, sum
-  float* qs = reinterpret_cast<float*>(st + 2 * R);     // [R][D]
+  float* qs = reinterpret_cast<float*>(st + 2 * R);     // [R][D + 1]
+  float* ks = qs + (size_t)R * DS;                       // [keys_per_split][D + 1]
+  float* vs = ks + (size_t)keys_per_split * DS;          // [keys_per_split][D + 1]
   const float* qg = static_cast<const float*>(a.q);
-  for (int i = tid; i < R * D; i += blockDim.x) {
-    const int r = i / D, e = i % D;
-    const int j = r / g, h = hk * g + (r - j * g);
-    qs[i] = qg[(((size_t)b * a.k + j) * a.Hq + h) * D + e];
-  }
-  __syncthreads();
   const float* kg = static_cast<const float*>(a.kc);
   const float* vg = static_cast<const float*>(a.vc);
+  for (int i = tid; i < R * D; i += blockDim.x) {
+    const int r = i / D, e = i - r * D;
+    const int j = r / g, h = hk * g + (r - j * g);
+    qs[r * DS + e] = qg[(((size_t)b * a.k + j) * a.Hq + h) * D + e];
+  }
+  for (int i = tid; i < nk * D; i += blockDim.x) {
+    const int tt = i / D, e = i - tt * D;
+    const size_t off = kv_offset<PAGED>(a, b, hk, k0 + tt, D) + e;
+    ks[tt * DS + e] = kg[off];
+    vs[tt * DS + e] = vg[off];
+  }
+  __syncthreads();
   const double scale = (double)a.scale;
+  // thread i: row i / nk, key i % nk (consecutive lanes take consecutive keys)
   for (int i = tid; i < nk * R; i += blockDim.x) {
-    const int tt = i / R, r = i % R;
-    const int t = k0 + tt;
+    const int r = i / nk, tt = i - r * nk;
     const int j = r / g;
     double s = -INFINITY;
-    if (t <= L - a.k + j) {
-      const float* kr = kg + kv_offset<PAGED>(a, b, hk, t, D);
-      const float* qr = qs + r * D;
+    if (k0 + tt <= L - a.k + j) {
+      const float* qr = qs + r * DS;
+      const float* kr = ks + tt * DS;
       double acc = 0.0;
       for (int e = 0; e < D; ++e) acc = fma((double)qr[e], (double)kr[e], acc);
       s = acc * scale;
@@ -654,16 +667,15 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
   __syncthreads();
   const size_t base = ((size_t)(b * a.Hkv + hk) * nsplit + split) * rows_padded;
   for (int i = tid; i < R * D; i += blockDim.x) {
-    const int r = i / D, e = i % D;
+    const int r = i / D, e = i - r * D;
     const double sum = st[2 * r + 1];
+    const double* pr = ss + (size_t)r * keys_per_split;
     double acc = 0.0;
-    // every load is issued regardless of p (keys k0 .. k0 + nk - 1 all lie
-    // inside the sequence), so the unrolled loads overlap; a zero weight
-    // still adds nothing, even against a non-finite value
+    // a zero weight adds nothing, even against a non-finite value
 #pragma unroll 8
     for (int tt = 0; tt < nk; ++tt) {
-      const double p = ss[(size_t)r * keys_per_split + tt];
-      const double v = (double)vg[kv_offset<PAGED>(a, b, hk, k0 + tt, D) + e];
+      const double p = pr[tt];
+      const double v = (double)vs[tt * DS + e];
       acc = fma(p, p != 0.0 ? v : 0.0, acc);
     }
     a.part_o[(base + r) * D + e] = sum > 0.0 ? (float)(acc / sum) : 0.f;
@@ -875,10 +887,14 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     p.row_blocks = blocks16;
     p.row_groups = 1;
     p.rows_padded = p.rows;
-    // fp32 queries, fp64 scores of all rows for one split and fp64 row
-    // statistics stay within 64 KB of LDS
-    int kps = ((65536 - 4 * p.rows * D - 16 * p.rows) / (8 * std::max(p.rows, 1))) / 32 * 32;
-    p.keys_per_split = std::max(32, std::min(1024, kps));
+    // short splits (64 keys at most) so that the grid spreads over the
+    // device; fp32 queries and the split's keys and values (rows padded by
+    // one float), fp64 scores and row statistics within 64 KB of LDS
+    int kps = 64;
+    while (kps > 8 && (size_t)p.rows * (D + 1) * 4 + (size_t)2 * kps * (D + 1) * 4 + (size_t)8 * p.rows * kps +
+                          16 * (size_t)p.rows > 65536)
+      kps /= 2;
+    p.keys_per_split = kps;
     p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
     p.part_rows = (size_t)B * Hkv * p.nsplit * p.rows_padded;
   } else {
@@ -910,7 +926,7 @@ hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hi
   hipError_t e;
   if (dtype == 0) {
     const size_t lds = (size_t)p.rows * p.keys_per_split * 8 + (size_t)p.rows * 16 +
-                       (size_t)p.rows * a.D * 4;
+                       (size_t)p.rows * (a.D + 1) * 4 + (size_t)2 * p.keys_per_split * (a.D + 1) * 4;
     dim3 grid(p.nsplit, a.Hkv, a.B);
     if (paged)
       hipLaunchKernelGGL(verify_split_f32<true>, grid, dim3(256), lds, st, a, p.keys_per_split,

@@ -103,9 +103,13 @@ int sd_version(void);
  *   scale               score multiplier (finite)
  * Requirements: B, N, C >= 1; d % num_heads == 0; dh in {64, 128} for
  * SD_BF16, dh in {64, 128, 256} for SD_F32; N <= 2^24; C <= 2^20.
- * For SD_BF16 the value aggregation runs on float16 matrix cores, so
- * |feats| must stay below 65504 (larger magnitudes are a precondition
- * violation).
+ * For SD_BF16 both products run on float16 matrix cores with the inputs
+ * converted exactly (fp16 holds zero and every bf16 magnitude in 2^-17 ..
+ * 65280 exactly).  Larger magnitudes convert to inf; each group of 32
+ * latents of one head whose results then come out non-finite, or all below
+ * 2^-12 in magnitude (inputs far below fp16's normal range), is recomputed
+ * in float64 from the bf16 values, so every finite input is handled (such
+ * calls are slower).
  * When the tokens are split across work-groups, the workspace holds one
  * partial result per split; for SD_BF16 the split count follows the
  * compute units of the current device, so query

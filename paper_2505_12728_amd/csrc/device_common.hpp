@@ -219,15 +219,15 @@ __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected
   return *lds_flag != 0;
 }
 
-// two bf16 -> two fp16 (exact inside the fp16 range; round toward zero
-// otherwise, so magnitudes beyond 65504 saturate at 65504)
+// two bf16 -> two fp16, rounded to nearest even: exact for zero and every
+// magnitude in 2^-17 .. 65280 (all bf16 values there fit fp16's 11-bit
+// significand); larger magnitudes become +-inf, which the callers detect.
+typedef _Float16 half2_ __attribute__((ext_vector_type(2)));
+typedef float float2_ __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t v) {
   const float lo = __uint_as_float(v << 16);
   const float hi = __uint_as_float(v & 0xffff0000u);
-  const auto h2 = __builtin_amdgcn_cvt_pkrtz(lo, hi);
-  uint32_t r;
-  __builtin_memcpy(&r, &h2, 4);
-  return r;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((float2_){lo, hi}, half2_));
 }
 
 // 16 int8 values q (one 16-byte piece) to 16 fp16 values q * 2^e, exact
@@ -235,7 +235,6 @@ __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t v) {
 // Per 4 values: the bytes biased to u = q + 128, placed under the fp16
 // pattern of 1024 (0x64uu = 1024 + u) by byte permutes, then 1152
 // subtracted and 2^e applied with packed fp16 arithmetic (both exact).
-typedef _Float16 half2_ __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void i8x16_to_f16_pow2(const u32x4& q, int e, u32x4& lo, u32x4& hi) {
   const uint32_t s_bits = (uint32_t)(e + 15) << 10;          // 2^e as fp16
   const half2_ s2 = __builtin_bit_cast(half2_, s_bits | (s_bits << 16));

@@ -11,7 +11,10 @@
 //     pieces of each token XOR-swizzled so that every read pattern below is
 //     free of LDS bank conflicts;
 //   - each tile is converted in place bf16 -> fp16 once per work-group (exact
-//     for |F_V| in [2^-14, 65504]), so both products run on fp16 matrix
+//     for zero and |F_V| in [2^-17, 65280], rounded to nearest otherwise, so
+//     larger magnitudes become inf; a wave whose outputs then come out
+//     non-finite, or all below 2^-12, recomputes its latents exactly in float64
+//     (compress_exact_wave)), so both products run on fp16 matrix
 //     cores: S^T = F_V Cq^T (lane = one latent row), online softmax in fp32
 //     with exp2, P (in [0, 2^15]) rounded to fp16, O^T += F_V^T P^T;
 //   - latent tiles of one (sequence, head) are placed on the same XCD
@@ -89,8 +92,19 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // one fence-free barrier (for eight-wave groups placed before the step's
 // last group, so the next step's first reads overlap that group's work).
 template <int NW, int DH, bool IN8>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
-                                                         int tokens_per_split, int nsplit) {
+struct CompressLds {
+  unsigned char ring[4][64 * DH * 2];                       // fp16 tiles
+  unsigned char stage[IN8 ? 4 : 1][IN8 ? 64 * DH : 16];    // int8 staging tiles
+  int8_t sexp[IN8 ? kQ8MaxSplit : 4];                      // int8: the split's token exponents
+};
+
+// The matrix-core pass of a work-group (NW waves x 32 latents of one
+// (sequence, head), one token split).  Returns, per thread, the range flags
+// of its outputs (bf16 input): bit 0 set when an accumulator is not finite,
+// bit 1 set when some output it wrote has magnitude 2^-12 or more.
+template <int NW, int DH, bool IN8>
+__device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh, int n_lt, int tokens_per_split,
+                                                  int nsplit, CompressLds<NW, DH, IN8>& sm) {
   constexpr int TT = 64;                    // tokens per tile
   constexpr int DC = DH / 32;               // 32-channel slices (QK)
   constexpr int DB = DH / 16;               // 16-channel output blocks (PV)
@@ -109,9 +123,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   static_assert(!IN8 || DH == 128, "int8 input: 128-channel heads");
   // fp16 tiles (bf16 input: the copy lands here and is converted in place;
   // int8 input: converted here from the staging ring)
-  __shared__ __align__(16) unsigned char ring[NBUF][TILE_BYTES];
-  __shared__ __align__(16) unsigned char stage[IN8 ? NBUF : 1][IN8 ? TT * IN_ROW : 16];
-  __shared__ int8_t sexp[IN8 ? kQ8MaxSplit : 4];   // int8 input: the split's token exponents
+  auto& ring = sm.ring;
+  auto& stage = sm.stage;
+  auto& sexp = sm.sexp;
+  static_assert(sizeof(sm.ring[0]) == TILE_BYTES, "ring slot size");
 
   int bh, lt;
   map_tile(blockIdx.x, n_bh, n_lt, bh, lt);
@@ -684,12 +699,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // no copy in flight at exit
 
   // normalise and write (directly, or as a partial for the merge)
+  unsigned flags = 0u;
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const float lt_ = __shfl(o[rb][DB][0], c, 64);   // l of row c sits in lane c
     const int r = lat0 + rb * 16 + c;
     if (r >= a.C) continue;
     const float inv = lt_ > 0.f ? 1.f / lt_ : 0.f;
+    if constexpr (!IN8) {
+      // range verdict: an input beyond fp16 became inf and made the scores
+      // or sums non-finite; inputs all far below 2^-8 give tiny outputs
+      float amax = 0.f;
+      bool fin = __builtin_isfinite(lt_) && __builtin_isfinite(m[rb]);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = o[rb][db][e] * inv;
+          fin = fin && __builtin_isfinite(x);
+          amax = fmaxf(amax, fabsf(x));
+        }
+      flags |= (fin ? 0u : 1u) | (amax >= 0.000244140625f ? 2u : 0u);
+    }
     float* dst;
     if (nsplit == 1) {
       dst = a.out + ((size_t)b * a.C + r) * a.d + h * DH;
@@ -701,6 +732,97 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int db = 0; db < DB; ++db)
       *reinterpret_cast<floatx4*>(dst + db * 16 + 4 * G) = o[rb][db] * inv;
+  }
+  return flags;
+}
+
+// Exact fallback of one wave's 32 latents when its first-pass outputs left
+// the range fp16 holds exactly (an accumulator not finite, or every output
+// below 2^-12): the same outputs (or split partials) recomputed in float64
+// from the bf16 values.  Registers and global memory only (no LDS, no
+// barrier), so the other waves of the work-group, still streaming tiles
+// through the ring, are neither disturbed nor held.  Per latent row, lanes
+// take 64 tokens at a time for the scores (online softmax over the chunks)
+// and then channels for P F_V.  Slow, and only run for such inputs.
+template <int DH>
+__device__ __forceinline__ void compress_exact_wave(const CompressArgs& a, int b, int h, int bh, int split,
+                                                    int nsplit, int tok0, int tok1, int lat0) {
+  constexpr int NC = DH / 64;                       // channels per lane
+  const int lane = threadIdx.x & 63;
+  const uint16_t* F = static_cast<const uint16_t*>(a.feats) + (size_t)b * a.N * a.d + h * DH;
+  const double scale = (double)a.scale;
+  // the first pass's stores to these outputs complete before any rewrite
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
+  const int lat1 = min(a.C, lat0 + 32);
+  for (int r = lat0; r < lat1; ++r) {
+    const uint16_t* q = static_cast<const uint16_t*>(a.latents) + (size_t)r * a.d + h * DH;
+    double m = -INFINITY, l = 0.0, acc[NC];
+#pragma unroll
+    for (int cc = 0; cc < NC; ++cc) acc[cc] = 0.0;
+    for (int t0 = tok0; t0 < tok1; t0 += 64) {
+      const int t = t0 + lane;
+      double s = -INFINITY;
+      if (t < tok1) {
+        const uint16_t* f = F + (size_t)t * a.d;
+        double x = 0.0;
+        for (int e = 0; e < DH; ++e) x = fma((double)bf16_bits_to_float(q[e]), (double)bf16_bits_to_float(f[e]), x);
+        s = x * scale;
+      }
+      double mx = s;
+      for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
+      const double mnew = fmax(m, mx);               // finite: lane 0 holds a token
+      const double p = t < tok1 ? exp(s - mnew) : 0.0;
+      double sum = p;
+      for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
+      const double alpha = exp(m - mnew);            // 0 on the first chunk
+      m = mnew;
+      l = l * alpha + sum;
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) acc[cc] *= alpha;
+      const int nt = min(64, tok1 - t0);
+      for (int j = 0; j < nt; ++j) {
+        const double pj = __shfl(p, j, 64);
+        const uint16_t* f = F + (size_t)(t0 + j) * a.d;
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) acc[cc] = fma(pj, (double)bf16_bits_to_float(f[lane + 64 * cc]), acc[cc]);
+      }
+    }
+#pragma unroll
+    for (int cc = 0; cc < NC; ++cc) {
+      const float v = (float)(acc[cc] / l);
+      const int e = lane + 64 * cc;
+      if (nsplit == 1) {
+        a.out[((size_t)b * a.C + r) * a.d + h * DH + e] = v;
+      } else {
+        const size_t pr = ((size_t)bh * nsplit + split) * a.C + r;
+        a.part_o[pr * DH + e] = v;
+        if (e == 0) a.part_lse[pr] = (float)((m + log(l)) * 1.4426950408889634);
+      }
+    }
+  }
+}
+
+template <int NW, int DH, bool IN8>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void compress_bf16(CompressArgs a, int n_bh, int n_lt,
+                                                         int tokens_per_split, int nsplit) {
+  __shared__ __align__(16) CompressLds<NW, DH, IN8> sm;
+  if constexpr (IN8) {
+    compress_pass<NW, DH, true>(a, n_bh, n_lt, tokens_per_split, nsplit, sm);
+  } else {
+    const unsigned f = compress_pass<NW, DH, false>(a, n_bh, n_lt, tokens_per_split, nsplit, sm);
+    // the wave's verdict (no barrier): rerun its latents exactly when some
+    // accumulator is not finite, or when it has latents and every output
+    // is below 2^-12
+    int bh, lt;
+    map_tile(blockIdx.x, n_bh, n_lt, bh, lt);
+    const int lat0 = lt * NW * 32 + (threadIdx.x >> 6) * 32;
+    const bool nonfinite = __ballot((f & 1u) != 0u) != 0ull;
+    const bool sized = __ballot((f & 2u) != 0u) != 0ull;
+    if (nonfinite || (lat0 < a.C && !sized)) {
+      const int split = blockIdx.y;
+      const int tok0 = split * tokens_per_split, tok1 = min(a.N, tok0 + tokens_per_split);
+      compress_exact_wave<DH>(a, bh / a.H, bh % a.H, bh, split, nsplit, tok0, tok1, lat0);
+    }
   }
 }
 

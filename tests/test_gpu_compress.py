@@ -81,6 +81,54 @@ def test_compress_edge_cases(case):
     assert_close(out, ref, dt, name)
 
 
+RANGE_CASES = [
+    # name, B, N, C, d, H, scale, what
+    ("large-feats-8w", 1, 3000, 256, 256, 2, 1 / 64, "large"),       # eight-wave groups, token splits
+    ("large-feats-4w", 2, 1000, 128, 256, 2, 1 / 64, "large"),
+    ("tiny-feats", 1, 2000, 256, 256, 2, 1.0, "tiny"),
+    ("tiny-feats-2w", 2, 700, 64, 256, 2, 1.0, "tiny"),
+    ("large-latents", 1, 1500, 256, 256, 2, 1e-6, "large-latents"),
+    ("mixed-subnormal", 1, 1200, 256, 256, 2, 1.0, "mixed"),
+]
+
+
+@pytest.mark.parametrize("case", RANGE_CASES, ids=[c[0] for c in RANGE_CASES])
+def test_compress_outside_fp16_range(case):
+    # bf16 values that fp16 does not hold exactly: magnitudes up to 1e5
+    # (above 65280), a tensor scaled to ~1e-6 (every value below 2^-14, most
+    # below fp16's subnormal resolution), latents above 65280, and a normal
+    # tensor with a tenth of its values below 2^-14; all within the float
+    # tolerance of the oracle on the same bf16 values
+    name, B, N, C, d, H, scale, what = case
+    print(f"compress range case {name}", flush=True)
+    w = synth.Workload(name, "bf16", batch=1, hq=1, hkv=1, head_dim=64, kv_len=1, block=1,
+                       c_batch=B, c_tokens=N, c_width=d, c_latents=C, c_heads=H)
+    lat, feats = synth.compress_inputs(w, seed=23)
+    rng = np.random.default_rng(29)
+    F = feats.values.astype(np.float32).copy()
+    Q = lat.values.astype(np.float32).copy()
+    if what == "large":
+        F *= np.float32(2000.0)                      # |F| up to ~1e4 everywhere
+        idx = rng.integers(0, F.size, size=F.size // 50)
+        F.reshape(-1)[idx] = rng.choice([-1.0, 1.0], size=idx.size).astype(np.float32) * \
+            rng.uniform(65536.0, 1e5, size=idx.size).astype(np.float32)
+    elif what == "tiny":
+        F *= np.float32(1e-6)
+    elif what == "large-latents":
+        Q *= np.float32(3e4)
+        Q.reshape(-1)[rng.integers(0, Q.size, size=Q.size // 20)] = np.float32(9e4)
+    elif what == "mixed":
+        idx = rng.integers(0, F.size, size=F.size // 10)
+        F.reshape(-1)[idx] *= np.float32(2.0 ** -20)
+    feats = synth.Tensor(F, "bf16")
+    lat = synth.Tensor(Q, "bf16")
+    if what == "large":
+        assert np.abs(feats.values).max() > 65280
+    out = run_gpu(lat, feats, H, scale)
+    ref = oracle.latent_compress(lat.values, feats.values, H, scale)
+    assert_close(out, ref, "bf16", name)
+
+
 def test_compress_zero_queries_is_average_pooling_on_gpu():
     w = synth.Workload("pool", "bf16", batch=1, hq=1, hkv=1, head_dim=64, kv_len=1, block=1,
                        c_batch=2, c_tokens=500, c_width=256, c_latents=64, c_heads=2)

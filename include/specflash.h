@@ -101,9 +101,12 @@ int sd_version(void);
  *   feats    [B, N, d]  dtype   visual features F_V, token-major
  *   out      [B, C, d]  float32 compressed features
  *   scale               score multiplier (finite)
- * Requirements: B, N, C >= 1; d % num_heads == 0; dh in {64, 128} for
- * SD_BF16, dh in {64, 128, 256} for SD_F32; N <= 2^24; C <= 2^20.
- * For SD_BF16 both products run on float16 matrix cores with the inputs
+ * Requirements: B, N, C >= 1; d % num_heads == 0; dh in {64, 128, 256};
+ * N <= 2^24; C <= 2^20.
+ * SD_F32, and SD_BF16 with dh = 256, run scores, softmax and aggregation in
+ * float64 on the vector units (bf16 values widened exactly).
+ * For SD_BF16 with dh in {64, 128} both products run on float16 matrix
+ * cores with the inputs
  * converted exactly (fp16 holds zero and every bf16 magnitude in 2^-17 ..
  * 65280 exactly).  Larger magnitudes convert to inf; each group of 32
  * latents of one head whose results then come out non-finite, or all below
@@ -199,8 +202,9 @@ int sd_avg_pool_compress(const void* feats, float* out, int B, int N, int C, int
  * Requirements: 1 <= k <= 16; Hq % Hkv == 0; k * (Hq / Hkv) <= 256;
  * D in {64, 128}; Lmax >= 1 (contiguous) or max_pages, num_pages >= 1
  * (paged); scale finite.  bf16: B * Hkv * ceil(capacity / 32) * ceil(k *
- * (Hq / Hkv) / 64) < 2^30, else SD_ERR_UNSUPPORTED (the workspace size is
- * then 0).
+ * (Hq / Hkv) / 64) < 2^30; fp32: B * Hkv * (key splits of at least 8
+ * keys) < 2^31, which B * Hkv * ceil(capacity / 8) < 2^31 guarantees;
+ * else SD_ERR_UNSUPPORTED (the workspace size is then 0).
  * The bf16 workspace holds partial results per work-group, and the
  * work-group count follows the compute units of the current device: query
  * sd_verify_workspace_size with the device the call will run on current
@@ -247,7 +251,7 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
  *   workspace   sd_spec_accept_workspace_size(B, k, V, mode) bytes, zeroed
  *               workspace (one arrival counter per sequence, then the
  *               per-chunk partial sums or maxima of the vocabulary pass)
- * Requirements: B >= 1; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1]
+ * Requirements: 1 <= B <= 2^22; 1 <= k <= 16; 1 <= V <= 2^18; p, q in [0, 1]
  * (values outside are clamped when forming the weights).
  * ---------------------------------------------------------------------- */
 size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode);
@@ -303,7 +307,7 @@ int sd_spec_accept_noalloc(const float* p, const float* q, const int32_t* draft,
  *   workspace   sd_spec_accept_logits_workspace_size(B, k, V, mode) bytes,
  *               zeroed workspace (row statistics of the logits, then the
  *               rule's counters and partials)
- * Requirements: as for sd_spec_accept; logits finite (others give an
+ * Requirements: as for sd_spec_accept, with B <= 2^19; logits finite (others give an
  * unspecified result, never an out-of-bounds access).
  * ---------------------------------------------------------------------- */
 size_t sd_spec_accept_logits_workspace_size(int B, int k, int V, int mode);

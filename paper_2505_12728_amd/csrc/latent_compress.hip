@@ -23,8 +23,8 @@
 // When the tokens are split across work-groups (small grids), each split
 // writes a normalised partial (o, lse) and a merge kernel combines them.
 //
-// fp32 path: a plain kernel (scores in LDS, float64 arithmetic) with the
-// same partial format, for fp32 inputs that need full fp32 accuracy.
+// fp32 inputs, and bf16 inputs with 256-channel heads: a plain kernel
+// (scores in LDS, float64 arithmetic) with the same partial format.
 #include <math.h>
 
 #include <algorithm>
@@ -826,95 +826,109 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   }
 }
 
-// ---------------------------------------------------------------- fp32
-// fp32 inputs: grid (8-latent block, token split, sequence x head) with
-// short token splits, so the work spreads over many compute units.  Scores,
-// softmax and P F_V run in float64 (literal Eq. 3 scores reach |s| ~ 60 for
-// unit-variance inputs, where fp32 rounding of s would already cost ~1e-5 of
-// relative accuracy in the weights).  The block's queries and the split's
-// feature rows are staged in LDS with coalesced loads (rows padded by one
-// float so that lanes reading one channel of consecutive rows hit distinct
-// banks); the scores of the block live in LDS.
+// ------------------------------------------------- fp32 (and bf16, dh 256)
+// fp32 inputs, and bf16 inputs with 256-channel heads: grid (8-latent
+// block, token split, sequence x head) with short token splits, so the work
+// spreads over many compute units.  Scores, softmax and P F_V run in float64
+// (literal Eq. 3 scores reach |s| ~ 60 for unit-variance inputs, where fp32
+// rounding of s would already cost ~1e-5 of relative accuracy in the
+// weights).  The block's queries and the split's feature rows are staged in
+// LDS as floats (bf16 widened exactly) with coalesced loads (rows padded by
+// one float so that lanes reading one channel of consecutive rows hit
+// distinct banks); the scores of the block live in LDS.  Splits and
+// (sequence, head) pairs beyond the grid's y / z extent are taken in
+// grid-stride loops.
 constexpr int kF32Rows = 8;
 
-__global__ __launch_bounds__(256) void compress_f32(CompressArgs a, int dh, int tokens_per_split,
-                                                    int nsplit) {
+__device__ __forceinline__ float load_elem(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ float load_elem(const uint16_t* p, size_t i) { return bf16_bits_to_float(p[i]); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void compress_lds(CompressArgs a, int dh, int tokens_per_split, int nsplit) {
   extern __shared__ __align__(16) unsigned char smem[];
-  const int lb = blockIdx.x, split = blockIdx.y, bh = blockIdx.z;
-  const int b = bh / a.H, h = bh % a.H;
+  const int lb = blockIdx.x;
   const int r0 = lb * kF32Rows;
   const int nr = min(kF32Rows, a.C - r0);
-  const int tok0 = split * tokens_per_split;
-  const int nt = min(a.N, tok0 + tokens_per_split) - tok0;
-  if (nt <= 0) return;
   const int DS = dh + 1;
   double* ss = reinterpret_cast<double*>(smem);                // [8][tokens_per_split]
   double* st = ss + (size_t)kF32Rows * tokens_per_split;        // [8][2]
   float* qs = reinterpret_cast<float*>(st + 2 * kF32Rows);      // [8][dh + 1]
   float* fs = qs + (size_t)kF32Rows * DS;                        // [tokens_per_split][dh + 1]
-  const float* lat = static_cast<const float*>(a.latents);
-  const float* F = static_cast<const float*>(a.feats) + (size_t)b * a.N * a.d + h * dh;
-  const int tid = threadIdx.x;
-  for (int i = tid; i < nr * dh; i += blockDim.x) {
-    const int r = i / dh, e = i - r * dh;
-    qs[r * DS + e] = lat[(size_t)(r0 + r) * a.d + h * dh + e];
-  }
-  for (int i = tid; i < nt * dh; i += blockDim.x) {
-    const int t = i / dh, e = i - t * dh;
-    fs[t * DS + e] = F[(size_t)(tok0 + t) * a.d + e];
-  }
-  __syncthreads();
+  const T* lat = static_cast<const T*>(a.latents);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const double scale = (double)a.scale;
-  // thread i: latent i / nt, token i % nt (consecutive lanes, consecutive tokens)
-  for (int i = tid; i < nt * nr; i += blockDim.x) {
-    const int r = i / nt, t = i - r * nt;
-    const float* xr = fs + t * DS;
-    const float* qr = qs + r * DS;
-    double acc = 0.0;
-    for (int e = 0; e < dh; ++e) acc = fma((double)qr[e], (double)xr[e], acc);
-    ss[(size_t)r * tokens_per_split + t] = acc * scale;
-  }
-  __syncthreads();
-  const int w = tid >> 6, lane = tid & 63;
-  for (int r = w; r < nr; r += blockDim.x / 64) {
-    double mx = -INFINITY;
-    for (int t = lane; t < nt; t += 64) mx = fmax(mx, ss[(size_t)r * tokens_per_split + t]);
-    for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
-    double sum = 0.0;
-    for (int t = lane; t < nt; t += 64) {
-      const double p = exp(ss[(size_t)r * tokens_per_split + t] - mx);
-      ss[(size_t)r * tokens_per_split + t] = p;
-      sum += p;
-    }
-    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
-    if (lane == 0) {
-      st[2 * r] = mx;
-      st[2 * r + 1] = sum;
-    }
-  }
-  __syncthreads();
-  for (int i = tid; i < nr * dh; i += blockDim.x) {
-    const int r = i / dh, e = i - r * dh;
-    const double* pr = ss + (size_t)r * tokens_per_split;
-    double acc = 0.0;
+  for (int bh = blockIdx.z; bh < a.B * a.H; bh += gridDim.z) {
+    const int b = bh / a.H, h = bh % a.H;
+    const T* F = static_cast<const T*>(a.feats) + (size_t)b * a.N * a.d + h * dh;
+    for (int split = blockIdx.y; split < nsplit; split += gridDim.y) {
+      const int tok0 = split * tokens_per_split;
+      const int nt = min(a.N, tok0 + tokens_per_split) - tok0;
+      __syncthreads();                          // the previous item's LDS reads are done
+      for (int i = tid; i < nr * dh; i += blockDim.x) {
+        const int r = i / dh, e = i - r * dh;
+        qs[r * DS + e] = load_elem(lat, (size_t)(r0 + r) * a.d + h * dh + e);
+      }
+      for (int i = tid; i < nt * dh; i += blockDim.x) {
+        const int t = i / dh, e = i - t * dh;
+        fs[t * DS + e] = load_elem(F, (size_t)(tok0 + t) * a.d + e);
+      }
+      __syncthreads();
+      // thread i: latent i / nt, token i % nt (consecutive lanes, consecutive tokens)
+      for (int i = tid; i < nt * nr; i += blockDim.x) {
+        const int r = i / nt, t = i - r * nt;
+        const float* xr = fs + t * DS;
+        const float* qr = qs + r * DS;
+        double acc = 0.0;
 #pragma unroll 8
-    for (int t = 0; t < nt; ++t) acc = fma(pr[t], (double)fs[t * DS + e], acc);
-    const double sum = st[2 * r + 1];
-    const float v = (float)(acc / sum);
-    if (nsplit == 1) {
-      a.out[((size_t)b * a.C + r0 + r) * a.d + h * dh + e] = v;
-    } else {
-      const size_t pr_ = ((size_t)bh * nsplit + split) * a.C + r0 + r;
-      a.part_o[pr_ * dh + e] = v;
-      if (e == 0) a.part_lse[pr_] = (float)((st[2 * r] + log(sum)) * 1.4426950408889634);
+        for (int e = 0; e < dh; ++e) acc = fma((double)qr[e], (double)xr[e], acc);
+        ss[(size_t)r * tokens_per_split + t] = acc * scale;
+      }
+      __syncthreads();
+      for (int r = w; r < nr; r += blockDim.x / 64) {
+        double mx = -INFINITY;
+        for (int t = lane; t < nt; t += 64) mx = fmax(mx, ss[(size_t)r * tokens_per_split + t]);
+        for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
+        double sum = 0.0;
+        for (int t = lane; t < nt; t += 64) {
+          const double p = exp(ss[(size_t)r * tokens_per_split + t] - mx);
+          ss[(size_t)r * tokens_per_split + t] = p;
+          sum += p;
+        }
+        for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
+        if (lane == 0) {
+          st[2 * r] = mx;
+          st[2 * r + 1] = sum;
+        }
+      }
+      __syncthreads();
+      for (int i = tid; i < nr * dh; i += blockDim.x) {
+        const int r = i / dh, e = i - r * dh;
+        const double* pr = ss + (size_t)r * tokens_per_split;
+        double acc = 0.0;
+#pragma unroll 8
+        for (int t = 0; t < nt; ++t) acc = fma(pr[t], (double)fs[t * DS + e], acc);
+        const double sum = st[2 * r + 1];
+        const float v = (float)(acc / sum);
+        if (nsplit == 1) {
+          a.out[((size_t)b * a.C + r0 + r) * a.d + h * dh + e] = v;
+        } else {
+          const size_t pr_ = ((size_t)bh * nsplit + split) * a.C + r0 + r;
+          a.part_o[pr_ * dh + e] = v;
+          if (e == 0) a.part_lse[pr_] = (float)((st[2 * r] + log(sum)) * 1.4426950408889634);
+        }
+      }
     }
   }
 }
 
 // Combine token splits: one thread per (sequence x head, latent, 4
 // channels).  Up to 16 splits are loaded at once; a running maximum
-// rescales the sums between rounds as in the online softmax.
+// rescales the sums between rounds as in the online softmax.  Acc is the
+// accumulation type: float for the matrix-core path, double for the
+// float64 path (whose many short splits would otherwise let fp32 rounding
+// of the running sums grow past its tolerance).
 constexpr int kMergeRound = 16;
+template <typename Acc>
 __global__ __launch_bounds__(256) void compress_merge(CompressArgs a, int dh, int nsplit) {
   const int d4n = dh / 4;
   const long long item = (long long)blockIdx.x * 256 + threadIdx.x;
@@ -927,8 +941,8 @@ __global__ __launch_bounds__(256) void compress_merge(CompressArgs a, int dh, in
   const float* lse = a.part_lse + (size_t)bh * nsplit * a.C + r;
   const float* po = a.part_o + ((size_t)bh * nsplit * a.C + r) * dh + d4 * 4;
   const size_t ostride = (size_t)a.C * dh;     // elements between splits
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  float mx = -INFINITY, wsum = 0.f;
+  Acc acc[4] = {0, 0, 0, 0};
+  Acc mx = -INFINITY, wsum = 0;
   for (int s0 = 0; s0 < nsplit; s0 += kMergeRound) {
     float l[kMergeRound];
     floatx4 v[kMergeRound];
@@ -941,21 +955,27 @@ __global__ __launch_bounds__(256) void compress_merge(CompressArgs a, int dh, in
     float cm = l[0];
 #pragma unroll
     for (int i = 1; i < kMergeRound; ++i) cm = fmaxf(cm, l[i]);
-    const float nm = fmaxf(mx, cm);
+    const Acc nm = mx > (Acc)cm ? mx : (Acc)cm;
     if (nm == -INFINITY) continue;
-    const float keep = mx == -INFINITY ? 0.f : exp2f(mx - nm);
-    acc = acc * keep;
+    // weights from fp32 exponentials of the exactly formed differences (the
+    // stored partial lse values are fp32, whose rounding is of the same
+    // order); only the running sums need the wider type
+    const Acc keep = mx == -INFINITY ? (Acc)0 : (Acc)exp2f((float)(mx - nm));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] *= keep;
     wsum *= keep;
 #pragma unroll
     for (int i = 0; i < kMergeRound; ++i) {
-      const float wgt = l[i] == -INFINITY ? 0.f : exp2f(l[i] - nm);
+      const Acc wgt = l[i] == -INFINITY ? (Acc)0 : (Acc)exp2f((float)((Acc)l[i] - nm));
       wsum += wgt;
-      acc += wgt * v[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] += wgt * (Acc)v[i][e];
     }
     mx = nm;
   }
+  const Acc inv = wsum > 0 ? (Acc)1 / wsum : (Acc)0;
   *reinterpret_cast<floatx4*>(a.out + ((size_t)b * a.C + r) * a.d + h * dh + d4 * 4) =
-      acc * (wsum > 0.f ? 1.f / wsum : 0.f);
+      floatx4{(float)(acc[0] * inv), (float)(acc[1] * inv), (float)(acc[2] * inv), (float)(acc[3] * inv)};
 }
 
 // Average pooling of the N tokens into C contiguous groups (the
@@ -1029,7 +1049,7 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus
   CompressPlan p{};
   p.dh = d / H;
   const long long n_bh = (long long)B * H;
-  if (dtype == 0) {
+  if (dtype == 0 || p.dh == 256) {
     p.lat_tile = kF32Rows;
     p.lat_tiles = (C + kF32Rows - 1) / kF32Rows;
     // short splits (64 tokens at most) so the grid spreads over the device;
@@ -1067,12 +1087,15 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus
 
 hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dtype, hipStream_t st) {
   hipError_t e;
-  if (dtype == 0) {
+  if (dtype == 0 || p.dh == 256) {
     const size_t lds = (size_t)kF32Rows * p.tokens_per_split * 8 + 16 * kF32Rows +
                        (size_t)kF32Rows * (p.dh + 1) * 4 + (size_t)p.tokens_per_split * (p.dh + 1) * 4;
-    dim3 grid(p.lat_tiles, p.nsplit, a.B * a.H);
-    hipLaunchKernelGGL(compress_f32, grid, dim3(256), lds, st, a, p.dh, p.tokens_per_split,
-                       p.nsplit);
+    dim3 grid(p.lat_tiles, std::min(p.nsplit, 65535), std::min(a.B * a.H, 65535));
+    if (dtype == 0)
+      hipLaunchKernelGGL(compress_lds<float>, grid, dim3(256), lds, st, a, p.dh, p.tokens_per_split, p.nsplit);
+    else
+      hipLaunchKernelGGL(compress_lds<uint16_t>, grid, dim3(256), lds, st, a, p.dh, p.tokens_per_split,
+                         p.nsplit);
     e = hipGetLastError();
   } else if (dtype == kCompressInt8) {
     e = dispatch_nw<128, true>(a, p, st);
@@ -1081,8 +1104,11 @@ hipError_t launch_compress(const CompressArgs& a, const CompressPlan& p, int dty
   }
   if (e != hipSuccess || p.nsplit == 1) return e;
   const long long items = (long long)a.B * a.H * a.C * (p.dh / 4);
-  hipLaunchKernelGGL(compress_merge, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a, p.dh,
-                     p.nsplit);
+  const dim3 mgrid((unsigned)((items + 255) / 256));
+  if (dtype == 0 || p.dh == 256)
+    hipLaunchKernelGGL(compress_merge<double>, mgrid, dim3(256), 0, st, a, p.dh, p.nsplit);
+  else
+    hipLaunchKernelGGL(compress_merge<float>, mgrid, dim3(256), 0, st, a, p.dh, p.nsplit);
   return hipGetLastError();
 }
 

@@ -1,7 +1,8 @@
 // Speculative acceptance with residual resampling (SpecFLASH Sec. 3.1 and
 // Sec. 3.3; greedy verification at temperature 0, Sec. 4.2).
 //
-// One kernel, grid (vocabulary chunk, sequence), 256 threads, in two phases:
+// One kernel, one work-group per (vocabulary chunk, sequence) on a 1-D grid
+// (chunks fastest), 256 threads, in two phases:
 //
 // 1. chunk phase, every work-group.
 //    Sampled mode: every work-group of a sequence repeats the k acceptance
@@ -31,7 +32,7 @@
 //
 // From logits (the target's k + 1 and the draft's k rows per sequence), the
 // same kernel reads p and q on demand as a temperature softmax of the
-// logits, after a statistics pass, grid (4096-entry chunk, row), that writes
+// logits, after a statistics pass, one work-group per (4096-entry chunk, row), that writes
 // each chunk's (max, sum of 2^(z s - max)) with s = log2(e) / tau.  Each
 // work-group of the rule first merges its sequence's 2k + 1 rows of chunk
 // statistics into (M, 1 / L) in LDS.  The uniforms come from Philox-4x64-10
@@ -520,7 +521,7 @@ __device__ void finish_phase(const AcceptArgs& a, const Src& src, const unsigned
   if (threadIdx.x == 0) a.n_accepted[b] = n;
 }
 
-// The rule: grid (chunk, sequence).  Every work-group writes its chunk's
+// The rule: one work-group per (chunk, sequence), chunks fastest on a 1-D grid.  Every work-group writes its chunk's
 // partials, publishes them (release fence) and counts its arrival; the one
 // that completes the count of its sequence runs the finish and resets the
 // counter.  Work-groups never wait for each other, so the grid always
@@ -529,7 +530,7 @@ template <typename Src>
 __global__ __launch_bounds__(kThreads) void accept_rule(AcceptArgs a, Src src, unsigned* count, unsigned char* parts,
                                                         int nchunks) {
   __shared__ RuleShared sh;
-  const int chunk = blockIdx.x, b = blockIdx.y;
+  const int chunk = (int)(blockIdx.x % (unsigned)nchunks), b = (int)(blockIdx.x / (unsigned)nchunks);
   src.prepare(b, sh.rows);
   __syncthreads();
   chunk_phase(a, src, parts, nchunks, chunk, b, sh);
@@ -537,7 +538,8 @@ __global__ __launch_bounds__(kThreads) void accept_rule(AcceptArgs a, Src src, u
   finish_phase(a, src, parts, nchunks, b, sh);
 }
 
-// Row statistics of the logits at temperature: grid (4096-entry chunk, row)
+// Row statistics of the logits at temperature: one work-group per (4096-entry
+// chunk, row), chunks fastest on a 1-D grid,
 // with rows b (k+1) + i of the target logits, then B (k+1) + b k + i of the
 // draft logits; each work-group writes (max, sum 2^(z s - max)) of its chunk.
 // Rows whose start is 16-byte aligned are read with 16-byte loads (4 fp32 or
@@ -563,7 +565,7 @@ __global__ __launch_bounds__(kThreads) void logit_stats_chunks(const T* zt, cons
   constexpr int PER = 16 / sizeof(T);                    // logits per 16-byte load
   constexpr int NX = kStatChunk / kThreads;              // logits per thread
   __shared__ float2 sm[kWaves];
-  const int chunk = blockIdx.x, r = blockIdx.y;
+  const int chunk = (int)(blockIdx.x % (unsigned)nchunks), r = (int)(blockIdx.x / (unsigned)nchunks);
   const int rt = B * (k + 1);
   const T* row = r < rt ? zt + (size_t)r * V : zd + (size_t)(r - rt) * V;
   const int v0 = chunk * kStatChunk, v1 = min(V, v0 + kStatChunk);
@@ -618,7 +620,7 @@ __global__ __launch_bounds__(kThreads) void philox_uniforms_kernel(uint64_t seed
 template <typename Src>
 hipError_t launch_rule(const AcceptArgs& a, const Src& src, unsigned* count, unsigned char* parts, hipStream_t st) {
   const int nchunks = (a.V + kChunk - 1) / kChunk;
-  hipLaunchKernelGGL((accept_rule<Src>), dim3(nchunks, a.B), dim3(kThreads), 0, st, a, src, count, parts, nchunks);
+  hipLaunchKernelGGL((accept_rule<Src>), dim3(nchunks * a.B), dim3(kThreads), 0, st, a, src, count, parts, nchunks);
   return hipGetLastError();
 }
 
@@ -638,7 +640,7 @@ hipError_t launch_logits(const AcceptLogitsArgs& la, void* ws, hipStream_t st) {
   unsigned char* base = static_cast<unsigned char*>(ws);
   if (a.mode != 0) {
     float2* part = reinterpret_cast<float2*>(base);
-    hipLaunchKernelGGL((logit_stats_chunks<T>), dim3(nchunks, nrows), dim3(kThreads), 0, st, src.zt, src.zd,
+    hipLaunchKernelGGL((logit_stats_chunks<T>), dim3(nchunks * nrows), dim3(kThreads), 0, st, src.zt, src.zd,
                        la.scale_log2, a.B, a.k, a.V, part, nchunks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

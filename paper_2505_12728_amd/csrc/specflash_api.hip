@@ -41,7 +41,7 @@ bool compress_shape_ok(int B, int N, int C, int d, int H, int dtype, int* status
     return false;
   }
   const int dh = d / H;
-  const bool ok = dtype == SD_BF16 ? (dh == 64 || dh == 128) : (dh == 64 || dh == 128 || dh == 256);
+  const bool ok = dh == 64 || dh == 128 || dh == 256;
   if (!ok || N > (1 << 24) || C > (1 << 20)) {
     *status = SD_ERR_UNSUPPORTED;
     return false;
@@ -270,8 +270,12 @@ int sd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
 }
 
 // --------------------------------------------------------------- accept
+// batch bounds: one work-group per (1024-entry chunk, sequence) and, from
+// logits, per (4096-entry chunk, logit row), counted on a 1-D grid below 2^31
+constexpr int kAcceptMaxSeqs = 1 << 22;
+constexpr int kAcceptLogitsMaxSeqs = 1 << 19;
 size_t sd_spec_accept_workspace_size(int B, int k, int V, int mode) {
-  if (B < 1 || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
+  if (B < 1 || B > kAcceptMaxSeqs || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
       (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
     return 0;
   return sd::accept_workspace_bytes(B, k, V, mode);
@@ -282,7 +286,7 @@ int sd_spec_accept(const float* p, const float* q, const int32_t* draft, const f
                    void* workspace, size_t workspace_bytes, void* stream) {
   if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
     return SD_ERR_INVALID_ARG;
-  if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (k > 16 || V > (1 << 18) || B > kAcceptMaxSeqs) return SD_ERR_UNSUPPORTED;
   if (!p || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
   if (mode == SD_ACCEPT_SAMPLED && (!q || !u)) return SD_ERR_INVALID_ARG;
   if (!aligned(p, 4) || !aligned(draft, 4) || !aligned(n_accepted, 4) || !aligned(tokens, 4) ||
@@ -337,7 +341,7 @@ int sd_spec_accept_noalloc(const float* p, const float* q, const int32_t* draft,
 
 // ------------------------------------------------------ accept (logits)
 size_t sd_spec_accept_logits_workspace_size(int B, int k, int V, int mode) {
-  if (B < 1 || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
+  if (B < 1 || B > kAcceptLogitsMaxSeqs || k < 1 || k > 16 || V < 1 || V > (1 << 18) ||
       (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED))
     return 0;
   return sd::accept_logits_workspace_bytes(B, k, V, mode);
@@ -350,7 +354,7 @@ int sd_spec_accept_logits(const void* target_logits, const void* draft_logits, c
   if (B < 1 || k < 1 || V < 1 || (mode != SD_ACCEPT_GREEDY && mode != SD_ACCEPT_SAMPLED) ||
       (dtype != SD_F32 && dtype != SD_BF16))
     return SD_ERR_INVALID_ARG;
-  if (k > 16 || V > (1 << 18)) return SD_ERR_UNSUPPORTED;
+  if (k > 16 || V > (1 << 18) || B > kAcceptLogitsMaxSeqs) return SD_ERR_UNSUPPORTED;
   if (!target_logits || !draft || !n_accepted || !tokens) return SD_ERR_INVALID_ARG;
   if (mode == SD_ACCEPT_SAMPLED && (!draft_logits || !isfinite(temperature) || !(temperature > 0.f)))
     return SD_ERR_INVALID_ARG;

@@ -587,7 +587,8 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
 // ----------------------------------------------------------- fp32 split
 // fp32 inputs: scores, softmax and P V run in float64, so the result keeps
 // full fp32 accuracy even when large scores make the softmax sensitive to
-// rounding.  Grid (key split, KV head, sequence) with short splits, so the
+// rounding.  One work-group per (key split, KV head, sequence), splits
+// fastest on a 1-D grid, with short splits, so the
 // work spreads over many compute units.  The block's queries and the
 // split's key and value rows are staged in LDS with coalesced loads (rows
 // padded by one float, so that lanes reading the same channel of
@@ -599,9 +600,10 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
                                                         int nsplit, int rows_padded) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int D = a.D, DS = D + 1;
-  const int split = blockIdx.x;
-  const int hk = blockIdx.y;
-  const int b = blockIdx.z;
+  const int split = (int)(blockIdx.x % (unsigned)nsplit);
+  const int pair = (int)(blockIdx.x / (unsigned)nsplit);
+  const int hk = pair % a.Hkv;
+  const int b = pair / a.Hkv;
   const int L = seq_len(a, b, PAGED);
   const int k0 = split * keys_per_split;
   if (k0 >= L) return;
@@ -691,17 +693,17 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 // loads the partial outputs of 8 splits (4 channels per lane), all in one
 // round of memory accesses; the chunk's weights 2^(lse - max) then rescale
 // a running sum as in the online softmax.  Every shuffle runs on all lanes.
-// Grid (rows / 4, sequence x KV head).
+// Grid (sequence x KV head, rows / 4).
 __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_split,
                                                     int nsplit, int rows_padded, int paged) {
-  const int pair = blockIdx.y;
+  const int pair = blockIdx.x;
   const int hk = pair % a.Hkv;
   const int b = pair / a.Hkv;
   const int D = a.D;
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + w;
+  const int r = blockIdx.y * 4 + w;
   if (r >= R) return;
   const int L = seq_len(a, b, paged != 0);
   const int nvalid = min(nsplit, (L + keys_per_split - 1) / keys_per_split);
@@ -758,10 +760,10 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
 // and load their lse while each half-wave loads the outputs of 16 of them
 // (4 channels per lane), in one round of memory accesses; the chunk's weights 2^(lse - max)
 // then rescale a running sum as in the online softmax.  Every shuffle runs
-// on all lanes.  Grid (ceil(rows per pair / 4), pairs).
+// on all lanes.  Grid (pairs, ceil(rows per pair / 4)).
 __global__ __launch_bounds__(256) void verify_stream_merge(VerifyArgs a, int G, int row_groups,
                                                            int KG, int rows_wg, int paged) {
-  const int pair = blockIdx.y;
+  const int pair = blockIdx.x;
   const int X = a.Hkv * row_groups;
   const int b = pair / X, x = pair - b * X;
   const int hk = x / row_groups, rg = x - hk * row_groups;
@@ -769,7 +771,7 @@ __global__ __launch_bounds__(256) void verify_stream_merge(VerifyArgs a, int G, 
   const int g = a.Hq / a.Hkv;
   const int R = a.k * g;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int lr = blockIdx.x * 4 + w;           // row within the pair
+  const int lr = blockIdx.y * 4 + w;           // row within the pair
   const int r = rg * rows_wg + lr;
   if (lr >= rows_wg || r >= R) return;
   const int cap = paged ? a.max_pages * 16 : a.Lmax;
@@ -897,6 +899,8 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     p.keys_per_split = kps;
     p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
     p.part_rows = (size_t)B * Hkv * p.nsplit * p.rows_padded;
+    // one work-group per (split, sequence, KV head) on the grid's x extent
+    if ((long long)p.nsplit * B * Hkv >= (1LL << 31)) p.ok = false;
   } else {
     // one wave per 16-row block, 1, 2 or 4 blocks per work-group.  Blocks
     // of 4 run as 8 waves in two key groups over a 128 KB ring, one work-
@@ -927,7 +931,7 @@ hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hi
   if (dtype == 0) {
     const size_t lds = (size_t)p.rows * p.keys_per_split * 8 + (size_t)p.rows * 16 +
                        (size_t)p.rows * (a.D + 1) * 4 + (size_t)2 * p.keys_per_split * (a.D + 1) * 4;
-    dim3 grid(p.nsplit, a.Hkv, a.B);
+    dim3 grid((unsigned)((long long)p.nsplit * a.Hkv * a.B));
     if (paged)
       hipLaunchKernelGGL(verify_split_f32<true>, grid, dim3(256), lds, st, a, p.keys_per_split,
                          p.nsplit, p.rows_padded);
@@ -942,10 +946,10 @@ hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hi
   }
   if (e != hipSuccess) return e;
   if (dtype == 0)
-    hipLaunchKernelGGL(verify_merge, dim3((p.rows + 3) / 4, a.Hkv * a.B), dim3(256), 0, st, a,
+    hipLaunchKernelGGL(verify_merge, dim3(a.Hkv * a.B, (p.rows + 3) / 4), dim3(256), 0, st, a,
                        p.keys_per_split, p.nsplit, p.rows_padded, paged ? 1 : 0);
   else
-    hipLaunchKernelGGL(verify_stream_merge, dim3((p.rows_wg + 3) / 4, a.B * a.Hkv * p.row_groups),
+    hipLaunchKernelGGL(verify_stream_merge, dim3(a.B * a.Hkv * p.row_groups, (p.rows_wg + 3) / 4),
                        dim3(256), 0, st, a, p.stream_wgs, p.row_groups, p.key_groups, p.rows_wg,
                        paged ? 1 : 0);
   return hipGetLastError();

@@ -79,6 +79,9 @@ def test_verify_validation_errors(lib):
     # bf16 tile list beyond 32-bit device indices: 4096 x 8 pairs x 2^15 tiles
     assert call(B=4096, Hq=8, Hkv=8, lmax=1 << 20) == sd.SD_ERR_UNSUPPORTED
     assert lib.sd_verify_workspace_size(4096, 4, 8, 8, 128, 1 << 20, 1) == 0
+    # fp32: one work-group per (64-key split, sequence, KV head) below 2^31
+    assert lib.sd_verify_workspace_size(1 << 20, 1, 1, 1, 64, 1 << 17, 0) == 0
+    assert lib.sd_verify_workspace_size(1 << 10, 1, 1, 1, 64, 1 << 17, 0) > 0
     assert call(ws=None) == sd.SD_ERR_WORKSPACE
     assert call(wsb=16) == sd.SD_ERR_WORKSPACE
     # paged: needs a page count
@@ -101,7 +104,11 @@ def test_compress_validation_errors(lib):
     assert call(d=250, H=4) == sd.SD_ERR_INVALID_ARG
     assert call(scale=float("inf")) == sd.SD_ERR_INVALID_ARG
     assert call(d=96, H=1) == sd.SD_ERR_UNSUPPORTED
-    assert call(d=512, H=2) == sd.SD_ERR_UNSUPPORTED     # bf16 head width 256
+    assert call(d=1024, H=2) == sd.SD_ERR_UNSUPPORTED    # head width 512
+    assert call(d=1024, H=2, dt=0) == sd.SD_ERR_UNSUPPORTED
+    assert call(dt=2) == sd.SD_ERR_INVALID_ARG
+    # bf16 with 256-channel heads: accepted, with one partial per short split
+    assert lib.sd_latent_compress_workspace_size(1, 1000, 16, 512, 2, 1) > 0
     need = lib.sd_latent_compress_workspace_size(1, 65536, 16, 256, 2, 1)
     assert need > 0
     assert f(lat, feats, out, 1, 65536, 16, 256, 2, 1.0, 1, None, 0, None) == sd.SD_ERR_WORKSPACE
@@ -122,6 +129,11 @@ def test_accept_validation_errors(lib):
     assert call(k=0) == sd.SD_ERR_INVALID_ARG
     assert call(k=17) == sd.SD_ERR_UNSUPPORTED
     assert call(V=(1 << 18) + 1) == sd.SD_ERR_UNSUPPORTED
+    assert call(B=(1 << 22) + 1) == sd.SD_ERR_UNSUPPORTED    # grid bound
+    assert lib.sd_spec_accept_workspace_size((1 << 22) + 1, 4, 100, 1) == 0
+    assert lib.sd_spec_accept_workspace_size(1 << 22, 4, 100, 1) > 0
+    assert lib.sd_spec_accept_logits_workspace_size((1 << 19) + 1, 4, 100, 1) == 0
+    assert lib.sd_spec_accept_logits_workspace_size(1 << 19, 4, 100, 1) > 0
 
 
 def test_accept_noalloc_validation_errors(lib):

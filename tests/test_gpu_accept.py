@@ -79,6 +79,19 @@ def test_accept_random_batches_both_modes():
         check(p, q, draft, u, oracle.ACCEPT_GREEDY, f"greedy B={B} k={k} V={V}")
 
 
+def test_accept_beyond_grid_extent():
+    # 66000 sequences: more than a grid's y extent (65535)
+    rng = np.random.default_rng(47)
+    B, k, V = 66000, 1, 5
+    print(f"accept grid case B={B}", flush=True)
+    p = _probs(rng, (B, k + 1, V))
+    q = _probs(rng, (B, k, V))
+    draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    u = (rng.integers(0, 1 << 24, size=(B, k + 1)) * 2.0 ** -24).astype(np.float32)
+    check(p, q, draft, u, oracle.ACCEPT_SAMPLED, f"sampled B={B}")
+    check(p, q, draft, u, oracle.ACCEPT_GREEDY, f"greedy B={B}")
+
+
 def test_accept_draft_equal_to_target_accepts_all():
     rng = np.random.default_rng(10)
     B, k, V = 16, 6, 32000

@@ -154,3 +154,15 @@ def test_accept_logits_first_token_law():
     expected = oracle.softmax_temperature(z1, tau)[0] * B
     chi2 = float(np.sum((counts - expected) ** 2 / expected))
     assert chi2 < 24.3, (counts, expected)             # P(chi2_7 > 24.3) ~ 0.001
+
+
+def test_accept_logits_beyond_grid_extent():
+    # 22000 sequences of 2k + 1 = 3 logit rows: 66000 rows of statistics,
+    # more than a grid's y extent (65535)
+    rng = np.random.default_rng(53)
+    B, k, V = 22000, 1, 5
+    print(f"accept logits grid case B={B}", flush=True)
+    zt = (rng.normal(size=(B, k + 1, V)) * 2).astype(np.float32)
+    zd = (zt[:, :k] + rng.normal(size=(B, k, V))).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    check_sampled(zt, zd, draft, 77, 3, 1.0)

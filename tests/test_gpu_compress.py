@@ -64,6 +64,9 @@ CASES = [
     ("split-tokens", "bf16", 1, 20000, 64, 128, 1, 1 / math.sqrt(128)),
     ("eight-waves-ragged-splits", "bf16", 1, 20037, 260, 256, 2, 1 / math.sqrt(128)),
     ("eight-waves-head-dim-64", "bf16", 1, 1500, 300, 128, 2, 1 / 8),
+    ("bf16-dh256", "bf16", 2, 700, 40, 512, 2, 1 / 16),
+    ("bf16-dh256-one-token", "bf16", 1, 1, 9, 256, 1, 1.0),
+    ("bf16-dh256-ragged", "bf16", 1, 3001, 17, 768, 3, 1 / 16),
     ("f32-heads", "f32", 2, 333, 20, 256, 2, 0.5),
     ("f32-dh256", "f32", 1, 2000, 16, 256, 1, 1 / 16),
 ]
@@ -78,6 +81,27 @@ def test_compress_edge_cases(case):
     lat, feats = synth.compress_inputs(w, seed=17)
     out = run_gpu(lat, feats, H, scale)
     ref = oracle.latent_compress(lat.values, feats.values, H, scale)
+    assert_close(out, ref, dt, name)
+
+
+GRID_CASES = [
+    # more (sequence, head) pairs, and more 64-token splits, than a grid's
+    # y / z extent (65535) holds: the float64 kernel takes the rest in
+    # grid-stride loops
+    ("many-sequences", "f32", 70000, 3, 8, 64, 1),
+    ("many-splits", "f32", 1, 65536 * 64 + 100, 8, 64, 1),
+]
+
+
+@pytest.mark.parametrize("case", GRID_CASES, ids=[c[0] for c in GRID_CASES])
+def test_compress_beyond_grid_extent(case):
+    name, dt, B, N, C, d, H = case
+    print(f"compress grid case {name}", flush=True)
+    w = synth.Workload(name, dt, batch=1, hq=1, hkv=1, head_dim=64, kv_len=1, block=1,
+                       c_batch=B, c_tokens=N, c_width=d, c_latents=C, c_heads=H)
+    lat, feats = synth.compress_inputs(w, seed=31)
+    out = run_gpu(lat, feats, H, 1 / 8)
+    ref = oracle.latent_compress(lat.values, feats.values, H, 1 / 8)
     assert_close(out, ref, dt, name)
 
 

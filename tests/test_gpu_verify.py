@@ -147,6 +147,24 @@ def test_verify_edge_cases(case):
     assert np.all(out[np.isneginf(rl)] == 0)
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_verify_beyond_grid_extent(dt):
+    # 70000 (sequence, KV head) pairs: more than a grid's y extent (65535)
+    # holds, on every kernel of the path (merges included)
+    B = 70000
+    print(f"verify grid case {dt} B={B}", flush=True)
+    lens = np.random.default_rng(41).integers(0, 40, size=B).astype(np.int32)
+    w = synth.Workload("many-pairs", dt, batch=B, hq=2, hkv=1, head_dim=64, kv_len=40, block=1)
+    d = synth.verify_inputs(w, seed=43, kv_len=lens)
+    scale = 1 / 8
+    out, lse = run_gpu(d, scale=scale)
+    ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                     d["kv_len"], scale)
+    assert_close(out, ro, dt, "many-pairs")
+    assert_lse_close(lse, rl, dt, "many-pairs")
+    assert np.all(out[lens == 0] == 0)
+
+
 def test_verify_nan_poison_beyond_length_is_never_read():
     w = synth.Workload("poison", "bf16", batch=2, hq=8, hkv=2, head_dim=128, kv_len=640, block=4)
     lens = np.array([600, 333], np.int32)

@@ -165,6 +165,42 @@ def test_verify_beyond_grid_extent(dt):
     assert np.all(out[lens == 0] == 0)
 
 
+@pytest.mark.parametrize("paged", [False, True])
+def test_verify_workspace_reuse_short_and_empty_sequences(paged):
+    # a 16K-capacity cache holding short sequences (fewer tiles than
+    # work-groups, so some work-groups have no range), empty sequences
+    # between non-empty ones, and one workspace reused over calls of
+    # different lengths
+    import torch
+    import paper_2505_12728_amd as sd
+    print(f"verify reuse paged={paged}", flush=True)
+    scale = 1 / math.sqrt(128)
+    cases = [[40, 0, 3, 0, 65], [0, 0, 1, 0, 0], [700, 0, 16384, 31, 0], [40, 0, 3, 0, 65]]
+    w = synth.Workload("reuse", "bf16", batch=5, hq=8, hkv=2, head_dim=128, kv_len=16384, block=3,
+                       paged=paged)
+    ws = None
+    for i, lens in enumerate(cases):
+        d = synth.verify_inputs(w, seed=50 + i, kv_len=np.array(lens, np.int32))
+        q, kc, vc = to_device(d["q"]), to_device(d["k_cache"]), to_device(d["v_cache"])
+        kl = np_to_device(d["kv_len"].astype(np.int32))
+        pt = None if d["page_table"] is None else np_to_device(d["page_table"].astype(np.int32))
+        if ws is None:
+            cap = 16384
+            n = sd.sd_verify_workspace_size(5, 3, 8, 2, 128, cap, sd.SD_BF16)
+            ws = torch.zeros(n, dtype=torch.uint8, device="cuda")
+        out, lse = sd.sd_verify_attention(q, kc, vc, kl, scale=scale, page_table=pt, workspace=ws)
+        torch.cuda.synchronize()
+        kw = {} if d["page_table"] is None else {"page_table": d["page_table"]}
+        ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                         d["kv_len"], scale, **kw)
+        out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        empty = np.array(lens) == 0
+        assert np.all(out[empty] == 0) and np.all(np.isneginf(lse[empty])), f"call {i}"
+        if np.any(ro != 0):
+            assert_close(out, ro, "bf16", f"reuse call {i}")
+        assert_lse_close(lse, rl, "bf16", f"reuse call {i}")
+
+
 def test_verify_nan_poison_beyond_length_is_never_read():
     w = synth.Workload("poison", "bf16", batch=2, hq=8, hkv=2, head_dim=128, kv_len=640, block=4)
     lens = np.array([600, 333], np.int32)

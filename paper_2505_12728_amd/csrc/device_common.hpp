@@ -142,22 +142,25 @@ __device__ __forceinline__ void tie(T& x) {
 
 // LDS swizzle of the 16-byte pieces of tile row t (a token or key) for rows
 // of PK pieces: piece p is stored at slot p ^ lds_swizzle<PK>(t).  gfx950's
-// LDS has 64 four-byte banks; a 16-byte read serves 16 lanes per pass and
-// the 8-byte transposing read 32 lanes, so
-//   - 16 consecutive rows read at one piece (matrix-core fragments of 16
-//     rows x 8 elements) must fill the 256 bank bytes, and
-//   - 8 consecutive rows read at two adjacent pieces each (transposed
-//     fragments of 4 rows x 4 elements per 16 lanes) must too.
-// For 256-byte rows (PK = 16) the swizzle is a permutation of 0..15 whose
-// bits 1..3 differ within each aligned 8 rows; for 128-byte rows (PK = 8,
-// two rows per bank row) a permutation of 0..7 on each row parity whose
+// LDS has 64 four-byte banks.  The 8-byte transposing read serves 32 lanes
+// per pass, so 8 consecutive rows read at two adjacent pieces each
+// (transposed fragments of 4 rows x 4 elements per 16 lanes) must fill the
+// 256 bank bytes.  The 16-byte read serves 16 lanes per pass, but the pass
+// pairs lanes 0..7 of one group of 16 with lanes 8..15 of the neighbouring
+// group (measured with the bank-conflict counter: matrix-core fragments of
+// 16 rows x 8 elements, lane 16 G + c reading row c at piece 4 dc + G, go
+// 2-way conflicted when rows c and c + 8 take slots that differ in bit 0,
+// conflict-free when the swizzle leaves bit 0 alone).
+// For 256-byte rows (PK = 16) the swizzle is (t & 7) << 1: bits 1..3 differ
+// within each aligned 8 rows and bit 0 never moves; for 128-byte rows (PK =
+// 8, two rows per bank row) a permutation of 0..7 on each row parity whose
 // bits 1..2 differ within each aligned quad of that parity.
 template <int PK>
 __device__ __forceinline__ constexpr int lds_swizzle(int t) {
   static_assert(PK == 8 || PK == 16, "rows of 128 or 256 bytes");
   t &= 15;
   if constexpr (PK == 16) {
-    return ((t & 7) << 1) | ((t >> 3) & 1);
+    return (t & 7) << 1;
   } else {
     const int u = (t >> 1) & 7;
     return ((u & 3) << 1) | (u >> 2);

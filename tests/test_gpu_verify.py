@@ -115,6 +115,10 @@ CASES = [
     ("rows48-short", "bf16", 1, 6, 8, 1, 128, [70], False),
     ("rows64-d64", "bf16", 2, 8, 8, 1, 64, [2500, 64], False),
     ("rows64-paged", "bf16", 2, 8, 16, 2, 128, [300, 1500], True),
+    # a few tiles per work-group: two key groups whose ranges span pairs
+    # (one group of a one-tile range gets no tile), and paged ragged rows
+    ("multi-pair-rows64-kg2", "bf16", 3, 8, 16, 2, 128, [1024, 200, 1], False),
+    ("multi-pair-paged-rows32", "bf16", 4, 6, 16, 4, 128, [1000, 16, 512, 999], True),
     # 47 key splits: an odd count above 32 in one 64-split chunk of the merge
     ("merge-odd-47", "bf16", 1, 4, 4, 1, 128, [1500], False),
     ("f32-ragged", "f32", 2, 4, 8, 2, 64, [608, 99], False),
@@ -250,3 +254,4 @@ def test_verify_is_deterministic():
     a, la = run_gpu(d)
     b, lb = run_gpu(d)
     assert np.array_equal(a, b) and np.array_equal(la, lb)
+

@@ -392,6 +392,28 @@ hipError_t launch_partial_nw(const LinearArgs& a, int rb, int passes, hipStream_
   return hipGetLastError();
 }
 
+// Work-groups of the bf16 projection kernel resident per compute unit, as
+// the runtime computes them from its registers, LDS and waves (for eight-
+// wave groups the registers bind: two per unit, where the LDS of two input
+// chunks would hold three); 0 when the runtime cannot tell.
+template <int NW>
+int resident_per_cu(int rb) {
+  const void* f = nullptr;
+  switch (rb) {
+    case 1: f = reinterpret_cast<const void*>(&linear_partial<1, NW, false>); break;
+    case 2: f = reinterpret_cast<const void*>(&linear_partial<2, NW, false>); break;
+    case 3: f = reinterpret_cast<const void*>(&linear_partial<3, NW, false>); break;
+    case 4: f = reinterpret_cast<const void*>(&linear_partial<4, NW, false>); break;
+    case 5: f = reinterpret_cast<const void*>(&linear_partial<5, NW, false>); break;
+    case 6: f = reinterpret_cast<const void*>(&linear_partial<6, NW, false>); break;
+    case 7: f = reinterpret_cast<const void*>(&linear_partial<7, NW, false>); break;
+    default: f = reinterpret_cast<const void*>(&linear_partial<8, NW, false>); break;
+  }
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, NW * 64, 0) != hipSuccess) return 0;
+  return n;
+}
+
 }  // namespace
 
 LinearPlan plan_linear(int R, int K, int N, int cus) {
@@ -399,11 +421,13 @@ LinearPlan plan_linear(int R, int K, int N, int cus) {
   const int rows = std::min(R, kLinearRowsPerPass);
   p.row_blocks = (rows + 15) / 16;
   p.passes = (R + kLinearRowsPerPass - 1) / kLinearRowsPerPass;
-  // work-groups resident per compute unit: LDS (two input chunks of
-  // row_blocks * 8 KB) and 32 waves
+  // work-groups resident per compute unit: the runtime's figure, else the
+  // LDS bound (two input chunks of row_blocks * 8 KB) and 32 waves
   const int lds_fit = (160 * 1024) / (p.row_blocks * 16 * 1024);
   auto resident = [&](int waves) {
-    return (long long)std::max(cus, 1) * std::max(1, std::min(lds_fit, 32 / waves));
+    int per_cu = waves == 8 ? resident_per_cu<8>(p.row_blocks) : resident_per_cu<4>(p.row_blocks);
+    if (per_cu <= 0) per_cu = std::max(1, std::min(lds_fit, 32 / waves));
+    return (long long)std::max(cus, 1) * per_cu;
   };
   auto groups = [&](int waves) { return (long long)((N + waves * 16 - 1) / (waves * 16)) * p.passes; };
   // eight waves per work-group (128 output columns), each chunk of the

@@ -222,6 +222,58 @@ __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected
   return *lds_flag != 0;
 }
 
+// Stage rows 0 .. nrows-1 of ncols elements (row r of source k at
+// src[k] + row_off(r), aligned to 4 NWORD bytes; ncols a multiple of the
+// elements per load) into LDS as floats, dst[k][r * DS + c] (bf16 widened
+// exactly), with loads of NWORD 32-bit words (4: 16 bytes), NB per thread
+// and source in flight: every load of a batch is issued before any of its
+// values is stored, so a batch costs one memory latency instead of one
+// per element.  NS sources share the rows.
+template <int NB, int NS, int NWORD, typename T, typename RowOff>
+__device__ __forceinline__ void stage_rows(float* const (&dst)[NS], int DS, const T* const (&src)[NS],
+                                           RowOff row_off, int nrows, int ncols) {
+  static_assert(NWORD == 1 || NWORD == 4, "4- or 16-byte loads");
+  typedef __attribute__((__vector_size__(NWORD * sizeof(uint32_t)))) uint32_t words;
+  constexpr int PER = (int)sizeof(uint32_t) / (int)sizeof(T);   // elements per word
+  constexpr int V = NWORD * PER;                                 // elements per load
+  const int per_row = ncols / V;
+  const int total = nrows * per_row;
+  for (int base = threadIdx.x; base < total; base += NB * (int)blockDim.x) {
+    words v[NS][NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int i = base + j * (int)blockDim.x;
+      if (i < total) {
+        const int r = i / per_row;
+        const size_t off = row_off(r) + (size_t)(i - r * per_row) * V;
+#pragma unroll
+        for (int k = 0; k < NS; ++k) v[k][j] = *reinterpret_cast<const words*>(src[k] + off);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int i = base + j * (int)blockDim.x;
+      if (i < total) {
+        const int r = i / per_row, c = (i - r * per_row) * V;
+#pragma unroll
+        for (int k = 0; k < NS; ++k) {
+          float* d = dst[k] + r * DS + c;
+#pragma unroll
+          for (int e = 0; e < NWORD; ++e) {
+            const uint32_t x = v[k][j][e];
+            if constexpr (PER == 1) {
+              d[e] = __uint_as_float(x);
+            } else {
+              d[2 * e] = __uint_as_float(x << 16);
+              d[2 * e + 1] = __uint_as_float(x & 0xffff0000u);
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
 // two bf16 -> two fp16, rounded to nearest even: exact for zero and every
 // magnitude in 2^-17 .. 65280 (all bf16 values there fit fp16's 11-bit
 // significand); larger magnitudes become +-inf, which the callers detect.

@@ -840,8 +840,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 // grid-stride loops.
 constexpr int kF32Rows = 8;
 
-__device__ __forceinline__ float load_elem(const float* p, size_t i) { return p[i]; }
-__device__ __forceinline__ float load_elem(const uint16_t* p, size_t i) { return bf16_bits_to_float(p[i]); }
 
 template <typename T>
 __global__ __launch_bounds__(256) void compress_lds(CompressArgs a, int dh, int tokens_per_split, int nsplit) {
@@ -864,13 +862,13 @@ __global__ __launch_bounds__(256) void compress_lds(CompressArgs a, int dh, int 
       const int tok0 = split * tokens_per_split;
       const int nt = min(a.N, tok0 + tokens_per_split) - tok0;
       __syncthreads();                          // the previous item's LDS reads are done
-      for (int i = tid; i < nr * dh; i += blockDim.x) {
-        const int r = i / dh, e = i - r * dh;
-        qs[r * DS + e] = load_elem(lat, (size_t)(r0 + r) * a.d + h * dh + e);
-      }
-      for (int i = tid; i < nt * dh; i += blockDim.x) {
-        const int t = i / dh, e = i - t * dh;
-        fs[t * DS + e] = load_elem(F, (size_t)(tok0 + t) * a.d + e);
+      {
+        float* const qd[1] = {qs};
+        const T* const qsrc[1] = {lat};
+        stage_rows<4, 1, 4>(qd, DS, qsrc, [&](int r) { return (size_t)(r0 + r) * a.d + h * dh; }, nr, dh);
+        float* const fd[1] = {fs};
+        const T* const fsrc[1] = {F};
+        stage_rows<8, 1, 4>(fd, DS, fsrc, [&](int t) { return (size_t)(tok0 + t) * a.d; }, nt, dh);
       }
       __syncthreads();
       // thread i: latent i / nt, token i % nt (consecutive lanes, consecutive tokens)
@@ -1059,6 +1057,9 @@ CompressPlan plan_compress(int B, int N, int C, int d, int H, int dtype, int cus
     while (tps > 8 && (4LL * kF32Rows * (p.dh + 1) + 4LL * tps * (p.dh + 1) + 8LL * kF32Rows * tps +
                        16 * kF32Rows) > 65536)
       tps /= 2;
+    // shorter splits (16 tokens at least) while the grid would leave
+    // compute units idle (the float64 chains of a work-group are serial)
+    while (tps > 16 && n_bh * p.lat_tiles * ((N + tps - 1) / tps) < std::max(cus, 1)) tps /= 2;
     p.tokens_per_split = (int)tps;
   } else {
     // 32 latents per wave; eight-wave groups (each F_V tile copied and

@@ -620,16 +620,26 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
   const float* qg = static_cast<const float*>(a.q);
   const float* kg = static_cast<const float*>(a.kc);
   const float* vg = static_cast<const float*>(a.vc);
-  for (int i = tid; i < R * D; i += blockDim.x) {
-    const int r = i / D, e = i - r * D;
-    const int j = r / g, h = hk * g + (r - j * g);
-    qs[r * DS + e] = qg[(((size_t)b * a.k + j) * a.Hq + h) * D + e];
-  }
-  for (int i = tid; i < nk * D; i += blockDim.x) {
-    const int tt = i / D, e = i - tt * D;
-    const size_t off = kv_offset<PAGED>(a, b, hk, k0 + tt, D) + e;
-    ks[tt * DS + e] = kg[off];
-    vs[tt * DS + e] = vg[off];
+  {
+    // rows start at multiples of D floats: 16-byte loads when the bases
+    // are 16-byte aligned, else 4-byte loads (fp32 needs only the latter)
+    float* const qd[1] = {qs};
+    const float* const qsrc[1] = {qg};
+    float* const kvd[2] = {ks, vs};
+    const float* const kvsrc[2] = {kg, vg};
+    auto qrow = [&](int r) {
+      const int j = r / g, h = hk * g + (r - j * g);
+      return (((size_t)b * a.k + j) * a.Hq + h) * D;
+    };
+    auto kvrow = [&](int tt) { return kv_offset<PAGED>(a, b, hk, k0 + tt, D); };
+    if (((reinterpret_cast<uintptr_t>(qg) | reinterpret_cast<uintptr_t>(kg) | reinterpret_cast<uintptr_t>(vg)) &
+         15) == 0) {
+      stage_rows<4, 1, 4>(qd, DS, qsrc, qrow, R, D);
+      stage_rows<4, 2, 4>(kvd, DS, kvsrc, kvrow, nk, D);
+    } else {
+      stage_rows<8, 1, 1>(qd, DS, qsrc, qrow, R, D);
+      stage_rows<8, 2, 1>(kvd, DS, kvsrc, kvrow, nk, D);
+    }
   }
   __syncthreads();
   const double scale = (double)a.scale;
@@ -689,8 +699,8 @@ __global__ __launch_bounds__(256) void verify_split_f32(VerifyArgs a, int keys_p
 
 // ---------------------------------------------------------------- merge
 // One wave per output row of one (sequence, KV head).  The splits are taken
-// 16 at a time: lanes 0..15 load their split's lse while each half-wave
-// loads the partial outputs of 8 splits (4 channels per lane), all in one
+// 32 at a time: lanes 0..31 load their split's lse while each half-wave
+// loads the partial outputs of 16 splits (4 channels per lane), all in one
 // round of memory accesses; the chunk's weights 2^(lse - max) then rescale
 // a running sum as in the online softmax.  Every shuffle runs on all lanes.
 // Grid (sequence x KV head, rows / 4).
@@ -712,12 +722,12 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
   const bool active = d4 < D / 4;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   float mx = -INFINITY, wsum = 0.f;
-  for (int s0 = 0; s0 < nvalid; s0 += 16) {
-    const int n = min(16, nvalid - s0);
+  for (int s0 = 0; s0 < nvalid; s0 += 32) {
+    const int n = min(32, nvalid - s0);
     const float ls = lane < n ? a.part_lse[base + (size_t)(s0 + lane) * rows_padded] : -INFINITY;
-    floatx4 po[8];
+    floatx4 po[16];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 16; ++i) {
       const int j = 2 * i + half;
       po[i] = floatx4{0.f, 0.f, 0.f, 0.f};
       if (j < n && active)
@@ -725,18 +735,18 @@ __global__ __launch_bounds__(256) void verify_merge(VerifyArgs a, int keys_per_s
     }
     float cm = ls;
 #pragma unroll
-    for (int off = 8; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
+    for (int off = 16; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
     const float nm = fmaxf(mx, __shfl(cm, 0, 64));
     if (nm == -INFINITY) continue;             // no key in any split so far (uniform)
     const float keep = mx == -INFINITY ? 0.f : exp2f(mx - nm);
     const float wl = ls == -INFINITY ? 0.f : exp2f(ls - nm);
     float ws = wl;
 #pragma unroll
-    for (int off = 8; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
+    for (int off = 16; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
     wsum = wsum * keep + __shfl(ws, 0, 64);
     acc = acc * keep;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc += __shfl(wl, 2 * i + half, 64) * po[i];
+    for (int i = 0; i < 16; ++i) acc += __shfl(wl, 2 * i + half, 64) * po[i];
     mx = nm;
   }
 #pragma unroll
@@ -896,6 +906,10 @@ VerifyPlan plan_verify(int B, int k, int Hq, int Hkv, int D, int capacity, int d
     while (kps > 8 && (size_t)p.rows * (D + 1) * 4 + (size_t)2 * kps * (D + 1) * 4 + (size_t)8 * p.rows * kps +
                           16 * (size_t)p.rows > 65536)
       kps /= 2;
+    // shorter splits (16 keys at least) while the grid would leave compute
+    // units idle: a work-group's scores and P V are serial float64 chains,
+    // so small shapes gain from more, shorter ones
+    while (kps > 16 && (long long)B * Hkv * ((capacity + kps - 1) / kps) < std::max(cus, 1)) kps /= 2;
     p.keys_per_split = kps;
     p.nsplit = std::max(1, (capacity + p.keys_per_split - 1) / p.keys_per_split);
     p.part_rows = (size_t)B * Hkv * p.nsplit * p.rows_padded;

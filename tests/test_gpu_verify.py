@@ -255,3 +255,30 @@ def test_verify_is_deterministic():
     b, lb = run_gpu(d)
     assert np.array_equal(a, b) and np.array_equal(la, lb)
 
+
+
+def test_verify_f32_unaligned_bases():
+    # fp32 caches and queries need only 4-byte alignment: bases 4 bytes off
+    # a 16-byte boundary take the kernel's 4-byte staging loads
+    import torch
+    import paper_2505_12728_amd as sd
+    print("verify f32 unaligned bases", flush=True)
+    lens = [300, 77]
+    w = synth.Workload("f32-unaligned", "f32", batch=2, hq=8, hkv=2, head_dim=64, kv_len=300, block=3)
+    d = synth.verify_inputs(w, seed=91, kv_len=np.array(lens, np.int32))
+
+    def shifted(x):
+        x = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+        buf = torch.empty(x.numel() + 1, dtype=torch.float32, device="cuda")
+        t = buf[1:].view(x.shape)
+        t.copy_(x.cuda())
+        assert t.data_ptr() % 16 == 4
+        return t
+    q, kc, vc = shifted(d["q"].values), shifted(d["k_cache"].values), shifted(d["v_cache"].values)
+    kl = np_to_device(d["kv_len"].astype(np.int32))
+    scale = 1 / 8
+    out, lse = sd.sd_verify_attention(q, kc, vc, kl, scale=scale)
+    torch.cuda.synchronize()
+    ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values, d["kv_len"], scale)
+    assert_close(out.cpu().numpy(), ro, "f32", "f32-unaligned")
+    assert_lse_close(lse.cpu().numpy(), rl, "f32", "f32-unaligned")

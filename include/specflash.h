@@ -102,7 +102,7 @@ int sd_version(void);
  *   out      [B, C, d]  float32 compressed features
  *   scale               score multiplier (finite)
  * Requirements: B, N, C >= 1; d % num_heads == 0; dh in {64, 128, 256};
- * N <= 2^24; C <= 2^20.
+ * N <= 2^24; C <= 2^20; d <= 2^22.
  * SD_F32, and SD_BF16 with dh = 256, run scores, softmax and aggregation in
  * float64 on the vector units (bf16 values widened exactly).
  * For SD_BF16 with dh in {64, 128} both products run on float16 matrix

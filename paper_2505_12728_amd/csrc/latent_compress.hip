@@ -135,7 +135,9 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   const int tok0 = split * tokens_per_split;
   const int tok1 = min(a.N, tok0 + tokens_per_split);
   const int tid = threadIdx.x;
-  const int w = tid >> 6, lane = tid & 63, G = lane >> 4, c = lane & 15;
+  // the wave index in a scalar register, so that the copies' LDS
+  // destinations (M0) are formed by scalar arithmetic
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, G = lane >> 4, c = lane & 15;
   const int lat0 = lt * NW * 32 + w * 32;
 
   // query fragments (fp16, B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..]
@@ -200,18 +202,23 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   // copy i of this wave moves input pieces P = (w * DMA_PER_WAVE + i) * 64 +
   // lane: token P / IN_PK.  bf16: LDS slot P % PK holds global piece
   // slot ^ swizzle(token) of the fp16 tile; int8: the staging tile is plain
-  // token-major.  Tokens past the split re-read its last token.
+  // token-major.  Tokens past the split re-read its last token.  The
+  // address is the tile's first row (uniform, scalar registers) plus a
+  // 32-bit lane offset formed with a 24-bit multiply-add (token < 64, row
+  // stride < 2^23), so the copy needs two full-rate vector ops.
+  const uint32_t row_bytes = (uint32_t)a.d * (IN8 ? 1u : 2u);
   auto issue = [&](int tile, int slot) {
     const int t0 = tok0 + tile * TT;
+    const int lim = tok1 - 1 - t0;            // last token of the split, tile-relative (>= 0)
+    const unsigned char* tbase = fbase + (size_t)t0 * row_bytes;
     unsigned char* buf = IN8 ? stage[slot] : ring[slot];
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) {
       const int P = (w * DMA_PER_WAVE + i) * 64 + lane;
       const int tk = P / IN_PK, piece = P % IN_PK;
-      const int tg = min(t0 + tk, tok1 - 1);
       const int src_piece = IN8 ? piece : (piece ^ swz<DH>(tk));
-      const unsigned char* src = fbase + (size_t)tg * a.d * (IN8 ? 1 : 2) + src_piece * 16;
-      __builtin_amdgcn_global_load_lds((gbl_cvoid*)src,
+      const uint32_t off = __umul24((uint32_t)min(tk, lim), row_bytes) + (uint32_t)src_piece * 16u;
+      __builtin_amdgcn_global_load_lds((gbl_cvoid*)(tbase + off),
                                        (lds_void*)(buf + (w * DMA_PER_WAVE + i) * 1024), 16, 0, 0);
     }
   };

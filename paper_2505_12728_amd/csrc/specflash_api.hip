@@ -42,7 +42,7 @@ bool compress_shape_ok(int B, int N, int C, int d, int H, int dtype, int* status
   }
   const int dh = d / H;
   const bool ok = dh == 64 || dh == 128 || dh == 256;
-  if (!ok || N > (1 << 24) || C > (1 << 20)) {
+  if (!ok || N > (1 << 24) || C > (1 << 20) || d > (1 << 22)) {
     *status = SD_ERR_UNSUPPORTED;
     return false;
   }

@@ -120,6 +120,12 @@ __device__ __forceinline__ void lds_write_b128(uint32_t addr, const u32x4& v) {
   asm volatile("ds_write_b128 %0, %1" : : "v"(addr), "v"(v));
 }
 
+template <int OFF>
+__device__ __forceinline__ void lds_write_b128_off(uint32_t addr, const u32x4& v) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  asm volatile("ds_write_b128 %0, %1 offset:%2" : : "v"(addr), "v"(v), "i"(OFF));
+}
+
 // Wait for every LDS operation of this wave (asm reads included).
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 

@@ -60,6 +60,24 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Byte offset of a ring slot from the ring's start: a compile-time constant
+// (CtOff, folded into the LDS instruction's offset field) or a runtime value
+// added to the lane's base address.
+template <int V>
+using CtOff = std::integral_constant<int, V>;
+template <int OFF, int V>
+__device__ __forceinline__ u32x4 rd_b128(uint32_t base, CtOff<V>) { return lds_read_b128_off<OFF + V>(base); }
+template <int OFF>
+__device__ __forceinline__ u32x4 rd_b128(uint32_t base, uint32_t rt) { return lds_read_b128_off<OFF>(base + rt); }
+template <int OFF, int V>
+__device__ __forceinline__ u32x2 rd_tr16(uint32_t base, CtOff<V>) { return lds_read_tr16_b64_off<OFF + V>(base); }
+template <int OFF>
+__device__ __forceinline__ u32x2 rd_tr16(uint32_t base, uint32_t rt) { return lds_read_tr16_b64_off<OFF>(base + rt); }
+template <int OFF, int V>
+__device__ __forceinline__ void wr_b128(uint32_t base, CtOff<V>, const u32x4& v) { lds_write_b128_off<OFF + V>(base, v); }
+template <int OFF>
+__device__ __forceinline__ void wr_b128(uint32_t base, uint32_t rt, const u32x4& v) { lds_write_b128_off<OFF>(base + rt, v); }
+
 // Map the linear work-group id to (sequence*head, latent tile) so that the
 // latent tiles of one (sequence, head) land on the same XCD.
 __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, int& lt) {
@@ -281,16 +299,21 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   // Transposed value reads: lane j of group G addresses token 4G + j/4 of a
   // 16-token block at channels db*16 + 4*(j%4), i.e. piece 2*db + ((j&3)>>1)
   // at byte 8*(j&1); one base per db plus the block's immediate offset.
+  // The bases include the ring's start, so a slot is an offset from them.
+  const uint32_t ring0 = lds_addr(ring[0]);
   uint32_t xbase[DC];
 #pragma unroll
-  for (int dc = 0; dc < DC; ++dc) xbase[dc] = c * ROW + ((dc * 4 + G) ^ swz<DH>(c)) * 16;
+  for (int dc = 0; dc < DC; ++dc) xbase[dc] = ring0 + c * ROW + ((dc * 4 + G) ^ swz<DH>(c)) * 16;
   uint32_t vbase[DB];
   {
     const int tt = 4 * G + (c >> 2);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
-      vbase[db] = tt * ROW + ((2 * db + ((c & 3) >> 1)) ^ swz<DH>(tt)) * 16 + (c & 1) * 8;
+      vbase[db] = ring0 + tt * ROW + ((2 * db + ((c & 3) >> 1)) ^ swz<DH>(tt)) * 16 + (c & 1) * 8;
   }
+  // this thread's conversion pieces: base of its input (ring or staging)
+  constexpr int IN_TILE = IN8 ? TT * DH : TILE_BYTES;    // input slot bytes
+  const uint32_t cvt_base = (IN8 ? lds_addr(stage[0]) : ring0) + tid * 16;
 
   // A negative scale is folded into the queries (softmax(s * q . x) =
   // softmax(|s| * (-q) . x)), so the loop below only handles sl2 >= 0.
@@ -437,7 +460,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   constexpr int NQK = DC;              // QK read groups
   constexpr int NPVH = DB / 4;         // PV read groups per half
   constexpr int NG = NQK + 2 * NPVH;
-  constexpr int EPG = 4 / NQK;         // exponential quarters per QK group
+  constexpr int KPG = 4 / NQK;         // 16-token blocks per QK group
   issue(0, 0);
   issue(min(1, last), 1);
   issue(min(2, last), 2);
@@ -447,7 +470,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   convert(1, 1);
   floatx4 scur[4][2];
   {
-    const uint32_t sb = lds_addr(ring[0]);
+    const uint32_t sb = 0;                      // ring slot 0
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 xr[DC];
@@ -469,22 +492,23 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
 
   // LDS reads of group g into the alternating register sets xr / vr (and
   // the conversion pieces cv with the first PV group)
-  auto reads = [&](auto gtag, uint32_t nb, uint32_t vb, uint32_t cb, u32x4 (&xr)[2][4],
+  auto reads = [&](auto gtag, auto nb, auto vb, auto cb, u32x4 (&xr)[2][4],
                    u32x2 (&vr)[2][4][2], u32x4 (&cv)[CVT_PER_THREAD], int (&ce)[CVT_PER_THREAD], int etile,
                    auto tie_only) {
     constexpr int g = decltype(gtag)::value;
     constexpr bool T = decltype(tie_only)::value;
     if constexpr (g < NQK) {
-      constexpr int dc = g;
+      // fragment j = kk * DC + dc: 16-token block g * KPG + kk, channel
+      // slice dc
       auto& x = xr[g & 1];
       if constexpr (T) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) tie(x[kb]);
+        for (int j = 0; j < 4; ++j) tie(x[j]);
       } else {
-        x[0] = lds_read_b128_off<0 * 16 * ROW>(nb + xbase[dc]);
-        x[1] = lds_read_b128_off<1 * 16 * ROW>(nb + xbase[dc]);
-        x[2] = lds_read_b128_off<2 * 16 * ROW>(nb + xbase[dc]);
-        x[3] = lds_read_b128_off<3 * 16 * ROW>(nb + xbase[dc]);
+        static_for<0, 4>([&](auto jtag) {
+          constexpr int j = decltype(jtag)::value, kb = g * KPG + j / DC, dc = j % DC;
+          x[j] = rd_b128<kb * 16 * ROW>(xbase[dc], nb);
+        });
       }
     } else if constexpr (g < NG) {
       constexpr int q = g - NQK, hf = q / NPVH, pb = q % NPVH;
@@ -505,15 +529,15 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
       } else {
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-          v[d][0] = lds_read_tr16_b64_off<hf * 32 * ROW>(vb + vbase[4 * pb + d]);
-          v[d][1] = lds_read_tr16_b64_off<hf * 32 * ROW + 16 * ROW>(vb + vbase[4 * pb + d]);
+          v[d][0] = rd_tr16<hf * 32 * ROW>(vbase[4 * pb + d], vb);
+          v[d][1] = rd_tr16<hf * 32 * ROW + 16 * ROW>(vbase[4 * pb + d], vb);
         }
         if constexpr (q == 0) {
-#pragma unroll
-          for (int i = 0; i < CVT_PER_THREAD; ++i) {
-            cv[i] = lds_read_b128(cb + (i * NW * 64 + tid) * 16);
+          static_for<0, CVT_PER_THREAD>([&](auto itag) {
+            constexpr int i = decltype(itag)::value;
+            cv[i] = rd_b128<i * NW * 64 * 16>(cvt_base, cb);
             if constexpr (IN8) ce[i] = lds_read_i8(exp_addr(etile, i));
-          }
+          });
         }
       }
     }
@@ -535,14 +559,27 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   u32x4 xr[2][4];
 
   // one step; the mask flag (compile time) is set only for it = last - 1, so
-  // the steady-state loop has no branch between its groups.  Entering a
-  // step: tile it+1 converted by every wave, tile it+2 landed, the copy of
-  // tile it+3 issued and (kRot) the first group's reads done.
-  auto step = [&](int it, auto mask_tag) {
-    const uint32_t nb = lds_addr(ring[(it + 1) % NBUF]);
-    const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);          // converted tile it+2
-    const uint32_t ci = IN8 ? lds_addr(stage[(it + 2) % NBUF]) : cb;   // its input
-    const uint32_t vb = lds_addr(ring[it % NBUF]);
+  // the steady-state loop has no branch between its groups.  The ring phase
+  // PH = it % NBUF is a compile-time constant in the unrolled main loop (the
+  // slots' offsets then sit in the LDS instructions' offset fields) and -1
+  // elsewhere (offsets added at run time).  Entering a step: tile it+1
+  // converted by every wave, tile it+2 landed, the copy of tile it+3 issued
+  // and (kRot) the first group's reads done.
+  auto step = [&](int it, auto mask_tag, auto ph_tag) {
+    constexpr int PH = decltype(ph_tag)::value;
+    // offset of the slot of tile it + K in a ring of slots of SZ bytes
+    auto slot = [&](auto k_tag, auto sz_tag) {
+      constexpr int K = decltype(k_tag)::value, SZ = decltype(sz_tag)::value;
+      if constexpr (PH >= 0)
+        return CtOff<((PH + K) % NBUF) * SZ>{};
+      else
+        return (uint32_t)(((it + K) % NBUF) * SZ);
+    };
+    const auto nb = slot(CtOff<1>{}, CtOff<TILE_BYTES>{});        // scores of tile it+1
+    const auto cs = slot(CtOff<2>{}, CtOff<TILE_BYTES>{});        // converted tile it+2
+    const auto ci = slot(CtOff<2>{}, CtOff<IN_TILE>{});           // its input
+    const auto vb = slot(CtOff<0>{}, CtOff<TILE_BYTES>{});        // P V of tile it
+    const uint32_t cb = lds_addr(ring[(it + 2) % NBUF]);          // int8: converted tile, absolute
     u32x2 vr[2][4][2];
     u32x4 cv[CVT_PER_THREAD];
     int ce[CVT_PER_THREAD];
@@ -574,39 +611,48 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
         // tile it+4 into buffer it, under this group's matrix-core work
         wait_vm_then_barrier<0>();
         if constexpr (!decltype(mask_tag)::value) {
-          reads(std::integral_constant<int, 0>{}, lds_addr(ring[(it + 2) % NBUF]), vb, ci, xr, vr, cv, ce,
-                it + 2, std::false_type{});
+          reads(std::integral_constant<int, 0>{}, cs, vb, ci, xr, vr, cv, ce, it + 2, std::false_type{});
           issue(min(it + 4, last), it % NBUF);
         }
       }
       if constexpr (g == NQK + NPVH) {
         // conversion finished in the first half: write it back
         if constexpr (!IN8) {
-#pragma unroll
-          for (int i = 0; i < CVT_PER_THREAD; ++i) lds_write_b128(cb + (i * NW * 64 + tid) * 16, cv[i]);
+          static_for<0, CVT_PER_THREAD>([&](auto itag) {
+            constexpr int i = decltype(itag)::value;
+            wr_b128<i * NW * 64 * 16>(cvt_base, cs, cv[i]);
+          });
         }
       }
       if constexpr (g < NQK) {
-        // scores of tile it+1 for channel slice dc = g
+        // scores of tile it+1 for the 16-token blocks kb of this group, each
+        // summed over the channel slices (2 KPG chains of DC dependent ops):
+        // the blocks of tile it+1 come to life as those of tile it die, so
+        // the two tiles' scores hold about 40 registers rather than 64
         const auto& x = xr[g & 1];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          Pack8 pk;
-          pk.u = x[kb];
+        for (int kk = 0; kk < KPG; ++kk) {
+          const int kb = g * KPG + kk;
 #pragma unroll
-          for (int rb = 0; rb < 2; ++rb)
-            snext[kb][rb] = mfma_f16(pk.h, qf[rb][g], g == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : snext[kb][rb]);
+          for (int dc = 0; dc < DC; ++dc) {
+            Pack8 pk;
+            pk.u = x[kk * DC + dc];
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb)
+              snext[kb][rb] = mfma_f16(pk.h, qf[rb][dc], dc == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : snext[kb][rb]);
+          }
         }
-        // exponentials of tile it, quarters e = (rb, h): pf[h][rb]
+        // exponentials of the same blocks of tile it: pf[kb / 2][rb]
 #pragma unroll
-        for (int e = g * EPG; e < (g + 1) * EPG; ++e) {
-          const int rb = e >> 1, h = e & 1;
-          const float nm = -m[rb];
+        for (int kk = 0; kk < KPG; ++kk) {
+          const int kb = g * KPG + kk;
 #pragma unroll
-          for (int k2 = 0; k2 < 2; ++k2)
+          for (int rb = 0; rb < 2; ++rb) {
+            const float nm = -m[rb];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              pf[h][rb][k2 * 4 + i] = (_Float16)fast_exp2(fmaf(scur[2 * h + k2][rb][i], sl2, nm));
+              pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)fast_exp2(fmaf(scur[kb][rb][i], sl2, nm));
+          }
         }
         SD_INTERLEAVE(8, 3, g + 1)
       } else {
@@ -668,18 +714,25 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
     u32x2 vr0[2][4][2];
     u32x4 cv0[CVT_PER_THREAD];
     int ce0[CVT_PER_THREAD];
-    const uint32_t nb0 = lds_addr(ring[1]);
+    const auto nb0 = CtOff<TILE_BYTES>{};        // ring slot 1
     reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, ce0, 0, std::false_type{});
     issue(min(3, last), 3 % NBUF);
     lds_wait();
     reads(std::integral_constant<int, 0>{}, nb0, nb0, nb0, xr, vr0, cv0, ce0, 0, std::true_type{});
   }
-  for (int it = 0; it + 1 < last; ++it) step(it, std::false_type{});
-  if (last >= 1) step(last - 1, std::true_type{});
+  int it = 0;
+  for (; it + NBUF < last; it += NBUF) {
+    step(it, std::false_type{}, CtOff<0>{});
+    step(it + 1, std::false_type{}, CtOff<1>{});
+    step(it + 2, std::false_type{}, CtOff<2>{});
+    step(it + 3, std::false_type{}, CtOff<3>{});
+  }
+  for (; it + 1 < last; ++it) step(it, std::false_type{}, CtOff<-1>{});
+  if (last >= 1) step(last - 1, std::true_type{}, CtOff<-1>{});
   {
     // last tile (masked and covered by the maxima): softmax and P V
     wait_vm_then_barrier<0>();
-    const uint32_t vb = lds_addr(ring[last % NBUF]);
+    const uint32_t vb = (last % NBUF) * TILE_BYTES;   // ring slot of the last tile
     f16x8 pf[2][2];
     SD_P_ROW(scur, pf, 0)
     SD_P_ROW(scur, pf, 1)

@@ -339,27 +339,22 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
     }
   };
 
-  // per-lane LDS offsets of the fragment reads inside a slot
-  uint32_t koff[2][DC];
+  // per-lane LDS offsets of the fragment reads inside a slot, for the first
+  // 16-key block; the swizzle depends on key % 16 only, so the second block
+  // (+16 keys) is an immediate offset of the read
+  uint32_t koff[DC];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      const int key = kb * 16 + c;
-      koff[kb][dc] = key * ROW_BYTES + (((dc * 4 + G4) ^ lds_swizzle<PK>(key)) * 16);
-    }
+  for (int dc = 0; dc < DC; ++dc) koff[dc] = c * ROW_BYTES + (((dc * 4 + G4) ^ lds_swizzle<PK>(c)) * 16);
   // ds_read_b64_tr_b16: lane j of group G4 addresses key 4 G4 + j / 4 (+16)
   // at channels db * 16 + 4 (j % 4); lane c then receives 4 keys at channel
   // db * 16 + c
-  uint32_t voff[2][DB];
+  uint32_t voff[DB];
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int key = hh * 16 + 4 * G4 + (c >> 2);
-      const int ch = db * 16 + 4 * (c & 3);
-      voff[hh][db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ lds_swizzle<PK>(key)) * 16) + (ch & 7) * 2;
-    }
+  for (int db = 0; db < DB; ++db) {
+    const int key = 4 * G4 + (c >> 2);
+    const int ch = db * 16 + 4 * (c & 3);
+    voff[db] = HALF_BYTES + key * ROW_BYTES + (((ch >> 3) ^ lds_swizzle<PK>(key)) * 16) + (ch & 7) * 2;
+  }
 
   // segment state of this wave: pair, query row, its B operand of
   // S^T = K Q^T, causal limit, running (max, sum, O^T)
@@ -369,6 +364,11 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
   bf16x8 qf[DC];
   float m = -INFINITY, l = 0.f;
   floatx4 o[DB];
+  // Scores stay raw (S = K Q^T); the scale enters the exponent as
+  // exp2(S sl2 - m).  A negative scale is folded into the queries
+  // (softmax(s q.k) = softmax(|s| (-q).k)), so sl2 >= 0 below.
+  const bool neg_scale = a.scale_log2 < 0.f;
+  const float sl2 = fabsf(a.scale_log2);
 
   auto start_segment = [&](const TileCursor& cu) {
     const int hk = cu.x / row_groups, rg = cu.x % row_groups;
@@ -389,6 +389,7 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc) {
         pk.u = src[dc * 4 + G4];
+        if (neg_scale) pk.u ^= u32x4{0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u};
         qf[dc] = pk.b;
       }
       lim = cu.L - a.k + j;                    // last visible key of this row
@@ -414,9 +415,10 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
     const uint32_t sb = lds_addr(slot);
     u32x4 kr[2][DC];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) kr[kb][dc] = lds_read_b128(sb + koff[kb][dc]);
+    for (int dc = 0; dc < DC; ++dc) {
+      kr[0][dc] = lds_read_b128_off<0>(sb + koff[dc]);
+      kr[1][dc] = lds_read_b128_off<16 * ROW_BYTES>(sb + koff[dc]);
+    }
     lds_wait();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -425,11 +427,12 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
     // V^T fragments for P V, issued now so they overlap the scores
     u32x2 vr[2][DB];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int db = 0; db < DB; ++db) vr[hh][db] = lds_read_tr16_b64(sb + voff[hh][db]);
+    for (int db = 0; db < DB; ++db) {
+      vr[0][db] = lds_read_tr16_b64_off<0>(sb + voff[db]);
+      vr[1][db] = lds_read_tr16_b64_off<16 * ROW_BYTES>(sb + voff[db]);
+    }
 
-    // S^T = K Q^T: lane holds S[row c][key t0 + kb*16 + 4 G4 + i] (log2 units)
+    // S^T = K Q^T: lane holds S[row c][key t0 + kb*16 + 4 G4 + i] (raw)
     float x[8];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -441,39 +444,59 @@ __global__ __launch_bounds__(NWR * KG * 64) void verify_stream_bf16(VerifyArgs a
         acc = mfma_bf16(pk.b, qf[dc], acc);
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[kb * 4 + i] = acc[i] * a.scale_log2;
-    }
-    if (t0 + TK - 1 > unmasked_end) {          // tail tile: causal mask
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int t = t0 + (e >> 2) * 16 + 4 * G4 + (e & 3);
-        if (t > lim) x[e] = -INFINITY;
-      }
+      for (int i = 0; i < 4; ++i) x[kb * 4 + i] = acc[i];
     }
 
-    // online softmax with a lazily raised maximum
-    float tmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
-                       fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-    tmax = wave_max_across_groups(tmax);
-    if (__ballot(tmax > m + kRescale) != 0ull) {
-      const float mnew = fmaxf(m, tmax);
-      const float alpha = (mnew == -INFINITY) ? 1.f : fast_exp2(m - mnew);
+    // Online softmax with a lazily raised maximum.  Each lane forms the
+    // exponents y = S sl2 - m of its 8 scores, taken before the causal mask
+    // (so their largest bounds the masked ones from above), and checks the
+    // largest against kRescale (+inf before the first raise, m = -inf);
+    // only when some lane passes it are the row maxima formed across the
+    // row's four lanes and m raised.  m may so exceed the masked tile's true
+    // maximum, which leaves o = O / l and lse = m + log2 l unchanged, and P
+    // (bf16 hi + lo, the fp32 exponent range) neither overflows nor loses
+    // precision.
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = fmaf(x[e], sl2, -m);
+    const float ly = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])),
+                           fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])));
+    if (__ballot(ly > kRescale) != 0ull) {
+      const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                             fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+      const float mnew = fmaxf(m, wave_max_across_groups(lm) * sl2);
+      const float alpha = (m == -INFINITY) ? 0.f : fast_exp2(m - mnew);   // O, l are still 0 before the first raise
       l *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db] *= alpha;
       m = mnew;
-    }
-    bf16x8 ph, pl;
-    float psum = 0.f;
-    const bool none = m == -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float pv = none ? 0.f : fast_exp2(x[e] - m);
-      psum += pv;
-      const __bf16 hi = float_to_bf16(pv);
-      ph[e] = hi;
-      pl[e] = float_to_bf16(pv - bf16_to_float(hi));
+      for (int e = 0; e < 8; ++e) y[e] = fmaf(x[e], sl2, -m);
     }
+    float pv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pv[e] = fast_exp2(y[e]);
+    if (t0 + TK - 1 > unmasked_end) {          // tail tile: causal mask
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int t = t0 + (e >> 2) * 16 + 4 * G4 + (e & 3);
+        if (t > lim) pv[e] = 0.f;
+      }
+    }
+    // P = hi + lo: hi the bf16 truncation (a mask of the fp32 bits), lo the
+    // exact remainder (|lo| < 2^-7 p) rounded to bf16, so P is kept to
+    // 2^-16 of p
+    Pack8 phk, plk;
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const uint32_t b0 = __float_as_uint(pv[e]), b1 = __float_as_uint(pv[e + 1]);
+      psum += pv[e] + pv[e + 1];
+      phk.u[e / 2] = __builtin_amdgcn_perm(b1, b0, 0x07060302u);   // high halves of b0 | b1
+      plk.b[e] = float_to_bf16(pv[e] - __uint_as_float(b0 & 0xffff0000u));
+      plk.b[e + 1] = float_to_bf16(pv[e + 1] - __uint_as_float(b1 & 0xffff0000u));
+    }
+    const bf16x8 ph = phk.b, pl = plk.b;
     l += psum;
 
     // O^T += V^T P^T.  The product's K index runs over keys {4G4..4G4+3,

@@ -151,6 +151,29 @@ def test_verify_edge_cases(case):
     assert np.all(out[np.isneginf(rl)] == 0)
 
 
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("mult", [-0.9, 0.0, 4.0])
+def test_verify_scale_sign_and_size(mult, dt, paged):
+    # a negative scale (folded into the queries), a zero scale (every
+    # visible key weighs the same) and a large one (the running maximum is
+    # raised on many tiles), on ragged lengths with a causal tail
+    D = 128
+    name = f"scale{mult}-{dt}-{'paged' if paged else 'contiguous'}"
+    print(f"verify case {name}", flush=True)
+    lens = [700, 33, 1]
+    w = synth.Workload(name, dt, batch=3, hq=8, hkv=2, head_dim=D, kv_len=max(lens), block=5,
+                       paged=paged)
+    d = synth.verify_inputs(w, seed=23, kv_len=np.array(lens, np.int32))
+    scale = mult / math.sqrt(D)
+    out, lse = run_gpu(d, scale=scale)
+    kw = {"page_table": d["page_table"]} if paged else {}
+    ro, rl = oracle.verify_attention(d["q"].values, d["k_cache"].values, d["v_cache"].values,
+                                     d["kv_len"], scale, **kw)
+    assert_close(out, ro, dt, name)
+    assert_lse_close(lse, rl, dt, name)
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_verify_beyond_grid_extent(dt):
     # 70000 (sequence, KV head) pairs: more than a grid's y extent (65535)

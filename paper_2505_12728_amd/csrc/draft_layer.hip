@@ -54,6 +54,9 @@ __device__ __forceinline__ uint32_t i8x2_to_bf16x2(uint32_t v, int k) {
 // Q8: the weight holds int8 rows with one fp32 scale per row (output
 // column); each lane then loads 64 bytes of its row per chunk (4 loads),
 // widens them to bf16 in registers and scales the accumulators once.
+// A work-group owns a.cols = 16 x (active waves) output columns; waves past
+// them only copy their share of the input chunks and meet the barriers, so
+// the planner can size the groups to fill every compute unit evenly.
 template <int RB, int NW, bool Q8>
 __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   constexpr int HROWS = RB * 16;
@@ -62,8 +65,9 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
   static_assert(HPIECES % (NW * 64) == 0, "whole copies per thread");
   __shared__ __align__(16) unsigned char hbuf[2][HPIECES * 16];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6, G = lane >> 4, c = lane & 15;
-  const int n0 = blockIdx.x * (NW * 16) + w * 16;
+  const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), G = lane >> 4, c = lane & 15;
+  const int n0 = blockIdx.x * a.cols + w * 16;
+  const bool active = w * 16 < a.cols;         // wave-uniform
   const int ks = blockIdx.y;
   const int r0 = blockIdx.z * HROWS;
   const int K = a.K, N = a.N, R = a.R;
@@ -135,6 +139,16 @@ __global__ __launch_bounds__(NW * 64) void linear_partial(LinearArgs a) {
     }
     if (n + 1 < ch1) issue(n + 1, buf ^ 1);
   };
+  if (!active) {
+    // input copies and barriers only, in the same order as the other waves
+    if (ch0 < ch1) issue(ch0, 0);
+#pragma unroll 1
+    for (int n = ch0; n < ch1; ++n) {
+      wait_vm_then_barrier<0>();
+      if (n + 1 < ch1) issue(n + 1, ((n - ch0) & 1) ^ 1);
+    }
+    return;
+  }
   u32x4 wa[WL], wb[WL];
   if (ch0 < ch1) {
     wload(wa, ch0);
@@ -377,7 +391,7 @@ __global__ __launch_bounds__(kEpiThreads) void kp_post(const float* probs, const
 
 template <int NW, bool Q8>
 hipError_t launch_partial_nw(const LinearArgs& a, int rb, int passes, hipStream_t st) {
-  const dim3 grid((a.N + NW * 16 - 1) / (NW * 16), a.ksplit, passes);
+  const dim3 grid((a.N + a.cols - 1) / a.cols, a.ksplit, passes);
   const dim3 block(NW * 64);
   switch (rb) {
     case 1: hipLaunchKernelGGL((linear_partial<1, NW, Q8>), grid, block, 0, st, a); break;
@@ -425,29 +439,48 @@ LinearPlan plan_linear(int R, int K, int N, int cus) {
   // LDS bound (two input chunks of row_blocks * 8 KB) and 32 waves
   const int lds_fit = (160 * 1024) / (p.row_blocks * 16 * 1024);
   auto resident = [&](int waves) {
-    int per_cu = waves == 8 ? resident_per_cu<8>(p.row_blocks) : resident_per_cu<4>(p.row_blocks);
+    int per_cu = resident_per_cu<8>(p.row_blocks);
     if (per_cu <= 0) per_cu = std::max(1, std::min(lds_fit, 32 / waves));
     return (long long)std::max(cus, 1) * per_cu;
   };
-  auto groups = [&](int waves) { return (long long)((N + waves * 16 - 1) / (waves * 16)) * p.passes; };
-  // eight waves per work-group (128 output columns), each chunk of the
-  // inputs copied once for all of them
+  // eight waves per work-group, each chunk of the inputs copied once for
+  // all of them
   p.waves = 8;
-  const long long g = groups(p.waves), cap = resident(p.waves);
+  const long long cap = resident(p.waves);
   const int nch = K / kChunkK;
-  // split the reduction to fill the resident slots in one round, keeping
-  // at least four chunks per split
-  long long ks = std::max(1LL, cap / g);
-  ks = std::min<long long>(ks, std::max(1, nch / 4));
-  p.ksplit = (int)std::max(1LL, std::min<long long>(ks, kLinearMaxSplits));
+  const long long ncu = std::max(cus, 1);
+  // A compute unit streams its weight rows at a bounded rate, so the time
+  // follows the most loaded unit: (work-groups it runs) x (rows x chunks
+  // per work-group).  For 4..8 column-owning waves, split the reduction to
+  // fill the resident slots in one round (at least four chunks per split)
+  // and keep the count with the least such load; ties go to more waves
+  // (more weight loads in flight per unit).  One wave fewer than eight
+  // fills every unit evenly where 128-column groups would leave units with
+  // one group less than others (57344 columns: 512 groups of 112 instead
+  // of 448 of 128).
+  long long best = -1;
+  for (int nwa = 8; nwa >= 4; --nwa) {
+    const long long g = (long long)((N + nwa * 16 - 1) / (nwa * 16)) * p.passes;
+    long long ks = std::max(1LL, cap / g);
+    ks = std::min<long long>(ks, std::max(1, nch / 4));
+    ks = std::max(1LL, std::min<long long>(ks, kLinearMaxSplits));
+    const long long per_cu = (g * ks + ncu - 1) / ncu;
+    const long long load = (long long)nwa * ((nch + ks - 1) / ks) * per_cu;
+    if (best < 0 || load < best) {
+      best = load;
+      p.cols = nwa * 16;
+      p.ksplit = (int)ks;
+    }
+  }
   p.part_bytes = (size_t)p.ksplit * R * N * sizeof(float);
   return p;
 }
 
-hipError_t launch_linear_partial(const LinearArgs& a, const LinearPlan& p, hipStream_t st) {
+hipError_t launch_linear_partial(const LinearArgs& args, const LinearPlan& p, hipStream_t st) {
+  LinearArgs a = args;
+  a.cols = p.cols;
   if (a.wscale != nullptr) return launch_partial_nw<8, true>(a, p.row_blocks, p.passes, st);
-  return p.waves == 8 ? launch_partial_nw<8, false>(a, p.row_blocks, p.passes, st)
-                      : launch_partial_nw<4, false>(a, p.row_blocks, p.passes, st);
+  return launch_partial_nw<8, false>(a, p.row_blocks, p.passes, st);
 }
 
 hipError_t launch_epi_add(const float* part, int ksplit, int R, int N, const float* bias, const float* residual,

@@ -138,12 +138,14 @@ struct LinearArgs {
   int R, K, N;
   int ksplit;
   const float* wscale;   // [N] scales of int8 rows, or NULL (bf16 weight)
+  int cols;        // output columns per work-group (set from the plan at launch)
 };
 
 struct LinearPlan {
   int row_blocks;  // 16-row blocks per pass (1..8)
   int passes;      // passes over the weight (ceil(R / 128))
-  int waves;       // waves per work-group (16 output columns each)
+  int waves;       // waves per work-group
+  int cols;        // output columns per work-group: 16 per wave that owns columns
   int ksplit;      // splits of the reduction
   size_t part_bytes;
 };

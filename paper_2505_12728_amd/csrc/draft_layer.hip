@@ -341,11 +341,6 @@ __global__ __launch_bounds__(kEpiThreads) void epi_swiglu(const float* part, int
   act[(size_t)r * I + i] = float_to_bf16(g / (1.f + expf(-g)) * u);
 }
 
-__global__ __launch_bounds__(kEpiThreads) void to_bf16(const float* x, __bf16* y, size_t n) {
-  const size_t i = (size_t)blockIdx.x * kEpiThreads + threadIdx.x;
-  if (i < n) y[i] = float_to_bf16(x[i]);
-}
-
 // ------------------------------------------------- K drafts in K / k' passes
 // Before the head: the k' placeholder rows of a pass's output (rows
 // r - k' .. r - 1 of each sequence) rounded to bf16 as the LM head's input
@@ -511,7 +506,6 @@ SemiArPlan plan_semi_ar(int B, int r, int d, int Hq, int Hkv, int I, int Lmax, i
   p.off_x0 = take((size_t)R * d * 4);
   p.off_h = take((size_t)R * d * 2);
   p.off_q = take((size_t)R * Hq * D * 2);
-  p.off_attn = take((size_t)R * Hq * D * 4);
   p.off_attn16 = take((size_t)R * Hq * D * 2);
   p.off_x1 = take((size_t)R * d * 4);
   p.off_act = take((size_t)R * I * 2);
@@ -529,7 +523,6 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   float* x0 = reinterpret_cast<float*>(ws + p.off_x0);
   __bf16* h = reinterpret_cast<__bf16*>(ws + p.off_h);
   __bf16* q = reinterpret_cast<__bf16*>(ws + p.off_q);
-  float* attn = reinterpret_cast<float*>(ws + p.off_attn);
   __bf16* attn16 = reinterpret_cast<__bf16*>(ws + p.off_attn16);
   float* x1 = reinterpret_cast<float*>(ws + p.off_x1);
   __bf16* act = reinterpret_cast<__bf16*>(ws + p.off_act);
@@ -563,7 +556,8 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   va.kv_len = kv_len;
   va.page_table = nullptr;
   va.Lmax = a.Lmax;
-  va.out = attn;
+  va.out = nullptr;
+  va.out_bf16 = attn16;                        // the merge writes the bf16 input of Wo
   va.lse = nullptr;
   va.B = a.B;
   va.k = a.r;
@@ -575,9 +569,6 @@ hipError_t launch_semi_ar(const SemiArArgs& a, const SemiArPlan& p, hipStream_t 
   va.part_o = reinterpret_cast<float*>(ws + p.off_verify);
   va.part_lse = va.part_o + p.verify.part_rows * D;
   if ((e = launch_verify(va, p.verify, 1, st)) != hipSuccess) return e;
-  const size_t na = (size_t)R * a.Hq * D;
-  hipLaunchKernelGGL(to_bf16, dim3((unsigned)((na + kEpiThreads - 1) / kEpiThreads)), dim3(kEpiThreads), 0, st,
-                     attn, attn16, na);
   // x1 = x0 + attn Wo^T, h = RMSNorm(x1)
   if ((e = lin(attn16, a.wo, a.wo_s, a.Hq * D, d, p.o)) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_add_cols, eg, dim3(kEpiThreads), 0, st, part, p.o.ksplit, R, d,

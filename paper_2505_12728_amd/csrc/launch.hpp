@@ -44,6 +44,8 @@ struct VerifyArgs {
   float scale_log2;     // scale * log2(e)
   float* part_o;        // [part_rows, D] partial outputs (normalised)
   float* part_lse;      // [part_rows] partial log-sum-exp (log2 units)
+  __bf16* out_bf16;     // bf16 stream path: when set, the merge writes out here
+                        // as bf16 (and not `out`); used inside the draft layer
 };
 
 hipError_t launch_verify(const VerifyArgs& a, const VerifyPlan& p, int dtype, hipStream_t s);
@@ -185,7 +187,7 @@ struct SemiArArgs {
 struct SemiArPlan {
   LinearPlan fc, qkv, o, gu, down;
   VerifyPlan verify;
-  size_t off_part, off_x0, off_h, off_q, off_attn, off_attn16, off_x1, off_act, off_kvlen, off_ss, off_verify;
+  size_t off_part, off_x0, off_h, off_q, off_attn16, off_x1, off_act, off_kvlen, off_ss, off_verify;
   size_t workspace_bytes;
   bool ok;
 };

@@ -888,7 +888,17 @@ __global__ __launch_bounds__(256) void verify_stream_merge(VerifyArgs a, int G, 
   const int h = hk * g + (r - j * g);
   const size_t orow = ((size_t)b * a.k + j) * a.Hq + h;
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  if (half == 0 && active) *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = acc * inv;
+  if (half == 0 && active) {
+    const floatx4 o = acc * inv;
+    if (a.out_bf16 != nullptr) {
+      Pack8 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pk.b[e] = float_to_bf16(o[e]);
+      *reinterpret_cast<u32x2*>(a.out_bf16 + orow * D + d4 * 4) = u32x2{pk.u[0], pk.u[1]};
+    } else {
+      *reinterpret_cast<floatx4*>(a.out + orow * D + d4 * 4) = o;
+    }
+  }
   if (a.lse != nullptr && lane == 0)
     a.lse[orow] = wsum > 0.f ? (mx + log2f(wsum)) * kLn2 : -INFINITY;
 }

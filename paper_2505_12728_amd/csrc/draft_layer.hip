@@ -9,17 +9,19 @@
 //
 // A drafting step has few rows (R = B r <= 128 per pass), so every
 // projection streams its weight once and is bound by HBM.  One kernel
-// serves all five: work-groups of NW waves own NW * 16 output columns and
-// a range of 256-channel chunks of the reduction; lane (c, G) of a wave
-// reads 128 contiguous bytes of weight row c per chunk (every row in
-// 512-byte runs) straight into registers, the chunk of all input rows is
-// copied into LDS by the global_load_lds DMA, and z^T = W x^T runs on bf16
-// matrix cores.  The reduction is split across work-groups until the grid
-// fills the device; each split writes fp32 partial sums, and one epilogue
-// kernel per projection adds the splits and applies what follows it:
-// bias + RMSNorm, RoPE + cache append, residual + RMSNorm, SwiGLU, or the
-// final residual.  The attention is the verification kernel: the new rows
-// are a block of r queries, causal inside the block, over the cache.
+// serves all five: work-groups of eight waves, 4..8 of which own 16 output
+// columns each, and a range of 256-channel chunks of the reduction; lane
+// (c, G) of a wave reads 128 contiguous bytes of weight row c per chunk
+// (every row in 512-byte runs) straight into registers, the chunk of all
+// input rows is copied into LDS by the global_load_lds DMA, and
+// z^T = W x^T runs on bf16 matrix cores.  A compute unit streams weights at
+// a bounded rate, so the planner sizes the column groups and reduction
+// splits to give every unit the same load; each split writes fp32 partial
+// sums, and one or two epilogue launches per projection add the splits
+// and apply what follows it: bias + RMSNorm, RoPE + cache append, residual
+// + RMSNorm, SwiGLU, or the final residual.  The attention is the
+// verification kernel (its merge writing the bf16 input of Wo): the new
+// rows are a block of r queries, causal inside the block, over the cache.
 #include <math.h>
 
 #include <algorithm>

@@ -39,7 +39,10 @@ def _bf16(x):
 @pytest.mark.parametrize("R,K,N,bias,res", [(1, 256, 1, False, False), (5, 512, 100, True, False),
                                             (36, 8192, 1000, True, True), (128, 1024, 4096, False, True),
                                             (130, 768, 515, True, True), (7, 28672, 64, False, False),
-                                            (16, 256, 65536, True, False)])
+                                            (16, 256, 65536, True, False),
+                                            # seven column-owning waves (512 groups of 112 columns),
+                                            # the last group ragged
+                                            (36, 512, 57304, True, True)])
 def test_linear_parity(R, K, N, bias, res):
     import torch
     import paper_2505_12728_amd as sd

@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 @pytest.mark.parametrize("R,K,N,bias,res", [(1, 256, 1, False, False), (9, 512, 100, True, False),
                                             (36, 8192, 1000, True, True), (130, 768, 515, False, True),
-                                            (16, 256, 65536, True, False)])
+                                            (16, 256, 65536, True, False), (36, 512, 57304, False, True)])
 def test_linear_q8_parity(R, K, N, bias, res):
     import torch
     import paper_2505_12728_amd as sd

@@ -107,6 +107,9 @@ def test_compress_validation_errors(lib):
     assert call(d=1024, H=2) == sd.SD_ERR_UNSUPPORTED    # head width 512
     assert call(d=1024, H=2, dt=0) == sd.SD_ERR_UNSUPPORTED
     assert call(dt=2) == sd.SD_ERR_INVALID_ARG
+    # feature rows wider than 2^22 channels (the copies' 24-bit row offsets)
+    assert call(d=(1 << 22) + 128, H=(1 << 15) + 1) == sd.SD_ERR_UNSUPPORTED
+    assert lib.sd_latent_compress_workspace_size(1, 64, 16, (1 << 22) + 128, (1 << 15) + 1, 1) == 0
     # bf16 with 256-channel heads: accepted, with one partial per short split
     assert lib.sd_latent_compress_workspace_size(1, 1000, 16, 512, 2, 1) > 0
     need = lib.sd_latent_compress_workspace_size(1, 65536, 16, 256, 2, 1)

@@ -654,7 +654,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
               pf[kb >> 1][rb][(kb & 1) * 4 + i] = (_Float16)fast_exp2(fmaf(scur[kb][rb][i], sl2, nm));
           }
         }
-        SD_INTERLEAVE(8, 3, g + 1)
+        SD_INTERLEAVE(8, 2, g + 1)
       } else {
         constexpr int q = g - NQK, hf = q / NPVH, pb = q % NPVH;
         if constexpr (q == 0 && decltype(mask_tag)::value) mask_tail(snext, tok0 + last * TT);
@@ -686,7 +686,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
         } else if constexpr (pb == NPVH - 1) {
           exceed = tile_exceeds(snext);
         }
-        SD_INTERLEAVE(8 + (pb == NPVH - 1 ? 2 : 0), 3, g + 1)
+        SD_INTERLEAVE(8 + (pb == NPVH - 1 ? 2 : 0), 2, g + 1)
       }
       if constexpr (kRot && g == NG - 1 && !decltype(mask_tag)::value) {
         // the next step's first group is complete before the loop edge

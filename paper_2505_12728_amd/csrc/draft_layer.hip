@@ -608,6 +608,7 @@ SemiArDraftPlan plan_semi_ar_draft(int B, int r0, int d, int Hq, int Hkv, int I,
   p.off_tok = take((size_t)R * 4);
   p.off_pos = take((size_t)2 * B * 4);
   p.workspace_bytes = off;
+  p.cus = cus;
   p.ok = p.first.ok && p.later.ok;
   return p;
 }
@@ -643,6 +644,7 @@ hipError_t launch_semi_ar_draft(const SemiArDraftArgs& a, const SemiArDraftPlan&
     lh.V = a.V;
     lh.scale_log2 = kLog2e / a.temperature;
     lh.stats = reinterpret_cast<float*>(ws + p.off_lmstats);
+    lh.cus = p.cus;
     if ((e = launch_lm_head(lh, 1, st)) != hipSuccess) return e;
     AcceptArgs sa{};
     sa.p = probs;

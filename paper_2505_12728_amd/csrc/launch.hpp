@@ -89,6 +89,8 @@ struct LmHeadArgs {
   int R, d, V;
   float scale_log2;    // log2(e) / temperature
   float* stats;        // workspace: [R][ceil(V/16)] block (max, sum), then [R] row (M, L)
+  int cus;             // compute units of the device (0: no per-unit balancing)
+  int nfull;           // set by the launch: work-groups with a block for every wave (< 0: all)
 };
 
 size_t lm_head_workspace_bytes(int R, int V);
@@ -215,6 +217,7 @@ struct SemiArDraftPlan {
   size_t off_layer, off_out, off_unext, off_hid, off_probs, off_lmstats, off_sample, off_nacc, off_ut, off_tok,
       off_pos;
   size_t workspace_bytes;
+  int cus;
   bool ok;
 };
 

@@ -233,6 +233,12 @@ __device__ __forceinline__ void write_block(const LmHeadArgs& a, const floatx4& 
 // global_load_lds DMA into two buffers; pieces of row r sit at slot
 // piece ^ (r & 15) so the 16 rows read at one piece hit 16 distinct bank
 // groups.
+//
+// With a.nfull >= 0 the first a.nfull work-groups give every wave its VB
+// blocks and the later ones leave their last wave without blocks (it only
+// moves its share of the hidden chunks): the grid then holds a whole number
+// of work-groups per compute unit with the larger ones dispatched first, so
+// no unit streams more than one 16-row block above the mean.
 template <int RB, int NW, int VB>
 __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
   constexpr int HROWS = RB * 16;
@@ -241,8 +247,11 @@ __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
   static_assert(HPIECES % (NW * 64) == 0, "whole copies per thread");
   __shared__ __align__(16) unsigned char hbuf[2][HPIECES * 16];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6, G = lane >> 4, c = lane & 15;
-  const int v0 = blockIdx.x * (NW * VB * 16) + w * (VB * 16);
+  const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), G = lane >> 4, c = lane & 15;
+  const int wg = blockIdx.x;
+  const bool full = a.nfull < 0 || wg < a.nfull;
+  const int unit0 = full ? wg * NW : a.nfull * NW + (wg - a.nfull) * (NW - 1);
+  const int v0 = (unit0 + w) * (VB * 16);
   const int d = a.d, V = a.V, R = a.R;
   const uint16_t* W = static_cast<const uint16_t*>(a.weight);
   const uint16_t* H = static_cast<const uint16_t*>(a.hidden);
@@ -276,6 +285,15 @@ __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
     for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int nch = d / 256;
   issue_hidden(0, 0);
+  if (!full && w == NW - 1) {
+    // same copies, waits and barriers as the other waves, no weight rows
+#pragma unroll 1
+    for (int n = 0; n < nch; ++n) {
+      wait_vm_then_barrier<0>();
+      if (n + 1 < nch) issue_hidden(n + 1, (n & 1) ^ 1);
+    }
+    return;
+  }
 #pragma unroll 1
   for (int n = 0; n < nch; ++n) {
     const int buf = n & 1;
@@ -400,10 +418,23 @@ template <int RB>
 hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st) {
   if constexpr (RB <= 4) {
     if (a.d % 256 == 0) {
+      LmHeadArgs b = a;
+      b.nfull = -1;
       if (a.V >= 65536) {
-        hipLaunchKernelGGL((lm_logits_burst<RB, 8, 1>), dim3((a.V + 127) / 128), dim3(512), 0, st, a);
+        // G work-groups, a multiple of the unit count, of 8 or 7 blocks
+        // (nfull = nb - 7 G of 8) when such a G covers the nb blocks
+        const int nb = (a.V + 15) / 16, g8 = (nb + 7) / 8;
+        int grid = g8;
+        if (a.cus > 0) {
+          const int G = (g8 + a.cus - 1) / a.cus * a.cus;
+          if (G > g8 && 7LL * G <= nb) {
+            grid = G;
+            b.nfull = nb - 7 * G;
+          }
+        }
+        hipLaunchKernelGGL((lm_logits_burst<RB, 8, 1>), dim3(grid), dim3(512), 0, st, b);
       } else {
-        hipLaunchKernelGGL((lm_logits_burst<RB, 4, 1>), dim3((a.V + 63) / 64), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((lm_logits_burst<RB, 4, 1>), dim3((a.V + 63) / 64), dim3(256), 0, st, b);
       }
       return hipGetLastError();
     }

@@ -417,6 +417,7 @@ int sd_lm_head_probs(const void* hidden, const void* weight, float* probs, int R
   a.V = V;
   a.scale_log2 = 1.4426950408889634f / temperature;
   a.stats = static_cast<float*>(workspace);
+  a.cus = device_cus();
   return status_from(sd::launch_lm_head(a, dtype, static_cast<hipStream_t>(stream)));
 }
 

@@ -5,18 +5,22 @@
 //
 // bf16 path (matrix cores), grid (sequence x head x latent tile, token split):
 //   - a work-group of NW waves owns NW * 32 latents of one (sequence, head);
-//     each wave keeps its 32 latents' query fragments (fp16) in registers;
+//     each wave keeps its 32 latents' query fragments in registers;
 //   - 64-token tiles of F_V[b][:, hs] are copied HBM -> LDS with the
 //     global_load_lds DMA (no VGPR staging) into a 4-buffer ring, the 16-byte
 //     pieces of each token XOR-swizzled so that every read pattern below is
 //     free of LDS bank conflicts;
-//   - each tile is converted in place bf16 -> fp16 once per work-group (exact
-//     for zero and |F_V| in [2^-17, 65280], rounded to nearest otherwise, so
+//   - each tile is converted bf16 -> fp16 once per work-group (exact for
+//     zero and |F_V| in [2^-17, 65280], rounded to nearest otherwise, so
 //     larger magnitudes become inf; a wave whose outputs then come out
 //     non-finite, or all below 2^-12, recomputes its latents exactly in float64
-//     (compress_exact_wave)), so both products run on fp16 matrix
-//     cores: S^T = F_V Cq^T (lane = one latent row), online softmax in fp32
-//     with exp2, P (in [0, 2^15]) rounded to fp16, O^T += F_V^T P^T;
+//     (compress_exact_wave)), so that P V runs on fp16 matrix cores:
+//     S^T = F_V Cq^T (lane = one latent row), online softmax in fp32 with
+//     exp2, P (in [0, 2^15]) rounded to fp16, O^T += F_V^T P^T.  Eight-wave
+//     groups over 128-channel heads take the scores from the bf16 tile as
+//     copied (bf16 matrix cores) and convert into a second, channel-major
+//     fp16 copy whose P V fragments are plain 16-byte reads; the others
+//     convert in place and read F_V^T fragments by transposing reads;
 //   - latent tiles of one (sequence, head) are placed on the same XCD
 //     (work-groups are dealt to the 8 XCDs round-robin) so their F_V reads
 //     hit the same L2.
@@ -94,12 +98,16 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // One work-group = NW waves x 32 latents of one (sequence, head), one token
 // split.  64-token tiles of F_V[b][:, hs] are copied HBM -> LDS by the
 // global_load_lds DMA into a ring of four buffers.  One tile ahead of its
-// score step, the work-group converts a tile in place from bf16 to fp16
-// (each 16-byte piece once per work-group), so every wave then runs both
-// products on fp16 matrix cores with no per-wave conversion:
+// score step, the work-group converts a tile from bf16 to fp16 (each
+// 16-byte piece once per work-group), so every wave then runs the P V
+// product on fp16 matrix cores with no per-wave conversion:
 //   S^T = F_V Cq^T   (lane = one latent row, 16 tokens per tile and row)
-//   O^T += F_V^T P^T (P = exp2(s - m) in [0, 2^15] rounded to fp16; F_V^T
-//                     fragments via the transposing ds_read_b64_tr_b16)
+//   O^T += F_V^T P^T (P = exp2(s - m) in [0, 2^15] rounded to fp16)
+// Eight-wave groups with 128-channel heads (CM below) run the scores on the
+// bf16 tile itself and write the fp16 tile channel-major into a second ring,
+// so an F_V^T fragment is one 16-byte read; the other shapes convert in
+// place, run the scores on fp16, and read F_V^T by the transposing
+// ds_read_b64_tr_b16 (two reads per fragment).
 // The loop is software-pipelined across tiles (scores of the next tile under
 // the exponentials of the current one) and split into groups whose LDS
 // reads are issued one group ahead.  The running maximum is raised (O, l
@@ -110,8 +118,12 @@ __device__ __forceinline__ void map_tile(int lin, int n_bh, int n_lt, int& bh, i
 // one fence-free barrier (for eight-wave groups placed before the step's
 // last group, so the next step's first reads overlap that group's work).
 template <int NW, int DH, bool IN8>
+constexpr bool kChannelMajor = !IN8 && NW == 8 && DH == 128;
+template <int NW, int DH, bool IN8>
 struct CompressLds {
-  unsigned char ring[4][64 * DH * 2];                       // fp16 tiles
+  static constexpr bool CM = kChannelMajor<NW, DH, IN8>;
+  unsigned char ring[4][64 * DH * 2];                       // bf16 tiles (CM) / fp16 tiles
+  unsigned char tr[CM ? 4 : 1][CM ? 64 * DH * 2 : 16];      // CM: channel-major fp16 tiles
   unsigned char stage[IN8 ? 4 : 1][IN8 ? 64 * DH : 16];    // int8 staging tiles
   int8_t sexp[IN8 ? kQ8MaxSplit : 4];                      // int8: the split's token exponents
 };
@@ -139,12 +151,19 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   constexpr float kRescale = 15.f;      // P = exp2(s - m) <= 2^15 < the fp16 maximum
   static_assert(DMA % NW == 0 && IN_PIECES % (NW * 64) == 0, "tile work must split evenly");
   static_assert(!IN8 || DH == 128, "int8 input: 128-channel heads");
+  // CM (eight-wave groups, 128-channel heads, bf16 input): the scores read
+  // the bf16 tile as copied, on bf16 matrix cores; the conversion writes an
+  // fp16 copy of the tile in channel-major order, from which the P V
+  // fragments are plain 16-byte reads.  Otherwise the tile is converted in
+  // place and the P V fragments come from transposing reads.
+  constexpr bool CM = kChannelMajor<NW, DH, IN8>;
   // fp16 tiles (bf16 input: the copy lands here and is converted in place;
   // int8 input: converted here from the staging ring)
   auto& ring = sm.ring;
   auto& stage = sm.stage;
   auto& sexp = sm.sexp;
   static_assert(sizeof(sm.ring[0]) == TILE_BYTES, "ring slot size");
+  static_assert(!CM || (CVT_PER_THREAD == 2 && sizeof(sm.tr[0]) == TILE_BYTES), "channel-major copy: two pieces per thread");
 
   int bh, lt;
   map_tile(blockIdx.x, n_bh, n_lt, bh, lt);
@@ -158,8 +177,9 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, G = lane >> 4, c = lane & 15;
   const int lat0 = lt * NW * 32 + w * 32;
 
-  // query fragments (fp16, B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..]
-  f16x8 qf[2][DC];
+  // query fragments (B operand): lane holds Cq[lat0 + rb*16 + c][h*DH + dc*32 + 8G ..],
+  // bf16 as stored when the scores read the bf16 tile (CM), else fp16
+  Pack8 qf[2][DC];
   if constexpr (IN8) {
     const int8_t* lat = static_cast<const int8_t*>(a.latents);
 #pragma unroll
@@ -172,9 +192,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
                                 : u32x2{0u, 0u};
         u32x4 lo, hi;
         i8x16_to_f16_pow2(u32x4{q[0], q[1], 0u, 0u}, e, lo, hi);
-        Pack8 pk;
-        pk.u = lo;
-        qf[rb][dc] = pk.h;
+        qf[rb][dc].u = lo;
       }
     }
   } else {
@@ -187,9 +205,11 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
         Pack8 pk;
         pk.u = r < a.C ? *reinterpret_cast<const u32x4*>(lat + (size_t)r * a.d + h * DH + dc * 32 + 8 * G)
                        : u32x4{0u, 0u, 0u, 0u};
+        if constexpr (!CM) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) pk.u[e] = bf16x2_to_f16x2(pk.u[e]);
-        qf[rb][dc] = pk.h;
+          for (int e = 0; e < 4; ++e) pk.u[e] = bf16x2_to_f16x2(pk.u[e]);
+        }
+        qf[rb][dc] = pk;
       }
     }
   }
@@ -256,11 +276,58 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   auto exp_addr = [&](int tile, int i) {
     return sexp_base + (uint32_t)min(min(tile, last) * TT + piece_token(i), tok1 - tok0 - 1);
   };
-  // conversion of this thread's pieces of a tile: bf16 in place, or int8
-  // from the staging slot into the fp16 slot
+  // Channel-major fp16 copy (CM): row ch (128 bytes) of a slot holds channel
+  // ch of the tile's 64 tokens as 8 pieces of 8 tokens, piece p = 4 hf + j
+  // holding tokens 32 hf + 4 j + {0..3} and 32 hf + 16 + 4 j + {0..3} (the
+  // K order of the P V products), at slot p ^ cm_swz(ch).  A 16-byte access
+  // serves lanes 0..7 of one group of 16 with lanes 8..15 of the
+  // neighbouring group; cm_swz keeps bit 0 of the slot, so the two halves of
+  // a pass, whose pieces differ in bit 0, never share a bank, and within a
+  // half it spreads the 4 rows of each parity over 4 slots.
+  constexpr int TROW = TT * 2;
+  auto cm_swz = [](int ch) { return ((ch >> 1) & 3) << 1; };
+  // Conversion pieces (CM): wave w takes channels 16 w .. 16 w + 15, group
+  // G the half hf = G / 2 and the pieces j = 2 (G & 1) + {0, 1}; each piece
+  // is two transposing reads of 4 tokens x 16 channels of the bf16 tile
+  // (one per 16-token block of the half), lane c receiving channel
+  // 16 w + c.  The two pieces are taken in the order (G & 1) ^ {0, 1}, so
+  // that in each read and each write the two groups that share a pass
+  // address different rows (reads) and pieces of opposite parity (writes).
+  uint32_t cm_rd[2] = {0u, 0u}, cm_wr[2] = {0u, 0u};
+  if constexpr (CM) {
+    const int hf_ = G >> 1, rp = G & 1;
+    const uint32_t tr0 = lds_addr(sm.tr[0]);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int pj = 2 * rp + (j ^ rp);                        // piece within the half
+      const int trow = hf_ * 32 + 4 * pj + (c >> 2);           // token row of the first block
+      cm_rd[j] = lds_addr(ring[0]) + trow * ROW + (((2 * w + ((c & 3) >> 1)) ^ swz<DH>(trow)) * 16) + (c & 1) * 8;
+      cm_wr[j] = tr0 + (w * 16 + c) * TROW + (((4 * hf_ + pj) ^ cm_swz(c)) * 16);
+    }
+  }
+  // conversion of this thread's pieces of a tile: bf16 in place (or, CM,
+  // into the channel-major copy), or int8 from the staging slot into the
+  // fp16 slot
   auto convert = [&](int slot, int tile) {
     const uint32_t base = lds_addr(ring[slot]);
-    if constexpr (IN8) {
+    if constexpr (CM) {
+      const uint32_t rs = (uint32_t)slot * TILE_BYTES;
+      u32x4 v[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const u32x2 r0 = lds_read_tr16_b64_off<0>(cm_rd[j] + rs);
+        const u32x2 r1 = lds_read_tr16_b64_off<16 * ROW>(cm_rd[j] + rs);
+        v[j] = u32x4{r0[0], r0[1], r1[0], r1[1]};
+      }
+      lds_wait();
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        tie(v[j]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[j][e] = bf16x2_to_f16x2(v[j][e]);
+        lds_write_b128(cm_wr[j] + rs, v[j]);
+      }
+    } else if constexpr (IN8) {
       const uint32_t sbase = lds_addr(stage[slot]);
       u32x4 v[CVT_PER_THREAD];
       int e[CVT_PER_THREAD];
@@ -311,6 +378,14 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
     for (int db = 0; db < DB; ++db)
       vbase[db] = ring0 + tt * ROW + ((2 * db + ((c & 3) >> 1)) ^ swz<DH>(tt)) * 16 + (c & 1) * 8;
   }
+  // CM: P V fragment of lane (c, G) for half hf and value block db: row
+  // 16 db + c of the channel-major copy, piece 4 hf + G (cm_swz(16 db + c) =
+  // cm_swz(c)); the block is an immediate offset
+  uint32_t cm_v[2] = {0u, 0u};
+  if constexpr (CM) {
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) cm_v[hf] = lds_addr(sm.tr[0]) + c * TROW + (((4 * hf + G) ^ cm_swz(c)) * 16);
+  }
   // this thread's conversion pieces: base of its input (ring or staging)
   constexpr int IN_TILE = IN8 ? TT * DH : TILE_BYTES;    // input slot bytes
   const uint32_t cvt_base = (IN8 ? lds_addr(stage[0]) : ring0) + tid * 16;
@@ -323,9 +398,20 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int dc = 0; dc < DC; ++dc) qf[rb][dc] = -qf[rb][dc];
+      for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qf[rb][dc].u[e] ^= 0x80008000u;
   }
 
+  // one score product: bf16 tile and queries (CM) or fp16 ones
+  auto qk_mfma = [](const u32x4& x, const Pack8& q, const floatx4& acc) {
+    Pack8 pk;
+    pk.u = x;
+    if constexpr (CM)
+      return mfma_bf16(pk.b, q.b, acc);
+    else
+      return mfma_f16(pk.h, q.h, acc);
+  };
   // Scores of one 16-token block of a tile (4 reads, 2 * DC matrix-core ops):
   // s[rb] lane holds S[row rb*16 + c][token kb*16 + 4G + i].
 #define SD_QK_READ(XR, SB, KB)                                                             \
@@ -334,11 +420,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
 #define SD_QK_MFMA(XR, S, KB)                                                              \
   _Pragma("unroll") for (int rb = 0; rb < 2; ++rb) {                                       \
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};                                                    \
-    _Pragma("unroll") for (int dc = 0; dc < DC; ++dc) {                                    \
-      Pack8 pk;                                                                            \
-      pk.u = XR[dc];                                                                       \
-      acc = mfma_f16(pk.h, qf[rb][dc], acc);                                               \
-    }                                                                                      \
+    _Pragma("unroll") for (int dc = 0; dc < DC; ++dc) acc = qk_mfma(XR[dc], qf[rb][dc], acc); \
     S[KB][rb] = acc;                                                                       \
   }
 
@@ -448,9 +530,11 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   //   QK groups (one per 32-channel slice dc): scores of tile it+1,
   //     accumulated over dc (8 independent ops per group) | exponentials of
   //     tile it (one quarter of them per group for DH = 128)
-  //   PV groups (4 value blocks of one half each): P V of tile it | in-place
-  //     conversion of tile it+2 (first half), the lane-local threshold check
-  //     of tile it+1 (second half)
+  //   PV groups (4 value blocks of one half each): P V of tile it |
+  //     conversion of tile it+2 (first half; in place, or CM into the
+  //     channel-major slot of tile it+2, whose last reader, the P V of tile
+  //     it-2, finished two barriers earlier), the lane-local threshold
+  //     check of tile it+1 (second half)
   // and, when some lane's scores passed its threshold, takes the exact row
   // maxima and raises them (rare rescale) for the next step, while tile it+3
   // is in flight.  Every step issues one tile (re-reading the last past the
@@ -527,15 +611,30 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
           }
         }
       } else {
+        if constexpr (CM) {
+          static_for<0, 4>([&](auto dtag) {
+            constexpr int d = decltype(dtag)::value;
+            const u32x4 x = rd_b128<(4 * pb + d) * 16 * TROW>(cm_v[hf], vb);
+            v[d][0] = u32x2{x[0], x[1]};
+            v[d][1] = u32x2{x[2], x[3]};
+          });
+        } else {
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          v[d][0] = rd_tr16<hf * 32 * ROW>(vbase[4 * pb + d], vb);
-          v[d][1] = rd_tr16<hf * 32 * ROW + 16 * ROW>(vbase[4 * pb + d], vb);
+          for (int d = 0; d < 4; ++d) {
+            v[d][0] = rd_tr16<hf * 32 * ROW>(vbase[4 * pb + d], vb);
+            v[d][1] = rd_tr16<hf * 32 * ROW + 16 * ROW>(vbase[4 * pb + d], vb);
+          }
         }
         if constexpr (q == 0) {
           static_for<0, CVT_PER_THREAD>([&](auto itag) {
             constexpr int i = decltype(itag)::value;
-            cv[i] = rd_b128<i * NW * 64 * 16>(cvt_base, cb);
+            if constexpr (CM) {
+              const u32x2 r0 = rd_tr16<0>(cm_rd[i], cb);
+              const u32x2 r1 = rd_tr16<16 * ROW>(cm_rd[i], cb);
+              cv[i] = u32x4{r0[0], r0[1], r1[0], r1[1]};
+            } else {
+              cv[i] = rd_b128<i * NW * 64 * 16>(cvt_base, cb);
+            }
             if constexpr (IN8) ce[i] = lds_read_i8(exp_addr(etile, i));
           });
         }
@@ -545,6 +644,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
 
   // LDS operations issued by reads() for group g
   constexpr auto reads_in = [](int g) {
+    if (CM) return g < NQK ? 4 : (g < NG ? 4 + (g == NQK ? 2 * CVT_PER_THREAD : 0) : 0);
     return g < NQK ? 4 : (g < NG ? 8 + (g == NQK ? CVT_PER_THREAD * (IN8 ? 2 : 1) : 0) : 0);
   };
 
@@ -617,7 +717,12 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
       }
       if constexpr (g == NQK + NPVH) {
         // conversion finished in the first half: write it back
-        if constexpr (!IN8) {
+        if constexpr (CM) {
+          static_for<0, CVT_PER_THREAD>([&](auto itag) {
+            constexpr int i = decltype(itag)::value;
+            wr_b128<0>(cm_wr[i], cs, cv[i]);
+          });
+        } else if constexpr (!IN8) {
           static_for<0, CVT_PER_THREAD>([&](auto itag) {
             constexpr int i = decltype(itag)::value;
             wr_b128<i * NW * 64 * 16>(cvt_base, cs, cv[i]);
@@ -635,11 +740,9 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
           const int kb = g * KPG + kk;
 #pragma unroll
           for (int dc = 0; dc < DC; ++dc) {
-            Pack8 pk;
-            pk.u = x[kk * DC + dc];
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb)
-              snext[kb][rb] = mfma_f16(pk.h, qf[rb][dc], dc == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : snext[kb][rb]);
+              snext[kb][rb] = qk_mfma(x[kk * DC + dc], qf[rb][dc], dc == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : snext[kb][rb]);
           }
         }
         // exponentials of the same blocks of tile it: pf[kb / 2][rb]
@@ -739,8 +842,17 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       u32x2 vr[DB][2];
-      if (hf == 0) SD_PV_READ(vr, vb, 0)
-      if (hf == 1) SD_PV_READ(vr, vb, 1)
+      if constexpr (CM) {
+        static_for<0, DB>([&](auto dtag) {
+          constexpr int db = decltype(dtag)::value;
+          const u32x4 x = lds_read_b128_off<db * 16 * TROW>(cm_v[hf] + vb);
+          vr[db][0] = u32x2{x[0], x[1]};
+          vr[db][1] = u32x2{x[2], x[3]};
+        });
+      } else {
+        if (hf == 0) SD_PV_READ(vr, vb, 0)
+        if (hf == 1) SD_PV_READ(vr, vb, 1)
+      }
       lds_wait();
 #pragma unroll
       for (int db = 0; db < DB; ++db) {

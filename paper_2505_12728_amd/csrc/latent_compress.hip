@@ -276,34 +276,23 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
   auto exp_addr = [&](int tile, int i) {
     return sexp_base + (uint32_t)min(min(tile, last) * TT + piece_token(i), tok1 - tok0 - 1);
   };
-  // Channel-major fp16 copy (CM): row ch (128 bytes) of a slot holds channel
-  // ch of the tile's 64 tokens as 8 pieces of 8 tokens, piece p = 4 hf + j
-  // holding tokens 32 hf + 4 j + {0..3} and 32 hf + 16 + 4 j + {0..3} (the
-  // K order of the P V products), at slot p ^ cm_swz(ch).  A 16-byte access
-  // serves lanes 0..7 of one group of 16 with lanes 8..15 of the
-  // neighbouring group; cm_swz keeps bit 0 of the slot, so the two halves of
-  // a pass, whose pieces differ in bit 0, never share a bank, and within a
-  // half it spreads the 4 rows of each parity over 4 slots.
-  constexpr int TROW = TT * 2;
-  auto cm_swz = [](int ch) { return ((ch >> 1) & 3) << 1; };
-  // Conversion pieces (CM): wave w takes channels 16 w .. 16 w + 15, group
-  // G the half hf = G / 2 and the pieces j = 2 (G & 1) + {0, 1}; each piece
-  // is two transposing reads of 4 tokens x 16 channels of the bf16 tile
-  // (one per 16-token block of the half), lane c receiving channel
-  // 16 w + c.  The two pieces are taken in the order (G & 1) ^ {0, 1}, so
-  // that in each read and each write the two groups that share a pass
-  // address different rows (reads) and pieces of opposite parity (writes).
-  uint32_t cm_rd[2] = {0u, 0u}, cm_wr[2] = {0u, 0u};
+  // Channel-major fp16 copy (CM), laid out by its fragments: a slot holds
+  // the 16-byte piece (hf, db, G, c) at byte hf * 8192 + db * 1024 +
+  // G * 256 + c * 16, namely channel 16 db + c at tokens 32 hf + 4 G +
+  // {0..3} and 32 hf + 16 + 4 G + {0..3} (the K order of the P V products).
+  // The P V fragment of lane (c, G) for half hf and value block db is then
+  // the piece at its own lane offset, and the conversion, in which wave w
+  // takes value block w and thread (G, c) the pieces (hf, w, G, c) of both
+  // halves, writes at its thread offset: both are 1024 contiguous bytes per
+  // wave and instruction, free of bank conflicts.  Each piece is two
+  // transposing reads of 4 tokens x 16 channels of the bf16 tile (tokens
+  // 32 hf + 16 blk + 4 G + {0..3}, lane c receiving channel 16 w + c), the
+  // pattern of the in-place kernel's F_V^T reads.
+  uint32_t cm_rd = 0u, cm_wr = 0u;
   if constexpr (CM) {
-    const int hf_ = G >> 1, rp = G & 1;
-    const uint32_t tr0 = lds_addr(sm.tr[0]);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int pj = 2 * rp + (j ^ rp);                        // piece within the half
-      const int trow = hf_ * 32 + 4 * pj + (c >> 2);           // token row of the first block
-      cm_rd[j] = lds_addr(ring[0]) + trow * ROW + (((2 * w + ((c & 3) >> 1)) ^ swz<DH>(trow)) * 16) + (c & 1) * 8;
-      cm_wr[j] = tr0 + (w * 16 + c) * TROW + (((4 * hf_ + pj) ^ cm_swz(c)) * 16);
-    }
+    const int trow = 4 * G + (c >> 2);                         // token row of half 0, block 0
+    cm_rd = lds_addr(ring[0]) + trow * ROW + (((2 * w + ((c & 3) >> 1)) ^ swz<DH>(trow)) * 16) + (c & 1) * 8;
+    cm_wr = lds_addr(sm.tr[0]) + tid * 16;
   }
   // conversion of this thread's pieces of a tile: bf16 in place (or, CM,
   // into the channel-major copy), or int8 from the staging slot into the
@@ -313,19 +302,19 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
     if constexpr (CM) {
       const uint32_t rs = (uint32_t)slot * TILE_BYTES;
       u32x4 v[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const u32x2 r0 = lds_read_tr16_b64_off<0>(cm_rd[j] + rs);
-        const u32x2 r1 = lds_read_tr16_b64_off<16 * ROW>(cm_rd[j] + rs);
+      static_for<0, 2>([&](auto jtag) {
+        constexpr int j = decltype(jtag)::value;
+        const u32x2 r0 = lds_read_tr16_b64_off<j * 32 * ROW>(cm_rd + rs);
+        const u32x2 r1 = lds_read_tr16_b64_off<j * 32 * ROW + 16 * ROW>(cm_rd + rs);
         v[j] = u32x4{r0[0], r0[1], r1[0], r1[1]};
-      }
+      });
       lds_wait();
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         tie(v[j]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[j][e] = bf16x2_to_f16x2(v[j][e]);
-        lds_write_b128(cm_wr[j] + rs, v[j]);
+        lds_write_b128(cm_wr + rs + j * 8192, v[j]);
       }
     } else if constexpr (IN8) {
       const uint32_t sbase = lds_addr(stage[slot]);
@@ -378,14 +367,9 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
     for (int db = 0; db < DB; ++db)
       vbase[db] = ring0 + tt * ROW + ((2 * db + ((c & 3) >> 1)) ^ swz<DH>(tt)) * 16 + (c & 1) * 8;
   }
-  // CM: P V fragment of lane (c, G) for half hf and value block db: row
-  // 16 db + c of the channel-major copy, piece 4 hf + G (cm_swz(16 db + c) =
-  // cm_swz(c)); the block is an immediate offset
-  uint32_t cm_v[2] = {0u, 0u};
-  if constexpr (CM) {
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) cm_v[hf] = lds_addr(sm.tr[0]) + c * TROW + (((4 * hf + G) ^ cm_swz(c)) * 16);
-  }
+  // CM: P V fragments at the lane's offset in the channel-major copy; the
+  // half and the value block are immediate offsets
+  const uint32_t cm_v = CM ? lds_addr(sm.tr[0]) + lane * 16 : 0u;
   // this thread's conversion pieces: base of its input (ring or staging)
   constexpr int IN_TILE = IN8 ? TT * DH : TILE_BYTES;    // input slot bytes
   const uint32_t cvt_base = (IN8 ? lds_addr(stage[0]) : ring0) + tid * 16;
@@ -614,7 +598,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
         if constexpr (CM) {
           static_for<0, 4>([&](auto dtag) {
             constexpr int d = decltype(dtag)::value;
-            const u32x4 x = rd_b128<(4 * pb + d) * 16 * TROW>(cm_v[hf], vb);
+            const u32x4 x = rd_b128<hf * 8192 + (4 * pb + d) * 1024>(cm_v, vb);
             v[d][0] = u32x2{x[0], x[1]};
             v[d][1] = u32x2{x[2], x[3]};
           });
@@ -629,8 +613,8 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
           static_for<0, CVT_PER_THREAD>([&](auto itag) {
             constexpr int i = decltype(itag)::value;
             if constexpr (CM) {
-              const u32x2 r0 = rd_tr16<0>(cm_rd[i], cb);
-              const u32x2 r1 = rd_tr16<16 * ROW>(cm_rd[i], cb);
+              const u32x2 r0 = rd_tr16<i * 32 * ROW>(cm_rd, cb);
+              const u32x2 r1 = rd_tr16<i * 32 * ROW + 16 * ROW>(cm_rd, cb);
               cv[i] = u32x4{r0[0], r0[1], r1[0], r1[1]};
             } else {
               cv[i] = rd_b128<i * NW * 64 * 16>(cvt_base, cb);
@@ -720,7 +704,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
         if constexpr (CM) {
           static_for<0, CVT_PER_THREAD>([&](auto itag) {
             constexpr int i = decltype(itag)::value;
-            wr_b128<0>(cm_wr[i], cs, cv[i]);
+            wr_b128<i * 8192>(cm_wr, cs, cv[i]);
           });
         } else if constexpr (!IN8) {
           static_for<0, CVT_PER_THREAD>([&](auto itag) {
@@ -845,7 +829,7 @@ __device__ __forceinline__ unsigned compress_pass(const CompressArgs a, int n_bh
       if constexpr (CM) {
         static_for<0, DB>([&](auto dtag) {
           constexpr int db = decltype(dtag)::value;
-          const u32x4 x = lds_read_b128_off<db * 16 * TROW>(cm_v[hf] + vb);
+          const u32x4 x = lds_read_b128_off<db * 1024>(cm_v + vb + hf * 8192);
           vr[db][0] = u32x2{x[0], x[1]};
           vr[db][1] = u32x2{x[2], x[3]};
         });

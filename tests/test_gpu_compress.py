@@ -64,6 +64,12 @@ CASES = [
     ("split-tokens", "bf16", 1, 20000, 64, 128, 1, 1 / math.sqrt(128)),
     ("eight-waves-ragged-splits", "bf16", 1, 20037, 260, 256, 2, 1 / math.sqrt(128)),
     ("eight-waves-head-dim-64", "bf16", 1, 1500, 300, 128, 2, 1 / 8),
+    # a negative scale is folded into the queries (bf16 sign flips on the
+    # channel-major path of eight-wave groups, fp16 ones elsewhere); a zero
+    # scale gives every token the same weight
+    ("eight-waves-negative-scale", "bf16", 1, 3000, 256, 256, 2, -1 / math.sqrt(128)),
+    ("four-waves-negative-scale", "bf16", 2, 900, 128, 256, 2, -0.5),
+    ("eight-waves-zero-scale", "bf16", 1, 700, 256, 256, 2, 0.0),
     ("bf16-dh256", "bf16", 2, 700, 40, 512, 2, 1 / 16),
     ("bf16-dh256-one-token", "bf16", 1, 1, 9, 256, 1, 1.0),
     ("bf16-dh256-ragged", "bf16", 1, 3001, 17, 768, 3, 1 / 16),

@@ -59,6 +59,7 @@ CASES = [
     ("one-token", 1, 1, 32, 128, 1, 1.0),
     ("eight-waves-splits", 1, 20037, 260, 256, 2, 1 / math.sqrt(128)),
     ("long-split", 1, 40000, 256, 128, 1, 1.0),
+    ("eight-waves-negative-scale", 1, 3000, 256, 256, 2, -1 / math.sqrt(128)),
 ]
 
 

@@ -88,7 +88,7 @@ struct LmHeadArgs {
   float* probs;        // [R, V]
   int R, d, V;
   float scale_log2;    // log2(e) / temperature
-  float* stats;        // workspace: [R][ceil(V/16)] block (max, sum), then [R] row (M, L)
+  float* stats;        // workspace: [R][pairs] (max, sum) pairs, pairs <= ceil(V/16) (per block or per work-group)
   int cus;             // compute units of the device (0: no per-unit balancing)
   int nfull;           // set by the launch: work-groups with a block for every wave (< 0: all)
 };

@@ -5,24 +5,26 @@
 //   probs[r, v] = softmax_v(hidden[r] . weight[v] / tau)
 //
 // The pass is bound by streaming the weight [V, d] once (R <= 256 rows share
-// every weight byte), so the three kernels are shaped around that stream:
+// every weight byte), so the two kernels are shaped around that stream:
 // 1. logits.  z^T = W H^T on bf16 matrix cores, the lane owning one hidden
 //    row; every wave covers its own vocabulary rows for all R hidden rows,
 //    so each weight byte is read once.  The scaled logits s = z log2(e) / tau
-//    are written to `probs` as fp32, with the (max, sum of 2^(s - max)) of
-//    every 16-entry vocabulary block and row.
+//    are written to `probs` as fp32, with (max, sum of 2^(s - max)) pairs
+//    of every row: one per work-group (its waves' blocks merged in LDS) or
+//    one per 16-entry vocabulary block.
 //    - `lm_logits_burst` (R <= 64, d % 256 == 0): 16 vocabulary rows per
 //      wave read in 512-byte runs per row, straight into registers; the
-//      hidden chunk of 256 channels of all rows staged through LDS by DMA.
+//      hidden chunk of 256 channels of all rows staged through LDS by DMA;
+//      one pair per row and work-group.
 //    - `lm_logits_bf16` (the other shapes): 16 or 32 vocabulary rows per
 //      wave read 128 bytes per row at a time, the next 64 channels in
 //      flight while the current ones are multiplied; the hidden chunk of 64
 //      channels staged through double-buffered, swizzled LDS.
-// 2. statistics, one work-group per row: the per-block pairs are merged
-//    into the row's (M, L).
-// 3. normalisation: probs = 2^(s - M) / L in place.
+// 2. normalisation: every work-group merges its row's pairs into (M, L)
+//    (a few kilobytes, read from L2), then rewrites probs = 2^(s - M) / L
+//    in place.
 // The fp32 path computes the logits as float64 dot products (one thread
-// per row and entry) and shares kernels 2 and 3.
+// per row and entry) and shares kernel 2.
 #include <math.h>
 
 #include <algorithm>
@@ -198,7 +200,8 @@ typedef __attribute__((address_space(1))) const void gbl_cvoid;
 // Scaled logits of 16 vocabulary rows (accumulator rows) x 16 hidden rows
 // (columns) to probs, with the (max, sum) of the 16-entry vocabulary block
 // for every hidden row
-__device__ __forceinline__ void write_block(const LmHeadArgs& a, const floatx4& acc, int vbase, int r) {
+template <bool STATS>
+__device__ __forceinline__ Stat write_block(const LmHeadArgs& a, const floatx4& acc, int vbase, int r) {
   const int lane = threadIdx.x & 63, G = lane >> 4;
   const int V = a.V;
   floatx4 s;
@@ -217,8 +220,9 @@ __device__ __forceinline__ void write_block(const LmHeadArgs& a, const floatx4& 
       for (int i = 0; i < 4; ++i)
         if (vbase + 4 * G + i < V) dst[i] = s[i];
     }
-    if (G == 0) reinterpret_cast<float2*>(a.stats)[(size_t)r * ((V + 15) / 16) + vbase / 16] = make_float2(st.m, st.l);
+    if (STATS && G == 0) reinterpret_cast<float2*>(a.stats)[(size_t)r * ((V + 15) / 16) + vbase / 16] = make_float2(st.m, st.l);
   }
+  return st;
 }
 
 // Logits for R <= 64 hidden rows and widths d % 256 == 0, shaped for long
@@ -246,6 +250,7 @@ __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
   constexpr int DMA = HPIECES / (NW * 64);     // copies per thread and chunk
   static_assert(HPIECES % (NW * 64) == 0, "whole copies per thread");
   __shared__ __align__(16) unsigned char hbuf[2][HPIECES * 16];
+  __shared__ Stat wst[NW][HROWS];              // per wave: its blocks' statistics of every hidden row
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), G = lane >> 4, c = lane & 15;
   const int wg = blockIdx.x;
@@ -285,15 +290,15 @@ __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
     for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int nch = d / 256;
   issue_hidden(0, 0);
-  if (!full && w == NW - 1) {
+  const bool idle = !full && w == NW - 1;
+  if (idle) {
     // same copies, waits and barriers as the other waves, no weight rows
 #pragma unroll 1
     for (int n = 0; n < nch; ++n) {
       wait_vm_then_barrier<0>();
       if (n + 1 < nch) issue_hidden(n + 1, (n & 1) ^ 1);
     }
-    return;
-  }
+  } else {
 #pragma unroll 1
   for (int n = 0; n < nch; ++n) {
     const int buf = n & 1;
@@ -323,10 +328,30 @@ __global__ __launch_bounds__(NW * 64) void lm_logits_burst(LmHeadArgs a) {
     }
     if (n + 1 < nch) issue_hidden(n + 1, buf ^ 1);
   }
+  }
+  // scaled logits to probs; the statistics of this work-group's blocks,
+  // merged over its waves, as one (max, sum) pair per hidden row at
+  // stats[r * gridDim.x + blockIdx.x]
+  Stat st[RB];
 #pragma unroll
-  for (int vb = 0; vb < VB; ++vb)
+  for (int rb = 0; rb < RB; ++rb) st[rb] = Stat{-INFINITY, 0.f};
+  if (!idle) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) write_block(a, acc[vb][rb], v0 + vb * 16, rb * 16 + c);
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) st[rb] = merge(st[rb], write_block<false>(a, acc[vb][rb], v0 + vb * 16, rb * 16 + c));
+  }
+  if (G == 0) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) wst[w][rb * 16 + c] = st[rb];
+  }
+  __syncthreads();
+  if (tid < HROWS && tid < R) {
+    Stat t = wst[0][tid];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) t = merge(t, wst[i][tid]);
+    reinterpret_cast<float2*>(a.stats)[(size_t)tid * gridDim.x + blockIdx.x] = make_float2(t.m, t.l);
+  }
 }
 
 // fp32 inputs: one thread per (row, vocabulary entry), float64 dot product;
@@ -355,21 +380,22 @@ __global__ __launch_bounds__(256) void lm_logits_f32(LmHeadArgs a) {
     reinterpret_cast<float2*>(a.stats)[(size_t)r * nblk + v / 16] = make_float2(m, l);
 }
 
-// one work-group of 1024 threads per row: merge the per-block statistics
-// into (M, L).  Each thread takes its pairs eight at a time (eight loads in
-// flight, then one rescale), so the row costs a few memory latencies.
-__global__ __launch_bounds__(1024) void lm_stats(LmHeadArgs a) {
-  __shared__ Stat part[16];
-  const int r = blockIdx.x;
-  const int nblk = (a.V + 15) / 16;
-  const float2* st = reinterpret_cast<const float2*>(a.stats) + (size_t)r * nblk;
+// probs = 2^(s - M) / L, in place, 16-byte accesses when the row allows.
+// Each work-group first merges the row's npairs (max, sum) pairs into
+// (M, L), every thread taking its pairs eight at a time (eight loads in
+// flight, then one rescale), so the merge costs a few memory latencies.
+__global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a, int npairs) {
+  __shared__ Stat part[4];
+  const int r = blockIdx.y;
+  const int V = a.V;
+  const float2* st = reinterpret_cast<const float2*>(a.stats) + (size_t)r * npairs;
   Stat acc{-INFINITY, 0.f};
-  for (int base = threadIdx.x; base < nblk; base += 1024 * 8) {
+  for (int base = threadIdx.x; base < npairs; base += 256 * 8) {
     float2 x[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int i = base + j * 1024;
-      x[j] = i < nblk ? st[i] : make_float2(-INFINITY, 0.f);
+      const int i = base + j * 256;
+      x[j] = i < npairs ? st[i] : make_float2(-INFINITY, 0.f);
     }
     float m = acc.m;
 #pragma unroll
@@ -385,20 +411,10 @@ __global__ __launch_bounds__(1024) void lm_stats(LmHeadArgs a) {
   for (int o = 32; o > 0; o >>= 1) acc = merge(acc, Stat{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.l, o, 64)});
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    Stat t = part[0];
-    for (int i = 1; i < 16; ++i) t = merge(t, part[i]);
-    reinterpret_cast<float2*>(a.stats)[(size_t)a.R * nblk + r] = make_float2(t.m, t.l);
-  }
-}
-
-// probs = 2^(s - M) / L, in place; 16-byte accesses when the row allows
-__global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
-  const int r = blockIdx.y;
-  const int V = a.V;
-  const int nblk = (V + 15) / 16;
-  const float2 ML = reinterpret_cast<const float2*>(a.stats)[(size_t)a.R * nblk + r];
-  const float inv = 1.f / ML.y;
+  Stat ML = part[0];
+#pragma unroll
+  for (int i = 1; i < 4; ++i) ML = merge(ML, part[i]);
+  const float inv = 1.f / ML.l;
   float* row = a.probs + (size_t)r * V;
   const int stride = gridDim.x * 256;
   if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(row) & 15) == 0) {
@@ -406,16 +422,20 @@ __global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a) {
     for (int v = blockIdx.x * 256 + threadIdx.x; v < V / 4; v += stride) {
       floatx4 x = row4[v];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = fast_exp2(x[i] - ML.x) * inv;
+      for (int i = 0; i < 4; ++i) x[i] = fast_exp2(x[i] - ML.m) * inv;
       row4[v] = x;
     }
   } else {
-    for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += stride) row[v] = fast_exp2(row[v] - ML.x) * inv;
+    for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += stride) row[v] = fast_exp2(row[v] - ML.m) * inv;
   }
 }
 
+// Launches the logits kernel; *npairs receives the statistics pairs it
+// writes per row (one per work-group for the long-row kernel, one per
+// 16-entry block otherwise).
 template <int RB>
-hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st) {
+hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st, int* npairs) {
+  *npairs = (a.V + 15) / 16;
   if constexpr (RB <= 4) {
     if (a.d % 256 == 0) {
       LmHeadArgs b = a;
@@ -433,8 +453,10 @@ hipError_t launch_rb(const LmHeadArgs& a, hipStream_t st) {
           }
         }
         hipLaunchKernelGGL((lm_logits_burst<RB, 8, 1>), dim3(grid), dim3(512), 0, st, b);
+        *npairs = grid;
       } else {
         hipLaunchKernelGGL((lm_logits_burst<RB, 4, 1>), dim3((a.V + 63) / 64), dim3(256), 0, st, b);
+        *npairs = (a.V + 63) / 64;
       }
       return hipGetLastError();
     }
@@ -456,37 +478,35 @@ size_t lm_head_workspace_bytes(int R, int V) {
 
 hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t st) {
   hipError_t e = hipSuccess;
+  int npairs = (a.V + 15) / 16;
   if (dtype == 0) {
     hipLaunchKernelGGL(lm_logits_f32, dim3((a.V + 255) / 256, a.R), dim3(256), 0, st, a);
     e = hipGetLastError();
   } else {
     switch ((a.R + 15) / 16) {
-      case 1: e = launch_rb<1>(a, st); break;
-      case 2: e = launch_rb<2>(a, st); break;
-      case 3: e = launch_rb<3>(a, st); break;
-      case 4: e = launch_rb<4>(a, st); break;
-      case 5: e = launch_rb<5>(a, st); break;
-      case 6: e = launch_rb<6>(a, st); break;
-      case 7: e = launch_rb<7>(a, st); break;
-      case 8: e = launch_rb<8>(a, st); break;
-      case 9: e = launch_rb<9>(a, st); break;
-      case 10: e = launch_rb<10>(a, st); break;
-      case 11: e = launch_rb<11>(a, st); break;
-      case 12: e = launch_rb<12>(a, st); break;
-      case 13: e = launch_rb<13>(a, st); break;
-      case 14: e = launch_rb<14>(a, st); break;
-      case 15: e = launch_rb<15>(a, st); break;
-      case 16: e = launch_rb<16>(a, st); break;
+      case 1: e = launch_rb<1>(a, st, &npairs); break;
+      case 2: e = launch_rb<2>(a, st, &npairs); break;
+      case 3: e = launch_rb<3>(a, st, &npairs); break;
+      case 4: e = launch_rb<4>(a, st, &npairs); break;
+      case 5: e = launch_rb<5>(a, st, &npairs); break;
+      case 6: e = launch_rb<6>(a, st, &npairs); break;
+      case 7: e = launch_rb<7>(a, st, &npairs); break;
+      case 8: e = launch_rb<8>(a, st, &npairs); break;
+      case 9: e = launch_rb<9>(a, st, &npairs); break;
+      case 10: e = launch_rb<10>(a, st, &npairs); break;
+      case 11: e = launch_rb<11>(a, st, &npairs); break;
+      case 12: e = launch_rb<12>(a, st, &npairs); break;
+      case 13: e = launch_rb<13>(a, st, &npairs); break;
+      case 14: e = launch_rb<14>(a, st, &npairs); break;
+      case 15: e = launch_rb<15>(a, st, &npairs); break;
+      case 16: e = launch_rb<16>(a, st, &npairs); break;
       default: return hipErrorInvalidValue;   // R <= 256 is checked by the caller
     }
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lm_stats, dim3(a.R), dim3(1024), 0, st, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
   // about two 16-byte pieces per thread
   const int per_row = (a.V + 2047) / 2048;
-  hipLaunchKernelGGL(lm_normalize, dim3(std::min(per_row, 64), a.R), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(lm_normalize, dim3(std::min(per_row, 64), a.R), dim3(256), 0, st, a, npairs);
   return hipGetLastError();
 }
 

@@ -418,12 +418,23 @@ __global__ __launch_bounds__(256) void lm_normalize(LmHeadArgs a, int npairs) {
   float* row = a.probs + (size_t)r * V;
   const int stride = gridDim.x * 256;
   if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(row) & 15) == 0) {
+    // a contiguous range of 16-byte pieces per work-group, eight loads in
+    // flight per thread before any store
     floatx4* row4 = reinterpret_cast<floatx4*>(row);
-    for (int v = blockIdx.x * 256 + threadIdx.x; v < V / 4; v += stride) {
-      floatx4 x = row4[v];
+    const int n4 = V / 4, per = (n4 + gridDim.x - 1) / gridDim.x;
+    const int c0 = blockIdx.x * per, c1 = min(n4, c0 + per);
+    for (int base = c0 + threadIdx.x; base < c1; base += 256 * 8) {
+      floatx4 x[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = fast_exp2(x[i] - ML.m) * inv;
-      row4[v] = x;
+      for (int j = 0; j < 8; ++j)
+        if (base + j * 256 < c1) x[j] = row4[base + j * 256];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (base + j * 256 < c1) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) x[j][i] = fast_exp2(x[j][i] - ML.m) * inv;
+          row4[base + j * 256] = x[j];
+        }
     }
   } else {
     for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += stride) row[v] = fast_exp2(row[v] - ML.m) * inv;
@@ -504,8 +515,12 @@ hipError_t launch_lm_head(const LmHeadArgs& a, int dtype, hipStream_t st) {
     }
   }
   if (e != hipSuccess) return e;
-  // about two 16-byte pieces per thread
-  const int per_row = (a.V + 2047) / 2048;
+  // up to eight 16-byte pieces per thread: each work-group also reads the
+  // row's pairs, so fewer, fuller work-groups read them fewer times; but
+  // at least two work-groups per compute unit over all rows while that
+  // leaves each thread two pieces or more
+  const int cus = a.cus > 0 ? a.cus : 256;
+  const int per_row = std::max((a.V + 8191) / 8192, std::min((a.V + 2047) / 2048, (2 * cus + a.R - 1) / a.R));
   hipLaunchKernelGGL(lm_normalize, dim3(std::min(per_row, 64), a.R), dim3(256), 0, st, a, npairs);
   return hipGetLastError();
 }

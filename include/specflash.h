@@ -348,8 +348,9 @@ int sd_philox_uniforms(uint64_t seed, uint64_t offset, float* u, int B,
  *   hidden  [R, d] dtype    hidden states (target rows, or the draft's rows)
  *   weight  [V, d] dtype    head weight (nn.Linear layout: one row per entry)
  *   probs   [R, V] float32  out
- *   workspace  sd_lm_head_workspace_size(R, d, V, dtype) bytes (per-block
- *              and per-row softmax statistics)
+ *   workspace  sd_lm_head_workspace_size(R, d, V, dtype) bytes (the rows'
+ *              partial softmax statistics, one (max, sum) pair per
+ *              16-entry block or per work-group of the logits pass)
  * Requirements: R, d, V >= 1; temperature > 0 and finite; V <= 2^24;
  * SD_BF16: R <= 256, d % 64 == 0, 16-byte aligned hidden and weight (the
  * weight is streamed from HBM once); SD_F32 (float64 dot products, for
